@@ -1,0 +1,90 @@
+/*
+ * bsref.h -- CPU oracle for low-precision bitserial operators.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This is a plain, slow, obviously correct host
+ * implementation of what the GPU library computes.  Only the tests, the smoke
+ * check and the benchmark's CPU-baseline leg may load it; the product path
+ * never does.  It shares no source, header, table or helper with the GPU
+ * library: every definition below is written out from the paper
+ * ("Automating Generation of Low Precision Deep Learning Operators",
+ * Cowan, Moreau, Chen, Ceze) and the readings listed in the design notes.
+ *
+ * All pointers are HOST pointers owned by the caller.  Every function returns
+ * 0 on success and a nonzero code on an invalid argument, in which case it
+ * has written nothing.
+ */
+#ifndef BSREF_H
+#define BSREF_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BSREF_OK 0
+#define BSREF_EINVAL 1
+#define BSREF_ERANGE 3
+
+#define BSREF_UNIPOLAR 0
+#define BSREF_BIPOLAR 1
+
+/* Quantization of float data to k bits (Sec. 3.1; contribution list, Sec. 1).
+ * The paper names the operator but prints no formula.  Reading used here:
+ *   unipolar: q = clamp(round_half_even(fl32(x * scale)), 0, 2^bits - 1),
+ *             NaN -> 0, +inf -> 2^bits - 1, -inf -> 0, denormals kept;
+ *   bipolar (bits == 1 only): q = 1 if x >= 0 (so -0.0 -> 1) else 0, NaN -> 0;
+ *             bit 1 encodes +1 and bit 0 encodes -1 (Sec. 2.2, bipolar format).
+ * x: [n] float32, q: [n] uint8.  scale must be finite and > 0. */
+int bsref_quantize(const float *x, uint8_t *q, int64_t n, float scale,
+                   int bits, int enc);
+
+/* Bit packing (Sec. 2.2 "bitpacked"; Sec. 3.1 bitpacking operator, layout MBK').
+ * q: [rows][k] uint8 -> packed: [rows][bits][ceil(k/32)] uint32 where bit u of
+ * word t of plane b is bit b of q[r][32t+u]; bits past k are 0; bits of q at or
+ * above `bits` are ignored. */
+int bsref_pack(const uint8_t *q, uint32_t *packed, int64_t rows, int64_t k,
+               int bits);
+
+/* Bitserial 2-D convolution, NHWC activations, OHWI filters (Sec. 3.2).
+ * The bitserial form (Eq. 1, Eq. 2) reaches exactly the integer convolution of
+ * the quantized values, so this oracle computes that convolution as written:
+ * decode each packed element to its integer value and sum products.
+ *   activation value  a = sum_i 2^i a_i                     (unipolar only)
+ *   weight value      w = sum_j 2^j w_j                     (unipolar)
+ *                     w = sum_j 2^j (2 w_j - 1)             (bipolar weights)
+ *   out[n][oh][ow][o] = sum over in-range taps (kh,kw) and channels c of a*w,
+ * taps that fall in the zero padding contribute nothing.
+ * act: [n][h][w][abits][ceil(c/32)], wts: [oc][kh][kw][wbits][ceil(c/32)],
+ * out: [n][oh][ow][oc] int32 with oh = (h + 2 pad_h - kh) / stride_h + 1. */
+typedef struct {
+    int32_t n, h, w, c;
+    int32_t oc, kh, kw;
+    int32_t stride_h, stride_w, pad_h, pad_w;
+    int32_t abits, wbits;
+    int32_t aenc, wenc;
+} bsref_conv2d_params;
+
+int bsref_conv2d_out_shape(const bsref_conv2d_params *p, int32_t *oh,
+                           int32_t *ow);
+int bsref_conv2d(const bsref_conv2d_params *p, const uint32_t *act,
+                 const uint32_t *wts, int32_t *out);
+/* Same definition, evaluated only at the flat output indices idx[0..count)
+ * (index into [n][oh][ow][oc]); vals[i] receives the output at idx[i]. */
+int bsref_conv2d_at(const bsref_conv2d_params *p, const uint32_t *act,
+                    const uint32_t *wts, const int64_t *idx, int64_t count,
+                    int32_t *vals);
+
+/* Bitserial dense / matrix multiply (Sec. 3.2; evaluated in Sec. 6.2.1):
+ * out[m][n] = sum_k a(m,k) * w(n,k) with the value decoding above.
+ * a: [m][abits][ceil(k/32)], w: [n][wbits][ceil(k/32)], out: [m][n] int32. */
+int bsref_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,
+                int wenc, const uint32_t *a, const uint32_t *w, int32_t *out);
+
+/* Number of host threads the oracle's parallel loops use. */
+int bsref_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BSREF_H */

@@ -1,0 +1,22 @@
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def pytest_configure(config):
+    config.addinivalue_line(
+        "markers", "gpu: needs an MI355X (runs the HIP library on the device)")
+    config.addinivalue_line(
+        "markers", "slow: full-size CPU check that takes more than a few seconds")
+
+
+@pytest.fixture(scope="session")
+def oracle():
+    from oracle import bsref
+    bsref.build(force=False)
+    return bsref
