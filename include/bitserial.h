@@ -1,0 +1,152 @@
+/*
+ * bitserial.h -- C ABI of libbitserial.so: low-precision bitserial operators
+ * (quantize, bit-pack, bitserial conv2d and dense) for AMD MI355X (gfx950).
+ *
+ * Method: "Automating Generation of Low Precision Deep Learning Operators"
+ * (Cowan, Moreau, Chen, Ceze).  A B-bit tensor is split into B bit-planes,
+ * each plane packed into uint32 words along the reduction axis (Sec. 2.2,
+ * Sec. 3.1); a dot product of an A-bit and a W-bit vector is then
+ *   sum_{i<A} sum_{j<W} 2^(i+j) popcount(a_i AND w_j)            (Eq. 1, Eq. 2)
+ * and, for weights in the bipolar (+1/-1) format, each AND term becomes
+ *   popcount(a_i AND w_j) - popcount(a_i AND NOT w_j).
+ *
+ * Conventions shared by every entry point:
+ *  - Data pointers are DEVICE pointers (HBM) owned by the caller; the library
+ *    never allocates, frees or keeps them.  Every base pointer must be
+ *    16-byte aligned (all torch / hipMalloc allocations are).
+ *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = null stream).
+ *    A returned BS_OK means the work was enqueued.  Faults inside a kernel
+ *    surface at the caller's next synchronisation of that stream.
+ *  - Arguments are validated on the host before anything is enqueued; an
+ *    invalid call returns its status and enqueues nothing, so no output byte
+ *    is written.  bs_last_error() then describes the problem.
+ *  - An empty problem (n == 0 or rows == 0) is valid and enqueues nothing.
+ *  - Outputs must not overlap inputs.
+ *  - Results are exact integers and do not depend on launch configuration;
+ *    no kernel uses atomics, so repeated calls are bit-identical.
+ *  - Thread safety: calls from several host threads are safe; the only
+ *    library state is per thread (the error string and the kernel mode).
+ */
+#ifndef BITSERIAL_H
+#define BITSERIAL_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BS_OK = 0,
+    BS_ERR_INVALID_ARG = 1, /* NULL/misaligned pointer, bad size or bit-width */
+    BS_ERR_UNSUPPORTED = 2, /* valid request this library does not implement */
+    BS_ERR_OVERFLOW = 3,    /* the exact result could exceed int32 */
+    BS_ERR_HIP = 4          /* the HIP runtime refused the launch */
+} bs_status;
+
+/* Encoding of 1-bit planes (Sec. 2.2): unipolar {0,1}, or bipolar where bit 1
+ * stands for +1 and bit 0 for -1. */
+typedef enum { BS_UNIPOLAR = 0, BS_BIPOLAR = 1 } bs_encoding;
+
+/* A hipStream_t, kept opaque so this header does not need HIP headers. */
+typedef void *bs_stream_t;
+
+/* Number of uint32 words one bit-plane of k elements packs into: ceil(k/32). */
+int64_t bs_packed_words(int64_t k);
+
+/* Quantization of float data to `bits`-bit codes (Sec. 3.1; Sec. 1 lists the
+ * quantization operator).  The paper gives no formula; this library fixes:
+ *   unipolar: q = clamp(round_half_to_even(fl32(x * scale)), 0, 2^bits - 1),
+ *             NaN -> 0, +inf -> 2^bits - 1, subnormals not flushed;
+ *   bipolar (bits must be 1): q = 1 if x >= 0 (including -0.0) else 0, NaN -> 0.
+ * x: [n] float32 (device), q: [n] uint8 (device).  scale: finite, > 0.
+ * Errors: BS_ERR_INVALID_ARG for NULL/misaligned pointers, n < 0, bits outside
+ * 1..8, bipolar with bits != 1, non-finite or non-positive scale. */
+bs_status bs_quantize(const float *x, uint8_t *q, int64_t n, float scale,
+                      int bits, bs_encoding enc, bs_stream_t stream);
+
+/* Bit packing (Sec. 2.2 packing into a storage word; Sec. 3.1 bitpacking
+ * operator with the bit axis placed between rows and the packed reduction
+ * axis, layout MBK').
+ * q: [rows][k] uint8 codes, row-major (device).
+ * packed: [rows][bits][ceil(k/32)] uint32 (device), fully overwritten:
+ *   bit u of word t of plane b of row r = bit b of q[r][32 t + u];
+ *   bits for elements past k are 0; bits of q at or above `bits` are ignored.
+ * Conv activations pack with rows = N*H*W, k = C; OHWI conv filters with
+ * rows = OC*KH*KW, k = C; dense operands with rows = M (or N_out), k = K.
+ * Errors: BS_ERR_INVALID_ARG for NULL/misaligned pointers, rows < 0, k < 1,
+ * bits outside 1..8. */
+bs_status bs_pack(const uint8_t *q, uint32_t *packed, int64_t rows, int64_t k,
+                  int bits, bs_stream_t stream);
+
+/* Fused quantize + pack: identical output to bs_quantize followed by bs_pack
+ * on the same [rows][k] float32 tensor, without the uint8 intermediate.
+ * Errors: as bs_quantize and bs_pack. */
+bs_status bs_quantize_pack(const float *x, uint32_t *packed, int64_t rows,
+                           int64_t k, float scale, int bits, bs_encoding enc,
+                           bs_stream_t stream);
+
+/* Bitserial 2-D convolution (Sec. 3.2; NHWC data, direct convolution without
+ * an im2col copy).  Activations must be unipolar; filters may be unipolar or
+ * bipolar.  Zero padding: taps outside the input contribute nothing.
+ *   act_packed: [n][h][w][abits][ceil(c/32)] uint32 (bs_pack of NHWC codes)
+ *   w_packed:   [oc][kh][kw][wbits][ceil(c/32)] uint32 (bs_pack of OHWI codes)
+ *   out:        [n][oh][ow][oc] int32, oh = (h + 2 pad_h - kh) / stride_h + 1,
+ *               ow likewise; every element is written.
+ *   out[n][y][x][o] = sum over in-range taps (r,s), planes i<abits, j<wbits of
+ *     2^(i+j) * sum_t f(a_i[t], w_j[t]),  f = popcount(a AND w) (unipolar) or
+ *     popcount(a AND w) - popcount(a AND NOT w) (bipolar weights),
+ *   which equals the integer convolution of the codes with weight values
+ *   sum_j 2^j w_j (unipolar) or sum_j 2^j (2 w_j - 1) (bipolar).
+ * Errors: BS_ERR_INVALID_ARG (NULL/misaligned pointers, non-positive sizes,
+ * bit-widths outside 1..8, stride < 1, pad < 0, oh or ow < 1);
+ * BS_ERR_UNSUPPORTED (bipolar activations, or sizes beyond the 2^31 pixel /
+ * 2^31 word-index range); BS_ERR_OVERFLOW when
+ * (2^abits - 1)(2^wbits - 1) kh kw c > 2^31 - 1. */
+typedef struct {
+    int32_t n, h, w, c;       /* NHWC activations */
+    int32_t oc, kh, kw;       /* OHWI filters: oc filters of kh x kw x c */
+    int32_t stride_h, stride_w;
+    int32_t pad_h, pad_w;
+    int32_t abits, wbits;     /* 1..8 */
+    int32_t aenc, wenc;       /* bs_encoding; aenc must be BS_UNIPOLAR */
+} bs_conv2d_params;
+
+/* Output height/width of a conv; BS_ERR_INVALID_ARG if either would be < 1. */
+bs_status bs_conv2d_out_shape(const bs_conv2d_params *p, int32_t *oh,
+                              int32_t *ow);
+
+bs_status bs_conv2d(const bs_conv2d_params *p, const uint32_t *act_packed,
+                    const uint32_t *w_packed, int32_t *out,
+                    bs_stream_t stream);
+
+/* Bitserial dense / matrix multiply (Sec. 3.2; evaluated in Sec. 6.2.1):
+ *   a_packed: [m][abits][ceil(k/32)], w_packed: [n][wbits][ceil(k/32)] uint32
+ *   (each output neuron's weights contiguous along the reduction axis),
+ *   out: [m][n] int32, out[r][o] = sum_{i,j} 2^(i+j) sum_t f(a_i[t], w_j[t]).
+ * Errors: as bs_conv2d, with the overflow bound (2^abits-1)(2^wbits-1) k. */
+bs_status bs_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,
+                   bs_encoding wenc, const uint32_t *a_packed,
+                   const uint32_t *w_packed, int32_t *out, bs_stream_t stream);
+
+/* Static description of a status code. */
+const char *bs_status_string(bs_status s);
+
+/* Detail of the last non-OK status returned on the calling thread ("" if
+ * none).  The string stays valid until the next call on that thread. */
+const char *bs_last_error(void);
+
+/* Selects which conv/dense kernels serve later calls made on the calling
+ * host thread:
+ * 0 = tuned fast kernels where they apply (default), 1 = the plain generic
+ * kernel for every shape.  Both give identical results; the switch exists so
+ * tests can check the two against each other. */
+bs_status bs_set_kernel_mode(int mode);
+
+/* ABI version of this header (major * 100 + minor). */
+int bs_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BITSERIAL_H */

@@ -1,0 +1,262 @@
+"""Python binding of libbitserial.so (include/bitserial.h).
+
+The ``bs_*`` functions carry the C entry points' names and semantics and only
+marshal arguments: torch tensors supply device pointers, shapes are checked,
+and the current HIP stream is passed through.  Every operation runs in the
+library's HIP kernels; there is no host fallback -- if the library is missing
+or the device is not a GPU, the call raises.
+
+Packed bit-plane tensors are torch.int32 tensors holding the uint32 words'
+bit patterns, shaped [rows, bits, ceil(k/32)] (activations: [n, h, w, bits,
+words]; conv filters: [oc, kh, kw, bits, words]).
+
+Convenience wrappers (``quantize``, ``pack``, ``quantize_pack``, ``conv2d``,
+``dense``) allocate the output with torch and call the entry point.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbitserial.so")
+
+BS_OK = 0
+BS_ERR_INVALID_ARG = 1
+BS_ERR_UNSUPPORTED = 2
+BS_ERR_OVERFLOW = 3
+BS_ERR_HIP = 4
+
+UNIPOLAR = 0
+BIPOLAR = 1
+
+EXPORTED = ("bs_packed_words", "bs_quantize", "bs_pack", "bs_quantize_pack",
+            "bs_conv2d_out_shape", "bs_conv2d", "bs_dense", "bs_status_string",
+            "bs_last_error", "bs_set_kernel_mode", "bs_abi_version")
+
+
+class BitserialError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__("bitserial status %d: %s" % (status, msg))
+        self.status = status
+
+
+class ConvParams(ctypes.Structure):
+    """Mirror of ``bs_conv2d_params``."""
+    _fields_ = [(name, ctypes.c_int32) for name in (
+        "n", "h", "w", "c", "oc", "kh", "kw", "stride_h", "stride_w",
+        "pad_h", "pad_w", "abits", "wbits", "aenc", "wenc")]
+
+
+_lock = threading.Lock()
+_lib = None
+
+
+def load_library():
+    """Load libbitserial.so (built in-tree by paper_1810_11066_amd.build)."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                "libbitserial.so is not built (%s); run "
+                "`python -m paper_1810_11066_amd.build`" % LIB_PATH)
+        lib = ctypes.CDLL(LIB_PATH)
+        P = ctypes.c_void_p
+        i64, ci, cf = ctypes.c_int64, ctypes.c_int, ctypes.c_float
+        sig = {
+            "bs_packed_words": (i64, [i64]),
+            "bs_quantize": (ci, [P, P, i64, cf, ci, ci, P]),
+            "bs_pack": (ci, [P, P, i64, i64, ci, P]),
+            "bs_quantize_pack": (ci, [P, P, i64, i64, cf, ci, ci, P]),
+            "bs_conv2d_out_shape": (ci, [ctypes.POINTER(ConvParams),
+                                         ctypes.POINTER(ctypes.c_int32),
+                                         ctypes.POINTER(ctypes.c_int32)]),
+            "bs_conv2d": (ci, [ctypes.POINTER(ConvParams), P, P, P, P]),
+            "bs_dense": (ci, [i64, i64, i64, ci, ci, ci, P, P, P, P]),
+            "bs_status_string": (ctypes.c_char_p, [ci]),
+            "bs_last_error": (ctypes.c_char_p, []),
+            "bs_set_kernel_mode": (ci, [ci]),
+            "bs_abi_version": (ci, []),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+        return lib
+
+
+def _check(status: int):
+    if status != BS_OK:
+        lib = load_library()
+        raise BitserialError(status, lib.bs_last_error().decode())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtype: torch.dtype, numel: int):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.device.type != "cuda":
+        raise ValueError("%s must be a GPU tensor (got %s)" % (name, t.device))
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s (got %s)" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if t.numel() != numel:
+        raise ValueError("%s has %d elements, expected %d" % (name, t.numel(),
+                                                             numel))
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def words(k: int) -> int:
+    return (k + 31) // 32
+
+
+# ---- entry points (same names as the C ABI) --------------------------------
+
+def bs_quantize(x: torch.Tensor, q: torch.Tensor, scale: float, bits: int,
+                enc: int = UNIPOLAR, stream=None) -> None:
+    n = x.numel()
+    _check(load_library().bs_quantize(
+        _dev(x, "x", torch.float32, n), _dev(q, "q", torch.uint8, n), n,
+        float(scale), int(bits), int(enc), _stream(stream)))
+
+
+def bs_pack(q: torch.Tensor, packed: torch.Tensor, rows: int, k: int,
+            bits: int, stream=None) -> None:
+    _check(load_library().bs_pack(
+        _dev(q, "q", torch.uint8, rows * k),
+        _dev(packed, "packed", torch.int32, rows * bits * words(k)),
+        rows, k, int(bits), _stream(stream)))
+
+
+def bs_quantize_pack(x: torch.Tensor, packed: torch.Tensor, rows: int, k: int,
+                     scale: float, bits: int, enc: int = UNIPOLAR,
+                     stream=None) -> None:
+    _check(load_library().bs_quantize_pack(
+        _dev(x, "x", torch.float32, rows * k),
+        _dev(packed, "packed", torch.int32, rows * bits * words(k)),
+        rows, k, float(scale), int(bits), int(enc), _stream(stream)))
+
+
+def bs_conv2d_out_shape(p: ConvParams):
+    oh, ow = ctypes.c_int32(), ctypes.c_int32()
+    _check(load_library().bs_conv2d_out_shape(ctypes.byref(p),
+                                              ctypes.byref(oh),
+                                              ctypes.byref(ow)))
+    return oh.value, ow.value
+
+
+def bs_conv2d(p: ConvParams, act_packed: torch.Tensor, w_packed: torch.Tensor,
+              out: torch.Tensor, stream=None) -> None:
+    lib = load_library()
+    oh, ow = bs_conv2d_out_shape(p)
+    cw = words(p.c)
+    _check(lib.bs_conv2d(
+        ctypes.byref(p),
+        _dev(act_packed, "act_packed", torch.int32,
+             p.n * p.h * p.w * p.abits * cw),
+        _dev(w_packed, "w_packed", torch.int32,
+             p.oc * p.kh * p.kw * p.wbits * cw),
+        _dev(out, "out", torch.int32, p.n * oh * ow * p.oc),
+        _stream(stream)))
+
+
+def bs_dense(m: int, n: int, k: int, abits: int, wbits: int, wenc: int,
+             a_packed: torch.Tensor, w_packed: torch.Tensor,
+             out: torch.Tensor, stream=None) -> None:
+    _check(load_library().bs_dense(
+        m, n, k, int(abits), int(wbits), int(wenc),
+        _dev(a_packed, "a_packed", torch.int32, m * abits * words(k)),
+        _dev(w_packed, "w_packed", torch.int32, n * wbits * words(k)),
+        _dev(out, "out", torch.int32, m * n), _stream(stream)))
+
+
+def bs_set_kernel_mode(mode: int) -> None:
+    _check(load_library().bs_set_kernel_mode(int(mode)))
+
+
+def bs_packed_words(k: int) -> int:
+    return load_library().bs_packed_words(k)
+
+
+def bs_abi_version() -> int:
+    return load_library().bs_abi_version()
+
+
+# ---- allocating conveniences -----------------------------------------------
+
+@dataclass
+class Conv2dSpec:
+    n: int
+    h: int
+    w: int
+    c: int
+    oc: int
+    kh: int
+    kw: int
+    stride: int = 1
+    pad: int = 0
+    abits: int = 1
+    wbits: int = 1
+    wenc: int = UNIPOLAR
+
+    def params(self) -> ConvParams:
+        return ConvParams(self.n, self.h, self.w, self.c, self.oc, self.kh,
+                          self.kw, self.stride, self.stride, self.pad,
+                          self.pad, self.abits, self.wbits, UNIPOLAR,
+                          self.wenc)
+
+
+def quantize(x: torch.Tensor, scale: float, bits: int, enc: int = UNIPOLAR):
+    q = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    bs_quantize(x, q, scale, bits, enc)
+    return q
+
+
+def pack(q: torch.Tensor, bits: int) -> torch.Tensor:
+    """q: [..., k] uint8 -> [..., bits, ceil(k/32)] int32 words."""
+    k = q.shape[-1]
+    rows = q.numel() // k
+    out = torch.empty(tuple(q.shape[:-1]) + (bits, words(k)),
+                      dtype=torch.int32, device=q.device)
+    bs_pack(q, out, rows, k, bits)
+    return out
+
+
+def quantize_pack(x: torch.Tensor, scale: float, bits: int,
+                  enc: int = UNIPOLAR) -> torch.Tensor:
+    k = x.shape[-1]
+    rows = x.numel() // k
+    out = torch.empty(tuple(x.shape[:-1]) + (bits, words(k)),
+                      dtype=torch.int32, device=x.device)
+    bs_quantize_pack(x, out, rows, k, scale, bits, enc)
+    return out
+
+
+def conv2d(spec: Conv2dSpec, act_packed: torch.Tensor,
+           w_packed: torch.Tensor) -> torch.Tensor:
+    p = spec.params()
+    oh, ow = bs_conv2d_out_shape(p)
+    out = torch.empty((spec.n, oh, ow, spec.oc), dtype=torch.int32,
+                      device=act_packed.device)
+    bs_conv2d(p, act_packed, w_packed, out)
+    return out
+
+
+def dense(a_packed: torch.Tensor, w_packed: torch.Tensor, m: int, n: int,
+          k: int, abits: int, wbits: int, wenc: int = UNIPOLAR):
+    out = torch.empty((m, n), dtype=torch.int32, device=a_packed.device)
+    bs_dense(m, n, k, abits, wbits, wenc, a_packed, w_packed, out)
+    return out

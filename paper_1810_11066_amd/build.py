@@ -1,0 +1,68 @@
+"""Build libbitserial.so in-tree with hipcc for gfx950.
+
+    python -m paper_1810_11066_amd.build
+
+Every HIP source under csrc/ is compiled to an object in parallel, then linked
+into paper_1810_11066_amd/libbitserial.so.  Flags:
+  --offload-arch=gfx950          MI355X only
+  -ffp-contract=off              the quantizer's product must stay a lone
+                                 binary32 multiply (no FMA contraction)
+  -target-feature -packed-fp32-ops
+                                 keep the compiler from emitting packed FP32
+                                 instructions
+"""
+from __future__ import annotations
+
+import concurrent.futures as cf
+import os
+import subprocess
+import sys
+import tempfile
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIB = os.path.join(HERE, "libbitserial.so")
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+
+SOURCES = ["api.hip", "quant_pack.hip", "conv.hip", "conv_fast_a1.hip",
+           "conv_fast_a2.hip", "conv_fast_a3.hip", "conv_fast_a4.hip"]
+
+CFLAGS = [
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
+    "-ffp-contract=off", "-Wall",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-I", INCLUDE, "-I", CSRC,
+]
+
+
+def _compile(src: str, obj: str) -> None:
+    cmd = [HIPCC] + CFLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc failed on %s:\n%s%s" % (src, r.stdout,
+                                                          r.stderr))
+
+
+def build(verbose: bool = False) -> str:
+    """Compile and link the library; returns its path."""
+    with tempfile.TemporaryDirectory(prefix="bs_build_") as tmp:
+        objs = [os.path.join(tmp, s.replace(".hip", ".o")) for s in SOURCES]
+        with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
+            list(ex.map(_compile, SOURCES, objs))
+        out_tmp = LIB + ".tmp%d" % os.getpid()
+        cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC"] + objs + \
+              ["-o", out_tmp]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError("link failed:\n%s%s" % (r.stdout, r.stderr))
+        os.replace(out_tmp, LIB)
+    if verbose:
+        print("built", LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    build(verbose=True)
+    sys.exit(0)

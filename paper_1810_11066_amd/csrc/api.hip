@@ -1,0 +1,248 @@
+// extern "C" entry points of libbitserial.so (declared in include/bitserial.h):
+// argument validation, the int32 overflow guard, and dispatch to the kernels.
+// Every check runs on the host before anything is enqueued, so an invalid
+// call never touches device memory.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "bitserial.h"
+#include "bs_internal.h"
+
+namespace {
+
+thread_local char g_err[512];
+thread_local int g_kernel_mode = 0;
+
+bs_status fail(bs_status st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+bs_status ok() {
+    g_err[0] = '\0';
+    return BS_OK;
+}
+
+bs_status from_hip(hipError_t e, const char* what) {
+    if (e == hipSuccess) return ok();
+    return fail(BS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+bs_status check_ptr(const void* p, const char* name) {
+    if (!p) return fail(BS_ERR_INVALID_ARG, "%s is NULL", name);
+    if (!aligned16(p))
+        return fail(BS_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+    return BS_OK;
+}
+
+bs_status check_bits(int bits, const char* name) {
+    if (bits < 1 || bits > 8)
+        return fail(BS_ERR_INVALID_ARG, "%s = %d is outside 1..8", name, bits);
+    return BS_OK;
+}
+
+bs_status check_scale_enc(float scale, int bits, bs_encoding enc) {
+    if (!isfinite(scale) || !(scale > 0.0f))
+        return fail(BS_ERR_INVALID_ARG, "scale must be finite and > 0");
+    if (enc != BS_UNIPOLAR && enc != BS_BIPOLAR)
+        return fail(BS_ERR_INVALID_ARG, "unknown encoding %d", (int)enc);
+    if (enc == BS_BIPOLAR && bits != 1)
+        return fail(BS_ERR_INVALID_ARG,
+                    "bipolar quantization is 1-bit (bits = %d)", bits);
+    return BS_OK;
+}
+
+// (2^a - 1)(2^w - 1) * taps * c must fit int32 for the exact result to.
+bs_status check_overflow(int abits, int wbits, int64_t taps, int64_t c) {
+    unsigned __int128 bound = (unsigned __int128)((1u << abits) - 1) *
+                              ((1u << wbits) - 1) * (uint64_t)taps *
+                              (uint64_t)c;
+    if (bound > (unsigned __int128)INT32_MAX)
+        return fail(BS_ERR_OVERFLOW,
+                    "(2^%d-1)(2^%d-1)*%lld*%lld exceeds int32", abits, wbits,
+                    (long long)taps, (long long)c);
+    return BS_OK;
+}
+
+// Shape checks shared by bs_conv2d and bs_dense; fills the kernel geometry.
+bs_status check_conv(const bs_conv2d_params* p, bs::ConvShape* s) {
+    if (!p) return fail(BS_ERR_INVALID_ARG, "params is NULL");
+    if (p->n < 1 || p->h < 1 || p->w < 1 || p->c < 1 || p->oc < 1 ||
+        p->kh < 1 || p->kw < 1)
+        return fail(BS_ERR_INVALID_ARG, "sizes must be >= 1");
+    if (p->stride_h < 1 || p->stride_w < 1)
+        return fail(BS_ERR_INVALID_ARG, "stride must be >= 1");
+    if (p->pad_h < 0 || p->pad_w < 0)
+        return fail(BS_ERR_INVALID_ARG, "padding must be >= 0");
+    bs_status st;
+    if ((st = check_bits(p->abits, "abits")) != BS_OK) return st;
+    if ((st = check_bits(p->wbits, "wbits")) != BS_OK) return st;
+    if (p->aenc != BS_UNIPOLAR && p->aenc != BS_BIPOLAR)
+        return fail(BS_ERR_INVALID_ARG, "unknown activation encoding");
+    if (p->wenc != BS_UNIPOLAR && p->wenc != BS_BIPOLAR)
+        return fail(BS_ERR_INVALID_ARG, "unknown weight encoding");
+    const int64_t eh = (int64_t)p->h + 2 * (int64_t)p->pad_h - p->kh;
+    const int64_t ew = (int64_t)p->w + 2 * (int64_t)p->pad_w - p->kw;
+    if (eh < 0 || ew < 0)
+        return fail(BS_ERR_INVALID_ARG, "kernel larger than padded input");
+    if (p->aenc != BS_UNIPOLAR)
+        return fail(BS_ERR_UNSUPPORTED, "bipolar activations are not supported");
+    if ((st = check_overflow(p->abits, p->wbits, (int64_t)p->kh * p->kw,
+                             p->c)) != BS_OK)
+        return st;
+    const int64_t oh = eh / p->stride_h + 1, ow = ew / p->stride_w + 1;
+    const int64_t pixels = (int64_t)p->n * oh * ow;
+    const int64_t cw = ((int64_t)p->c + 31) / 32;
+    if (pixels * p->oc > INT32_MAX)
+        return fail(BS_ERR_UNSUPPORTED, "output has more than 2^31-1 elements");
+    if ((int64_t)p->n * p->h * p->w * p->abits * cw > ((int64_t)1 << 40) ||
+        (int64_t)p->oc * p->kh * p->kw * p->wbits * cw > INT32_MAX)
+        return fail(BS_ERR_UNSUPPORTED, "packed operand too large");
+    s->n = p->n; s->h = p->h; s->w = p->w; s->c = p->c; s->oc = p->oc;
+    s->kh = p->kh; s->kw = p->kw; s->sh = p->stride_h; s->sw = p->stride_w;
+    s->ph = p->pad_h; s->pw = p->pad_w;
+    s->oh = (int32_t)oh; s->ow = (int32_t)ow;
+    s->abits = p->abits; s->wbits = p->wbits;
+    s->bipolar_w = p->wenc == BS_BIPOLAR;
+    return BS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int bs_abi_version(void) { return 100; }
+
+int64_t bs_packed_words(int64_t k) { return k <= 0 ? 0 : (k + 31) / 32; }
+
+const char* bs_status_string(bs_status s) {
+    switch (s) {
+        case BS_OK: return "ok";
+        case BS_ERR_INVALID_ARG: return "invalid argument";
+        case BS_ERR_UNSUPPORTED: return "unsupported";
+        case BS_ERR_OVERFLOW: return "int32 overflow possible";
+        case BS_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+const char* bs_last_error(void) { return g_err; }
+
+bs_status bs_set_kernel_mode(int mode) {
+    if (mode != 0 && mode != 1)
+        return fail(BS_ERR_INVALID_ARG, "kernel mode must be 0 or 1");
+    g_kernel_mode = mode;
+    return ok();
+}
+
+bs_status bs_quantize(const float* x, uint8_t* q, int64_t n, float scale,
+                      int bits, bs_encoding enc, bs_stream_t stream) {
+    bs_status st;
+    if ((st = check_ptr(x, "x")) != BS_OK) return st;
+    if ((st = check_ptr(q, "q")) != BS_OK) return st;
+    if (n < 0) return fail(BS_ERR_INVALID_ARG, "n < 0");
+    if ((st = check_bits(bits, "bits")) != BS_OK) return st;
+    if ((st = check_scale_enc(scale, bits, enc)) != BS_OK) return st;
+    if (n == 0) return ok();
+    return from_hip(bs::launch_quantize(x, q, n, scale, bits,
+                                        enc == BS_BIPOLAR,
+                                        (hipStream_t)stream),
+                    "bs_quantize launch");
+}
+
+bs_status bs_pack(const uint8_t* q, uint32_t* packed, int64_t rows, int64_t k,
+                  int bits, bs_stream_t stream) {
+    bs_status st;
+    if ((st = check_ptr(q, "q")) != BS_OK) return st;
+    if ((st = check_ptr(packed, "packed")) != BS_OK) return st;
+    if (rows < 0) return fail(BS_ERR_INVALID_ARG, "rows < 0");
+    if (k < 1) return fail(BS_ERR_INVALID_ARG, "k < 1");
+    if ((st = check_bits(bits, "bits")) != BS_OK) return st;
+    if (rows > ((int64_t)1 << 40) / k)
+        return fail(BS_ERR_UNSUPPORTED, "tensor too large");
+    if (rows == 0) return ok();
+    return from_hip(bs::launch_pack(q, packed, rows, k, bits,
+                                    (hipStream_t)stream),
+                    "bs_pack launch");
+}
+
+bs_status bs_quantize_pack(const float* x, uint32_t* packed, int64_t rows,
+                           int64_t k, float scale, int bits, bs_encoding enc,
+                           bs_stream_t stream) {
+    bs_status st;
+    if ((st = check_ptr(x, "x")) != BS_OK) return st;
+    if ((st = check_ptr(packed, "packed")) != BS_OK) return st;
+    if (rows < 0) return fail(BS_ERR_INVALID_ARG, "rows < 0");
+    if (k < 1) return fail(BS_ERR_INVALID_ARG, "k < 1");
+    if ((st = check_bits(bits, "bits")) != BS_OK) return st;
+    if ((st = check_scale_enc(scale, bits, enc)) != BS_OK) return st;
+    if (rows > ((int64_t)1 << 40) / k)
+        return fail(BS_ERR_UNSUPPORTED, "tensor too large");
+    if (rows == 0) return ok();
+    return from_hip(bs::launch_quantize_pack(x, packed, rows, k, scale, bits,
+                                             enc == BS_BIPOLAR,
+                                             (hipStream_t)stream),
+                    "bs_quantize_pack launch");
+}
+
+bs_status bs_conv2d_out_shape(const bs_conv2d_params* p, int32_t* oh,
+                              int32_t* ow) {
+    if (!p || !oh || !ow) return fail(BS_ERR_INVALID_ARG, "NULL argument");
+    if (p->kh < 1 || p->kw < 1 || p->stride_h < 1 || p->stride_w < 1 ||
+        p->pad_h < 0 || p->pad_w < 0 || p->h < 1 || p->w < 1)
+        return fail(BS_ERR_INVALID_ARG, "invalid geometry");
+    const int64_t eh = (int64_t)p->h + 2 * (int64_t)p->pad_h - p->kh;
+    const int64_t ew = (int64_t)p->w + 2 * (int64_t)p->pad_w - p->kw;
+    if (eh < 0 || ew < 0)
+        return fail(BS_ERR_INVALID_ARG, "kernel larger than padded input");
+    *oh = (int32_t)(eh / p->stride_h + 1);
+    *ow = (int32_t)(ew / p->stride_w + 1);
+    return ok();
+}
+
+bs_status bs_conv2d(const bs_conv2d_params* p, const uint32_t* act_packed,
+                    const uint32_t* w_packed, int32_t* out,
+                    bs_stream_t stream) {
+    bs_status st;
+    if ((st = check_ptr(act_packed, "act_packed")) != BS_OK) return st;
+    if ((st = check_ptr(w_packed, "w_packed")) != BS_OK) return st;
+    if ((st = check_ptr(out, "out")) != BS_OK) return st;
+    bs::ConvShape s;
+    if ((st = check_conv(p, &s)) != BS_OK) return st;
+    return from_hip(bs::launch_conv(s, act_packed, w_packed, out,
+                                    g_kernel_mode, (hipStream_t)stream),
+                    "bs_conv2d launch");
+}
+
+bs_status bs_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,
+                   bs_encoding wenc, const uint32_t* a_packed,
+                   const uint32_t* w_packed, int32_t* out, bs_stream_t stream) {
+    bs_status st;
+    if ((st = check_ptr(a_packed, "a_packed")) != BS_OK) return st;
+    if ((st = check_ptr(w_packed, "w_packed")) != BS_OK) return st;
+    if ((st = check_ptr(out, "out")) != BS_OK) return st;
+    if (m < 1 || n < 1 || k < 1)
+        return fail(BS_ERR_INVALID_ARG, "m, n, k must be >= 1");
+    if (m > INT32_MAX || n > INT32_MAX || k > INT32_MAX)
+        return fail(BS_ERR_UNSUPPORTED, "dimension beyond int32");
+    // dense == 1x1 convolution over an m-pixel image
+    bs_conv2d_params p;
+    p.n = 1; p.h = 1; p.w = (int32_t)m; p.c = (int32_t)k; p.oc = (int32_t)n;
+    p.kh = 1; p.kw = 1; p.stride_h = 1; p.stride_w = 1; p.pad_h = 0;
+    p.pad_w = 0; p.abits = abits; p.wbits = wbits; p.aenc = BS_UNIPOLAR;
+    p.wenc = wenc;
+    bs::ConvShape s;
+    if ((st = check_conv(&p, &s)) != BS_OK) return st;
+    return from_hip(bs::launch_conv(s, a_packed, w_packed, out, g_kernel_mode,
+                                    (hipStream_t)stream),
+                    "bs_dense launch");
+}
+
+}  // extern "C"

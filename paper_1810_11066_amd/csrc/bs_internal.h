@@ -1,0 +1,59 @@
+// Internal declarations shared by the HIP sources of libbitserial.so.
+// Not installed; the public interface is include/bitserial.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bs {
+
+// Division of a non-negative int32 by a fixed positive divisor with one
+// 64-bit multiply and a shift: q = (n * m) >> s, m = ceil(2^s / d),
+// s = 32 + ceil(log2 d).  Exact for every n < 2^31 (the rounding error
+// n (m d - 2^s) / (d 2^s) stays below 1/d because m d - 2^s < d <= 2^(s-32)).
+struct FastDiv {
+    uint64_t m;
+    uint32_t s;
+    uint32_t d;
+
+    __host__ void init(uint32_t divisor) {
+        d = divisor;
+        uint32_t sh = 0;
+        while ((1ull << sh) < divisor) ++sh;
+        s = 32 + sh;
+        m = ((1ull << s) + divisor - 1) / divisor;
+    }
+    __host__ __device__ __forceinline__ uint32_t div(uint32_t n) const {
+        return (uint32_t)(((uint64_t)n * m) >> s);
+    }
+};
+
+// ---- launchers (each returns hipSuccess or the launch error) -------------
+
+hipError_t launch_quantize(const float* x, uint8_t* q, int64_t n, float scale,
+                           int bits, bool bipolar, hipStream_t st);
+
+hipError_t launch_pack(const uint8_t* q, uint32_t* packed, int64_t rows,
+                       int64_t k, int bits, hipStream_t st);
+
+hipError_t launch_quantize_pack(const float* x, uint32_t* packed,
+                                int64_t rows, int64_t k, float scale, int bits,
+                                bool bipolar, hipStream_t st);
+
+// Geometry of a convolution as the kernels see it; dense is the 1x1 case
+// with n = 1, h = 1, w = m.
+struct ConvShape {
+    int32_t n, h, w, c, oc, kh, kw, sh, sw, ph, pw, oh, ow;
+    int32_t abits, wbits;
+    bool bipolar_w;
+};
+
+// mode 0: fast kernels where a specialisation exists; 1: generic only.
+hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
+                       const uint32_t* wts, int32_t* out, int mode,
+                       hipStream_t st);
+
+// True when launch_conv with mode 0 would use a specialised kernel.
+bool conv_has_fast_path(const ConvShape& s);
+
+}  // namespace bs

@@ -1,0 +1,173 @@
+// Bitserial conv2d / dense kernels for gfx950 (wave64).
+//
+// Both kernels evaluate, for every output, Eq. 2 over packed bit-planes:
+//   out = sum_{i<A} sum_{j<W} 2^(i+j) sum_t f(a_i[t], w_j[t])
+// with f = popcount(a AND w) for unipolar weights and
+// f = popcount(a AND w) - popcount(a AND NOT w) for bipolar weights (Sec. 2.2).
+// Accumulation is in uint32 and wraps; the host rejects any problem whose
+// exact result could leave int32, so the wrapped sum equals the exact result.
+//
+// conv_generic_kernel  one output per thread, runtime everything; serves
+//                      every shape the fast kernel does not.
+// conv_ocl_kernel      "output channels on lanes": lane l of a wave owns
+//                      output channel oc0 + l, the wave walks groups of P
+//                      output pixels of one output row.  The activation words
+//                      of a pixel are the same for every lane, so they are
+//                      read with scalar loads into SGPRs; the filter words of
+//                      the block's 64 channels are staged once in LDS, laid
+//                      out [tap][plane][word pair][lane] so that every lane
+//                      reads its own 8 bytes without bank conflicts.  The
+//                      inner loop is one v_and_b32 (SGPR x VGPR) and one
+//                      accumulating v_bcnt_u32_b32 per word pair, into
+//                      A+W-1 per-shift accumulators per output pixel; the
+//                      shift-add (and bipolar correction) runs once per
+//                      output.  Stores are 64 consecutive int32 per pixel.
+#include "conv_fast.h"
+
+namespace bs {
+namespace {
+
+using fast::kBlock;
+using fast::kWavesPerBlock;
+using fast::FastArgs;
+using fast::KernelFn;
+
+// ---------------------------------------------------------------------------
+struct GenericArgs {
+    const uint32_t* act;
+    const uint32_t* wts;
+    int32_t* out;
+    ConvShape s;
+    int32_t cw;
+    uint32_t total;   // n*oh*ow*oc, < 2^31
+    FastDiv div_oc, div_ow, div_oh;
+};
+
+__global__ __launch_bounds__(kBlock) void conv_generic_kernel(GenericArgs g) {
+    const ConvShape& s = g.s;
+    const int cw = g.cw;
+    for (uint32_t f = blockIdx.x * kBlock + threadIdx.x; f < g.total;
+         f += gridDim.x * kBlock) {
+        const uint32_t pix = g.div_oc.div(f), o = f - pix * (uint32_t)s.oc;
+        const uint32_t rowi = g.div_ow.div(pix), ox = pix - rowi * (uint32_t)s.ow;
+        const uint32_t img = g.div_oh.div(rowi), oy = rowi - img * (uint32_t)s.oh;
+        uint32_t sum = 0;
+        for (int r = 0; r < s.kh; ++r) {
+            const int iy = (int)oy * s.sh - s.ph + r;
+            if (iy < 0 || iy >= s.h) continue;          // zero padding
+            for (int c = 0; c < s.kw; ++c) {
+                const int ix = (int)ox * s.sw - s.pw + c;
+                if (ix < 0 || ix >= s.w) continue;      // zero padding
+                const uint32_t* ap =
+                    g.act + (((int64_t)img * s.h + iy) * s.w + ix) *
+                                (int64_t)s.abits * cw;
+                const uint32_t* wp =
+                    g.wts + (((int64_t)o * s.kh + r) * s.kw + c) *
+                                (int64_t)s.wbits * cw;
+                for (int t = 0; t < cw; ++t) {
+                    for (int i = 0; i < s.abits; ++i) {
+                        const uint32_t a = ap[i * cw + t];
+                        for (int j = 0; j < s.wbits; ++j) {
+                            const uint32_t w = wp[j * cw + t];
+                            uint32_t term = __builtin_popcount(a & w);
+                            if (s.bipolar_w) term -= __builtin_popcount(a & ~w);
+                            sum += term << (i + j);
+                        }
+                    }
+                }
+            }
+        }
+        g.out[f] = (int32_t)sum;
+    }
+}
+
+KernelFn pick_fast(int a, int w, bool b, int k, int s, int p) {
+    switch (a) {
+        case 1: return fast::pick_w<1>(w, b, k, s, p);
+        case 2: return fast::pick_w<2>(w, b, k, s, p);
+        case 3: return fast::pick_w<3>(w, b, k, s, p);
+        default: return fast::pick_w<4>(w, b, k, s, p);
+    }
+}
+
+constexpr int64_t kMaxLdsBytes = 64 * 1024;
+
+int64_t fast_lds_bytes(const ConvShape& s) {
+    const int64_t cw = (s.c + 31) / 32;
+    return 64 * (int64_t)s.kh * s.kw * s.wbits * cw * 4;
+}
+
+int pick_group_pixels(int ow) { return ow % 7 == 0 ? 7 : 8; }
+
+}  // namespace
+
+bool conv_has_fast_path(const ConvShape& s) {
+    const int64_t cw = (s.c + 31) / 32;
+    if (s.abits > 4 || s.wbits > 4) return false;
+    if (s.kh != s.kw || (s.kh != 1 && s.kh != 3)) return false;
+    if (s.sh != s.sw || (s.sh != 1 && s.sh != 2)) return false;
+    if (cw % 2 != 0) return false;
+    if (fast_lds_bytes(s) > kMaxLdsBytes) return false;
+    const int p = pick_group_pixels(s.ow);
+    const int64_t gpr = (s.ow + p - 1) / p;
+    const int64_t groups = (int64_t)s.n * s.oh * gpr;
+    if (groups >= INT32_MAX / 2) return false;
+    // scalar-load addressing uses 32-bit byte offsets into the activations
+    const int64_t act_bytes = (int64_t)s.n * s.h * s.w * s.abits * cw * 4;
+    if (act_bytes >= INT32_MAX) return false;
+    return true;
+}
+
+hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
+                       const uint32_t* wts, int32_t* out, int mode,
+                       hipStream_t st) {
+    const int32_t cw = (s.c + 31) / 32;
+    if (mode == 0 && conv_has_fast_path(s)) {
+        const int p = pick_group_pixels(s.ow);
+        FastArgs g;
+        g.h = s.h; g.w = s.w; g.cw = cw; g.oc = s.oc; g.oh = s.oh; g.ow = s.ow;
+        g.ph = s.ph; g.pw = s.pw;
+        g.plane_bytes = cw * 4;
+        g.pix_bytes = s.abits * cw * 4;
+        g.gpr = (s.ow + p - 1) / p;
+        g.total_groups = s.n * s.oh * g.gpr;
+        g.div_gpr.init((uint32_t)g.gpr);
+        g.div_oh.init((uint32_t)s.oh);
+        const int oc_blocks = (s.oc + 63) / 64;
+        // about 8 waves per SIMD across the chip (256 CUs x 4 SIMDs)
+        const int64_t target_waves = 256 * 4 * 8;
+        int64_t gpw = ((int64_t)g.total_groups * oc_blocks + target_waves - 1) /
+                      target_waves;
+        if (gpw < 1) gpw = 1;
+        if (gpw > 64) gpw = 64;
+        g.gpw = (int32_t)gpw;
+        const int64_t per_block = gpw * kWavesPerBlock;
+        const int64_t bx = (g.total_groups + per_block - 1) / per_block;
+        const KernelFn fn = pick_fast(s.abits, s.wbits, s.bipolar_w, s.kh,
+                                      s.sh, p);
+        const uint32_t* a_arg = act;
+        const uint32_t* w_arg = wts;
+        int32_t* o_arg = out;
+        void* args[] = {&a_arg, &w_arg, &o_arg, &g};
+        return hipLaunchKernel((const void*)fn, dim3((uint32_t)bx, oc_blocks),
+                               dim3(kBlock), args, (size_t)fast_lds_bytes(s),
+                               st);
+    }
+    GenericArgs g;
+    g.act = act;
+    g.wts = wts;
+    g.out = out;
+    g.s = s;
+    g.cw = cw;
+    g.total = (uint32_t)((int64_t)s.n * s.oh * s.ow * s.oc);
+    g.div_oc.init((uint32_t)s.oc);
+    g.div_ow.init((uint32_t)s.ow);
+    g.div_oh.init((uint32_t)s.oh);
+    int64_t blocks = ((int64_t)g.total + kBlock - 1) / kBlock;
+    if (blocks > 65535) blocks = 65535;
+    if (blocks < 1) blocks = 1;
+    conv_generic_kernel<<<(uint32_t)blocks, kBlock, 0, st>>>(g);
+    return hipGetLastError();
+}
+
+}  // namespace bs

@@ -1,0 +1,172 @@
+"""The C-ABI library loads and validates arguments on the host (no GPU).
+
+Every call below is built to fail validation, which happens before anything
+is enqueued, so none of them reaches the HIP runtime; the fake pointers are
+never dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1810_11066_amd import bitserial as bs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bitserial.h")
+
+FAKE = ctypes.c_void_p(0x10000)        # aligned, never dereferenced
+MISALIGNED = ctypes.c_void_p(0x10004)
+NULL = ctypes.c_void_p(0)
+STREAM = ctypes.c_void_p(0)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return bs.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bs_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert "bs_conv2d" in names and "bs_pack" in names
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(bs.EXPORTED)
+
+
+def test_abi_version_and_words(lib):
+    assert lib.bs_abi_version() == 100
+    for k, w in [(0, 0), (1, 1), (31, 1), (32, 1), (33, 2), (4096, 128)]:
+        assert lib.bs_packed_words(k) == w
+
+
+def test_status_strings(lib):
+    for s in range(5):
+        assert lib.bs_status_string(s)
+    assert lib.bs_status_string(99) == b"unknown status"
+
+
+def test_quantize_validation(lib):
+    q = lib.bs_quantize
+    assert q(NULL, FAKE, 8, 1.0, 2, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert b"x is NULL" in lib.bs_last_error()
+    assert q(FAKE, MISALIGNED, 8, 1.0, 2, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert b"aligned" in lib.bs_last_error()
+    assert q(FAKE, FAKE, -1, 1.0, 2, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+    for bits in (0, 9):
+        assert q(FAKE, FAKE, 8, 1.0, bits, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+    for scale in (0.0, -1.0, float("inf"), float("nan")):
+        assert q(FAKE, FAKE, 8, scale, 2, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert q(FAKE, FAKE, 8, 1.0, 2, 1, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert q(FAKE, FAKE, 8, 1.0, 1, 7, STREAM) == bs.BS_ERR_INVALID_ARG
+
+
+def test_empty_is_ok_without_launch(lib):
+    # n == 0 / rows == 0 enqueue nothing
+    assert lib.bs_quantize(FAKE, FAKE, 0, 1.0, 2, 0, STREAM) == bs.BS_OK
+    assert lib.bs_pack(FAKE, FAKE, 0, 64, 2, STREAM) == bs.BS_OK
+    assert lib.bs_quantize_pack(FAKE, FAKE, 0, 64, 1.0, 2, 0, STREAM) == bs.BS_OK
+    assert lib.bs_last_error() == b""
+
+
+def test_pack_validation(lib):
+    p = lib.bs_pack
+    assert p(NULL, FAKE, 4, 64, 2, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert p(FAKE, NULL, 4, 64, 2, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert p(FAKE, FAKE, -1, 64, 2, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert p(FAKE, FAKE, 4, 0, 2, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert p(FAKE, FAKE, 4, 64, 9, STREAM) == bs.BS_ERR_INVALID_ARG
+    qp = lib.bs_quantize_pack
+    assert qp(FAKE, FAKE, 4, 64, 1.0, 2, 1, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert qp(FAKE, FAKE, 4, 64, 0.0, 2, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+
+
+def params(**kw):
+    base = dict(n=1, h=8, w=8, c=64, oc=64, kh=3, kw=3, stride_h=1,
+                stride_w=1, pad_h=1, pad_w=1, abits=2, wbits=1, aenc=0,
+                wenc=0)
+    base.update(kw)
+    return bs.ConvParams(**base)
+
+
+@pytest.mark.parametrize("bad,status", [
+    (dict(n=0), bs.BS_ERR_INVALID_ARG),
+    (dict(c=0), bs.BS_ERR_INVALID_ARG),
+    (dict(oc=-3), bs.BS_ERR_INVALID_ARG),
+    (dict(kh=0), bs.BS_ERR_INVALID_ARG),
+    (dict(stride_w=0), bs.BS_ERR_INVALID_ARG),
+    (dict(pad_h=-1), bs.BS_ERR_INVALID_ARG),
+    (dict(abits=0), bs.BS_ERR_INVALID_ARG),
+    (dict(wbits=9), bs.BS_ERR_INVALID_ARG),
+    (dict(wenc=2), bs.BS_ERR_INVALID_ARG),
+    (dict(kh=11, pad_h=1), bs.BS_ERR_INVALID_ARG),     # oh < 1
+    (dict(aenc=1), bs.BS_ERR_UNSUPPORTED),             # bipolar activations
+    (dict(abits=8, wbits=8, c=(1 << 31) // (255 * 255 * 9) + 1),
+     bs.BS_ERR_OVERFLOW),
+])
+def test_conv_validation(lib, bad, status):
+    p = params(**bad)
+    assert lib.bs_conv2d(ctypes.byref(p), FAKE, FAKE, FAKE, STREAM) == status
+    assert lib.bs_last_error() != b""
+
+
+def test_conv_pointer_validation(lib):
+    p = params()
+    assert lib.bs_conv2d(ctypes.byref(p), NULL, FAKE, FAKE,
+                         STREAM) == bs.BS_ERR_INVALID_ARG
+    assert lib.bs_conv2d(ctypes.byref(p), FAKE, MISALIGNED, FAKE,
+                         STREAM) == bs.BS_ERR_INVALID_ARG
+    assert lib.bs_conv2d(None, FAKE, FAKE, FAKE,
+                         STREAM) == bs.BS_ERR_INVALID_ARG
+
+
+def test_overflow_guard_boundary(lib):
+    # (2^8-1)^2 * 9 * c <= 2^31-1  <=>  c <= 3669
+    limit = (2 ** 31 - 1) // (255 * 255 * 9)
+    p = params(abits=8, wbits=8, c=limit + 1)
+    assert lib.bs_conv2d(ctypes.byref(p), FAKE, FAKE, FAKE,
+                         STREAM) == bs.BS_ERR_OVERFLOW
+    # dense bound (2^a-1)(2^w-1) k
+    k = (2 ** 31 - 1) // (255 * 255) + 1
+    assert lib.bs_dense(4, 4, k, 8, 8, 0, FAKE, FAKE, FAKE,
+                        STREAM) == bs.BS_ERR_OVERFLOW
+
+
+def test_dense_validation(lib):
+    d = lib.bs_dense
+    assert d(0, 4, 64, 2, 2, 0, FAKE, FAKE, FAKE, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert d(4, 4, 64, 2, 2, 3, FAKE, FAKE, FAKE, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert d(4, 4, 64, 0, 2, 0, FAKE, FAKE, FAKE, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert d(4, 4, 64, 2, 2, 0, FAKE, NULL, FAKE, STREAM) == bs.BS_ERR_INVALID_ARG
+
+
+def test_out_shape(lib):
+    oh, ow = ctypes.c_int32(), ctypes.c_int32()
+    for (h, k, s, pd) in [(56, 3, 1, 1), (56, 3, 2, 1), (56, 1, 2, 0),
+                          (7, 3, 1, 1), (9, 5, 3, 2)]:
+        p = params(h=h, w=h + 1, kh=k, kw=k, stride_h=s, stride_w=s, pad_h=pd,
+                   pad_w=pd)
+        assert lib.bs_conv2d_out_shape(ctypes.byref(p), ctypes.byref(oh),
+                                       ctypes.byref(ow)) == bs.BS_OK
+        assert oh.value == (h + 2 * pd - k) // s + 1
+        assert ow.value == (h + 1 + 2 * pd - k) // s + 1
+
+
+def test_kernel_mode(lib):
+    assert lib.bs_set_kernel_mode(2) == bs.BS_ERR_INVALID_ARG
+    assert lib.bs_set_kernel_mode(1) == bs.BS_OK
+    assert lib.bs_set_kernel_mode(0) == bs.BS_OK
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros(16, dtype=torch.float32)
+    q = torch.zeros(16, dtype=torch.uint8)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        bs.bs_quantize(x, q, 1.0, 2)

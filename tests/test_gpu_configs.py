@@ -1,0 +1,146 @@
+"""GPU parity at the benchmark workloads' full sizes, through the same library
+calls and launch configuration the benchmark times.
+
+Small workloads are checked against the oracle element by element; for the
+batch-128 ResNet-18 layers the oracle evaluates a sample of outputs one by one
+(the first and last image completely, plus random positions), and the fast
+kernel is also checked against the generic kernel on the whole output.
+Packed activations and weights are compared with the oracle's in full.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_1810_11066_amd import bitserial as bs
+from paper_1810_11066_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU parity tests need the MI355X"
+    bs.load_library()
+    bs.bs_set_kernel_mode(0)
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def words_np(t):
+    return t.cpu().numpy().view(np.uint32)
+
+
+def prepare(oracle, case: wl.ConvCase):
+    """Host inputs, oracle-packed operands, and the GPU-packed operands."""
+    x = case.activations()
+    wsrc = case.weights()
+    if case.act_scale is not None:
+        a_codes = oracle.quantize(x, case.act_scale, case.abits)
+        a_dev = bs.quantize_pack(dev(x), case.act_scale, case.abits)
+    else:
+        a_codes = x
+        a_dev = bs.pack(dev(x), case.abits)
+    if case.weights_from_signs:
+        w_codes = oracle.quantize(wsrc, 1.0, 1, oracle.BIPOLAR)
+        w_dev = bs.pack(bs.quantize(dev(wsrc), 1.0, 1, bs.BIPOLAR), 1)
+    else:
+        w_codes = wsrc
+        w_dev = bs.pack(dev(wsrc), case.wbits)
+    ap = oracle.pack(a_codes, case.abits)
+    wp = oracle.pack(w_codes, case.wbits)
+    torch.cuda.synchronize()
+    assert np.array_equal(words_np(a_dev).reshape(ap.shape), ap)
+    assert np.array_equal(words_np(w_dev).reshape(wp.shape), wp)
+    return ap, wp, a_dev, w_dev
+
+
+def spec_of(case):
+    return bs.Conv2dSpec(case.n, case.h, case.w, case.c, case.oc, case.k,
+                         case.k, case.stride, case.pad, case.abits,
+                         case.wbits, case.wenc)
+
+
+def oracle_params(oracle, case):
+    return oracle.conv_params(case.n, case.h, case.w, case.c, case.oc,
+                              case.k, case.k, case.stride, case.pad,
+                              case.abits, case.wbits, wenc=case.wenc)
+
+
+def check_full(oracle, case):
+    ap, wp, a_dev, w_dev = prepare(oracle, case)
+    got = bs.conv2d(spec_of(case), a_dev, w_dev).cpu().numpy()
+    want = oracle.conv2d(oracle_params(oracle, case), ap, wp)
+    assert np.array_equal(got, want)
+
+
+def check_sampled(oracle, case, n_random=16384):
+    ap, wp, a_dev, w_dev = prepare(oracle, case)
+    spec = spec_of(case)
+    out = bs.conv2d(spec, a_dev, w_dev)
+    # the generic kernel on the whole output
+    bs.bs_set_kernel_mode(1)
+    try:
+        ref = bs.conv2d(spec, a_dev, w_dev)
+    finally:
+        bs.bs_set_kernel_mode(0)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
+    got = out.cpu().numpy().ravel()
+    per_image = case.oh * case.ow * case.oc
+    rng = np.random.default_rng(case.seed)
+    idx = np.concatenate([
+        np.arange(per_image),                                   # first image
+        np.arange(got.size - per_image, got.size),              # last image
+        rng.integers(0, got.size, n_random)])
+    want = oracle.conv2d_at(oracle_params(oracle, case), ap, wp, idx)
+    assert np.array_equal(got[idx], want)
+
+
+def test_config1_a1w1(oracle):
+    case = wl.config1()
+    say(case.name)
+    check_full(oracle, case)
+
+
+def test_config2_a2w1(oracle):
+    case = wl.config2()
+    say(case.name)
+    check_full(oracle, case)
+
+
+def test_config3_dense(oracle):
+    case = wl.config3()
+    say(case.name)
+    a, w = case.activations(), case.weights()
+    a_dev = bs.pack(dev(a), case.abits)
+    w_dev = bs.pack(dev(w), case.wbits)
+    ap, wp = oracle.pack(a, case.abits), oracle.pack(w, case.wbits)
+    got = bs.dense(a_dev, w_dev, case.m, case.n, case.k, case.abits,
+                   case.wbits).cpu().numpy()
+    assert np.array_equal(words_np(a_dev).reshape(ap.shape), ap)
+    assert np.array_equal(words_np(w_dev).reshape(wp.shape), wp)
+    rows = np.r_[0:16, case.m - 16:case.m]
+    want = oracle.dense(ap[rows], wp, rows.size, case.n, case.k, case.abits,
+                        case.wbits)
+    assert np.array_equal(got[rows], want)
+    # every row through an exact float64 product of the codes
+    ref = a.astype(np.float64) @ w.astype(np.float64).T
+    assert np.array_equal(got.astype(np.int64), ref.astype(np.int64))
+
+
+@pytest.mark.parametrize("case", wl.config4(), ids=lambda c: c.name)
+def test_config4_resnet18_layer(oracle, case):
+    say(case.name)
+    check_sampled(oracle, case)
+
+
+@pytest.mark.parametrize("case", wl.config5(), ids=lambda c: c.name)
+def test_config5_bipolar_a3w3(oracle, case):
+    say(case.name)
+    check_sampled(oracle, case)

@@ -1,0 +1,253 @@
+"""GPU parity: the HIP library against the CPU oracle, bit for bit.
+
+All calls go through the C ABI (the ctypes binding).  Outputs are written into
+buffers pre-filled with a sentinel and flanked by guard bands, so a test also
+fails if a kernel leaves an element unwritten or writes past its output.
+Results are exact integers; the bar is equality.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_1810_11066_amd import bitserial as bs
+from paper_1810_11066_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+SENT32 = 0x7FFFFFFF
+GUARD = 1024       # elements on each side (4 KiB for int32)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU parity tests need the MI355X"
+    bs.load_library()
+    bs.bs_set_kernel_mode(0)
+    yield
+    bs.bs_set_kernel_mode(0)
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+class Guarded:
+    """A device buffer of `numel` elements with sentinel-filled guard bands."""
+
+    def __init__(self, numel, dtype, sentinel):
+        self.numel, self.sent = numel, sentinel
+        self.buf = torch.full((numel + 2 * GUARD,), sentinel, dtype=dtype,
+                              device="cuda")
+        self.t = self.buf[GUARD:GUARD + numel]
+
+    def view(self, *shape):
+        return self.t.view(*shape)
+
+    def check_guards(self):
+        b = self.buf.cpu()
+        assert bool((b[:GUARD] == self.sent).all()), "write before output"
+        assert bool((b[GUARD + self.numel:] == self.sent).all()), \
+            "write past output"
+
+
+def dev(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def as_words(t: torch.Tensor) -> np.ndarray:
+    return t.cpu().numpy().view(np.uint32)
+
+
+# ---------------------------------------------------------------- quantize --
+
+def special_floats(rng, n):
+    parts = [rng.standard_normal(n).astype(np.float32) * 3,
+             (rng.integers(-20, 600, n) / 2).astype(np.float32),
+             rng.uniform(-1e-38, 1e-38, n).astype(np.float32),
+             np.array([np.nan, np.inf, -np.inf, -0.0, 0.0, 1e30, -1e30,
+                       0.5, 1.5, 2.5, 3.5], np.float32)]
+    return np.concatenate(parts)
+
+
+@pytest.mark.parametrize("n", [1, 15, 16, 17, 1000, 100003])
+@pytest.mark.parametrize("bits,scale,enc", [
+    (1, 1.0, 0), (2, 1.0, 0), (2, 1.5, 0), (3, 0.7, 0), (4, 3.0, 0),
+    (8, 1.3, 0), (2, 3e38, 0), (1, 1.0, 1)])
+def test_quantize(oracle, n, bits, scale, enc):
+    say("quantize n=%d bits=%d scale=%g enc=%d" % (n, bits, scale, enc))
+    rng = np.random.default_rng(n + bits)
+    x = rng.permutation(special_floats(rng, n))[:n]
+    want = oracle.quantize(x, scale, bits, enc)
+    g = Guarded(n, torch.uint8, 0xAB)
+    bs.bs_quantize(dev(x), g.t, scale, bits, enc)
+    torch.cuda.synchronize()
+    assert np.array_equal(g.t.cpu().numpy(), want)
+    g.check_guards()
+
+
+def test_quantize_golden(oracle):
+    import json
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden",
+                        "quantize_cases.json")
+    for c in json.load(open(path))["cases"]:
+        x = np.array([int(c["x"], 16)], np.uint32).view(np.float32)
+        s = np.array([int(c["scale"], 16)], np.uint32).view(np.float32)[0]
+        enc = 1 if c["enc"] == "bipolar" else 0
+        q = torch.empty(1, dtype=torch.uint8, device="cuda")
+        bs.bs_quantize(dev(x), q, float(s), c["bits"], enc)
+        assert int(q.item()) == c["q"], c
+
+
+# -------------------------------------------------------------------- pack --
+
+@pytest.mark.parametrize("k", [1, 5, 31, 32, 33, 64, 70, 96, 128, 257, 512,
+                               4096])
+@pytest.mark.parametrize("bits", [1, 2, 3, 8])
+@pytest.mark.parametrize("rows", [1, 3, 257])
+def test_pack(oracle, k, bits, rows):
+    say("pack rows=%d k=%d bits=%d" % (rows, k, bits))
+    rng = np.random.default_rng(k * 7 + bits + rows)
+    q = rng.integers(0, 256, size=(rows, k), dtype=np.uint8)  # high bits too
+    want = oracle.pack(q, bits)
+    g = Guarded(want.size, torch.int32, SENT32)
+    bs.bs_pack(dev(q), g.t, rows, k, bits)
+    torch.cuda.synchronize()
+    assert np.array_equal(as_words(g.t).reshape(want.shape), want)
+    g.check_guards()
+
+
+@pytest.mark.parametrize("k", [32, 64, 96, 100, 128, 256, 33, 4096])
+@pytest.mark.parametrize("rows", [1, 5, 130])
+@pytest.mark.parametrize("bits,enc", [(1, 0), (2, 0), (3, 0), (8, 0), (1, 1)])
+def test_quantize_pack(oracle, k, rows, bits, enc):
+    say("quantize_pack rows=%d k=%d bits=%d enc=%d" % (rows, k, bits, enc))
+    rng = np.random.default_rng(k + rows * 3 + bits)
+    x = rng.permutation(special_floats(rng, rows * k))[:rows * k]
+    x = x.reshape(rows, k)
+    want = oracle.pack(oracle.quantize(x, 1.7, bits, enc), bits)
+    g = Guarded(want.size, torch.int32, SENT32)
+    bs.bs_quantize_pack(dev(x), g.t, rows, k, 1.7, bits, enc)
+    torch.cuda.synchronize()
+    assert np.array_equal(as_words(g.t).reshape(want.shape), want)
+    g.check_guards()
+
+
+# -------------------------------------------------------------------- conv --
+
+def run_conv(oracle, n, h, w, c, oc, kh, kw, sh, sw, ph, pw, abits, wbits,
+             bipolar, seed, mode=0, check="full"):
+    rng = np.random.default_rng(seed)
+    a = rng.integers(0, 1 << abits, size=(n, h, w, c), dtype=np.uint8)
+    wq = rng.integers(0, 1 << wbits, size=(oc, kh, kw, c), dtype=np.uint8)
+    op = oracle.ConvParams(n, h, w, c, oc, kh, kw, sh, sw, ph, pw, abits,
+                           wbits, 0, int(bipolar))
+    ap, wp = oracle.pack(a, abits), oracle.pack(wq, wbits)
+    p = bs.ConvParams(n, h, w, c, oc, kh, kw, sh, sw, ph, pw, abits, wbits,
+                      0, int(bipolar))
+    oh, ow = bs.bs_conv2d_out_shape(p)
+    g = Guarded(n * oh * ow * oc, torch.int32, SENT32)
+    # the library's own pack feeds the conv, as on the benchmark path
+    a_dev = bs.pack(dev(a), abits)
+    w_dev = bs.pack(dev(wq), wbits)
+    bs.bs_set_kernel_mode(mode)
+    try:
+        bs.bs_conv2d(p, a_dev, w_dev, g.t)
+    finally:
+        bs.bs_set_kernel_mode(0)
+    torch.cuda.synchronize()
+    assert np.array_equal(as_words(a_dev).reshape(ap.shape), ap)
+    assert np.array_equal(as_words(w_dev).reshape(wp.shape), wp)
+    got = g.t.cpu().numpy().reshape(n, oh, ow, oc)
+    g.check_guards()
+    want = oracle.conv2d(op, ap, wp)
+    assert np.array_equal(got, want)
+    return got
+
+
+def random_conv(rng):
+    n = int(rng.integers(1, 3))
+    h, w = int(rng.integers(1, 12)), int(rng.integers(1, 12))
+    c = int(rng.integers(1, 140))
+    oc = int(rng.integers(1, 80))
+    kh, kw = int(rng.choice([1, 2, 3, 5])), int(rng.choice([1, 2, 3, 5]))
+    sh, sw = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+    ph, pw = int(rng.integers(0, 3)), int(rng.integers(0, 3))
+    if h + 2 * ph < kh:
+        ph = (kh - h + 1) // 2
+    if w + 2 * pw < kw:
+        pw = (kw - w + 1) // 2
+    abits, wbits = int(rng.integers(1, 9)), int(rng.integers(1, 9))
+    return (n, h, w, c, oc, kh, kw, sh, sw, ph, pw, abits, wbits,
+            bool(rng.integers(0, 2)))
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_conv_random_generic(oracle, seed):
+    args = random_conv(np.random.default_rng(900 + seed))
+    say("conv generic", args)
+    run_conv(oracle, *args, seed=seed, mode=1)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_conv_random_default(oracle, seed):
+    args = random_conv(np.random.default_rng(900 + seed))
+    say("conv default", args)
+    run_conv(oracle, *args, seed=seed, mode=0)
+
+
+# shapes that take the specialised kernel: K in {1,3}, S in {1,2}, even word
+# count, A, W <= 4; ragged oc, widths that are not multiples of the group
+# size, borders on every side, several images
+FAST_SHAPES = [
+    # n, h, w, c, oc, k, s, pad
+    (2, 9, 11, 64, 64, 3, 1, 1),
+    (1, 14, 14, 64, 100, 3, 1, 1),
+    (3, 7, 7, 128, 64, 3, 1, 1),
+    (2, 10, 13, 64, 70, 3, 2, 1),
+    (1, 8, 8, 192, 64, 1, 1, 0),
+    (2, 9, 9, 64, 65, 1, 2, 0),
+    (1, 5, 17, 256, 33, 3, 1, 0),
+    (1, 6, 6, 64, 128, 3, 2, 0),
+    (2, 16, 9, 64, 64, 3, 1, 2),
+]
+
+
+@pytest.mark.parametrize("shape", FAST_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("abits,wbits,bip", [
+    (1, 1, False), (1, 1, True), (2, 1, False), (2, 1, True), (2, 2, False),
+    (3, 3, False), (3, 3, True), (4, 4, False), (1, 4, False), (4, 1, True)])
+def test_conv_fast_shapes(oracle, shape, abits, wbits, bip):
+    n, h, w, c, oc, k, s, pad = shape
+    say("conv fast", shape, abits, wbits, bip)
+    run_conv(oracle, n, h, w, c, oc, k, k, s, s, pad, pad, abits, wbits, bip,
+             seed=hash((shape, abits, wbits, bip)) % 10000)
+
+
+def test_conv_deterministic(oracle):
+    args = (2, 14, 14, 64, 64, 3, 3, 1, 1, 1, 1, 2, 1, False)
+    a = run_conv(oracle, *args, seed=5)
+    b = run_conv(oracle, *args, seed=5)
+    assert np.array_equal(a, b)
+
+
+# ------------------------------------------------------------------- dense --
+
+@pytest.mark.parametrize("seed", range(16))
+def test_dense_random(oracle, seed):
+    rng = np.random.default_rng(300 + seed)
+    m, n = int(rng.integers(1, 300)), int(rng.integers(1, 200))
+    k = int(rng.choice([1, 31, 64, 100, 256, 1000, 2048]))
+    abits, wbits = int(rng.integers(1, 5)), int(rng.integers(1, 5))
+    bip = bool(rng.integers(0, 2))
+    say("dense", m, n, k, abits, wbits, bip)
+    a = rng.integers(0, 1 << abits, size=(m, k), dtype=np.uint8)
+    w = rng.integers(0, 1 << wbits, size=(n, k), dtype=np.uint8)
+    ap, wp = oracle.pack(a, abits), oracle.pack(w, wbits)
+    want = oracle.dense(ap, wp, m, n, k, abits, wbits, int(bip))
+    g = Guarded(m * n, torch.int32, SENT32)
+    bs.bs_dense(m, n, k, abits, wbits, int(bip), dev(ap.view(np.int32)),
+                dev(wp.view(np.int32)), g.t)
+    torch.cuda.synchronize()
+    assert np.array_equal(g.t.cpu().numpy().reshape(m, n), want)
+    g.check_guards()
