@@ -138,9 +138,14 @@ const char *bs_last_error(void);
 
 /* Selects which conv/dense kernels serve later calls made on the calling
  * host thread:
- * 0 = tuned fast kernels where they apply (default), 1 = the plain generic
- * kernel for every shape.  Both give identical results; the switch exists so
- * tests can check the two against each other. */
+ *   0 = the fastest kernel that applies to the shape (default),
+ *   1 = the plain generic kernel for every shape,
+ *   2 = the output-channels-on-lanes kernel where it applies,
+ *   3 = the pixels-on-lanes kernel where it applies
+ * (2 and 3 use the generic kernel for shapes they do not cover).  All give
+ * identical results; the switch exists so tests can check each kernel
+ * against the others and against the reference.
+ * Errors: BS_ERR_INVALID_ARG for a mode outside 0..3. */
 bs_status bs_set_kernel_mode(int mode);
 
 /* ABI version of this header (major * 100 + minor). */

@@ -23,7 +23,9 @@ from dataclasses import dataclass
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libbitserial.so")
+# BITSERIAL_LIBRARY selects another build of the same library
+LIB_PATH = os.environ.get("BITSERIAL_LIBRARY",
+                          os.path.join(_HERE, "libbitserial.so"))
 
 BS_OK = 0
 BS_ERR_INVALID_ARG = 1

@@ -27,7 +27,8 @@ LIB = os.path.join(HERE, "libbitserial.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["api.hip", "quant_pack.hip", "conv.hip", "conv_fast_a1.hip",
-           "conv_fast_a2.hip", "conv_fast_a3.hip", "conv_fast_a4.hip"]
+           "conv_fast_a2.hip", "conv_fast_a3.hip", "conv_fast_a4.hip",
+           "conv_pix.hip"]
 
 CFLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
@@ -37,30 +38,34 @@ CFLAGS = [
 ]
 
 
-def _compile(src: str, obj: str) -> None:
-    cmd = [HIPCC] + CFLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(src: str, obj: str, extra=()) -> None:
+    cmd = [HIPCC] + CFLAGS + list(extra) + ["-c", os.path.join(CSRC, src),
+                                            "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed on %s:\n%s%s" % (src, r.stdout,
                                                           r.stderr))
 
 
-def build(verbose: bool = False) -> str:
-    """Compile and link the library; returns its path."""
+def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
+    """Compile and link the library (to `out`, with extra -D `defines`);
+    returns its path."""
+    extra = ["-D" + d for d in defines]
     with tempfile.TemporaryDirectory(prefix="bs_build_") as tmp:
         objs = [os.path.join(tmp, s.replace(".hip", ".o")) for s in SOURCES]
         with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-            list(ex.map(_compile, SOURCES, objs))
-        out_tmp = LIB + ".tmp%d" % os.getpid()
+            list(ex.map(lambda a: _compile(a[0], a[1], extra),
+                        zip(SOURCES, objs)))
+        out_tmp = out + ".tmp%d" % os.getpid()
         cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC"] + objs + \
               ["-o", out_tmp]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError("link failed:\n%s%s" % (r.stdout, r.stderr))
-        os.replace(out_tmp, LIB)
+        os.replace(out_tmp, out)
     if verbose:
-        print("built", LIB)
-    return LIB
+        print("built", out)
+    return out
 
 
 if __name__ == "__main__":

@@ -136,8 +136,8 @@ const char* bs_status_string(bs_status s) {
 const char* bs_last_error(void) { return g_err; }
 
 bs_status bs_set_kernel_mode(int mode) {
-    if (mode != 0 && mode != 1)
-        return fail(BS_ERR_INVALID_ARG, "kernel mode must be 0 or 1");
+    if (mode < 0 || mode > 3)
+        return fail(BS_ERR_INVALID_ARG, "kernel mode must be 0..3");
     g_kernel_mode = mode;
     return ok();
 }

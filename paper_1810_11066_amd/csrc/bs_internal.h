@@ -48,7 +48,9 @@ struct ConvShape {
     bool bipolar_w;
 };
 
-// mode 0: fast kernels where a specialisation exists; 1: generic only.
+// mode 0: the fastest applicable kernel; 1: generic only; 2: the
+// channels-on-lanes kernel where it applies; 3: the pixels-on-lanes kernel
+// where it applies (2 and 3 fall back to the generic kernel).
 hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
                        const uint32_t* wts, int32_t* out, int mode,
                        hipStream_t st);

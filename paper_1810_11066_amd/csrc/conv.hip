@@ -23,6 +23,7 @@
 //                      shift-add (and bipolar correction) runs once per
 //                      output.  Stores are 64 consecutive int32 per pixel.
 #include "conv_fast.h"
+#include "conv_pix.h"
 
 namespace bs {
 namespace {
@@ -81,16 +82,20 @@ __global__ __launch_bounds__(kBlock) void conv_generic_kernel(GenericArgs g) {
     }
 }
 
-KernelFn pick_fast(int a, int w, bool b, int k, int s, int p) {
+KernelFn pick_fast(int a, int w, bool b, int k, int s, int p, int cw) {
     switch (a) {
-        case 1: return fast::pick_w<1>(w, b, k, s, p);
-        case 2: return fast::pick_w<2>(w, b, k, s, p);
-        case 3: return fast::pick_w<3>(w, b, k, s, p);
-        default: return fast::pick_w<4>(w, b, k, s, p);
+        case 1: return fast::pick_w<1>(w, b, k, s, p, cw);
+        case 2: return fast::pick_w<2>(w, b, k, s, p, cw);
+        case 3: return fast::pick_w<3>(w, b, k, s, p, cw);
+        default: return fast::pick_w<4>(w, b, k, s, p, cw);
     }
 }
 
 constexpr int64_t kMaxLdsBytes = 64 * 1024;
+
+#ifndef BS_CONV_WAVES_PER_SIMD
+#define BS_CONV_WAVES_PER_SIMD 4
+#endif
 
 int64_t fast_lds_bytes(const ConvShape& s) {
     const int64_t cw = (s.c + 31) / 32;
@@ -103,12 +108,15 @@ int pick_group_pixels(int ow) { return ow % 7 == 0 ? 7 : 8; }
 
 bool conv_has_fast_path(const ConvShape& s) {
     const int64_t cw = (s.c + 31) / 32;
+    const int p = pick_group_pixels(s.ow);
     if (s.abits > 4 || s.wbits > 4) return false;
     if (s.kh != s.kw || (s.kh != 1 && s.kh != 3)) return false;
     if (s.sh != s.sw || (s.sh != 1 && s.sh != 2)) return false;
     if (cw % 2 != 0) return false;
     if (fast_lds_bytes(s) > kMaxLdsBytes) return false;
-    const int p = pick_group_pixels(s.ow);
+    // padded input pixels of a group row are read from the zero buffer
+    const int64_t ni = (int64_t)(p - 1) * s.sw + s.kw;
+    if (ni * s.abits * cw * 4 > fast::kZeroBytes) return false;
     const int64_t gpr = (s.ow + p - 1) / p;
     const int64_t groups = (int64_t)s.n * s.oh * gpr;
     if (groups >= INT32_MAX / 2) return false;
@@ -118,11 +126,65 @@ bool conv_has_fast_path(const ConvShape& s) {
     return true;
 }
 
+namespace {
+
+// Pixels-on-lanes kernel for this shape, or nullptr.
+pix::PixKernelFn pix_kernel_for(const ConvShape& s, int* ocb) {
+    const int64_t cw = (s.c + 31) / 32;
+    if (s.abits > 4 || s.wbits > 4) return nullptr;
+    if (s.kh != s.kw || s.sh != s.sw) return nullptr;
+    if ((int64_t)s.n * s.oh * s.ow >= INT32_MAX) return nullptr;
+    pix::PixKernelFn fn = pix::pick(s.abits, s.wbits, s.bipolar_w, s.kh, s.sh,
+                                    (int)cw, ocb);
+    // output tiles are written in 16-byte quads of channels
+    if (!fn || s.oc % 4 != 0) return nullptr;
+    return fn;
+}
+
+hipError_t launch_pix(const ConvShape& s, pix::PixKernelFn fn, int ocb,
+                      const uint32_t* act, const uint32_t* wts, int32_t* out,
+                      hipStream_t st) {
+    pix::PixArgs g;
+    g.h = s.h; g.w = s.w; g.oc = s.oc; g.oh = s.oh; g.ow = s.ow;
+    g.sh = s.sh; g.sw = s.sw; g.ph = s.ph; g.pw = s.pw;
+    g.npix = s.n * s.oh * s.ow;
+    g.div_ow.init((uint32_t)s.ow);
+    g.div_oh.init((uint32_t)s.oh);
+    const int64_t bx = ((int64_t)g.npix + pix::kBlock - 1) / pix::kBlock;
+    // split the output channels so that the chip holds several rounds of
+    // waves (256 CUs x 4 SIMDs x 8)
+    const int64_t waves_x = bx * (pix::kBlock / 64);
+    int64_t ysplit = (256 * 4 * 8 + waves_x - 1) / waves_x;
+    const int64_t max_split = (s.oc + pix::kChunk - 1) / pix::kChunk;
+    if (ysplit > max_split) ysplit = max_split;
+    if (ysplit < 1) ysplit = 1;
+    (void)ocb;   // a divisor of kChunk
+    int64_t per = (s.oc + ysplit - 1) / ysplit;
+    per = (per + pix::kChunk - 1) / pix::kChunk * pix::kChunk;
+    if (per > s.oc) per = s.oc;
+    g.oc_per_block = (int32_t)per;
+    const int64_t by = (s.oc + per - 1) / per;
+    const size_t lds = (size_t)(pix::kBlock / 64) * pix::kTileWords * 4;
+    void* args[] = {&act, &wts, &out, &g};
+    return hipLaunchKernel((const void*)fn, dim3((uint32_t)bx, (uint32_t)by),
+                           dim3(pix::kBlock), args, lds, st);
+}
+
+}  // namespace
+
 hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
                        const uint32_t* wts, int32_t* out, int mode,
                        hipStream_t st) {
     const int32_t cw = (s.c + 31) / 32;
-    if (mode == 0 && conv_has_fast_path(s)) {
+    // mode 0: pixels-on-lanes kernel where it applies, else channels-on-lanes,
+    // else generic; 2: channels-on-lanes or generic; 3: pixels-on-lanes or
+    // generic; 1: generic only.
+    if (mode == 0 || mode == 3) {
+        int ocb = 1;
+        if (pix::PixKernelFn fn = pix_kernel_for(s, &ocb))
+            return launch_pix(s, fn, ocb, act, wts, out, st);
+    }
+    if ((mode == 0 || mode == 2) && conv_has_fast_path(s)) {
         const int p = pick_group_pixels(s.ow);
         FastArgs g;
         g.h = s.h; g.w = s.w; g.cw = cw; g.oc = s.oc; g.oh = s.oh; g.ow = s.ow;
@@ -134,17 +196,16 @@ hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
         g.div_gpr.init((uint32_t)g.gpr);
         g.div_oh.init((uint32_t)s.oh);
         const int oc_blocks = (s.oc + 63) / 64;
-        // about 8 waves per SIMD across the chip (256 CUs x 4 SIMDs)
-        const int64_t target_waves = 256 * 4 * 8;
-        int64_t gpw = ((int64_t)g.total_groups * oc_blocks + target_waves - 1) /
-                      target_waves;
-        if (gpw < 1) gpw = 1;
-        if (gpw > 64) gpw = 64;
-        g.gpw = (int32_t)gpw;
-        const int64_t per_block = gpw * kWavesPerBlock;
-        const int64_t bx = (g.total_groups + per_block - 1) / per_block;
+        // persistent grid: about BS_CONV_WAVES_PER_SIMD resident waves on
+        // each SIMD (256 CUs x 4 SIMDs), no more blocks than groups need
+        const int64_t want_blocks =
+            (256 * 4 * (int64_t)BS_CONV_WAVES_PER_SIMD / kWavesPerBlock +
+             oc_blocks - 1) / oc_blocks;
+        const int64_t need_blocks =
+            ((int64_t)g.total_groups + kWavesPerBlock - 1) / kWavesPerBlock;
+        const int64_t bx = want_blocks < need_blocks ? want_blocks : need_blocks;
         const KernelFn fn = pick_fast(s.abits, s.wbits, s.bipolar_w, s.kh,
-                                      s.sh, p);
+                                      s.sh, p, cw);
         const uint32_t* a_arg = act;
         const uint32_t* w_arg = wts;
         int32_t* o_arg = out;

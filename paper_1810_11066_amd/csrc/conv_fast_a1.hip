@@ -5,30 +5,54 @@ namespace bs {
 namespace fast {
 namespace {
 
-template <int A, int W, bool B, int K, int S>
-KernelFn pick_p(int p) {
-    return p == 7 ? conv_ocl_kernel<A, W, B, K, S, 7>
-                  : conv_ocl_kernel<A, W, B, K, S, 8>;
+// Bit-width/encoding combinations that also get compile-time word counts
+// (the ResNet-18 workloads at A1W1, A2W1, A2W2, A3W3 and bipolar weights);
+// every other combination runs with the word count as an argument.
+template <int A_, int W_, bool B_>
+constexpr bool kSpecialiseWords =
+    (A_ == 1 && W_ == 1) || (A_ == 2 && W_ == 1) ||
+    (A_ == 2 && W_ == 2 && !B_) || (A_ == 3 && W_ == 3 && !B_);
+
+template <int A_, int W_, bool B_, int K, int S, int P>
+KernelFn pick_cw(int cw) {
+    if constexpr (kSpecialiseWords<A_, W_, B_>) {
+        switch (cw) {
+            case 2: return conv_ocl_kernel<A_, W_, B_, K, S, P, 2>;
+            case 4: return conv_ocl_kernel<A_, W_, B_, K, S, P, 4>;
+            case 8: return conv_ocl_kernel<A_, W_, B_, K, S, P, 8>;
+            case 16: return conv_ocl_kernel<A_, W_, B_, K, S, P, 16>;
+            default: break;
+        }
+    }
+    return conv_ocl_kernel<A_, W_, B_, K, S, P, 0>;
 }
-template <int A, int W, bool B>
-KernelFn pick_ks(int k, int s, int p) {
-    if (k == 1) return s == 1 ? pick_p<A, W, B, 1, 1>(p) : pick_p<A, W, B, 1, 2>(p);
-    return s == 1 ? pick_p<A, W, B, 3, 1>(p) : pick_p<A, W, B, 3, 2>(p);
+template <int A_, int W_, bool B_, int K, int S>
+KernelFn pick_p(int p, int cw) {
+    return p == 7 ? pick_cw<A_, W_, B_, K, S, 7>(cw)
+                  : pick_cw<A_, W_, B_, K, S, 8>(cw);
 }
-template <int A, int W>
-KernelFn pick_b(bool b, int k, int s, int p) {
-    return b ? pick_ks<A, W, true>(k, s, p) : pick_ks<A, W, false>(k, s, p);
+template <int A_, int W_, bool B_>
+KernelFn pick_ks(int k, int s, int p, int cw) {
+    if (k == 1) return s == 1 ? pick_p<A_, W_, B_, 1, 1>(p, cw)
+                              : pick_p<A_, W_, B_, 1, 2>(p, cw);
+    return s == 1 ? pick_p<A_, W_, B_, 3, 1>(p, cw)
+                  : pick_p<A_, W_, B_, 3, 2>(p, cw);
 }
+template <int A_, int W_>
+KernelFn pick_b(bool b, int k, int s, int p, int cw) {
+    return b ? pick_ks<A_, W_, true>(k, s, p, cw)
+             : pick_ks<A_, W_, false>(k, s, p, cw);
+}
+
 }  // namespace
 
 template <>
-KernelFn pick_w<1>(int w, bool b, int k, int s, int p) {
-    constexpr int A = 1;
+KernelFn pick_w<1>(int w, bool b, int k, int s, int p, int cw) {
     switch (w) {
-        case 1: return pick_b<A, 1>(b, k, s, p);
-        case 2: return pick_b<A, 2>(b, k, s, p);
-        case 3: return pick_b<A, 3>(b, k, s, p);
-        default: return pick_b<A, 4>(b, k, s, p);
+        case 1: return pick_b<1, 1>(b, k, s, p, cw);
+        case 2: return pick_b<1, 2>(b, k, s, p, cw);
+        case 3: return pick_b<1, 3>(b, k, s, p, cw);
+        default: return pick_b<1, 4>(b, k, s, p, cw);
     }
 }
 

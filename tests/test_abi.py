@@ -159,8 +159,10 @@ def test_out_shape(lib):
 
 
 def test_kernel_mode(lib):
-    assert lib.bs_set_kernel_mode(2) == bs.BS_ERR_INVALID_ARG
-    assert lib.bs_set_kernel_mode(1) == bs.BS_OK
+    assert lib.bs_set_kernel_mode(4) == bs.BS_ERR_INVALID_ARG
+    assert lib.bs_set_kernel_mode(-1) == bs.BS_ERR_INVALID_ARG
+    for m in (1, 2, 3):
+        assert lib.bs_set_kernel_mode(m) == bs.BS_OK
     assert lib.bs_set_kernel_mode(0) == bs.BS_OK
 
 

@@ -74,23 +74,29 @@ def oracle_params(oracle, case):
 
 def check_full(oracle, case):
     ap, wp, a_dev, w_dev = prepare(oracle, case)
-    got = bs.conv2d(spec_of(case), a_dev, w_dev).cpu().numpy()
     want = oracle.conv2d(oracle_params(oracle, case), ap, wp)
-    assert np.array_equal(got, want)
+    for mode in (0, 2, 3):        # default, channels-on-lanes, pixels-on-lanes
+        bs.bs_set_kernel_mode(mode)
+        try:
+            got = bs.conv2d(spec_of(case), a_dev, w_dev).cpu().numpy()
+        finally:
+            bs.bs_set_kernel_mode(0)
+        assert np.array_equal(got, want), "kernel mode %d" % mode
 
 
 def check_sampled(oracle, case, n_random=16384):
     ap, wp, a_dev, w_dev = prepare(oracle, case)
     spec = spec_of(case)
     out = bs.conv2d(spec, a_dev, w_dev)
-    # the generic kernel on the whole output
-    bs.bs_set_kernel_mode(1)
-    try:
-        ref = bs.conv2d(spec, a_dev, w_dev)
-    finally:
-        bs.bs_set_kernel_mode(0)
-    torch.cuda.synchronize()
-    assert torch.equal(out, ref)
+    # the generic kernel and each specialised kernel on the whole output
+    for mode in (1, 2, 3):
+        bs.bs_set_kernel_mode(mode)
+        try:
+            ref = bs.conv2d(spec, a_dev, w_dev)
+        finally:
+            bs.bs_set_kernel_mode(0)
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), "kernel mode %d" % mode
     got = out.cpu().numpy().ravel()
     per_image = case.oh * case.ow * case.oc
     rng = np.random.default_rng(case.seed)

@@ -189,11 +189,12 @@ def test_conv_random_generic(oracle, seed):
     run_conv(oracle, *args, seed=seed, mode=1)
 
 
+@pytest.mark.parametrize("mode", [0, 2, 3])
 @pytest.mark.parametrize("seed", range(40))
-def test_conv_random_default(oracle, seed):
+def test_conv_random_fast(oracle, seed, mode):
     args = random_conv(np.random.default_rng(900 + seed))
-    say("conv default", args)
-    run_conv(oracle, *args, seed=seed, mode=0)
+    say("conv mode", mode, args)
+    run_conv(oracle, *args, seed=seed, mode=mode)
 
 
 # shapes that take the specialised kernel: K in {1,3}, S in {1,2}, even word
@@ -202,6 +203,9 @@ def test_conv_random_default(oracle, seed):
 FAST_SHAPES = [
     # n, h, w, c, oc, k, s, pad
     (2, 9, 11, 64, 64, 3, 1, 1),
+    (1, 10, 9, 32, 68, 3, 1, 1),
+    (2, 8, 7, 20, 36, 3, 2, 1),
+    (1, 12, 12, 128, 40, 1, 1, 0),
     (1, 14, 14, 64, 100, 3, 1, 1),
     (3, 7, 7, 128, 64, 3, 1, 1),
     (2, 10, 13, 64, 70, 3, 2, 1),
@@ -213,15 +217,18 @@ FAST_SHAPES = [
 ]
 
 
+# mode 2: output-channels-on-lanes kernel, mode 3: pixels-on-lanes kernel
+# (each falls back to the generic kernel where it does not apply)
+@pytest.mark.parametrize("mode", [2, 3])
 @pytest.mark.parametrize("shape", FAST_SHAPES, ids=lambda s: "x".join(map(str, s)))
 @pytest.mark.parametrize("abits,wbits,bip", [
     (1, 1, False), (1, 1, True), (2, 1, False), (2, 1, True), (2, 2, False),
     (3, 3, False), (3, 3, True), (4, 4, False), (1, 4, False), (4, 1, True)])
-def test_conv_fast_shapes(oracle, shape, abits, wbits, bip):
+def test_conv_fast_shapes(oracle, shape, abits, wbits, bip, mode):
     n, h, w, c, oc, k, s, pad = shape
-    say("conv fast", shape, abits, wbits, bip)
+    say("conv fast", shape, abits, wbits, bip, "mode", mode)
     run_conv(oracle, n, h, w, c, oc, k, k, s, s, pad, pad, abits, wbits, bip,
-             seed=hash((shape, abits, wbits, bip)) % 10000)
+             seed=hash((shape, abits, wbits, bip)) % 10000, mode=mode)
 
 
 def test_conv_deterministic(oracle):
