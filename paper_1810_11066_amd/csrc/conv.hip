@@ -93,6 +93,10 @@ KernelFn pick_fast(int a, int w, bool b, int k, int s, int p, int cw) {
 
 constexpr int64_t kMaxLdsBytes = 64 * 1024;
 
+#ifndef BS_PIX_WAVES_PER_SIMD
+#define BS_PIX_WAVES_PER_SIMD 8
+#endif
+
 #ifndef BS_CONV_WAVES_PER_SIMD
 #define BS_CONV_WAVES_PER_SIMD 4
 #endif
@@ -152,9 +156,10 @@ hipError_t launch_pix(const ConvShape& s, pix::PixKernelFn fn, int ocb,
     g.div_oh.init((uint32_t)s.oh);
     const int64_t bx = ((int64_t)g.npix + pix::kBlock - 1) / pix::kBlock;
     // split the output channels so that the chip holds several rounds of
-    // waves (256 CUs x 4 SIMDs x 8)
+    // waves (256 CUs x 4 SIMDs x BS_PIX_WAVES_PER_SIMD)
     const int64_t waves_x = bx * (pix::kBlock / 64);
-    int64_t ysplit = (256 * 4 * 8 + waves_x - 1) / waves_x;
+    int64_t ysplit = (256 * 4 * (int64_t)BS_PIX_WAVES_PER_SIMD + waves_x - 1) /
+                     waves_x;
     const int64_t max_split = (s.oc + pix::kChunk - 1) / pix::kChunk;
     if (ysplit > max_split) ysplit = max_split;
     if (ysplit < 1) ysplit = 1;

@@ -41,6 +41,15 @@ __device__ __forceinline__ void bcnt_acc(uint32_t& acc, uint32_t x) {
     asm("v_bcnt_u32_b32 %0, %1, %0" : "+v"(acc) : "v"(x));
 }
 
+// Order this wave's LDS writes before its following LDS reads (and the reads
+// before later writes).  The tile is private to the wave, so no block-wide
+// barrier is needed.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 __device__ __forceinline__ void wait_scalar_loads() {
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), vmcnt/expcnt untouched
 }
@@ -72,28 +81,38 @@ __device__ __forceinline__ void load_filters(FilterBatch<K, W, CW, OCB>& fb,
                     fb.w[o][t][j][c] = src[((o * K * K + t) * W + j) * CW + c];
 }
 
+// The OCB channels of a batch are interleaved and each accumulator is split
+// in two (even / odd taps), so consecutive popcounts go to 2 * OCB * (A+W-1)
+// independent accumulators instead of one dependency chain per channel.
 template <int A, int W, bool BIP, int K, int CW, int OCB>
 __device__ __forceinline__ void compute_batch(
     const uint32_t (&patch)[K * K][A][CW],
     const FilterBatch<K, W, CW, OCB>& fb, uint32_t sa, uint32_t (&val)[OCB]) {
     constexpr int NS = A + W - 1;
+    uint32_t acc[2][OCB][NS];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int o = 0; o < OCB; ++o)
+#pragma unroll
+            for (int s = 0; s < NS; ++s) acc[h][o][s] = 0;
+#pragma unroll
+    for (int t = 0; t < K * K; ++t)
+#pragma unroll
+        for (int c = 0; c < CW; ++c)
+#pragma unroll
+            for (int j = 0; j < W; ++j)
+#pragma unroll
+                for (int i = 0; i < A; ++i)
+#pragma unroll
+                    for (int o = 0; o < OCB; ++o)
+                        bcnt_acc(acc[(t * CW + c) & 1][o][i + j],
+                                 patch[t][i][c] & fb.w[o][t][j][c]);
 #pragma unroll
     for (int o = 0; o < OCB; ++o) {
-        uint32_t acc[NS];
-#pragma unroll
-        for (int s = 0; s < NS; ++s) acc[s] = 0;
-#pragma unroll
-        for (int t = 0; t < K * K; ++t)
-#pragma unroll
-            for (int c = 0; c < CW; ++c)
-#pragma unroll
-                for (int j = 0; j < W; ++j)
-#pragma unroll
-                    for (int i = 0; i < A; ++i)
-                        bcnt_acc(acc[i + j], patch[t][i][c] & fb.w[o][t][j][c]);
         uint32_t v = 0;
 #pragma unroll
-        for (int s = 0; s < NS; ++s) v += acc[s] << s;
+        for (int s = 0; s < NS; ++s) v += (acc[0][o][s] + acc[1][o][s]) << s;
         // bipolar weight value 2w - (2^W - 1): 2*sum - (2^W - 1)*sum(a)
         if (BIP) v = 2u * v - (uint32_t)((1 << W) - 1) * sa;
         val[o] = v;
@@ -230,10 +249,10 @@ __global__ __launch_bounds__(kBlock) void conv_pix_kernel(
         const int done = oc + 2 * OCB - oc0;
         if (done % kChunk == 0 || oc + 2 * OCB >= oc1) {
             const int base = oc0 + ((done - 1) / kChunk) * kChunk;
-            __syncthreads();
+            wave_lds_sync();
             flush_tile(tile, out, pix0, g.npix, g.oc, base,
                        min(kChunk, oc1 - base), lane);
-            __syncthreads();
+            wave_lds_sync();
         }
     }
 }
