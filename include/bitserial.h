@@ -120,6 +120,17 @@ bs_status bs_conv2d(const bs_conv2d_params *p, const uint32_t *act_packed,
                     const uint32_t *w_packed, int32_t *out,
                     bs_stream_t stream);
 
+/* Describes, as text, the kernel and launch configuration that bs_conv2d
+ * would use for p under the calling thread's kernel mode (template
+ * parameters, grid, block, LDS bytes).  Writes at most len bytes including
+ * the terminating NUL into the caller's buffer buf (truncating); host only,
+ * nothing is enqueued.  A dense call of shape (m, n, k) is described by the
+ * 1x1 conv n = 1, h = 1, w = m, c = k, oc = n.
+ * Errors: as bs_conv2d's parameter checks; BS_ERR_INVALID_ARG for a NULL
+ * buf or len < 1. */
+bs_status bs_conv2d_describe(const bs_conv2d_params *p, char *buf,
+                             int32_t len);
+
 /* Bitserial dense / matrix multiply (Sec. 3.2; evaluated in Sec. 6.2.1):
  *   a_packed: [m][abits][ceil(k/32)], w_packed: [n][wbits][ceil(k/32)] uint32
  *   (each output neuron's weights contiguous along the reduction axis),

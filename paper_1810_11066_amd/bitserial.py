@@ -37,7 +37,8 @@ UNIPOLAR = 0
 BIPOLAR = 1
 
 EXPORTED = ("bs_packed_words", "bs_quantize", "bs_pack", "bs_quantize_pack",
-            "bs_conv2d_out_shape", "bs_conv2d", "bs_dense", "bs_status_string",
+            "bs_conv2d_out_shape", "bs_conv2d", "bs_conv2d_describe",
+            "bs_dense", "bs_status_string",
             "bs_last_error", "bs_set_kernel_mode", "bs_abi_version")
 
 
@@ -80,6 +81,8 @@ def load_library():
                                          ctypes.POINTER(ctypes.c_int32),
                                          ctypes.POINTER(ctypes.c_int32)]),
             "bs_conv2d": (ci, [ctypes.POINTER(ConvParams), P, P, P, P]),
+            "bs_conv2d_describe": (ci, [ctypes.POINTER(ConvParams),
+                                        ctypes.c_char_p, ctypes.c_int32]),
             "bs_dense": (ci, [i64, i64, i64, ci, ci, ci, P, P, P, P]),
             "bs_status_string": (ctypes.c_char_p, [ci]),
             "bs_last_error": (ctypes.c_char_p, []),
@@ -158,6 +161,14 @@ def bs_conv2d_out_shape(p: ConvParams):
                                               ctypes.byref(oh),
                                               ctypes.byref(ow)))
     return oh.value, ow.value
+
+
+def bs_conv2d_describe(p: ConvParams) -> str:
+    """Kernel and launch configuration bs_conv2d would use for ``p`` under
+    this thread's kernel mode (host only)."""
+    buf = ctypes.create_string_buffer(256)
+    _check(load_library().bs_conv2d_describe(ctypes.byref(p), buf, 256))
+    return buf.value.decode()
 
 
 def bs_conv2d(p: ConvParams, act_packed: torch.Tensor, w_packed: torch.Tensor,

@@ -118,7 +118,7 @@ bs_status check_conv(const bs_conv2d_params* p, bs::ConvShape* s) {
 
 extern "C" {
 
-int bs_abi_version(void) { return 100; }
+int bs_abi_version(void) { return 101; }
 
 int64_t bs_packed_words(int64_t k) { return k <= 0 ? 0 : (k + 31) / 32; }
 
@@ -219,6 +219,17 @@ bs_status bs_conv2d(const bs_conv2d_params* p, const uint32_t* act_packed,
     return from_hip(bs::launch_conv(s, act_packed, w_packed, out,
                                     g_kernel_mode, (hipStream_t)stream),
                     "bs_conv2d launch");
+}
+
+bs_status bs_conv2d_describe(const bs_conv2d_params* p, char* buf,
+                             int32_t len) {
+    if (!buf || len < 1) return fail(BS_ERR_INVALID_ARG, "buf/len");
+    buf[0] = '\0';
+    bs_status st;
+    bs::ConvShape s;
+    if ((st = check_conv(p, &s)) != BS_OK) return st;
+    bs::describe_conv(s, g_kernel_mode, buf, (size_t)len);
+    return ok();
 }
 
 bs_status bs_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,

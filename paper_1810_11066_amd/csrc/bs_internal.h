@@ -55,6 +55,10 @@ hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
                        const uint32_t* wts, int32_t* out, int mode,
                        hipStream_t st);
 
+// Writes the kernel and launch configuration launch_conv would use for this
+// shape and mode into buf (snprintf semantics); returns the snprintf result.
+int describe_conv(const ConvShape& s, int mode, char* buf, size_t len);
+
 // True when launch_conv with mode 0 would use a specialised kernel.
 bool conv_has_fast_path(const ConvShape& s);
 

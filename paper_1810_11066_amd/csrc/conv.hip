@@ -7,21 +7,30 @@
 // Accumulation is in uint32 and wraps; the host rejects any problem whose
 // exact result could leave int32, so the wrapped sum equals the exact result.
 //
-// conv_generic_kernel  one output per thread, runtime everything; serves
-//                      every shape the fast kernel does not.
-// conv_ocl_kernel      "output channels on lanes": lane l of a wave owns
+// Three kernel families; the host picks one per call (launch_conv):
+//
+// conv_pix_kernel      "pixels on lanes" (conv_pix.h): lane l owns one output
+//                      pixel and keeps its packed input patch in VGPRs; the
+//                      filter words of each output channel are uniform across
+//                      the wave and arrive by scalar loads as the SGPR operand
+//                      of v_and_b32.  The fastest family for the 3x3 and 1x1
+//                      ResNet layers; used first where it applies.
+// conv_ocl_kernel      "output channels on lanes" (conv_fast.h): lane l owns
 //                      output channel oc0 + l, the wave walks groups of P
-//                      output pixels of one output row.  The activation words
-//                      of a pixel are the same for every lane, so they are
-//                      read with scalar loads into SGPRs; the filter words of
-//                      the block's 64 channels are staged once in LDS, laid
-//                      out [tap][plane][word pair][lane] so that every lane
-//                      reads its own 8 bytes without bank conflicts.  The
-//                      inner loop is one v_and_b32 (SGPR x VGPR) and one
-//                      accumulating v_bcnt_u32_b32 per word pair, into
-//                      A+W-1 per-shift accumulators per output pixel; the
-//                      shift-add (and bipolar correction) runs once per
-//                      output.  Stores are 64 consecutive int32 per pixel.
+//                      output pixels of one row; activation words are uniform
+//                      across the wave (scalar loads), filter words of the
+//                      block's 64 channels are staged once in LDS.  Serves
+//                      the shapes the pixel kernel does not (wide channels,
+//                      oc not a multiple of 4).
+// conv_generic_kernel  one output per thread, runtime everything; serves
+//                      every remaining shape.
+//
+// In both fast families the inner loop is one v_and_b32 (SGPR x VGPR) and one
+// accumulating v_bcnt_u32_b32 per word pair, into A+W-1 per-shift
+// accumulators per output; the shift-add (and bipolar correction) runs once
+// per output.
+#include <cstdio>
+
 #include "conv_fast.h"
 #include "conv_pix.h"
 
@@ -145,16 +154,14 @@ pix::PixKernelFn pix_kernel_for(const ConvShape& s, int* ocb) {
     return fn;
 }
 
-hipError_t launch_pix(const ConvShape& s, pix::PixKernelFn fn, int ocb,
-                      const uint32_t* act, const uint32_t* wts, int32_t* out,
-                      hipStream_t st) {
-    pix::PixArgs g;
-    g.h = s.h; g.w = s.w; g.oc = s.oc; g.oh = s.oh; g.ow = s.ow;
-    g.sh = s.sh; g.sw = s.sw; g.ph = s.ph; g.pw = s.pw;
-    g.npix = s.n * s.oh * s.ow;
-    g.div_ow.init((uint32_t)s.ow);
-    g.div_oh.init((uint32_t)s.oh);
-    const int64_t bx = ((int64_t)g.npix + pix::kBlock - 1) / pix::kBlock;
+// Launch configuration of a pixels-on-lanes call.
+void plan_pix(const ConvShape& s, pix::PixArgs* g, dim3* grid, size_t* lds) {
+    g->h = s.h; g->w = s.w; g->oc = s.oc; g->oh = s.oh; g->ow = s.ow;
+    g->sh = s.sh; g->sw = s.sw; g->ph = s.ph; g->pw = s.pw;
+    g->npix = s.n * s.oh * s.ow;
+    g->div_ow.init((uint32_t)s.ow);
+    g->div_oh.init((uint32_t)s.oh);
+    const int64_t bx = ((int64_t)g->npix + pix::kBlock - 1) / pix::kBlock;
     // split the output channels so that the chip holds several rounds of
     // waves (256 CUs x 4 SIMDs x BS_PIX_WAVES_PER_SIMD)
     const int64_t waves_x = bx * (pix::kBlock / 64);
@@ -163,16 +170,69 @@ hipError_t launch_pix(const ConvShape& s, pix::PixKernelFn fn, int ocb,
     const int64_t max_split = (s.oc + pix::kChunk - 1) / pix::kChunk;
     if (ysplit > max_split) ysplit = max_split;
     if (ysplit < 1) ysplit = 1;
-    (void)ocb;   // a divisor of kChunk
     int64_t per = (s.oc + ysplit - 1) / ysplit;
     per = (per + pix::kChunk - 1) / pix::kChunk * pix::kChunk;
     if (per > s.oc) per = s.oc;
-    g.oc_per_block = (int32_t)per;
+    g->oc_per_block = (int32_t)per;
     const int64_t by = (s.oc + per - 1) / per;
-    const size_t lds = (size_t)(pix::kBlock / 64) * pix::kTileWords * 4;
-    void* args[] = {&act, &wts, &out, &g};
-    return hipLaunchKernel((const void*)fn, dim3((uint32_t)bx, (uint32_t)by),
-                           dim3(pix::kBlock), args, lds, st);
+    *grid = dim3((uint32_t)bx, (uint32_t)by);
+    *lds = (size_t)(pix::kBlock / 64) * pix::kTileWords * 4;
+}
+
+// Launch configuration of a channels-on-lanes call.
+void plan_fast(const ConvShape& s, FastArgs* g, dim3* grid, size_t* lds) {
+    const int32_t cw = (s.c + 31) / 32;
+    const int p = pick_group_pixels(s.ow);
+    g->h = s.h; g->w = s.w; g->cw = cw; g->oc = s.oc; g->oh = s.oh;
+    g->ow = s.ow; g->ph = s.ph; g->pw = s.pw;
+    g->plane_bytes = cw * 4;
+    g->pix_bytes = s.abits * cw * 4;
+    g->gpr = (s.ow + p - 1) / p;
+    g->total_groups = s.n * s.oh * g->gpr;
+    g->div_gpr.init((uint32_t)g->gpr);
+    g->div_oh.init((uint32_t)s.oh);
+    const int oc_blocks = (s.oc + 63) / 64;
+    // persistent grid: about BS_CONV_WAVES_PER_SIMD resident waves on each
+    // SIMD (256 CUs x 4 SIMDs), no more blocks than groups need
+    const int64_t want_blocks =
+        (256 * 4 * (int64_t)BS_CONV_WAVES_PER_SIMD / kWavesPerBlock +
+         oc_blocks - 1) / oc_blocks;
+    const int64_t need_blocks =
+        ((int64_t)g->total_groups + kWavesPerBlock - 1) / kWavesPerBlock;
+    const int64_t bx = want_blocks < need_blocks ? want_blocks : need_blocks;
+    *grid = dim3((uint32_t)bx, oc_blocks);
+    *lds = (size_t)fast_lds_bytes(s);
+}
+
+void plan_generic(const ConvShape& s, const uint32_t* act, const uint32_t* wts,
+                  int32_t* out, GenericArgs* g, dim3* grid) {
+    g->act = act;
+    g->wts = wts;
+    g->out = out;
+    g->s = s;
+    g->cw = (s.c + 31) / 32;
+    g->total = (uint32_t)((int64_t)s.n * s.oh * s.ow * s.oc);
+    g->div_oc.init((uint32_t)s.oc);
+    g->div_ow.init((uint32_t)s.ow);
+    g->div_oh.init((uint32_t)s.oh);
+    int64_t blocks = ((int64_t)g->total + kBlock - 1) / kBlock;
+    if (blocks > 65535) blocks = 65535;
+    if (blocks < 1) blocks = 1;
+    *grid = dim3((uint32_t)blocks);
+}
+
+enum class Family { kPixels, kChannels, kGeneric };
+
+// The kernel family a call takes: mode 0 tries pixels-on-lanes, then
+// channels-on-lanes, then generic; 3 and 2 try only their own family before
+// generic; 1 is generic only.
+Family choose(const ConvShape& s, int mode, pix::PixKernelFn* pfn, int* ocb) {
+    if (mode == 0 || mode == 3) {
+        if ((*pfn = pix_kernel_for(s, ocb)) != nullptr) return Family::kPixels;
+    }
+    if ((mode == 0 || mode == 2) && conv_has_fast_path(s))
+        return Family::kChannels;
+    return Family::kGeneric;
 }
 
 }  // namespace
@@ -180,60 +240,76 @@ hipError_t launch_pix(const ConvShape& s, pix::PixKernelFn fn, int ocb,
 hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
                        const uint32_t* wts, int32_t* out, int mode,
                        hipStream_t st) {
-    const int32_t cw = (s.c + 31) / 32;
-    // mode 0: pixels-on-lanes kernel where it applies, else channels-on-lanes,
-    // else generic; 2: channels-on-lanes or generic; 3: pixels-on-lanes or
-    // generic; 1: generic only.
-    if (mode == 0 || mode == 3) {
-        int ocb = 1;
-        if (pix::PixKernelFn fn = pix_kernel_for(s, &ocb))
-            return launch_pix(s, fn, ocb, act, wts, out, st);
+    pix::PixKernelFn pfn = nullptr;
+    int ocb = 1;
+    dim3 grid;
+    size_t lds = 0;
+    switch (choose(s, mode, &pfn, &ocb)) {
+        case Family::kPixels: {
+            pix::PixArgs g;
+            plan_pix(s, &g, &grid, &lds);
+            void* args[] = {&act, &wts, &out, &g};
+            return hipLaunchKernel((const void*)pfn, grid, dim3(pix::kBlock),
+                                   args, lds, st);
+        }
+        case Family::kChannels: {
+            FastArgs g;
+            plan_fast(s, &g, &grid, &lds);
+            const KernelFn fn = pick_fast(s.abits, s.wbits, s.bipolar_w, s.kh,
+                                          s.sh, pick_group_pixels(s.ow),
+                                          g.cw);
+            void* args[] = {&act, &wts, &out, &g};
+            return hipLaunchKernel((const void*)fn, grid, dim3(kBlock), args,
+                                   lds, st);
+        }
+        case Family::kGeneric:
+        default: {
+            GenericArgs g;
+            plan_generic(s, act, wts, out, &g, &grid);
+            conv_generic_kernel<<<grid, kBlock, 0, st>>>(g);
+            return hipGetLastError();
+        }
     }
-    if ((mode == 0 || mode == 2) && conv_has_fast_path(s)) {
-        const int p = pick_group_pixels(s.ow);
-        FastArgs g;
-        g.h = s.h; g.w = s.w; g.cw = cw; g.oc = s.oc; g.oh = s.oh; g.ow = s.ow;
-        g.ph = s.ph; g.pw = s.pw;
-        g.plane_bytes = cw * 4;
-        g.pix_bytes = s.abits * cw * 4;
-        g.gpr = (s.ow + p - 1) / p;
-        g.total_groups = s.n * s.oh * g.gpr;
-        g.div_gpr.init((uint32_t)g.gpr);
-        g.div_oh.init((uint32_t)s.oh);
-        const int oc_blocks = (s.oc + 63) / 64;
-        // persistent grid: about BS_CONV_WAVES_PER_SIMD resident waves on
-        // each SIMD (256 CUs x 4 SIMDs), no more blocks than groups need
-        const int64_t want_blocks =
-            (256 * 4 * (int64_t)BS_CONV_WAVES_PER_SIMD / kWavesPerBlock +
-             oc_blocks - 1) / oc_blocks;
-        const int64_t need_blocks =
-            ((int64_t)g.total_groups + kWavesPerBlock - 1) / kWavesPerBlock;
-        const int64_t bx = want_blocks < need_blocks ? want_blocks : need_blocks;
-        const KernelFn fn = pick_fast(s.abits, s.wbits, s.bipolar_w, s.kh,
-                                      s.sh, p, cw);
-        const uint32_t* a_arg = act;
-        const uint32_t* w_arg = wts;
-        int32_t* o_arg = out;
-        void* args[] = {&a_arg, &w_arg, &o_arg, &g};
-        return hipLaunchKernel((const void*)fn, dim3((uint32_t)bx, oc_blocks),
-                               dim3(kBlock), args, (size_t)fast_lds_bytes(s),
-                               st);
+}
+
+int describe_conv(const ConvShape& s, int mode, char* buf, size_t len) {
+    pix::PixKernelFn pfn = nullptr;
+    int ocb = 1;
+    dim3 grid;
+    size_t lds = 0;
+    const int cw = (s.c + 31) / 32;
+    const char* enc = s.bipolar_w ? "bipolar" : "unipolar";
+    switch (choose(s, mode, &pfn, &ocb)) {
+        case Family::kPixels: {
+            pix::PixArgs g;
+            plan_pix(s, &g, &grid, &lds);
+            return snprintf(buf, len,
+                            "conv_pix_kernel<A=%d,W=%d,%s,K=%d,S=%d,CW=%d,"
+                            "OCB=%d> grid=%ux%u block=%d lds=%zu "
+                            "oc_per_block=%d",
+                            s.abits, s.wbits, enc, s.kh, s.sh, cw, ocb, grid.x,
+                            grid.y, pix::kBlock, lds, g.oc_per_block);
+        }
+        case Family::kChannels: {
+            FastArgs g;
+            plan_fast(s, &g, &grid, &lds);
+            return snprintf(buf, len,
+                            "conv_ocl_kernel<A=%d,W=%d,%s,K=%d,S=%d,P=%d,"
+                            "CW=%d> grid=%ux%u block=%d lds=%zu",
+                            s.abits, s.wbits, enc, s.kh, s.sh,
+                            pick_group_pixels(s.ow), cw, grid.x, grid.y,
+                            kBlock, lds);
+        }
+        case Family::kGeneric:
+        default: {
+            GenericArgs g;
+            plan_generic(s, nullptr, nullptr, nullptr, &g, &grid);
+            return snprintf(buf, len,
+                            "conv_generic_kernel A=%d W=%d %s grid=%u "
+                            "block=%d",
+                            s.abits, s.wbits, enc, grid.x, kBlock);
+        }
     }
-    GenericArgs g;
-    g.act = act;
-    g.wts = wts;
-    g.out = out;
-    g.s = s;
-    g.cw = cw;
-    g.total = (uint32_t)((int64_t)s.n * s.oh * s.ow * s.oc);
-    g.div_oc.init((uint32_t)s.oc);
-    g.div_ow.init((uint32_t)s.ow);
-    g.div_oh.init((uint32_t)s.oh);
-    int64_t blocks = ((int64_t)g.total + kBlock - 1) / kBlock;
-    if (blocks > 65535) blocks = 65535;
-    if (blocks < 1) blocks = 1;
-    conv_generic_kernel<<<(uint32_t)blocks, kBlock, 0, st>>>(g);
-    return hipGetLastError();
 }
 
 }  // namespace bs

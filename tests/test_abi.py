@@ -41,7 +41,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_words(lib):
-    assert lib.bs_abi_version() == 100
+    assert lib.bs_abi_version() == 101
     for k, w in [(0, 0), (1, 1), (31, 1), (32, 1), (33, 2), (4096, 128)]:
         assert lib.bs_packed_words(k) == w
 
@@ -172,3 +172,37 @@ def test_binding_refuses_cpu_tensors():
     q = torch.zeros(16, dtype=torch.uint8)
     with pytest.raises(ValueError, match="GPU tensor"):
         bs.bs_quantize(x, q, 1.0, 2)
+
+
+def test_describe_names_the_kernel_each_mode_picks(lib):
+    # host-only planning: no device memory is touched
+    p = params(n=64, h=56, w=56, c=64, oc=64)
+    try:
+        assert bs.bs_conv2d_describe(p).startswith(
+            "conv_pix_kernel<A=2,W=1,unipolar,K=3,S=1,CW=2,OCB=2>")
+        bs.bs_set_kernel_mode(2)
+        assert bs.bs_conv2d_describe(p).startswith(
+            "conv_ocl_kernel<A=2,W=1,unipolar,K=3,S=1,P=7,CW=2>")
+        bs.bs_set_kernel_mode(1)
+        assert bs.bs_conv2d_describe(p).startswith("conv_generic_kernel")
+        bs.bs_set_kernel_mode(3)
+        # oc not a multiple of 4: the pixel kernel does not apply
+        assert bs.bs_conv2d_describe(params(oc=70)).startswith(
+            "conv_generic_kernel")
+    finally:
+        bs.bs_set_kernel_mode(0)
+    # 5-bit activations: no specialised kernel
+    assert bs.bs_conv2d_describe(params(abits=5)).startswith(
+        "conv_generic_kernel")
+
+
+def test_describe_validation_and_truncation(lib):
+    buf = ctypes.create_string_buffer(8)
+    assert lib.bs_conv2d_describe(ctypes.byref(params()), buf, 8) == bs.BS_OK
+    assert len(buf.value) == 7
+    assert lib.bs_conv2d_describe(ctypes.byref(params()), None,
+                                  8) == bs.BS_ERR_INVALID_ARG
+    assert lib.bs_conv2d_describe(ctypes.byref(params()), buf,
+                                  0) == bs.BS_ERR_INVALID_ARG
+    assert lib.bs_conv2d_describe(ctypes.byref(params(kh=0)), buf,
+                                  8) == bs.BS_ERR_INVALID_ARG
