@@ -159,6 +159,14 @@ const char *bs_last_error(void);
  * Errors: BS_ERR_INVALID_ARG for a mode outside 0..3. */
 bs_status bs_set_kernel_mode(int mode);
 
+/* Overrides, for later conv/dense calls on the calling host thread, how much
+ * work each wave of the pixels-on-lanes kernel takes: a contiguous run of
+ * `units` units of (64 output pixels x 4 output channels).  0 (the default)
+ * lets the library choose the run that fills the GPU in one balanced round.
+ * Results do not depend on it; it exists for tests of the run boundaries and
+ * for tuning.  Errors: BS_ERR_INVALID_ARG for units < 0. */
+bs_status bs_set_units_per_wave(int units);
+
 /* ABI version of this header (major * 100 + minor). */
 int bs_abi_version(void);
 

@@ -39,7 +39,8 @@ BIPOLAR = 1
 EXPORTED = ("bs_packed_words", "bs_quantize", "bs_pack", "bs_quantize_pack",
             "bs_conv2d_out_shape", "bs_conv2d", "bs_conv2d_describe",
             "bs_dense", "bs_status_string",
-            "bs_last_error", "bs_set_kernel_mode", "bs_abi_version")
+            "bs_last_error", "bs_set_kernel_mode", "bs_set_units_per_wave",
+            "bs_abi_version")
 
 
 class BitserialError(RuntimeError):
@@ -87,6 +88,7 @@ def load_library():
             "bs_status_string": (ctypes.c_char_p, [ci]),
             "bs_last_error": (ctypes.c_char_p, []),
             "bs_set_kernel_mode": (ci, [ci]),
+            "bs_set_units_per_wave": (ci, [ci]),
             "bs_abi_version": (ci, []),
         }
         for name, (res, args) in sig.items():
@@ -198,6 +200,10 @@ def bs_dense(m: int, n: int, k: int, abits: int, wbits: int, wenc: int,
 
 def bs_set_kernel_mode(mode: int) -> None:
     _check(load_library().bs_set_kernel_mode(int(mode)))
+
+
+def bs_set_units_per_wave(units: int) -> None:
+    _check(load_library().bs_set_units_per_wave(int(units)))
 
 
 def bs_packed_words(k: int) -> int:

@@ -13,7 +13,7 @@
 namespace {
 
 thread_local char g_err[512];
-thread_local int g_kernel_mode = 0;
+thread_local bs::ConvOptions g_conv_opt;
 
 bs_status fail(bs_status st, const char* fmt, ...) {
     va_list ap;
@@ -138,7 +138,13 @@ const char* bs_last_error(void) { return g_err; }
 bs_status bs_set_kernel_mode(int mode) {
     if (mode < 0 || mode > 3)
         return fail(BS_ERR_INVALID_ARG, "kernel mode must be 0..3");
-    g_kernel_mode = mode;
+    g_conv_opt.mode = mode;
+    return ok();
+}
+
+bs_status bs_set_units_per_wave(int units) {
+    if (units < 0) return fail(BS_ERR_INVALID_ARG, "units per wave must be >= 0");
+    g_conv_opt.units_per_wave = units;
     return ok();
 }
 
@@ -217,7 +223,7 @@ bs_status bs_conv2d(const bs_conv2d_params* p, const uint32_t* act_packed,
     bs::ConvShape s;
     if ((st = check_conv(p, &s)) != BS_OK) return st;
     return from_hip(bs::launch_conv(s, act_packed, w_packed, out,
-                                    g_kernel_mode, (hipStream_t)stream),
+                                    g_conv_opt, (hipStream_t)stream),
                     "bs_conv2d launch");
 }
 
@@ -228,7 +234,7 @@ bs_status bs_conv2d_describe(const bs_conv2d_params* p, char* buf,
     bs_status st;
     bs::ConvShape s;
     if ((st = check_conv(p, &s)) != BS_OK) return st;
-    bs::describe_conv(s, g_kernel_mode, buf, (size_t)len);
+    bs::describe_conv(s, g_conv_opt, buf, (size_t)len);
     return ok();
 }
 
@@ -251,7 +257,7 @@ bs_status bs_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,
     p.wenc = wenc;
     bs::ConvShape s;
     if ((st = check_conv(&p, &s)) != BS_OK) return st;
-    return from_hip(bs::launch_conv(s, a_packed, w_packed, out, g_kernel_mode,
+    return from_hip(bs::launch_conv(s, a_packed, w_packed, out, g_conv_opt,
                                     (hipStream_t)stream),
                     "bs_dense launch");
 }

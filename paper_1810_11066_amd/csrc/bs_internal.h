@@ -48,16 +48,24 @@ struct ConvShape {
     bool bipolar_w;
 };
 
-// mode 0: the fastest applicable kernel; 1: generic only; 2: the
-// channels-on-lanes kernel where it applies; 3: the pixels-on-lanes kernel
-// where it applies (2 and 3 fall back to the generic kernel).
+// Kernel selection for a conv call.  mode 0: the fastest applicable kernel;
+// 1: generic only; 2: the channels-on-lanes kernel where it applies; 3: the
+// pixels-on-lanes kernel where it applies (2 and 3 fall back to the generic
+// kernel).  units_per_wave > 0 overrides the run length the host would pick
+// for the pixels-on-lanes kernel (units of 64 pixels x 4 output channels).
+struct ConvOptions {
+    int mode = 0;
+    int units_per_wave = 0;
+};
+
 hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
-                       const uint32_t* wts, int32_t* out, int mode,
-                       hipStream_t st);
+                       const uint32_t* wts, int32_t* out,
+                       const ConvOptions& opt, hipStream_t st);
 
 // Writes the kernel and launch configuration launch_conv would use for this
 // shape and mode into buf (snprintf semantics); returns the snprintf result.
-int describe_conv(const ConvShape& s, int mode, char* buf, size_t len);
+int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
+                  size_t len);
 
 // True when launch_conv with mode 0 would use a specialised kernel.
 bool conv_has_fast_path(const ConvShape& s);

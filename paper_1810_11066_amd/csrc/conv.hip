@@ -29,7 +29,10 @@
 // accumulating v_bcnt_u32_b32 per word pair, into A+W-1 per-shift
 // accumulators per output; the shift-add (and bipolar correction) runs once
 // per output.
+#include <atomic>
 #include <cstdio>
+#include <mutex>
+#include <vector>
 
 #include "conv_fast.h"
 #include "conv_pix.h"
@@ -102,10 +105,6 @@ KernelFn pick_fast(int a, int w, bool b, int k, int s, int p, int cw) {
 
 constexpr int64_t kMaxLdsBytes = 64 * 1024;
 
-#ifndef BS_PIX_WAVES_PER_SIMD
-#define BS_PIX_WAVES_PER_SIMD 8
-#endif
-
 #ifndef BS_CONV_WAVES_PER_SIMD
 #define BS_CONV_WAVES_PER_SIMD 4
 #endif
@@ -142,41 +141,93 @@ bool conv_has_fast_path(const ConvShape& s) {
 namespace {
 
 // Pixels-on-lanes kernel for this shape, or nullptr.
-pix::PixKernelFn pix_kernel_for(const ConvShape& s, int* ocb) {
+pix::PixKernelFn pix_kernel_for(const ConvShape& s, int* ocb, int* ts) {
     const int64_t cw = (s.c + 31) / 32;
     if (s.abits > 4 || s.wbits > 4) return nullptr;
     if (s.kh != s.kw || s.sh != s.sw) return nullptr;
-    if ((int64_t)s.n * s.oh * s.ow >= INT32_MAX) return nullptr;
-    pix::PixKernelFn fn = pix::pick(s.abits, s.wbits, s.bipolar_w, s.kh, s.sh,
-                                    (int)cw, ocb);
     // output tiles are written in 16-byte quads of channels
-    if (!fn || s.oc % 4 != 0) return nullptr;
-    return fn;
+    if (s.oc % 4 != 0) return nullptr;
+    const int64_t npix = (int64_t)s.n * s.oh * s.ow;
+    const int64_t units = (npix + 63) / 64 * (s.oc / 4);
+    if (npix >= INT32_MAX || units >= INT32_MAX / 2) return nullptr;
+    return pix::pick(s.abits, s.wbits, s.bipolar_w, s.kh, s.sh, (int)cw, ocb,
+                     ts);
 }
 
-// Launch configuration of a pixels-on-lanes call.
-void plan_pix(const ConvShape& s, pix::PixArgs* g, dim3* grid, size_t* lds) {
-    g->h = s.h; g->w = s.w; g->oc = s.oc; g->oh = s.oh; g->ow = s.ow;
-    g->sh = s.sh; g->sw = s.sw; g->ph = s.ph; g->pw = s.pw;
+// Compute units of the current device (cached per device).
+int device_cus() {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v > 0) return v;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount,
+                              dev) != hipSuccess || v < 1)
+        v = 256;
+    cache[dev].store(v, std::memory_order_relaxed);
+    return v;
+}
+
+// Resident blocks of fn per CU (register, LDS and wave-slot limits), cached
+// per kernel and device.  The pixel kernels stay within 80 SGPRs, where the
+// runtime's count agrees with the hardware.
+int resident_blocks(pix::PixKernelFn fn, size_t lds) {
+    struct Entry { pix::PixKernelFn fn; int dev; size_t lds; int blocks; };
+    static std::mutex mu;
+    static std::vector<Entry> cache;
+    int dev = 0;
+    (void)hipGetDevice(&dev);
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        for (const Entry& e : cache)
+            if (e.fn == fn && e.dev == dev && e.lds == lds) return e.blocks;
+    }
+    int blocks = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &blocks, (const void*)fn, pix::kBlock, lds) != hipSuccess ||
+        blocks < 1)
+        return 1;
+    std::lock_guard<std::mutex> lock(mu);
+    cache.push_back({fn, dev, lds, blocks});
+    return blocks;
+}
+
+// Launch configuration of a pixels-on-lanes call.  The work is units of
+// (64-pixel group, 4 output channels); each wave takes a contiguous run of
+// L units.  L is the smallest run that keeps the grid resident in one round
+// (at most `resident` blocks per CU), adjusted upwards while that lowers the
+// busiest CU's load (blocks per CU x L), so that CUs end together.
+void plan_pix(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
+              pix::PixArgs* g, dim3* grid, size_t* lds) {
+    g->h = s.h; g->w = s.w; g->oh = s.oh; g->ow = s.ow;
+    g->ph = s.ph; g->pw = s.pw;
+    g->oc = s.oc;
     g->npix = s.n * s.oh * s.ow;
+    g->quads = s.oc / 4;
+    const int64_t groups = ((int64_t)g->npix + 63) / 64;
+    const int64_t units = groups * g->quads;
+    g->units = (int32_t)units;
     g->div_ow.init((uint32_t)s.ow);
     g->div_oh.init((uint32_t)s.oh);
-    const int64_t bx = ((int64_t)g->npix + pix::kBlock - 1) / pix::kBlock;
-    // split the output channels so that the chip holds several rounds of
-    // waves (256 CUs x 4 SIMDs x BS_PIX_WAVES_PER_SIMD)
-    const int64_t waves_x = bx * (pix::kBlock / 64);
-    int64_t ysplit = (256 * 4 * (int64_t)BS_PIX_WAVES_PER_SIMD + waves_x - 1) /
-                     waves_x;
-    const int64_t max_split = (s.oc + pix::kChunk - 1) / pix::kChunk;
-    if (ysplit > max_split) ysplit = max_split;
-    if (ysplit < 1) ysplit = 1;
-    int64_t per = (s.oc + ysplit - 1) / ysplit;
-    per = (per + pix::kChunk - 1) / pix::kChunk * pix::kChunk;
-    if (per > s.oc) per = s.oc;
-    g->oc_per_block = (int32_t)per;
-    const int64_t by = (s.oc + per - 1) / per;
-    *grid = dim3((uint32_t)bx, (uint32_t)by);
-    *lds = (size_t)(pix::kBlock / 64) * pix::kTileWords * 4;
+    g->div_quads.init((uint32_t)g->quads);
+    *lds = (size_t)pix::kWavesPerBlock * pix::kTileWords * 4;
+    const int64_t cus = device_cus();
+    const int64_t slots = cus * resident_blocks(fn, *lds);   // blocks
+    const int64_t wpb = pix::kWavesPerBlock;
+    int64_t lmin = (units + slots * wpb - 1) / (slots * wpb);
+    if (lmin < 1) lmin = 1;
+    auto load = [&](int64_t l) {   // busiest CU: blocks per CU x units
+        const int64_t waves = (units + l - 1) / l;
+        const int64_t blocks = (waves + wpb - 1) / wpb;
+        return (blocks + cus - 1) / cus * l;
+    };
+    int64_t best = lmin;
+    for (int64_t l = lmin + 1; l <= 2 * lmin; ++l)
+        if (load(l) < load(best)) best = l;
+    if (forced_run > 0) best = forced_run < units ? forced_run : units;
+    g->per_wave = (int32_t)best;
+    const int64_t waves = (units + best - 1) / best;
+    *grid = dim3((uint32_t)((waves + wpb - 1) / wpb));
 }
 
 // Launch configuration of a channels-on-lanes call.
@@ -226,9 +277,11 @@ enum class Family { kPixels, kChannels, kGeneric };
 // The kernel family a call takes: mode 0 tries pixels-on-lanes, then
 // channels-on-lanes, then generic; 3 and 2 try only their own family before
 // generic; 1 is generic only.
-Family choose(const ConvShape& s, int mode, pix::PixKernelFn* pfn, int* ocb) {
+Family choose(const ConvShape& s, int mode, pix::PixKernelFn* pfn, int* ocb,
+              int* ts) {
     if (mode == 0 || mode == 3) {
-        if ((*pfn = pix_kernel_for(s, ocb)) != nullptr) return Family::kPixels;
+        if ((*pfn = pix_kernel_for(s, ocb, ts)) != nullptr)
+            return Family::kPixels;
     }
     if ((mode == 0 || mode == 2) && conv_has_fast_path(s))
         return Family::kChannels;
@@ -238,16 +291,17 @@ Family choose(const ConvShape& s, int mode, pix::PixKernelFn* pfn, int* ocb) {
 }  // namespace
 
 hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
-                       const uint32_t* wts, int32_t* out, int mode,
-                       hipStream_t st) {
+                       const uint32_t* wts, int32_t* out,
+                       const ConvOptions& opt, hipStream_t st) {
+    const int mode = opt.mode;
     pix::PixKernelFn pfn = nullptr;
-    int ocb = 1;
+    int ocb = 1, ts = 1;
     dim3 grid;
     size_t lds = 0;
-    switch (choose(s, mode, &pfn, &ocb)) {
+    switch (choose(s, mode, &pfn, &ocb, &ts)) {
         case Family::kPixels: {
             pix::PixArgs g;
-            plan_pix(s, &g, &grid, &lds);
+            plan_pix(s, pfn, opt.units_per_wave, &g, &grid, &lds);
             void* args[] = {&act, &wts, &out, &g};
             return hipLaunchKernel((const void*)pfn, grid, dim3(pix::kBlock),
                                    args, lds, st);
@@ -272,23 +326,25 @@ hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
     }
 }
 
-int describe_conv(const ConvShape& s, int mode, char* buf, size_t len) {
+int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
+                  size_t len) {
+    const int mode = opt.mode;
     pix::PixKernelFn pfn = nullptr;
-    int ocb = 1;
+    int ocb = 1, ts = 1;
     dim3 grid;
     size_t lds = 0;
     const int cw = (s.c + 31) / 32;
     const char* enc = s.bipolar_w ? "bipolar" : "unipolar";
-    switch (choose(s, mode, &pfn, &ocb)) {
+    switch (choose(s, mode, &pfn, &ocb, &ts)) {
         case Family::kPixels: {
             pix::PixArgs g;
-            plan_pix(s, &g, &grid, &lds);
+            plan_pix(s, pfn, opt.units_per_wave, &g, &grid, &lds);
             return snprintf(buf, len,
-                            "conv_pix_kernel<A=%d,W=%d,%s,K=%d,S=%d,CW=%d,"
-                            "OCB=%d> grid=%ux%u block=%d lds=%zu "
-                            "oc_per_block=%d",
-                            s.abits, s.wbits, enc, s.kh, s.sh, cw, ocb, grid.x,
-                            grid.y, pix::kBlock, lds, g.oc_per_block);
+                            "conv_pix_kernel<A=%d,W=%d,%s,K=%d,S=%d,CW=%d> "
+                            "slice=%dch x %dtaps grid=%u block=%d lds=%zu "
+                            "units=%d units_per_wave=%d",
+                            s.abits, s.wbits, enc, s.kh, s.sh, cw, ocb, ts,
+                            grid.x, pix::kBlock, lds, g.units, g.per_wave);
         }
         case Family::kChannels: {
             FastArgs g;

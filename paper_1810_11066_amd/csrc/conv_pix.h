@@ -1,25 +1,38 @@
 // Pixels-on-lanes bitserial conv kernel template; instantiated in
 // conv_pix.hip.
 //
-// Mapping.  Lane l of a block owns one output pixel (n, oy, ox); a block of
-// 256 lanes covers 256 consecutive output pixels in NHWC order, and
-// blockIdx.y selects a contiguous range of output channels.  Each lane loads
-// the packed words of its K x K input patch once (vector loads; consecutive
-// lanes read consecutive pixels), zeroes the taps that fall in the padding,
-// and keeps the patch in VGPRs for all of its output channels.  The filter
-// words of an output channel are the same for every lane, so they are read
-// with scalar loads (the filters of a layer are small and stay in the scalar
-// cache) and used as the SGPR operand of v_and_b32.
+// Mapping.  Lane l of a wave owns one output pixel of a 64-pixel group
+// (consecutive output pixels in NHWC order).  The work of a layer is the
+// sequence of units (group, quad of 4 output channels), group-major; each
+// wave takes one contiguous run of units, so a wave visits at most a few
+// groups and, inside a group, a contiguous range of output channels.  The
+// host sizes the runs so that the whole grid is resident at once and every
+// CU holds the same number of waves (no second round, no straggler CUs).
+//
+// Per group, each lane loads the packed words of its K x K input patch once
+// (vector loads; consecutive lanes read consecutive pixels), zeroes the taps
+// in the padding, and keeps the patch in VGPRs for all the channels of its
+// run.  Filter words are the same for every lane, so they are read with
+// scalar loads (a layer's filters are small and stay in the scalar cache) and
+// used as the SGPR operand of v_and_b32.
 //
 // Inner loop: per (tap, plane pair, word) one v_and_b32 (SGPR x VGPR) and one
-// accumulating v_bcnt_u32_b32 into one of A+W-1 per-shift accumulators; the
-// shift-add (and bipolar correction, whose popcount sum over the patch is
-// computed once per lane) runs once per output.  Scalar work is one wait and
-// a few offset adds per OCB output channels, so the vector unit stays fed.
+// accumulating v_bcnt_u32_b32 into one of 2 (A+W-1) per-shift accumulators
+// (split by tap parity so consecutive popcounts are independent); the
+// shift-add (and bipolar correction, whose patch popcount sum is computed
+// once per group) runs once per output.
 //
-// The filter loads of channel batch b+1 are issued before batch b is
-// computed (two SGPR buffers); scalar loads return out of order, so the wait
-// for batch b is placed explicitly before batch b+1 is issued.
+// Filter words stream through two SGPR slices of at most kSliceWords words
+// each: the slice for step s+1 is requested before step s computes, and the
+// wait for it sits explicitly before step s+1 (scalar loads return out of
+// order, so only a full lgkmcnt(0) wait is exact).
+//
+// Occupancy.  The hardware reserves more SGPRs per wave than the compiler's
+// count: measured on gfx950, 8 waves fit on a SIMD up to 80 SGPRs, 7 up to
+// 96 and 6 above.  The kernel is therefore compiled for at most 80 SGPRs
+// (the slice bound keeps the channel loop within that; what does not fit is
+// spilled to VGPR lanes in the per-group code), and the host's occupancy
+// query, which counts the way the compiler does, is then exact.
 #pragma once
 
 #include "bs_internal.h"
@@ -28,17 +41,24 @@ namespace bs {
 namespace pix {
 
 constexpr int kBlock = 256;
+constexpr int kWavesPerBlock = kBlock / 64;
+constexpr int kSliceWords = 24;     // filter words per SGPR slice
 
 struct PixArgs {
-    int32_t h, w, oc, oh, ow, sh, sw, ph, pw;
+    int32_t h, w, oh, ow, ph, pw;
+    int32_t oc;            // output channels, a multiple of 4
     int32_t npix;          // n * oh * ow
-    int32_t oc_per_block;  // output channels per blockIdx.y: a multiple of
-                           // kChunk, or all of them (oc % 4 == 0)
-    FastDiv div_ow, div_oh;
+    int32_t quads;         // oc / 4
+    int32_t units;         // ceil(npix / 64) * quads, < 2^31
+    int32_t per_wave;      // units per wave (the last waves may get fewer)
+    FastDiv div_ow, div_oh, div_quads;
 };
 
 __device__ __forceinline__ void bcnt_acc(uint32_t& acc, uint32_t x) {
     asm("v_bcnt_u32_b32 %0, %1, %0" : "+v"(acc) : "v"(x));
+}
+__device__ __forceinline__ void bcnt_first(uint32_t& acc, uint32_t x) {
+    asm("v_bcnt_u32_b32 %0, %1, 0" : "=v"(acc) : "v"(x));
 }
 
 // Order this wave's LDS writes before its following LDS reads (and the reads
@@ -56,74 +76,43 @@ __device__ __forceinline__ void wait_scalar_loads() {
 
 typedef const uint32_t __attribute__((address_space(1))) gu32;
 
-// Filter words of OCB consecutive output channels: OHWI packing puts each
-// filter's K*K*W*CW words contiguously and consecutive filters next to each
-// other, so a batch is one contiguous run (merged into wide scalar loads).
-template <int K, int W, int CW, int OCB>
-struct FilterBatch {
-    uint32_t w[OCB][K * K][W][CW];
+// Static shape of the filter stream.  A filter (OHWI) is K*K*W*CW
+// contiguous words, and consecutive filters are adjacent, so the filters of a
+// channel range are one contiguous run.  Small filters are consumed OCB = 2
+// channels per slice; large ones one channel at a time, TS taps per slice.
+// Either way step s of a range reads words [s*SW, (s+1)*SW) of the run.
+template <int K, int W, int CW>
+struct Stream {
+    static constexpr int KK = K * K;
+    static constexpr int FW = KK * W * CW;              // words per filter
+    static constexpr int OCB = FW * 2 <= kSliceWords ? 2 : 1;
+    static constexpr int TS =                           // taps per slice
+        FW <= kSliceWords ? KK
+        : (KK % 3 == 0 && 3 * W * CW <= kSliceWords) ? 3 : 1;
+    static constexpr int NP = KK / TS;                  // slices per filter
+    static constexpr int SW = OCB * TS * W * CW;        // words per slice
+    static constexpr int STEPS = 4 / OCB * NP;          // slices per quad
+    static constexpr bool kFits = TS * W * CW <= kSliceWords;
+    static_assert(OCB == 1 || NP == 1, "a slice is whole filters or part of one");
+    static_assert(STEPS % 2 == 0, "slice buffers alternate within a quad");
 };
 
-template <int K, int W, int CW, int OCB>
-__device__ __forceinline__ void load_filters(FilterBatch<K, W, CW, OCB>& fb,
-                                             gu32* __restrict__ wts,
-                                             int oc) {
-    constexpr int FW = K * K * W * CW;   // words per filter
-    gu32* src = wts + (size_t)oc * FW;
-#pragma unroll
-    for (int o = 0; o < OCB; ++o)
-#pragma unroll
-        for (int t = 0; t < K * K; ++t)
-#pragma unroll
-            for (int j = 0; j < W; ++j)
-#pragma unroll
-                for (int c = 0; c < CW; ++c)
-                    fb.w[o][t][j][c] = src[((o * K * K + t) * W + j) * CW + c];
-}
+template <int SW>
+struct Slice {
+    uint32_t w[SW];
+};
 
-// The OCB channels of a batch are interleaved and each accumulator is split
-// in two (even / odd taps), so consecutive popcounts go to 2 * OCB * (A+W-1)
-// independent accumulators instead of one dependency chain per channel.
-template <int A, int W, bool BIP, int K, int CW, int OCB>
-__device__ __forceinline__ void compute_batch(
-    const uint32_t (&patch)[K * K][A][CW],
-    const FilterBatch<K, W, CW, OCB>& fb, uint32_t sa, uint32_t (&val)[OCB]) {
-    constexpr int NS = A + W - 1;
-    uint32_t acc[2][OCB][NS];
+template <int SW>
+__device__ __forceinline__ void load_slice(Slice<SW>& s, gu32* src) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int o = 0; o < OCB; ++o)
-#pragma unroll
-            for (int s = 0; s < NS; ++s) acc[h][o][s] = 0;
-#pragma unroll
-    for (int t = 0; t < K * K; ++t)
-#pragma unroll
-        for (int c = 0; c < CW; ++c)
-#pragma unroll
-            for (int j = 0; j < W; ++j)
-#pragma unroll
-                for (int i = 0; i < A; ++i)
-#pragma unroll
-                    for (int o = 0; o < OCB; ++o)
-                        bcnt_acc(acc[(t * CW + c) & 1][o][i + j],
-                                 patch[t][i][c] & fb.w[o][t][j][c]);
-#pragma unroll
-    for (int o = 0; o < OCB; ++o) {
-        uint32_t v = 0;
-#pragma unroll
-        for (int s = 0; s < NS; ++s) v += (acc[0][o][s] + acc[1][o][s]) << s;
-        // bipolar weight value 2w - (2^W - 1): 2*sum - (2^W - 1)*sum(a)
-        if (BIP) v = 2u * v - (uint32_t)((1 << W) - 1) * sa;
-        val[o] = v;
-    }
+    for (int k = 0; k < SW; ++k) s.w[k] = src[k];
 }
 
 // Output tile staging.  With pixels on lanes, the NHWC output of one output
 // channel is 4 bytes per lane at a stride of oc * 4 bytes -- one memory
 // request per lane.  Results are therefore collected per wave in LDS as a
 // 64-pixel x kChunk-channel tile and written back with each lane storing 16
-// contiguous bytes (4 lanes per pixel row of the chunk).
+// contiguous bytes (nch / 4 lanes per pixel).
 constexpr int kChunk = 16;                 // output channels per LDS tile
 constexpr int kTileStride = kChunk + 1;    // words per pixel row (padded)
 constexpr int kTileWords = 64 * kTileStride;
@@ -131,15 +120,18 @@ constexpr int kTileWords = 64 * kTileStride;
 __device__ __forceinline__ void flush_tile(
     const uint32_t* __restrict__ tile, int32_t* __restrict__ out,
     int pix0, int npix, int oc_total, int oc_base, int nch, int lane) {
-    // nch (a multiple of 4, at most kChunk) channels of 64 pixels:
-    // nch / 4 lanes per pixel row
-    const int lanes_per_pix = nch >> 2;
-    const int pix_per_round = 64 / lanes_per_pix;
-    const bool active = lane < pix_per_round * lanes_per_pix;
-    for (int r = 0; r < 64; r += pix_per_round) {
-        const int px = r + lane / lanes_per_pix;
-        const int q = lane % lanes_per_pix;
-        if (active && px < 64 && pix0 + px < npix) {
+    // nch in {4, 8, 12, 16}: lpp = nch / 4 lanes per pixel, lpp rounds of
+    // 64 (pixel, quad) entries.  e / lpp for e < 256 is (e * m) >> 16 with
+    // m = ceil(2^16 / lpp): the error e (m lpp - 2^16) / (lpp 2^16) stays
+    // below 1/lpp - frac(e / lpp) for every such e.
+    const int lpp = nch >> 2;
+    const uint32_t m = lpp == 1 ? 65536u : lpp == 2 ? 32768u
+                     : lpp == 3 ? 21846u : 16384u;
+    for (int r = 0; r < lpp; ++r) {
+        const uint32_t e = (uint32_t)(r * 64 + lane);
+        const int px = (int)((e * m) >> 16);
+        const int q = (int)e - px * lpp;
+        if (pix0 + px < npix) {
             const uint32_t* t = tile + px * kTileStride + 4 * q;
             *reinterpret_cast<uint4*>(
                 out + (int64_t)(pix0 + px) * oc_total + oc_base + 4 * q) =
@@ -148,112 +140,183 @@ __device__ __forceinline__ void flush_tile(
     }
 }
 
-// A, W: bit-widths; BIP: bipolar weights; K: square kernel size; S: stride;
-// CW: words per bit-plane; OCB: output channels per filter batch.
-template <int A, int W, bool BIP, int K, int S, int CW, int OCB>
-__global__ __launch_bounds__(kBlock) void conv_pix_kernel(
-    const uint32_t* __restrict__ act, const uint32_t* __restrict__ wts,
-    int32_t* __restrict__ out, PixArgs g) {
-    constexpr int PW = A * CW;           // words per packed input pixel
-    const int p = blockIdx.x * kBlock + threadIdx.x;
-    const bool valid = p < g.npix;
-    const uint32_t pc = (uint32_t)(valid ? p : g.npix - 1);
-    const uint32_t rowi = g.div_ow.div(pc);
-    const int ox = (int)(pc - rowi * (uint32_t)g.ow);
-    const uint32_t img = g.div_oh.div(rowi);
-    const int oy = (int)(rowi - img * (uint32_t)g.oh);
-
-    // the lane's input patch; taps in the zero padding are zero
-    uint32_t patch[K * K][A][CW];
+// One quad of output channels: 4 / OCB batches of OCB channels, NP slices
+// each.  Slice buffer f[s & 1] holds step s; on entry f[0] holds (or is
+// receiving) step 0, and on exit f[0] is receiving the next quad's first
+// slice when `prefetch` is set.
+template <int A, int W, bool BIP, int K, int CW>
+__device__ __forceinline__ void compute_quad(
+    const uint32_t (&patch)[K * K][A][CW], uint32_t sa, gu32* src,
+    bool prefetch, Slice<Stream<K, W, CW>::SW> (&f)[2], uint32_t (&val)[4]) {
+    using St = Stream<K, W, CW>;
+    constexpr int NS = A + W - 1;
+    constexpr int OCB = St::OCB, TS = St::TS, NP = St::NP, SW = St::SW;
 #pragma unroll
-    for (int r = 0; r < K; ++r) {
-        const int iy = oy * S - g.ph + r;
+    for (int b = 0; b < 4 / OCB; ++b) {
+        uint32_t acc[2][OCB][NS];
+        bool fresh[2][OCB][NS];
 #pragma unroll
-        for (int s = 0; s < K; ++s) {
-            const int ix = ox * S - g.pw + s;
-            const bool in = (unsigned)iy < (unsigned)g.h &&
-                            (unsigned)ix < (unsigned)g.w;
-            const int64_t pix = in ? ((int64_t)img * g.h + iy) * g.w + ix : 0;
-            const uint32_t* src = act + pix * PW;
-            uint32_t wv[PW];
-            if constexpr (PW % 4 == 0) {
-#pragma unroll
-                for (int k = 0; k < PW; k += 4) {
-                    const uint4 x = *reinterpret_cast<const uint4*>(src + k);
-                    wv[k] = x.x; wv[k + 1] = x.y; wv[k + 2] = x.z; wv[k + 3] = x.w;
-                }
-            } else if constexpr (PW % 2 == 0) {
-#pragma unroll
-                for (int k = 0; k < PW; k += 2) {
-                    const uint2 x = *reinterpret_cast<const uint2*>(src + k);
-                    wv[k] = x.x; wv[k + 1] = x.y;
-                }
-            } else {
-#pragma unroll
-                for (int k = 0; k < PW; ++k) wv[k] = src[k];
-            }
-#pragma unroll
-            for (int i = 0; i < A; ++i)
-#pragma unroll
-                for (int c = 0; c < CW; ++c)
-                    patch[r * K + s][i][c] = in ? wv[i * CW + c] : 0u;
-        }
-    }
-    uint32_t sa = 0;   // bipolar: sum_i 2^i popcount(a_i) over the patch
-    if (BIP) {
-#pragma unroll
-        for (int t = 0; t < K * K; ++t)
-#pragma unroll
-            for (int i = 0; i < A; ++i)
-#pragma unroll
-                for (int c = 0; c < CW; ++c)
-                    sa += (uint32_t)__builtin_popcount(patch[t][i][c]) << i;
-    }
-
-    gu32* gw = (gu32*)(wts);
-    const int oc0 = blockIdx.y * g.oc_per_block;
-    const int oc1 = min(oc0 + g.oc_per_block, g.oc);
-
-    // per-wave output tile in LDS
-    extern __shared__ uint32_t lds[];
-    const int lane = threadIdx.x & 63;
-    uint32_t* tile = lds + (threadIdx.x >> 6) * kTileWords;
-    const int pix0 = p - lane;   // first pixel of this wave
-
-    FilterBatch<K, W, CW, OCB> f0, f1;
-    uint32_t val[OCB];
-    load_filters<K, W, CW, OCB>(f0, gw, oc0);
-    for (int oc = oc0; oc < oc1; oc += 2 * OCB) {
-        wait_scalar_loads();
-        const bool more = oc + OCB < oc1;
-        if (more) load_filters<K, W, CW, OCB>(f1, gw, oc + OCB);
-        __builtin_amdgcn_sched_barrier(0);
-        compute_batch<A, W, BIP, K, CW, OCB>(patch, f0, sa, val);
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int o = 0; o < OCB; ++o)
-            tile[lane * kTileStride + (oc - oc0) % kChunk + o] = val[o];
-        if (more) {
-            wait_scalar_loads();
-            if (oc + 2 * OCB < oc1)
-                load_filters<K, W, CW, OCB>(f0, gw, oc + 2 * OCB);
-            __builtin_amdgcn_sched_barrier(0);
-            compute_batch<A, W, BIP, K, CW, OCB>(patch, f1, sa, val);
-            __builtin_amdgcn_sched_barrier(0);
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
             for (int o = 0; o < OCB; ++o)
-                tile[lane * kTileStride + (oc + OCB - oc0) % kChunk + o] =
-                    val[o];
+#pragma unroll
+                for (int s = 0; s < NS; ++s) fresh[h][o][s] = true;
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            const int st = b * NP + p;
+            wait_scalar_loads();
+            if (st + 1 < St::STEPS)
+                load_slice<SW>(f[(st + 1) & 1], src + (st + 1) * SW);
+            else if (prefetch)
+                load_slice<SW>(f[0], src + St::STEPS * SW);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int tt = 0; tt < TS; ++tt)
+#pragma unroll
+                for (int c = 0; c < CW; ++c)
+#pragma unroll
+                    for (int j = 0; j < W; ++j)
+#pragma unroll
+                        for (int i = 0; i < A; ++i)
+#pragma unroll
+                            for (int o = 0; o < OCB; ++o) {
+                                const int t = p * TS + tt;
+                                const int h = (t * CW + c) & 1;
+                                const uint32_t x =
+                                    patch[t][i][c] &
+                                    f[st & 1].w[((o * TS + tt) * W + j) * CW + c];
+                                if (fresh[h][o][i + j]) {
+                                    bcnt_first(acc[h][o][i + j], x);
+                                    fresh[h][o][i + j] = false;
+                                } else {
+                                    bcnt_acc(acc[h][o][i + j], x);
+                                }
+                            }
+            __builtin_amdgcn_sched_barrier(0);
         }
-        // a full chunk of channels (or the last, shorter one) is ready
-        const int done = oc + 2 * OCB - oc0;
-        if (done % kChunk == 0 || oc + 2 * OCB >= oc1) {
-            const int base = oc0 + ((done - 1) / kChunk) * kChunk;
-            wave_lds_sync();
-            flush_tile(tile, out, pix0, g.npix, g.oc, base,
-                       min(kChunk, oc1 - base), lane);
-            wave_lds_sync();
+#pragma unroll
+        for (int o = 0; o < OCB; ++o) {
+            uint32_t v = 0;
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                const uint32_t a0 = fresh[0][o][s] ? 0u : acc[0][o][s];
+                const uint32_t a1 = fresh[1][o][s] ? 0u : acc[1][o][s];
+                v += (a0 + a1) << s;
+            }
+            // bipolar weight value 2w - (2^W - 1): 2*sum - (2^W - 1)*sum(a)
+            if (BIP) v = 2u * v - (uint32_t)((1 << W) - 1) * sa;
+            val[b * OCB + o] = v;
         }
+    }
+}
+
+// A, W: bit-widths; BIP: bipolar weights; K: square kernel size; S: stride;
+// CW: words per bit-plane.
+template <int A, int W, bool BIP, int K, int S, int CW>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_num_sgpr(80)))
+void conv_pix_kernel(
+    const uint32_t* __restrict__ act, const uint32_t* __restrict__ wts,
+    int32_t* __restrict__ out, PixArgs g) {
+    using St = Stream<K, W, CW>;
+    constexpr int PW = A * CW;           // words per packed input pixel
+    constexpr int FW = St::FW;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(
+        (int)(blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)));
+    // units [u, u_end) of this wave; per_wave * waves < 2^31 (host)
+    int u = wave * g.per_wave;
+    const int u_end = min(u + g.per_wave, g.units);
+
+    extern __shared__ uint32_t lds[];
+    uint32_t* tile = lds + (threadIdx.x >> 6) * kTileWords;
+    gu32* gw = (gu32*)(wts);
+
+    while (u < u_end) {
+        const int grp = (int)g.div_quads.div((uint32_t)u);
+        const int q0 = u - grp * g.quads;
+        const int q1 = min(g.quads, q0 + (u_end - u));
+        const int pix0 = grp * 64;
+
+        // the lane's input patch; taps in the zero padding are zero
+        const int p = pix0 + lane;
+        const uint32_t pc = (uint32_t)(p < g.npix ? p : g.npix - 1);
+        const uint32_t rowi = g.div_ow.div(pc);
+        const int ox = (int)(pc - rowi * (uint32_t)g.ow);
+        const uint32_t img = g.div_oh.div(rowi);
+        const int oy = (int)(rowi - img * (uint32_t)g.oh);
+        uint32_t patch[K * K][A][CW];
+#pragma unroll
+        for (int r = 0; r < K; ++r) {
+            const int iy = oy * S - g.ph + r;
+#pragma unroll
+            for (int s = 0; s < K; ++s) {
+                const int ix = ox * S - g.pw + s;
+                const bool in = (unsigned)iy < (unsigned)g.h &&
+                                (unsigned)ix < (unsigned)g.w;
+                const int64_t pix =
+                    in ? ((int64_t)img * g.h + iy) * g.w + ix : 0;
+                const uint32_t* src = act + pix * PW;
+                uint32_t wv[PW];
+                if constexpr (PW % 4 == 0) {
+#pragma unroll
+                    for (int k = 0; k < PW; k += 4) {
+                        const uint4 x = *reinterpret_cast<const uint4*>(src + k);
+                        wv[k] = x.x; wv[k + 1] = x.y;
+                        wv[k + 2] = x.z; wv[k + 3] = x.w;
+                    }
+                } else if constexpr (PW % 2 == 0) {
+#pragma unroll
+                    for (int k = 0; k < PW; k += 2) {
+                        const uint2 x = *reinterpret_cast<const uint2*>(src + k);
+                        wv[k] = x.x; wv[k + 1] = x.y;
+                    }
+                } else {
+#pragma unroll
+                    for (int k = 0; k < PW; ++k) wv[k] = src[k];
+                }
+#pragma unroll
+                for (int i = 0; i < A; ++i)
+#pragma unroll
+                    for (int c = 0; c < CW; ++c)
+                        patch[r * K + s][i][c] = in ? wv[i * CW + c] : 0u;
+            }
+        }
+        uint32_t sa = 0;   // bipolar: sum_i 2^i popcount(a_i) over the patch
+        if (BIP) {
+#pragma unroll
+            for (int t = 0; t < K * K; ++t)
+#pragma unroll
+                for (int i = 0; i < A; ++i)
+#pragma unroll
+                    for (int c = 0; c < CW; ++c)
+                        sa += (uint32_t)__builtin_popcount(patch[t][i][c]) << i;
+        }
+
+        // channels [4 q0, 4 q1): filter run starts at channel 4 q0
+        gu32* src = gw + (size_t)(4 * q0) * FW;
+        Slice<St::SW> f[2];
+        load_slice<St::SW>(f[0], src);
+        const int nq = q1 - q0;
+        int chunk_base = 4 * q0;   // first channel held in the tile
+        int held = 0;              // quads held in the tile
+        for (int qi = 0; qi < nq; ++qi) {
+            uint32_t val[4];
+            compute_quad<A, W, BIP, K, CW>(patch, sa, src + (size_t)qi * 4 * FW,
+                                           qi + 1 < nq, f, val);
+#pragma unroll
+            for (int o = 0; o < 4; ++o)
+                tile[lane * kTileStride + held * 4 + o] = val[o];
+            ++held;
+            if (held == kChunk / 4 || qi + 1 == nq) {
+                wave_lds_sync();
+                flush_tile(tile, out, pix0, g.npix, g.oc, chunk_base,
+                           held * 4, lane);
+                wave_lds_sync();
+                chunk_base += held * 4;
+                held = 0;
+            }
+        }
+        u += nq;
     }
 }
 
@@ -261,8 +324,9 @@ using PixKernelFn = void (*)(const uint32_t*, const uint32_t*, int32_t*,
                              PixArgs);
 
 // Kernel for a supported (A, W, bipolar, K, S, CW) or nullptr; also reports
-// the filter batch size the kernel uses.
-PixKernelFn pick(int a, int w, bool b, int k, int s, int cw, int* ocb);
+// the output channels per filter slice (ocb) and taps per slice (ts).
+PixKernelFn pick(int a, int w, bool b, int k, int s, int cw, int* ocb,
+                 int* ts);
 
 }  // namespace pix
 }  // namespace bs

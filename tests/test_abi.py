@@ -166,6 +166,20 @@ def test_kernel_mode(lib):
     assert lib.bs_set_kernel_mode(0) == bs.BS_OK
 
 
+def test_units_per_wave(lib):
+    assert lib.bs_set_units_per_wave(-1) == bs.BS_ERR_INVALID_ARG
+    p = params(n=64, h=56, w=56, c=64, oc=64)
+    try:
+        assert lib.bs_set_units_per_wave(5) == bs.BS_OK
+        d = bs.bs_conv2d_describe(p)
+        # 64*56*56 / 64 groups x 16 quads = 50176 units, 5 per wave
+        assert "units=50176 units_per_wave=5" in d
+        waves = -(-50176 // 5)
+        assert "grid=%d " % -(-waves // 4) in d
+    finally:
+        assert lib.bs_set_units_per_wave(0) == bs.BS_OK
+
+
 def test_binding_refuses_cpu_tensors():
     import torch
     x = torch.zeros(16, dtype=torch.float32)
@@ -179,7 +193,7 @@ def test_describe_names_the_kernel_each_mode_picks(lib):
     p = params(n=64, h=56, w=56, c=64, oc=64)
     try:
         assert bs.bs_conv2d_describe(p).startswith(
-            "conv_pix_kernel<A=2,W=1,unipolar,K=3,S=1,CW=2,OCB=2>")
+            "conv_pix_kernel<A=2,W=1,unipolar,K=3,S=1,CW=2> slice=1ch x 9taps")
         bs.bs_set_kernel_mode(2)
         assert bs.bs_conv2d_describe(p).startswith(
             "conv_ocl_kernel<A=2,W=1,unipolar,K=3,S=1,P=7,CW=2>")

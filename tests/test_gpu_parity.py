@@ -231,6 +231,33 @@ def test_conv_fast_shapes(oracle, shape, abits, wbits, bip, mode):
              seed=hash((shape, abits, wbits, bip)) % 10000, mode=mode)
 
 
+# Runs of units (64 pixels x 4 channels) that start and end inside groups,
+# cross group boundaries, and flush 4, 8, 12 and 16 channel tiles.
+RUN_SHAPES = [
+    # n, h, w, c, oc, k, s, pad
+    (2, 9, 11, 64, 64, 3, 1, 1),      # 4 groups (last one partial) x 16 quads
+    (1, 10, 9, 32, 12, 3, 1, 1),      # 3 quads per group
+    (2, 8, 7, 64, 36, 3, 2, 1),       # 9 quads, stride 2
+    (1, 12, 12, 128, 40, 1, 1, 0),    # 1x1, 10 quads, 3 groups
+    (3, 7, 7, 128, 20, 3, 1, 1),      # 4 words per plane
+]
+
+
+@pytest.mark.parametrize("run", [1, 2, 3, 5, 7, 16, 37, 100000])
+@pytest.mark.parametrize("shape", RUN_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("abits,wbits,bip", [(2, 1, False), (1, 1, True),
+                                             (2, 2, False)])
+def test_conv_pixel_runs(oracle, shape, run, abits, wbits, bip):
+    n, h, w, c, oc, k, s, pad = shape
+    say("conv pixel runs", shape, run, abits, wbits, bip)
+    bs.bs_set_units_per_wave(run)
+    try:
+        run_conv(oracle, n, h, w, c, oc, k, k, s, s, pad, pad, abits, wbits,
+                 bip, seed=run * 7 + oc, mode=3)
+    finally:
+        bs.bs_set_units_per_wave(0)
+
+
 def test_conv_deterministic(oracle):
     args = (2, 14, 14, 64, 64, 3, 3, 1, 1, 1, 1, 2, 1, False)
     a = run_conv(oracle, *args, seed=5)
