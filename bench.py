@@ -104,6 +104,178 @@ def cpu_baseline(case, a_host, w_host, gpu_out_fn, budget_s: float):
     }, bool(np.array_equal(gpu, ref))
 
 
+class Measured:
+    """Times of one workload: the clean step, and per-launch kernel times."""
+
+    def __init__(self, ms_step, host_ms, pre_ms, main_ms, describe):
+        self.ms_step = ms_step
+        self.host_ms = host_ms
+        self.pre_ms = pre_ms          # activation (quantize +) pack kernel
+        self.main_ms = main_ms        # conv / dense kernel
+        self.describe = describe
+
+
+def prepare(case, n_sets, bs, torch, np):
+    """Device buffers for `n_sets` rotated steps of a conv or dense case, and
+    the per-step launch function.  Inputs are the workload's seeded host
+    arrays (rolled along the batch axis for sets beyond the first); weights
+    are packed once, outside the timed steps."""
+    from paper_1810_11066_amd import workloads as wl
+    stream = torch.cuda.current_stream()
+    dense = isinstance(case, wl.DenseCase)
+    if dense:
+        rows, k, abits = case.m, case.k, case.abits
+    else:
+        rows, k, abits = case.n * case.h * case.w, case.c, case.abits
+    words = bs.words(k)
+    x_host = case.activations()
+    wsrc = case.weights()
+    if not dense and case.weights_from_signs:
+        w_packed = bs.pack(bs.quantize(torch.from_numpy(wsrc).cuda(), 1.0, 1,
+                                       bs.BIPOLAR), 1)
+    else:
+        w_packed = bs.pack(torch.from_numpy(wsrc).cuda(), case.wbits)
+    if dense:
+        out_shape = (case.m, case.n)
+        params = None
+    else:
+        params = bs.Conv2dSpec(case.n, case.h, case.w, case.c, case.oc,
+                               case.k, case.k, case.stride, case.pad,
+                               case.abits, case.wbits, case.wenc).params()
+        oh, ow = bs.bs_conv2d_out_shape(params)
+        out_shape = (case.n, oh, ow, case.oc)
+    quantized = (not dense) and case.act_scale is not None
+    sets = []
+    for i in range(n_sets):
+        xi = x_host if i == 0 else np.roll(x_host, i, axis=0)
+        x = torch.from_numpy(np.ascontiguousarray(xi)).cuda()
+        packed = torch.empty((rows, abits, words), dtype=torch.int32,
+                             device="cuda")
+        out = torch.empty(out_shape, dtype=torch.int32, device="cuda")
+        sets.append((x, packed, out))
+    torch.cuda.synchronize()
+
+    def step(i, ev=None):
+        x, packed, out = sets[i % len(sets)]
+        if ev is not None:
+            ev[0].record(stream)
+        if quantized:
+            bs.bs_quantize_pack(x, packed, rows, k, case.act_scale, abits,
+                                bs.UNIPOLAR, stream)
+        else:
+            bs.bs_pack(x, packed, rows, k, abits, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        if dense:
+            bs.bs_dense(case.m, case.n, case.k, case.abits, case.wbits,
+                        bs.UNIPOLAR, packed, w_packed, out, stream)
+        else:
+            bs.bs_conv2d(params, packed, w_packed, out, stream)
+        if ev is not None:
+            ev[2].record(stream)
+
+    if dense:
+        describe = bs.bs_conv2d_describe(bs.Conv2dSpec(
+            1, 1, case.m, case.k, case.n, 1, 1, 1, 0, case.abits,
+            case.wbits).params())
+    else:
+        describe = bs.bs_conv2d_describe(params)
+    return sets, step, params, w_packed, describe, quantized
+
+
+def measure(step, describe, steps, warmup, torch):
+    """Clean timed region (one event pair around all steps), then the same
+    steps again with an event pair around each launch for kernel times."""
+    stream = torch.cuda.current_stream()
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    h0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(steps):
+        step(i)
+    t_end.record(stream)
+    host_ms = (time.perf_counter() - h0) * 1e3 / steps
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / steps
+    # events between launches add gaps, so they stay out of the timed region
+    ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3))
+          for _ in range(steps)]
+    for i in range(steps):
+        step(i, ev[i])
+    torch.cuda.synchronize()
+    pre_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
+    main_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / steps
+    return Measured(ms_step, host_ms, pre_ms, main_ms, describe)
+
+
+def case_bytes(case):
+    """Algorithmic HBM bytes of (activation pack, main kernel)."""
+    from paper_1810_11066_amd import workloads as wl
+    if isinstance(case, wl.DenseCase):
+        rows, k, out = case.m, case.k, case.m * case.n * 4
+        wbytes = case.n * case.wbits * ((case.k + 31) // 32) * 4
+    else:
+        rows, k = case.n * case.h * case.w, case.c
+        out = case.n * case.oh * case.ow * case.oc * 4
+        wbytes = case.oc * case.k * case.k * case.wbits * \
+            ((case.c + 31) // 32) * 4
+    packed = rows * case.abits * ((k + 31) // 32) * 4
+    src = rows * k * (4 if getattr(case, "act_scale", None) else 1)
+    return src + packed, packed + wbytes + out
+
+
+def case_line(case, m, args):
+    """One JSON result object for a workload other than the headline one."""
+    from paper_1810_11066_amd import workloads as wl
+    dense = isinstance(case, wl.DenseCase)
+    ops = 2 * case.macs
+    peak = popcount_roofline_tops(case.abits, case.wbits)
+    pre_bytes, main_bytes = case_bytes(case)
+    t_alu = ops / (peak * 1e12)
+    t_hbm = main_bytes / (HBM_PEAK_GBS * 1e9)
+    bound = "alu" if t_alu >= t_hbm else "hbm"
+    main_s = m.main_ms * 1e-3
+    roof = {"bound": bound, "kernel": m.describe,
+            "kernel_ms": round(m.main_ms, 5)}
+    if bound == "alu":
+        roof.update(achieved=round(ops / main_s / 1e12, 2),
+                    peak=round(peak, 1), unit="TOPS (effective ops, "
+                    "popcount VALU)", frac=round(t_alu / main_s, 4))
+    else:
+        roof.update(achieved=round(main_bytes / main_s / 1e9, 1),
+                    peak=HBM_PEAK_GBS, unit="GB/s (algorithmic bytes)",
+                    frac=round(t_hbm / main_s, 4))
+    return {
+        "metric": "bitserial conv2d effective GOPS (2*MACs/s) + % of "
+                  "popcount-VALU roofline",
+        "value": round(ops / (m.ms_step * 1e-3) / 1e9, 1),
+        "unit": "GOPS", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(m.ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "u32", "data": "synthetic",
+        "config": {"workload": case.name,
+                   "per_step": ("bs_quantize_pack" if getattr(
+                       case, "act_scale", None) else "bs_pack") +
+                   "(activations) + " + ("bs_dense" if dense
+                                         else "bs_conv2d"),
+                   "abits": case.abits, "wbits": case.wbits,
+                   "encoding": "bipolar" if getattr(case, "wenc", 0)
+                   else "unipolar"},
+        "roofline": roof,
+        "pack_roofline": {
+            "bound": "hbm",
+            "achieved": round(pre_bytes / (m.pre_ms * 1e-3) / 1e9, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(pre_bytes / (m.pre_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                          4),
+            "bytes": pre_bytes, "kernel_ms": round(m.pre_ms, 5)},
+        "host_enqueue_ms_per_step": round(m.host_ms, 5),
+    }
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -117,6 +289,10 @@ def main() -> int:
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one device copy of this size (for HBM "
                          "counter calibration under rocprofv3 --pmc)")
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5],
+                    help="workload: 2 (default) is the headline ResNet-18 "
+                         "layer-2 A2W1 line; 1, 3, 4, 5 print one line per "
+                         "case of that workload")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -135,76 +311,29 @@ def main() -> int:
     torch.cuda.set_device(0)
     bs.load_library()
 
+    if args.config != 2:
+        cases = {1: lambda: [wl.config1()], 3: lambda: [wl.config3()],
+                 4: wl.config4, 5: wl.config5}[args.config]()
+        for case in cases:
+            sets, step, _, _, describe, _ = prepare(case, args.sets, bs,
+                                                    torch, np)
+            m = measure(step, describe, args.steps, args.warmup, torch)
+            print(json.dumps(case_line(case, m, args)), flush=True)
+            del sets
+            torch.cuda.empty_cache()
+        return 0
+
     case = wl.config2(batch=args.batch)
-    spec = bs.Conv2dSpec(case.n, case.h, case.w, case.c, case.oc, case.k,
-                         case.k, case.stride, case.pad, case.abits,
-                         case.wbits)
-    params = spec.params()
-    oh, ow = bs.bs_conv2d_out_shape(params)
     rows, k = case.n * case.h * case.w, case.c
-    words = bs.words(k)
-
-    a_host = case.activations()
-    w_host = case.weights()
-    w_packed = bs.pack(torch.from_numpy(w_host).cuda(), case.wbits)
-    sets = []
-    for i in range(args.sets):
-        q = torch.from_numpy(a_host).cuda() if i == 0 else \
-            torch.from_numpy(np.roll(a_host, i, axis=0)).cuda()
-        packed = torch.empty((case.n, case.h, case.w, case.abits, words),
-                             dtype=torch.int32, device="cuda")
-        out = torch.empty((case.n, oh, ow, case.oc), dtype=torch.int32,
-                          device="cuda")
-        sets.append((q, packed, out))
-    torch.cuda.synchronize()
-
+    sets, step, params, w_packed, describe, _ = prepare(case, args.sets, bs,
+                                                        torch, np)
+    m = measure(step, describe, args.steps, args.warmup, torch)
     stream = torch.cuda.current_stream()
-
-    def step(i, ev=None):
-        q, packed, out = sets[i % len(sets)]
-        if ev is not None:
-            ev[0].record(stream)
-        bs.bs_pack(q, packed, rows, k, case.abits, stream)
-        if ev is not None:
-            ev[1].record(stream)
-        bs.bs_conv2d(params, packed, w_packed, out, stream)
-        if ev is not None:
-            ev[2].record(stream)
-
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-
-    # timed region: the steps back to back, bracketed by one pair of events
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    h0 = time.perf_counter()
-    t_start.record(stream)
-    for i in range(args.steps):
-        step(i)
-    t_end.record(stream)
-    host_ms = (time.perf_counter() - h0) * 1e3 / args.steps
-    torch.cuda.synchronize()
-    ms_total = t_start.elapsed_time(t_end)
-    ms_step = ms_total / args.steps
-
-    # kernel durations: the same steps again with an event pair around each
-    # launch (events between launches add gaps, so they stay out of the
-    # timed region above)
-    step_ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3))
-               for _ in range(args.steps)]
-    for i in range(args.steps):
-        step(i, step_ev[i])
-    torch.cuda.synchronize()
-    pack_ms = sum(e[0].elapsed_time(e[1]) for e in step_ev) / args.steps
-    conv_ms = sum(e[1].elapsed_time(e[2]) for e in step_ev) / args.steps
-    # packing moves its codes in (one byte each) and its bit-planes out
-    pack_bytes = rows * k + rows * case.abits * words * 4
     macs = case.macs
-    value_gops = 2 * macs / (ms_step * 1e-3) / 1e9
+    value_gops = 2 * macs / (m.ms_step * 1e-3) / 1e9
     peak = popcount_roofline_tops(case.abits, case.wbits)
-    achieved = 2 * macs / (conv_ms * 1e-3) / 1e12
+    achieved = 2 * macs / (m.main_ms * 1e-3) / 1e12
+    pack_bytes, _ = case_bytes(case)
 
     if args.copy_calibration_mib > 0:
         nbytes = args.copy_calibration_mib << 20
@@ -222,7 +351,7 @@ def main() -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 5),
+        "ms_per_step": round(m.ms_step, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -244,31 +373,32 @@ def main() -> int:
             "unit": "TOPS (effective A2W1 ops, popcount VALU)",
             "frac": round(achieved / peak, 4),
             "traffic": committed_traffic(workload),
-            "kernel": bs.bs_conv2d_describe(params),
-            "kernel_ms": round(conv_ms, 5),
+            "kernel": m.describe,
+            "kernel_ms": round(m.main_ms, 5),
             "timing": "per-launch HIP events on the launch stream, in a "
                       "second pass over the same steps",
         },
-        "host_enqueue_ms_per_step": round(host_ms, 5),
+        "host_enqueue_ms_per_step": round(m.host_ms, 5),
         "pack_roofline": {
             "bound": "hbm",
-            "achieved": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1),
+            "achieved": round(pack_bytes / (m.pre_ms * 1e-3) / 1e9, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": round(pack_bytes / (pack_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
-                          4),
+            "frac": round(pack_bytes / (m.pre_ms * 1e-3) / 1e9 /
+                          HBM_PEAK_GBS, 4),
             "bytes": pack_bytes,
-            "kernel_ms": round(pack_ms, 5),
+            "kernel_ms": round(m.pre_ms, 5),
         },
     }
 
     if args.cpu_budget > 0:
+        a_host = case.activations()
+        w_host = case.weights()
+
         def gpu_slice(n_img):
-            q, packed, out = sets[0]
-            bs.bs_pack(q, packed, rows, k, case.abits, stream)
-            bs.bs_conv2d(params, packed, w_packed, out, stream)
+            step(0)
             torch.cuda.synchronize()
-            return out[:n_img].cpu().numpy()
+            return sets[0][2][:n_img].cpu().numpy()
         cpu, ok = cpu_baseline(case, a_host, w_host, gpu_slice,
                                args.cpu_budget)
         result["cpu_baseline"] = cpu
