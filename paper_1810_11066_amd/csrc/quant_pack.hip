@@ -7,8 +7,10 @@
 // quantize_pack  both in one pass over the float32 data
 //
 // All three stream HBM once and do a few integer ops per element, so they
-// are bound by memory bandwidth; the kernels are shaped for coalesced
-// 16-byte (or 256-byte-per-wave) accesses.
+// are bound by memory bandwidth.  Every load is a 16-byte vector load with
+// consecutive lanes reading consecutive addresses; the bits of one packed
+// word are gathered in registers and joined across lanes with DPP ORs (or
+// wave ballots in the any-k fallback).
 #include "bs_internal.h"
 
 namespace bs {
@@ -74,24 +76,77 @@ __device__ __forceinline__ uint32_t nibble_of(uint32_t v, int b) {
     return (x | (x >> 14)) & 0xFu;      // bits 0..3
 }
 
+// Cross-lane OR with a DPP lane permutation (all source lanes are inside the
+// 8-lane group, so every lane reads a defined value).
+constexpr int kDppQuadXor1 = 0xB1;     // quad_perm [1,0,3,2]: lane ^ 1
+constexpr int kDppQuadXor2 = 0x4E;     // quad_perm [2,3,0,1]: lane ^ 2
+constexpr int kDppHalfMirror = 0x141;  // row_half_mirror: lane i <-> 7 - i
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t or_dpp(uint32_t v) {
+    return v | (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF,
+                                                     false);
+}
+
+// pack, k % 32 == 0: a wave packs 128 consecutive words of the flat
+// [rows][k / 32] word array (4096 codes, which never split a word across
+// rows).  Load j (0..3) reads 16 codes per lane, lanes consecutive, so every
+// load is one coalesced 1 KiB.  Lanes 2p, 2p+1 of load j hold the two halves
+// of word 32 j + p: each gathers its 16 bits of plane b in registers and one
+// DPP OR joins the halves.  Lane 2p + i keeps word 32 j + p when j % 2 == i
+// (slot j / 2); one ds_bpermute per plane and slot then moves word w to lane
+// w % 64, so the stores write 64 consecutive words.
 template <int A>
-__global__ __launch_bounds__(kBlock) void pack32_kernel(
+__global__ __launch_bounds__(kBlock) void pack_dpp_kernel(
     const uint8_t* __restrict__ q, uint32_t* __restrict__ packed,
-    uint32_t groups, FastDiv kwdiv) {
+    uint32_t nwords, FastDiv kwdiv) {
+    const int lane = threadIdx.x & 63;
     const uint32_t kw = kwdiv.d;
     const uint4* src = reinterpret_cast<const uint4*>(q);
-    for (uint32_t g = blockIdx.x * kBlock + threadIdx.x; g < groups;
-         g += gridDim.x * kBlock) {
-        const uint4 lo = src[2 * (size_t)g], hi = src[2 * (size_t)g + 1];
-        const uint32_t v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-        const uint32_t row = kwdiv.div(g), t = g - row * kw;
-        uint32_t* dst = packed + (size_t)row * A * kw + t;
+    const uint32_t wave0 = (blockIdx.x * kBlock + threadIdx.x) >> 6;
+    const uint32_t nwaves = (gridDim.x * kBlock) >> 6;
+    // lane l's words (l and 64 + l of the chunk) come from lane 2 (l % 32) +
+    // l / 32, which holds them in slots 0 and 1
+    const int from = (2 * (lane & 31) + (lane >> 5)) * 4;
+    for (uint32_t base = wave0 * 128u; base < nwords; base += nwaves * 128u) {
+        const uint32_t left = nwords - base;
+        uint4 v[4];
 #pragma unroll
-        for (int b = 0; b < A; ++b) {
-            uint32_t word = 0;
+        for (int j = 0; j < 4; ++j) {
+            // this lane's 16 codes belong to word 32 j + lane / 2
+            const bool ok = (uint32_t)(32 * j + (lane >> 1)) < left;
+            v[j] = ok ? src[(size_t)base * 2 + 64 * j + lane]
+                      : make_uint4(0, 0, 0, 0);
+        }
+        uint32_t keep[A][2];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) word |= nibble_of(v[i], b) << (4 * i);
-            dst[(size_t)b * kw] = word;
+        for (int b = 0; b < A; ++b) keep[b][0] = keep[b][1] = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int b = 0; b < A; ++b) {
+                uint32_t h = nibble_of(v[j].x, b) | nibble_of(v[j].y, b) << 4 |
+                             nibble_of(v[j].z, b) << 8 |
+                             nibble_of(v[j].w, b) << 12;
+                h <<= 16 * (lane & 1);
+                h = or_dpp<kDppQuadXor1>(h);
+                if ((lane & 1) == (j & 1)) keep[b][j >> 1] = h;
+            }
+        }
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+            const uint32_t wi = base + 64 * s + lane;
+            uint32_t word[A];
+#pragma unroll
+            for (int b = 0; b < A; ++b)
+                word[b] = (uint32_t)__builtin_amdgcn_ds_bpermute(
+                    from, (int)keep[b][s]);
+            if (wi < nwords) {
+                const uint32_t row = kwdiv.div(wi), t = wi - row * kw;
+                uint32_t* dst = packed + (size_t)row * A * kw + t;
+#pragma unroll
+                for (int b = 0; b < A; ++b) dst[(size_t)b * kw] = word[b];
+            }
         }
     }
 }
@@ -134,45 +189,58 @@ __global__ __launch_bounds__(kBlock) void pack_ballot_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// quantize_pack, k % 32 == 0: one wave produces 64 consecutive output words
-// (2048 consecutive elements of the flat [rows][k] array, which never splits
-// a word across rows).  Each step loads 64 consecutive floats (256 coalesced
-// bytes per wave), quantizes them and takes one ballot per plane; the ballot
-// is words 2c, 2c+1 of the block and is parked in lanes 2c, 2c+1.  After 32
-// steps lane l holds word l of every plane and stores it.
+// quantize_pack, k % 32 == 0: a wave produces 64 consecutive words of the
+// flat [rows][k / 32] word array (2048 floats).  Load j (0..7) reads one
+// float4 per lane, lanes consecutive (coalesced 1 KiB).  The 8 lanes
+// 8m .. 8m+7 of load j hold word 8 j + m, 4 elements each: every lane
+// quantizes its 4 values, places their plane-b bits at 4 (lane % 8), and
+// three DPP ORs combine the group.  Lane 8m + i keeps word 8 j + m when
+// j == i; a ds_bpermute per plane then moves word w to lane w.
 template <int A, bool BIP>
-__global__ __launch_bounds__(kBlock) void quantize_pack_ballot_kernel(
+__global__ __launch_bounds__(kBlock) void quantize_pack_dpp_kernel(
     const float* __restrict__ x, uint32_t* __restrict__ packed,
     uint32_t nwords, FastDiv kwdiv, float scale, float qmax) {
     const int lane = threadIdx.x & 63;
     const uint32_t kw = kwdiv.d;
+    const float4* xv = reinterpret_cast<const float4*>(x);
     const uint32_t wave0 = (blockIdx.x * kBlock + threadIdx.x) >> 6;
     const uint32_t nwaves = (gridDim.x * kBlock) >> 6;
+    // word l is held by lane 8 (l % 8) + l / 8
+    const int from = (8 * (lane & 7) + (lane >> 3)) * 4;
     for (uint32_t base = wave0 * 64u; base < nwords; base += nwaves * 64u) {
-        uint32_t words[A];
+        const uint32_t left = nwords - base;
+        float4 f[8];
 #pragma unroll
-        for (int b = 0; b < A; ++b) words[b] = 0;
-        const float* xb = x + (size_t)base * 32 + lane;
-        const uint32_t left = nwords - base;   // words still to produce
-#pragma unroll 8
-        for (int c = 0; c < 32; ++c) {
-            uint32_t code = 0;
-            // lanes 0-31 feed word 2c, lanes 32-63 word 2c+1
-            if ((uint32_t)(2 * c + (lane >> 5)) < left)
-                code = code_of<BIP>(xb[(size_t)c * 64], scale, qmax);
+        for (int j = 0; j < 8; ++j) {
+            const bool ok = (uint32_t)(8 * j + (lane >> 3)) < left;
+            f[j] = ok ? xv[(size_t)base * 8 + 64 * j + lane]
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        uint32_t keep[A];
+#pragma unroll
+        for (int b = 0; b < A; ++b) keep[b] = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint32_t c4 = codes4<BIP>(f[j], scale, qmax);
 #pragma unroll
             for (int b = 0; b < A; ++b) {
-                const uint64_t m = __ballot((code >> b) & 1u);
-                words[b] = lane == 2 * c ? (uint32_t)m : words[b];
-                words[b] = lane == 2 * c + 1 ? (uint32_t)(m >> 32) : words[b];
+                uint32_t h = nibble_of(c4, b) << (4 * (lane & 7));
+                h = or_dpp<kDppQuadXor1>(h);
+                h = or_dpp<kDppQuadXor2>(h);
+                h = or_dpp<kDppHalfMirror>(h);
+                if ((lane & 7) == j) keep[b] = h;
             }
         }
+        uint32_t word[A];
+#pragma unroll
+        for (int b = 0; b < A; ++b)
+            word[b] = (uint32_t)__builtin_amdgcn_ds_bpermute(from, (int)keep[b]);
         const uint32_t wi = base + lane;
         if (wi < nwords) {
             const uint32_t row = kwdiv.div(wi), t = wi - row * kw;
             uint32_t* dst = packed + (size_t)row * A * kw + t;
 #pragma unroll
-            for (int b = 0; b < A; ++b) dst[(size_t)b * kw] = words[b];
+            for (int b = 0; b < A; ++b) dst[(size_t)b * kw] = word[b];
         }
     }
 }
@@ -185,10 +253,11 @@ int grid_for(int64_t work_items, int per_block) {
 }
 
 template <int A>
-hipError_t launch_pack32(const uint8_t* q, uint32_t* packed, uint32_t groups,
+hipError_t launch_pack32(const uint8_t* q, uint32_t* packed, uint32_t nwords,
                          const FastDiv& d, hipStream_t st) {
-    pack32_kernel<A><<<grid_for(groups, kBlock), kBlock, 0, st>>>(q, packed,
-                                                                  groups, d);
+    // 128 words per wave, 4 waves per block
+    pack_dpp_kernel<A><<<grid_for(nwords, 512), kBlock, 0, st>>>(q, packed,
+                                                                 nwords, d);
     return hipGetLastError();
 }
 
@@ -197,7 +266,7 @@ hipError_t launch_qpack(const float* x, uint32_t* packed, uint32_t nwords,
                         const FastDiv& d, float scale, float qmax,
                         hipStream_t st) {
     // 64 words per wave, 4 waves per block
-    quantize_pack_ballot_kernel<A, BIP>
+    quantize_pack_dpp_kernel<A, BIP>
         <<<grid_for(nwords, 256), kBlock, 0, st>>>(x, packed, nwords, d,
                                                     scale, qmax);
     return hipGetLastError();
@@ -220,7 +289,7 @@ hipError_t launch_pack(const uint8_t* q, uint32_t* packed, int64_t rows,
                        int64_t k, int bits, hipStream_t st) {
     const int64_t kw = (k + 31) / 32;
     const int64_t groups = rows * kw;
-    if (k % 32 == 0 && groups < (int64_t)INT32_MAX) {
+    if (k % 32 == 0 && groups < (int64_t)INT32_MAX - 128) {
         FastDiv d;
         d.init((uint32_t)kw);
         switch (bits) {

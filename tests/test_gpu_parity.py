@@ -117,6 +117,35 @@ def test_pack(oracle, k, bits, rows):
     g.check_guards()
 
 
+def test_pack_grid_stride(oracle):
+    # more words than one pass of the largest grid covers (8192 blocks x 512
+    # words), so waves take several chunks, and a ragged last chunk
+    rows, k, bits = 70001, 2048, 2
+    say("pack grid stride rows=%d k=%d" % (rows, k))
+    rng = np.random.default_rng(11)
+    q = rng.integers(0, 256, size=(rows, k), dtype=np.uint8)
+    want = oracle.pack(q, bits)
+    g = Guarded(want.size, torch.int32, SENT32)
+    bs.bs_pack(dev(q), g.t, rows, k, bits)
+    torch.cuda.synchronize()
+    assert np.array_equal(as_words(g.t).reshape(want.shape), want)
+    g.check_guards()
+
+
+def test_quantize_pack_grid_stride(oracle):
+    # more words than one pass of the largest grid (8192 blocks x 256 words)
+    rows, k, bits = 70001, 1024, 2
+    say("quantize_pack grid stride rows=%d k=%d" % (rows, k))
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((rows, k), dtype=np.float32)
+    want = oracle.pack(oracle.quantize(x, 1.3, bits), bits)
+    g = Guarded(want.size, torch.int32, SENT32)
+    bs.bs_quantize_pack(dev(x), g.t, rows, k, 1.3, bits)
+    torch.cuda.synchronize()
+    assert np.array_equal(as_words(g.t).reshape(want.shape), want)
+    g.check_guards()
+
+
 @pytest.mark.parametrize("k", [32, 64, 96, 100, 128, 256, 33, 4096])
 @pytest.mark.parametrize("rows", [1, 5, 130])
 @pytest.mark.parametrize("bits,enc", [(1, 0), (2, 0), (3, 0), (8, 0), (1, 1)])
