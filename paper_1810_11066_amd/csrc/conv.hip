@@ -141,7 +141,8 @@ bool conv_has_fast_path(const ConvShape& s) {
 namespace {
 
 // Pixels-on-lanes kernel for this shape, or nullptr.
-pix::PixKernelFn pix_kernel_for(const ConvShape& s, int* ocb, int* ts) {
+pix::PixKernelFn pix_kernel_for(const ConvShape& s, int* ocb, int* ts,
+                                int* tb) {
     const int64_t cw = (s.c + 31) / 32;
     if (s.abits > 4 || s.wbits > 4) return nullptr;
     if (s.kh != s.kw || s.sh != s.sw) return nullptr;
@@ -150,8 +151,10 @@ pix::PixKernelFn pix_kernel_for(const ConvShape& s, int* ocb, int* ts) {
     const int64_t npix = (int64_t)s.n * s.oh * s.ow;
     const int64_t units = (npix + 63) / 64 * (s.oc / 4);
     if (npix >= INT32_MAX || units >= INT32_MAX / 2) return nullptr;
+    // the kernel addresses activation words with 32-bit offsets
+    if ((int64_t)s.n * s.h * s.w * s.abits * cw >= INT32_MAX) return nullptr;
     return pix::pick(s.abits, s.wbits, s.bipolar_w, s.kh, s.sh, (int)cw, ocb,
-                     ts);
+                     ts, tb);
 }
 
 // Compute units of the current device (cached per device).
@@ -278,9 +281,9 @@ enum class Family { kPixels, kChannels, kGeneric };
 // channels-on-lanes, then generic; 3 and 2 try only their own family before
 // generic; 1 is generic only.
 Family choose(const ConvShape& s, int mode, pix::PixKernelFn* pfn, int* ocb,
-              int* ts) {
+              int* ts, int* tb) {
     if (mode == 0 || mode == 3) {
-        if ((*pfn = pix_kernel_for(s, ocb, ts)) != nullptr)
+        if ((*pfn = pix_kernel_for(s, ocb, ts, tb)) != nullptr)
             return Family::kPixels;
     }
     if ((mode == 0 || mode == 2) && conv_has_fast_path(s))
@@ -295,10 +298,10 @@ hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
                        const ConvOptions& opt, hipStream_t st) {
     const int mode = opt.mode;
     pix::PixKernelFn pfn = nullptr;
-    int ocb = 1, ts = 1;
+    int ocb = 1, ts = 1, tb = 1;
     dim3 grid;
     size_t lds = 0;
-    switch (choose(s, mode, &pfn, &ocb, &ts)) {
+    switch (choose(s, mode, &pfn, &ocb, &ts, &tb)) {
         case Family::kPixels: {
             pix::PixArgs g;
             plan_pix(s, pfn, opt.units_per_wave, &g, &grid, &lds);
@@ -330,21 +333,22 @@ int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
                   size_t len) {
     const int mode = opt.mode;
     pix::PixKernelFn pfn = nullptr;
-    int ocb = 1, ts = 1;
+    int ocb = 1, ts = 1, tb = 1;
     dim3 grid;
     size_t lds = 0;
     const int cw = (s.c + 31) / 32;
     const char* enc = s.bipolar_w ? "bipolar" : "unipolar";
-    switch (choose(s, mode, &pfn, &ocb, &ts)) {
+    switch (choose(s, mode, &pfn, &ocb, &ts, &tb)) {
         case Family::kPixels: {
             pix::PixArgs g;
             plan_pix(s, pfn, opt.units_per_wave, &g, &grid, &lds);
             return snprintf(buf, len,
                             "conv_pix_kernel<A=%d,W=%d,%s,K=%d,S=%d,CW=%d> "
-                            "slice=%dch x %dtaps grid=%u block=%d lds=%zu "
-                            "units=%d units_per_wave=%d",
-                            s.abits, s.wbits, enc, s.kh, s.sh, cw, ocb, ts,
-                            grid.x, pix::kBlock, lds, g.units, g.per_wave);
+                            "patch=%dtaps slice=%dch x %dtaps grid=%u "
+                            "block=%d lds=%zu units=%d units_per_wave=%d",
+                            s.abits, s.wbits, enc, s.kh, s.sh, cw, tb, ocb,
+                            ts, grid.x, pix::kBlock, lds, g.units,
+                            g.per_wave);
         }
         case Family::kChannels: {
             FastArgs g;

@@ -9,12 +9,15 @@
 // host sizes the runs so that the whole grid is resident at once and every
 // CU holds the same number of waves (no second round, no straggler CUs).
 //
-// Per group, each lane loads the packed words of its K x K input patch once
+// Per group, each lane loads the packed words of its K x K input patch
 // (vector loads; consecutive lanes read consecutive pixels), zeroes the taps
 // in the padding, and keeps the patch in VGPRs for all the channels of its
-// run.  Filter words are the same for every lane, so they are read with
-// scalar loads (a layer's filters are small and stay in the scalar cache) and
-// used as the SGPR operand of v_and_b32.
+// run.  When the whole patch does not fit (wide layers), it is taken one tap
+// block at a time -- a filter row, or a single tap -- with tap blocks as the
+// outer loop and partial sums added into the LDS output tile.  Filter words
+// are the same for every lane, so they are read with scalar loads (a layer's
+// filters are small and stay in the scalar cache) and used as the SGPR
+// operand of v_and_b32.
 //
 // Inner loop: per (tap, plane pair, word) one v_and_b32 (SGPR x VGPR) and one
 // accumulating v_bcnt_u32_b32 into one of 2 (A+W-1) per-shift accumulators
@@ -76,23 +79,35 @@ __device__ __forceinline__ void wait_scalar_loads() {
 
 typedef const uint32_t __attribute__((address_space(1))) gu32;
 
-// Static shape of the filter stream.  A filter (OHWI) is K*K*W*CW
-// contiguous words, and consecutive filters are adjacent, so the filters of a
-// channel range are one contiguous run.  Small filters are consumed OCB = 2
-// channels per slice; large ones one channel at a time, TS taps per slice.
-// Either way step s of a range reads words [s*SW, (s+1)*SW) of the run.
-template <int K, int W, int CW>
-struct Stream {
+// Static plan of a specialisation.
+//
+// Patch: TB taps of the K x K window are held in VGPRs at a time -- all of
+// them when they fit in kMaxPatchWords, else one filter row, else one tap --
+// so there are NTB = K*K / TB tap blocks.
+//
+// Filter stream: a filter (OHWI) is K*K*W*CW contiguous words and
+// consecutive filters are adjacent.  Within a tap block a channel's words are
+// TB*W*CW contiguous words.  They are consumed in SGPR slices of at most
+// kSliceWords: OCB = 2 whole filters when two fit (single tap block only),
+// else one channel and TS taps per slice (NP = TB / TS slices).
+template <int A, int W, int K, int CW>
+struct Plan {
+    static constexpr int kMaxPatchWords = 72;
     static constexpr int KK = K * K;
+    static constexpr int TB = KK * A * CW <= kMaxPatchWords ? KK
+                            : K * A * CW <= kMaxPatchWords ? K : 1;
+    static constexpr int NTB = KK / TB;
     static constexpr int FW = KK * W * CW;              // words per filter
-    static constexpr int OCB = FW * 2 <= kSliceWords ? 2 : 1;
+    static constexpr int BW = TB * W * CW;              // per tap block
+    static constexpr int OCB = NTB == 1 && BW * 2 <= kSliceWords ? 2 : 1;
     static constexpr int TS =                           // taps per slice
-        FW <= kSliceWords ? KK
-        : (KK % 3 == 0 && 3 * W * CW <= kSliceWords) ? 3 : 1;
-    static constexpr int NP = KK / TS;                  // slices per filter
+        BW <= kSliceWords ? TB
+        : (TB % 3 == 0 && 3 * W * CW <= kSliceWords) ? 3 : 1;
+    static constexpr int NP = TB / TS;                  // slices per block
     static constexpr int SW = OCB * TS * W * CW;        // words per slice
     static constexpr int STEPS = 4 / OCB * NP;          // slices per quad
-    static constexpr bool kFits = TS * W * CW <= kSliceWords;
+    static constexpr bool kFits = TS * W * CW <= kSliceWords &&
+                                  TB * A * CW <= kMaxPatchWords;
     static_assert(OCB == 1 || NP == 1, "a slice is whole filters or part of one");
     static_assert(STEPS % 2 == 0, "slice buffers alternate within a quad");
 };
@@ -140,17 +155,21 @@ __device__ __forceinline__ void flush_tile(
     }
 }
 
-// One quad of output channels: 4 / OCB batches of OCB channels, NP slices
-// each.  Slice buffer f[s & 1] holds step s; on entry f[0] holds (or is
-// receiving) step 0, and on exit f[0] is receiving the next quad's first
-// slice when `prefetch` is set.
+// One quad of output channels over tap block tb: 4 / OCB batches of OCB
+// channels, NP slices each.  `src` points at the quad's first channel's words
+// of this tap block; batch b, slice p reads src + b*OCB*FW + p*TS*W*CW.
+// Slice buffer f[s & 1] holds step s; on entry f[0] holds (or is receiving)
+// step 0, and on exit f[0] is receiving the next quad's first slice (at
+// src + 4*FW) when `prefetch` is set.  `patch` holds the block's TB taps.
 template <int A, int W, bool BIP, int K, int CW>
 __device__ __forceinline__ void compute_quad(
-    const uint32_t (&patch)[K * K][A][CW], uint32_t sa, gu32* src,
-    bool prefetch, Slice<Stream<K, W, CW>::SW> (&f)[2], uint32_t (&val)[4]) {
-    using St = Stream<K, W, CW>;
+    const uint32_t (&patch)[Plan<A, W, K, CW>::TB][A][CW], uint32_t sa,
+    gu32* src, bool prefetch, Slice<Plan<A, W, K, CW>::SW> (&f)[2],
+    uint32_t (&val)[4]) {
+    using Pl = Plan<A, W, K, CW>;
     constexpr int NS = A + W - 1;
-    constexpr int OCB = St::OCB, TS = St::TS, NP = St::NP, SW = St::SW;
+    constexpr int OCB = Pl::OCB, TS = Pl::TS, NP = Pl::NP, SW = Pl::SW;
+    constexpr int FW = Pl::FW, TSW = TS * W * CW;
 #pragma unroll
     for (int b = 0; b < 4 / OCB; ++b) {
         uint32_t acc[2][OCB][NS];
@@ -165,10 +184,13 @@ __device__ __forceinline__ void compute_quad(
         for (int p = 0; p < NP; ++p) {
             const int st = b * NP + p;
             wait_scalar_loads();
-            if (st + 1 < St::STEPS)
-                load_slice<SW>(f[(st + 1) & 1], src + (st + 1) * SW);
-            else if (prefetch)
-                load_slice<SW>(f[0], src + St::STEPS * SW);
+            if (st + 1 < Pl::STEPS) {
+                const int nb = (st + 1) / NP, np = (st + 1) % NP;
+                load_slice<SW>(f[(st + 1) & 1],
+                               src + nb * OCB * FW + np * TSW);
+            } else if (prefetch) {
+                load_slice<SW>(f[0], src + 4 * FW);
+            }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int tt = 0; tt < TS; ++tt)
@@ -210,6 +232,68 @@ __device__ __forceinline__ void compute_quad(
     }
 }
 
+// Loads the lane's input words for taps [t0, t0 + TB) of the window (zero
+// for taps in the padding) and, for bipolar weights, their popcount sum
+// sum_i 2^i popcount(a_i).
+template <int A, bool BIP, int K, int S, int CW, int TB>
+__device__ __forceinline__ uint32_t load_patch(
+    uint32_t (&patch)[TB][A][CW], const uint32_t* __restrict__ act,
+    const PixArgs& g, uint32_t img, int oy, int ox, int t0) {
+    constexpr int PW = A * CW;           // words per packed input pixel
+#pragma unroll
+    for (int tt = 0; tt < TB; ++tt) {
+        const int t = t0 + tt;
+        const int r = t / K, s = t - r * K;
+        const int iy = oy * S - g.ph + r;
+        const int ix = ox * S - g.pw + s;
+        const bool in = (unsigned)iy < (unsigned)g.h &&
+                        (unsigned)ix < (unsigned)g.w;
+        // 32-bit word offsets: the host keeps the activations below 2^31
+        // words; a padded tap reads pixel 0 and is masked below
+        const uint32_t pix =
+            in ? ((uint32_t)img * (uint32_t)g.h + (uint32_t)iy) *
+                         (uint32_t)g.w + (uint32_t)ix
+               : 0u;
+        const uint32_t* src = act + (size_t)(pix * (uint32_t)PW);
+        uint32_t wv[PW];
+        if constexpr (PW % 4 == 0) {
+#pragma unroll
+            for (int k = 0; k < PW; k += 4) {
+                const uint4 x = *reinterpret_cast<const uint4*>(src + k);
+                wv[k] = x.x; wv[k + 1] = x.y; wv[k + 2] = x.z; wv[k + 3] = x.w;
+            }
+        } else if constexpr (PW % 2 == 0) {
+#pragma unroll
+            for (int k = 0; k < PW; k += 2) {
+                const uint2 x = *reinterpret_cast<const uint2*>(src + k);
+                wv[k] = x.x; wv[k + 1] = x.y;
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < PW; ++k) wv[k] = src[k];
+        }
+        // the load is unconditional (a padded tap reads pixel 0) and its
+        // value masked, so the loads stay straight-line code
+        const uint32_t keep = in ? 0xFFFFFFFFu : 0u;
+#pragma unroll
+        for (int i = 0; i < A; ++i)
+#pragma unroll
+            for (int c = 0; c < CW; ++c)
+                patch[tt][i][c] = wv[i * CW + c] & keep;
+    }
+    uint32_t sa = 0;
+    if (BIP) {
+#pragma unroll
+        for (int tt = 0; tt < TB; ++tt)
+#pragma unroll
+            for (int i = 0; i < A; ++i)
+#pragma unroll
+                for (int c = 0; c < CW; ++c)
+                    sa += (uint32_t)__builtin_popcount(patch[tt][i][c]) << i;
+    }
+    return sa;
+}
+
 // A, W: bit-widths; BIP: bipolar weights; K: square kernel size; S: stride;
 // CW: words per bit-plane.
 template <int A, int W, bool BIP, int K, int S, int CW>
@@ -217,9 +301,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_num_sgpr(80)))
 void conv_pix_kernel(
     const uint32_t* __restrict__ act, const uint32_t* __restrict__ wts,
     int32_t* __restrict__ out, PixArgs g) {
-    using St = Stream<K, W, CW>;
-    constexpr int PW = A * CW;           // words per packed input pixel
-    constexpr int FW = St::FW;
+    using Pl = Plan<A, W, K, CW>;
+    constexpr int FW = Pl::FW, TB = Pl::TB, NTB = Pl::NTB;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(
         (int)(blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)));
@@ -237,86 +320,78 @@ void conv_pix_kernel(
         const int q1 = min(g.quads, q0 + (u_end - u));
         const int pix0 = grp * 64;
 
-        // the lane's input patch; taps in the zero padding are zero
+        // this lane's output pixel (the last pixel stands in past the end)
         const int p = pix0 + lane;
         const uint32_t pc = (uint32_t)(p < g.npix ? p : g.npix - 1);
         const uint32_t rowi = g.div_ow.div(pc);
         const int ox = (int)(pc - rowi * (uint32_t)g.ow);
         const uint32_t img = g.div_oh.div(rowi);
         const int oy = (int)(rowi - img * (uint32_t)g.oh);
-        uint32_t patch[K * K][A][CW];
-#pragma unroll
-        for (int r = 0; r < K; ++r) {
-            const int iy = oy * S - g.ph + r;
-#pragma unroll
-            for (int s = 0; s < K; ++s) {
-                const int ix = ox * S - g.pw + s;
-                const bool in = (unsigned)iy < (unsigned)g.h &&
-                                (unsigned)ix < (unsigned)g.w;
-                const int64_t pix =
-                    in ? ((int64_t)img * g.h + iy) * g.w + ix : 0;
-                const uint32_t* src = act + pix * PW;
-                uint32_t wv[PW];
-                if constexpr (PW % 4 == 0) {
-#pragma unroll
-                    for (int k = 0; k < PW; k += 4) {
-                        const uint4 x = *reinterpret_cast<const uint4*>(src + k);
-                        wv[k] = x.x; wv[k + 1] = x.y;
-                        wv[k + 2] = x.z; wv[k + 3] = x.w;
-                    }
-                } else if constexpr (PW % 2 == 0) {
-#pragma unroll
-                    for (int k = 0; k < PW; k += 2) {
-                        const uint2 x = *reinterpret_cast<const uint2*>(src + k);
-                        wv[k] = x.x; wv[k + 1] = x.y;
-                    }
-                } else {
-#pragma unroll
-                    for (int k = 0; k < PW; ++k) wv[k] = src[k];
-                }
-#pragma unroll
-                for (int i = 0; i < A; ++i)
-#pragma unroll
-                    for (int c = 0; c < CW; ++c)
-                        patch[r * K + s][i][c] = in ? wv[i * CW + c] : 0u;
-            }
-        }
-        uint32_t sa = 0;   // bipolar: sum_i 2^i popcount(a_i) over the patch
-        if (BIP) {
-#pragma unroll
-            for (int t = 0; t < K * K; ++t)
-#pragma unroll
-                for (int i = 0; i < A; ++i)
-#pragma unroll
-                    for (int c = 0; c < CW; ++c)
-                        sa += (uint32_t)__builtin_popcount(patch[t][i][c]) << i;
-        }
 
-        // channels [4 q0, 4 q1): filter run starts at channel 4 q0
-        gu32* src = gw + (size_t)(4 * q0) * FW;
-        Slice<St::SW> f[2];
-        load_slice<St::SW>(f[0], src);
-        const int nq = q1 - q0;
-        int chunk_base = 4 * q0;   // first channel held in the tile
-        int held = 0;              // quads held in the tile
-        for (int qi = 0; qi < nq; ++qi) {
-            uint32_t val[4];
-            compute_quad<A, W, BIP, K, CW>(patch, sa, src + (size_t)qi * 4 * FW,
-                                           qi + 1 < nq, f, val);
+        uint32_t patch[TB][A][CW];
+        if constexpr (NTB == 1) {
+            // whole patch: one pass over the segment's quads, the slice
+            // pipeline running across tile flushes
+            const uint32_t sa =
+                load_patch<A, BIP, K, S, CW, TB>(patch, act, g, img, oy, ox, 0);
+            gu32* src = gw + (size_t)(4 * q0) * FW;
+            Slice<Pl::SW> f[2];
+            load_slice<Pl::SW>(f[0], src);
+            const int nq = q1 - q0;
+            int chunk_base = 4 * q0;   // first channel held in the tile
+            int held = 0;              // quads held in the tile
+            for (int qi = 0; qi < nq; ++qi) {
+                uint32_t val[4];
+                compute_quad<A, W, BIP, K, CW>(patch, sa,
+                                               src + (size_t)qi * 4 * FW,
+                                               qi + 1 < nq, f, val);
 #pragma unroll
-            for (int o = 0; o < 4; ++o)
-                tile[lane * kTileStride + held * 4 + o] = val[o];
-            ++held;
-            if (held == kChunk / 4 || qi + 1 == nq) {
+                for (int o = 0; o < 4; ++o)
+                    tile[lane * kTileStride + held * 4 + o] = val[o];
+                ++held;
+                if (held == kChunk / 4 || qi + 1 == nq) {
+                    wave_lds_sync();
+                    flush_tile(tile, out, pix0, g.npix, g.oc, chunk_base,
+                               held * 4, lane);
+                    wave_lds_sync();
+                    chunk_base += held * 4;
+                    held = 0;
+                }
+            }
+        } else {
+            // tap blocks outermost, per tile chunk of up to kChunk channels;
+            // partial sums of later blocks are added in the tile
+            for (int sub = q0; sub < q1; sub += kChunk / 4) {
+                const int nq = min(kChunk / 4, q1 - sub);
+                for (int tb = 0; tb < NTB; ++tb) {
+                    const uint32_t sa = load_patch<A, BIP, K, S, CW, TB>(
+                        patch, act, g, img, oy, ox, tb * TB);
+                    gu32* src = gw + (size_t)(4 * sub) * FW + tb * Pl::BW;
+                    Slice<Pl::SW> f[2];
+                    load_slice<Pl::SW>(f[0], src);
+                    for (int qi = 0; qi < nq; ++qi) {
+                        uint32_t val[4];
+                        compute_quad<A, W, BIP, K, CW>(
+                            patch, sa, src + (size_t)qi * 4 * FW, qi + 1 < nq,
+                            f, val);
+                        // only this lane touches its tile row until the flush
+                        uint32_t* t = tile + lane * kTileStride + qi * 4;
+                        if (tb == 0) {
+#pragma unroll
+                            for (int o = 0; o < 4; ++o) t[o] = val[o];
+                        } else {
+#pragma unroll
+                            for (int o = 0; o < 4; ++o) t[o] += val[o];
+                        }
+                    }
+                }
                 wave_lds_sync();
-                flush_tile(tile, out, pix0, g.npix, g.oc, chunk_base,
-                           held * 4, lane);
+                flush_tile(tile, out, pix0, g.npix, g.oc, 4 * sub, nq * 4,
+                           lane);
                 wave_lds_sync();
-                chunk_base += held * 4;
-                held = 0;
             }
         }
-        u += nq;
+        u += q1 - q0;
     }
 }
 
@@ -324,9 +399,10 @@ using PixKernelFn = void (*)(const uint32_t*, const uint32_t*, int32_t*,
                              PixArgs);
 
 // Kernel for a supported (A, W, bipolar, K, S, CW) or nullptr; also reports
-// the output channels per filter slice (ocb) and taps per slice (ts).
+// the output channels per filter slice (ocb), taps per slice (ts) and taps
+// per tap block (tb).
 PixKernelFn pick(int a, int w, bool b, int k, int s, int cw, int* ocb,
-                 int* ts);
+                 int* ts, int* tb);
 
 }  // namespace pix
 }  // namespace bs

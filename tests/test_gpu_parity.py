@@ -287,6 +287,42 @@ def test_conv_pixel_runs(oracle, shape, run, abits, wbits, bip):
         bs.bs_set_units_per_wave(0)
 
 
+# Wide layers: the pixel kernel holds one filter row or one tap of the patch
+# at a time and adds tap-block partial sums in its LDS tile.
+WIDE_SHAPES = [
+    # n, h, w, c, oc, k, s, pad
+    (2, 6, 7, 256, 24, 3, 1, 1),
+    (1, 5, 5, 512, 20, 3, 2, 1),
+    (2, 7, 6, 256, 36, 3, 2, 0),
+    (1, 4, 9, 512, 8, 3, 1, 1),
+    (1, 9, 4, 224, 28, 3, 1, 1),     # 7 words per plane: generic fallback
+]
+
+
+@pytest.mark.parametrize("shape", WIDE_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("abits,wbits,bip", [
+    (1, 1, False), (1, 1, True), (2, 1, False), (2, 1, True), (2, 2, False),
+    (3, 3, False)])
+def test_conv_wide_shapes(oracle, shape, abits, wbits, bip):
+    n, h, w, c, oc, k, s, pad = shape
+    say("conv wide", shape, abits, wbits, bip)
+    run_conv(oracle, n, h, w, c, oc, k, k, s, s, pad, pad, abits, wbits, bip,
+             seed=hash((shape, abits, wbits, bip, 1)) % 10000, mode=3)
+
+
+@pytest.mark.parametrize("run", [1, 3, 5, 9, 100000])
+@pytest.mark.parametrize("shape", WIDE_SHAPES[:3], ids=lambda s: "x".join(map(str, s)))
+def test_conv_wide_runs(oracle, shape, run):
+    n, h, w, c, oc, k, s, pad = shape
+    say("conv wide runs", shape, run)
+    bs.bs_set_units_per_wave(run)
+    try:
+        run_conv(oracle, n, h, w, c, oc, k, k, s, s, pad, pad, 2, 1, True,
+                 seed=run + oc, mode=3)
+    finally:
+        bs.bs_set_units_per_wave(0)
+
+
 def test_conv_deterministic(oracle):
     args = (2, 14, 14, 64, 64, 3, 3, 1, 1, 1, 1, 2, 1, False)
     a = run_conv(oracle, *args, seed=5)
