@@ -142,7 +142,7 @@ namespace {
 
 // Pixels-on-lanes kernel for this shape, or nullptr.
 pix::PixKernelFn pix_kernel_for(const ConvShape& s, int* ocb, int* ts,
-                                int* tb) {
+                                int* tb, int* cb) {
     const int64_t cw = (s.c + 31) / 32;
     if (s.abits > 4 || s.wbits > 4) return nullptr;
     if (s.kh != s.kw || s.sh != s.sw) return nullptr;
@@ -154,7 +154,7 @@ pix::PixKernelFn pix_kernel_for(const ConvShape& s, int* ocb, int* ts,
     // the kernel addresses activation words with 32-bit offsets
     if ((int64_t)s.n * s.h * s.w * s.abits * cw >= INT32_MAX) return nullptr;
     return pix::pick(s.abits, s.wbits, s.bipolar_w, s.kh, s.sh, (int)cw, ocb,
-                     ts, tb);
+                     ts, tb, cb);
 }
 
 // Compute units of the current device (cached per device).
@@ -281,9 +281,9 @@ enum class Family { kPixels, kChannels, kGeneric };
 // channels-on-lanes, then generic; 3 and 2 try only their own family before
 // generic; 1 is generic only.
 Family choose(const ConvShape& s, int mode, pix::PixKernelFn* pfn, int* ocb,
-              int* ts, int* tb) {
+              int* ts, int* tb, int* cb) {
     if (mode == 0 || mode == 3) {
-        if ((*pfn = pix_kernel_for(s, ocb, ts, tb)) != nullptr)
+        if ((*pfn = pix_kernel_for(s, ocb, ts, tb, cb)) != nullptr)
             return Family::kPixels;
     }
     if ((mode == 0 || mode == 2) && conv_has_fast_path(s))
@@ -298,10 +298,10 @@ hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
                        const ConvOptions& opt, hipStream_t st) {
     const int mode = opt.mode;
     pix::PixKernelFn pfn = nullptr;
-    int ocb = 1, ts = 1, tb = 1;
+    int ocb = 1, ts = 1, tb = 1, cb = 1;
     dim3 grid;
     size_t lds = 0;
-    switch (choose(s, mode, &pfn, &ocb, &ts, &tb)) {
+    switch (choose(s, mode, &pfn, &ocb, &ts, &tb, &cb)) {
         case Family::kPixels: {
             pix::PixArgs g;
             plan_pix(s, pfn, opt.units_per_wave, &g, &grid, &lds);
@@ -333,21 +333,22 @@ int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
                   size_t len) {
     const int mode = opt.mode;
     pix::PixKernelFn pfn = nullptr;
-    int ocb = 1, ts = 1, tb = 1;
+    int ocb = 1, ts = 1, tb = 1, cb = 1;
     dim3 grid;
     size_t lds = 0;
     const int cw = (s.c + 31) / 32;
     const char* enc = s.bipolar_w ? "bipolar" : "unipolar";
-    switch (choose(s, mode, &pfn, &ocb, &ts, &tb)) {
+    switch (choose(s, mode, &pfn, &ocb, &ts, &tb, &cb)) {
         case Family::kPixels: {
             pix::PixArgs g;
             plan_pix(s, pfn, opt.units_per_wave, &g, &grid, &lds);
             return snprintf(buf, len,
                             "conv_pix_kernel<A=%d,W=%d,%s,K=%d,S=%d,CW=%d> "
-                            "patch=%dtaps slice=%dch x %dtaps grid=%u "
-                            "block=%d lds=%zu units=%d units_per_wave=%d",
-                            s.abits, s.wbits, enc, s.kh, s.sh, cw, tb, ocb,
-                            ts, grid.x, pix::kBlock, lds, g.units,
+                            "patch=%dtaps x %dwords slice=%dch x %dtaps "
+                            "grid=%u block=%d lds=%zu units=%d "
+                            "units_per_wave=%d",
+                            s.abits, s.wbits, enc, s.kh, s.sh, cw, tb, cb,
+                            ocb, ts, grid.x, pix::kBlock, lds, g.units,
                             g.per_wave);
         }
         case Family::kChannels: {

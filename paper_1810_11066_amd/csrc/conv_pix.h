@@ -81,35 +81,53 @@ typedef const uint32_t __attribute__((address_space(1))) gu32;
 
 // Static plan of a specialisation.
 //
-// Patch: TB taps of the K x K window are held in VGPRs at a time -- all of
-// them when they fit in kMaxPatchWords, else one filter row, else one tap --
-// so there are NTB = K*K / TB tap blocks.
+// Reduction blocks: the K*K taps x CW words per plane of a window are split
+// into NB = (K*K / TB) * (CW / CB) blocks of TB taps x CB words.  A block's
+// patch (TB*A*CB words per lane) is what sits in VGPRs: the whole window when
+// it fits in kMaxPatchWords, else one filter row, else one tap, else (very
+// wide 1x1 layers, dense) one tap and CB words of each plane.  With NB > 1
+// blocks are the outer loop and their partial sums are added in the LDS
+// tile; small block patches are double-buffered (the next block's words load
+// while the current block computes).
 //
-// Filter stream: a filter (OHWI) is K*K*W*CW contiguous words and
-// consecutive filters are adjacent.  Within a tap block a channel's words are
-// TB*W*CW contiguous words.  They are consumed in SGPR slices of at most
-// kSliceWords: OCB = 2 whole filters when two fit (single tap block only),
-// else one channel and TS taps per slice (NP = TB / TS slices).
+// Filter stream: a filter (OHWI) is FW = K*K*W*CW contiguous words and
+// consecutive filters are adjacent.  Within a block, a channel's words are
+// TB taps x W planes x CB words (contiguous when CB == CW).  They are consumed
+// in SGPR slices of at most kSliceWords: OCB = 2 whole filters when two fit
+// (NB == 1 only), else one channel and TS taps per slice (NP = TB / TS
+// slices per block).
 template <int A, int W, int K, int CW>
 struct Plan {
     static constexpr int kMaxPatchWords = 72;
     static constexpr int KK = K * K;
     static constexpr int TB = KK * A * CW <= kMaxPatchWords ? KK
                             : K * A * CW <= kMaxPatchWords ? K : 1;
-    static constexpr int NTB = KK / TB;
+    // words per plane in a block: all of them, or the largest power of two
+    // whose patch and one-tap slice stay small
+    static constexpr int cb_split() {
+        int cb = CW;
+        while (cb > 1 && (A * cb > 32 || W * cb > kSliceWords)) cb >>= 1;
+        return cb;
+    }
+    static constexpr int CB = TB * A * CW <= kMaxPatchWords ? CW : cb_split();
+    static constexpr int NCB = CW / CB;                 // word chunks
+    static constexpr int NB = KK / TB * NCB;            // reduction blocks
+    static constexpr int PB = TB * A * CB;              // patch words / block
+    static constexpr bool DBUF = NB > 1 && 2 * PB <= 48;
     static constexpr int FW = KK * W * CW;              // words per filter
-    static constexpr int BW = TB * W * CW;              // per tap block
-    static constexpr int OCB = NTB == 1 && BW * 2 <= kSliceWords ? 2 : 1;
+    static constexpr int BW = TB * W * CB;              // per block, channel
+    static constexpr int OCB = NB == 1 && BW * 2 <= kSliceWords ? 2 : 1;
     static constexpr int TS =                           // taps per slice
         BW <= kSliceWords ? TB
-        : (TB % 3 == 0 && 3 * W * CW <= kSliceWords) ? 3 : 1;
+        : (TB % 3 == 0 && 3 * W * CB <= kSliceWords) ? 3 : 1;
     static constexpr int NP = TB / TS;                  // slices per block
-    static constexpr int SW = OCB * TS * W * CW;        // words per slice
+    static constexpr int SW = OCB * TS * W * CB;        // words per slice
     static constexpr int STEPS = 4 / OCB * NP;          // slices per quad
-    static constexpr bool kFits = TS * W * CW <= kSliceWords &&
-                                  TB * A * CW <= kMaxPatchWords;
+    static constexpr bool kFits = TS * W * CB <= kSliceWords &&
+                                  PB <= kMaxPatchWords && CW % CB == 0;
     static_assert(OCB == 1 || NP == 1, "a slice is whole filters or part of one");
     static_assert(STEPS % 2 == 0, "slice buffers alternate within a quad");
+    static_assert(CB == CW || TB == 1, "word chunks only with one tap");
 };
 
 template <int SW>
@@ -117,10 +135,23 @@ struct Slice {
     uint32_t w[SW];
 };
 
-template <int SW>
-__device__ __forceinline__ void load_slice(Slice<SW>& s, gu32* src) {
+// One slice: OCB channels x TS taps x W planes x CB words, gathered from the
+// OHWI filters at channel stride FW, tap stride W*CW and plane stride CW
+// (compile-time offsets, so contiguous runs merge into wide scalar loads).
+template <int A, int W, int K, int CW>
+__device__ __forceinline__ void load_slice(
+    Slice<Plan<A, W, K, CW>::SW>& s, gu32* src) {
+    using Pl = Plan<A, W, K, CW>;
 #pragma unroll
-    for (int k = 0; k < SW; ++k) s.w[k] = src[k];
+    for (int o = 0; o < Pl::OCB; ++o)
+#pragma unroll
+        for (int tt = 0; tt < Pl::TS; ++tt)
+#pragma unroll
+            for (int j = 0; j < W; ++j)
+#pragma unroll
+                for (int c = 0; c < Pl::CB; ++c)
+                    s.w[((o * Pl::TS + tt) * W + j) * Pl::CB + c] =
+                        src[o * Pl::FW + (tt * W + j) * CW + c];
 }
 
 // Output tile staging.  With pixels on lanes, the NHWC output of one output
@@ -155,20 +186,22 @@ __device__ __forceinline__ void flush_tile(
     }
 }
 
-// One quad of output channels over tap block tb: 4 / OCB batches of OCB
-// channels, NP slices each.  `src` points at the quad's first channel's words
-// of this tap block; batch b, slice p reads src + b*OCB*FW + p*TS*W*CW.
+// One quad of output channels over one reduction block: 4 / OCB batches of
+// OCB channels, NP slices each.  `src` points at the quad's first channel's
+// words of this block; batch b, slice p starts at src + b*OCB*FW + p*TS*W*CW.
 // Slice buffer f[s & 1] holds step s; on entry f[0] holds (or is receiving)
-// step 0, and on exit f[0] is receiving the next quad's first slice (at
-// src + 4*FW) when `prefetch` is set.  `patch` holds the block's TB taps.
+// step 0, and on exit f[0] is receiving the slice at `next` (the next quad's
+// or block's first slice; callers with nothing left pass any valid slice
+// address, so the load never needs a branch or a null check).  `patch` holds
+// the block's TB taps x A planes x CB words.
 template <int A, int W, bool BIP, int K, int CW>
 __device__ __forceinline__ void compute_quad(
-    const uint32_t (&patch)[Plan<A, W, K, CW>::TB][A][CW], uint32_t sa,
-    gu32* src, bool prefetch, Slice<Plan<A, W, K, CW>::SW> (&f)[2],
+    const uint32_t (&patch)[Plan<A, W, K, CW>::TB][A][Plan<A, W, K, CW>::CB],
+    uint32_t sa, gu32* src, gu32* next, Slice<Plan<A, W, K, CW>::SW> (&f)[2],
     uint32_t (&val)[4]) {
     using Pl = Plan<A, W, K, CW>;
     constexpr int NS = A + W - 1;
-    constexpr int OCB = Pl::OCB, TS = Pl::TS, NP = Pl::NP, SW = Pl::SW;
+    constexpr int OCB = Pl::OCB, TS = Pl::TS, NP = Pl::NP, CB = Pl::CB;
     constexpr int FW = Pl::FW, TSW = TS * W * CW;
 #pragma unroll
     for (int b = 0; b < 4 / OCB; ++b) {
@@ -186,16 +219,16 @@ __device__ __forceinline__ void compute_quad(
             wait_scalar_loads();
             if (st + 1 < Pl::STEPS) {
                 const int nb = (st + 1) / NP, np = (st + 1) % NP;
-                load_slice<SW>(f[(st + 1) & 1],
-                               src + nb * OCB * FW + np * TSW);
-            } else if (prefetch) {
-                load_slice<SW>(f[0], src + 4 * FW);
+                load_slice<A, W, K, CW>(f[(st + 1) & 1],
+                                        src + nb * OCB * FW + np * TSW);
+            } else {
+                load_slice<A, W, K, CW>(f[0], next);
             }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int tt = 0; tt < TS; ++tt)
 #pragma unroll
-                for (int c = 0; c < CW; ++c)
+                for (int c = 0; c < CB; ++c)
 #pragma unroll
                     for (int j = 0; j < W; ++j)
 #pragma unroll
@@ -203,10 +236,10 @@ __device__ __forceinline__ void compute_quad(
 #pragma unroll
                             for (int o = 0; o < OCB; ++o) {
                                 const int t = p * TS + tt;
-                                const int h = (t * CW + c) & 1;
+                                const int h = (t * CB + c) & 1;
                                 const uint32_t x =
                                     patch[t][i][c] &
-                                    f[st & 1].w[((o * TS + tt) * W + j) * CW + c];
+                                    f[st & 1].w[((o * TS + tt) * W + j) * CB + c];
                                 if (fresh[h][o][i + j]) {
                                     bcnt_first(acc[h][o][i + j], x);
                                     fresh[h][o][i + j] = false;
@@ -232,13 +265,13 @@ __device__ __forceinline__ void compute_quad(
     }
 }
 
-// Loads the lane's input words for taps [t0, t0 + TB) of the window (zero
-// for taps in the padding) and, for bipolar weights, their popcount sum
-// sum_i 2^i popcount(a_i).
-template <int A, bool BIP, int K, int S, int CW, int TB>
-__device__ __forceinline__ uint32_t load_patch(
-    uint32_t (&patch)[TB][A][CW], const uint32_t* __restrict__ act,
-    const PixArgs& g, uint32_t img, int oy, int ox, int t0) {
+// Loads the lane's input words of one reduction block: taps [t0, t0 + TB)
+// of the window and words [c0, c0 + CB) of each of the A planes (zero for
+// taps in the padding).
+template <int A, int K, int S, int CW, int TB, int CB>
+__device__ __forceinline__ void load_patch(
+    uint32_t (&patch)[TB][A][CB], const uint32_t* __restrict__ act,
+    const PixArgs& g, uint32_t img, int oy, int ox, int t0, int c0) {
     constexpr int PW = A * CW;           // words per packed input pixel
 #pragma unroll
     for (int tt = 0; tt < TB; ++tt) {
@@ -254,44 +287,86 @@ __device__ __forceinline__ uint32_t load_patch(
             in ? ((uint32_t)img * (uint32_t)g.h + (uint32_t)iy) *
                          (uint32_t)g.w + (uint32_t)ix
                : 0u;
-        const uint32_t* src = act + (size_t)(pix * (uint32_t)PW);
-        uint32_t wv[PW];
-        if constexpr (PW % 4 == 0) {
-#pragma unroll
-            for (int k = 0; k < PW; k += 4) {
-                const uint4 x = *reinterpret_cast<const uint4*>(src + k);
-                wv[k] = x.x; wv[k + 1] = x.y; wv[k + 2] = x.z; wv[k + 3] = x.w;
-            }
-        } else if constexpr (PW % 2 == 0) {
-#pragma unroll
-            for (int k = 0; k < PW; k += 2) {
-                const uint2 x = *reinterpret_cast<const uint2*>(src + k);
-                wv[k] = x.x; wv[k + 1] = x.y;
-            }
-        } else {
-#pragma unroll
-            for (int k = 0; k < PW; ++k) wv[k] = src[k];
-        }
-        // the load is unconditional (a padded tap reads pixel 0) and its
-        // value masked, so the loads stay straight-line code
         const uint32_t keep = in ? 0xFFFFFFFFu : 0u;
+#pragma unroll
+        for (int i = 0; i < A; ++i) {
+            const uint32_t* src =
+                act + (size_t)(pix * (uint32_t)PW + (uint32_t)(i * CW + c0));
+            uint32_t wv[CB];
+            if constexpr (CB % 4 == 0) {
+#pragma unroll
+                for (int k = 0; k < CB; k += 4) {
+                    const uint4 x = *reinterpret_cast<const uint4*>(src + k);
+                    wv[k] = x.x; wv[k + 1] = x.y;
+                    wv[k + 2] = x.z; wv[k + 3] = x.w;
+                }
+            } else if constexpr (CB % 2 == 0) {
+#pragma unroll
+                for (int k = 0; k < CB; k += 2) {
+                    const uint2 x = *reinterpret_cast<const uint2*>(src + k);
+                    wv[k] = x.x; wv[k + 1] = x.y;
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < CB; ++k) wv[k] = src[k];
+            }
+#pragma unroll
+            for (int c = 0; c < CB; ++c) patch[tt][i][c] = wv[c] & keep;
+        }
+    }
+}
+
+// Bipolar correction term of a block: sum_i 2^i popcount(a_i) over its words.
+template <int A, int TB, int CB>
+__device__ __forceinline__ uint32_t patch_sum(
+    const uint32_t (&patch)[TB][A][CB]) {
+    uint32_t sa = 0;
+#pragma unroll
+    for (int tt = 0; tt < TB; ++tt)
 #pragma unroll
         for (int i = 0; i < A; ++i)
 #pragma unroll
-            for (int c = 0; c < CW; ++c)
-                patch[tt][i][c] = wv[i * CW + c] & keep;
-    }
-    uint32_t sa = 0;
-    if (BIP) {
-#pragma unroll
-        for (int tt = 0; tt < TB; ++tt)
-#pragma unroll
-            for (int i = 0; i < A; ++i)
-#pragma unroll
-                for (int c = 0; c < CW; ++c)
-                    sa += (uint32_t)__builtin_popcount(patch[tt][i][c]) << i;
-    }
+            for (int c = 0; c < CB; ++c)
+                sa += (uint32_t)__builtin_popcount(patch[tt][i][c]) << i;
     return sa;
+}
+
+// Offset of reduction block nb's words inside a filter.
+template <int A, int W, int K, int CW>
+__device__ __forceinline__ int block_offset(int nb) {
+    using Pl = Plan<A, W, K, CW>;
+    const int tb = nb / Pl::NCB, cb = nb - tb * Pl::NCB;
+    return tb * Pl::TB * W * CW + cb * Pl::CB;
+}
+
+// Quads [0, nq) of a tile chunk over reduction block nb: results written to
+// (nb == 0) or added to (nb > 0) the lane's tile row.  On exit f[0] is
+// receiving `next_block` (the next block's first slice, or any valid slice
+// address when there is none).
+template <int A, int W, bool BIP, int K, int CW>
+__device__ __forceinline__ void run_block(
+    const uint32_t (&patch)[Plan<A, W, K, CW>::TB][A][Plan<A, W, K, CW>::CB],
+    gu32* src, int nq, int nb, gu32* next_block,
+    Slice<Plan<A, W, K, CW>::SW> (&f)[2], uint32_t* row) {
+    using Pl = Plan<A, W, K, CW>;
+    const uint32_t sa =
+        BIP ? patch_sum<A, Pl::TB, Pl::CB>(patch) : 0u;
+#pragma unroll 1
+    for (int qi = 0; qi < nq; ++qi) {
+        uint32_t val[4];
+        gu32* q = src + (size_t)qi * 4 * Pl::FW;
+        compute_quad<A, W, BIP, K, CW>(
+            patch, sa, q, qi + 1 < nq ? q + 4 * Pl::FW : next_block, f, val);
+        // only this lane touches its tile row until the flush
+        uint32_t* t = row + qi * 4;
+        if (nb == 0) {
+#pragma unroll
+            for (int o = 0; o < 4; ++o) t[o] = val[o];
+        } else {
+#pragma unroll
+            for (int o = 0; o < 4; ++o) t[o] += val[o];
+        }
+    }
 }
 
 // A, W: bit-widths; BIP: bipolar weights; K: square kernel size; S: stride;
@@ -302,7 +377,7 @@ void conv_pix_kernel(
     const uint32_t* __restrict__ act, const uint32_t* __restrict__ wts,
     int32_t* __restrict__ out, PixArgs g) {
     using Pl = Plan<A, W, K, CW>;
-    constexpr int FW = Pl::FW, TB = Pl::TB, NTB = Pl::NTB;
+    constexpr int FW = Pl::FW, NB = Pl::NB;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(
         (int)(blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)));
@@ -328,23 +403,25 @@ void conv_pix_kernel(
         const uint32_t img = g.div_oh.div(rowi);
         const int oy = (int)(rowi - img * (uint32_t)g.oh);
 
-        uint32_t patch[TB][A][CW];
-        if constexpr (NTB == 1) {
+        if constexpr (NB == 1) {
             // whole patch: one pass over the segment's quads, the slice
             // pipeline running across tile flushes
+            uint32_t patch[Pl::TB][A][CW];
+            load_patch<A, K, S, CW, Pl::TB, CW>(patch, act, g, img, oy, ox, 0,
+                                               0);
             const uint32_t sa =
-                load_patch<A, BIP, K, S, CW, TB>(patch, act, g, img, oy, ox, 0);
+                BIP ? patch_sum<A, Pl::TB, CW>(patch) : 0u;
             gu32* src = gw + (size_t)(4 * q0) * FW;
             Slice<Pl::SW> f[2];
-            load_slice<Pl::SW>(f[0], src);
+            load_slice<A, W, K, CW>(f[0], src);
             const int nq = q1 - q0;
             int chunk_base = 4 * q0;   // first channel held in the tile
             int held = 0;              // quads held in the tile
             for (int qi = 0; qi < nq; ++qi) {
                 uint32_t val[4];
-                compute_quad<A, W, BIP, K, CW>(patch, sa,
-                                               src + (size_t)qi * 4 * FW,
-                                               qi + 1 < nq, f, val);
+                gu32* q = src + (size_t)qi * 4 * FW;
+                compute_quad<A, W, BIP, K, CW>(
+                    patch, sa, q, qi + 1 < nq ? q + 4 * FW : src, f, val);
 #pragma unroll
                 for (int o = 0; o < 4; ++o)
                     tile[lane * kTileStride + held * 4 + o] = val[o];
@@ -359,30 +436,49 @@ void conv_pix_kernel(
                 }
             }
         } else {
-            // tap blocks outermost, per tile chunk of up to kChunk channels;
-            // partial sums of later blocks are added in the tile
+            // reduction blocks outermost, per tile chunk of up to kChunk
+            // channels; partial sums of later blocks are added in the tile
+            using Patch = uint32_t[Pl::TB][A][Pl::CB];
+            uint32_t* row = tile + lane * kTileStride;
             for (int sub = q0; sub < q1; sub += kChunk / 4) {
                 const int nq = min(kChunk / 4, q1 - sub);
-                for (int tb = 0; tb < NTB; ++tb) {
-                    const uint32_t sa = load_patch<A, BIP, K, S, CW, TB>(
-                        patch, act, g, img, oy, ox, tb * TB);
-                    gu32* src = gw + (size_t)(4 * sub) * FW + tb * Pl::BW;
-                    Slice<Pl::SW> f[2];
-                    load_slice<Pl::SW>(f[0], src);
-                    for (int qi = 0; qi < nq; ++qi) {
-                        uint32_t val[4];
-                        compute_quad<A, W, BIP, K, CW>(
-                            patch, sa, src + (size_t)qi * 4 * FW, qi + 1 < nq,
-                            f, val);
-                        // only this lane touches its tile row until the flush
-                        uint32_t* t = tile + lane * kTileStride + qi * 4;
-                        if (tb == 0) {
-#pragma unroll
-                            for (int o = 0; o < 4; ++o) t[o] = val[o];
-                        } else {
-#pragma unroll
-                            for (int o = 0; o < 4; ++o) t[o] += val[o];
+                gu32* qsrc = gw + (size_t)(4 * sub) * FW;
+                Slice<Pl::SW> f[2];
+                load_slice<A, W, K, CW>(f[0], qsrc);
+                auto blk = [&](int nb) {
+                    return qsrc + block_offset<A, W, K, CW>(nb);
+                };
+                auto load_block = [&](Patch& pt, int nb) {
+                    const int tb = nb / Pl::NCB;
+                    load_patch<A, K, S, CW, Pl::TB, Pl::CB>(
+                        pt, act, g, img, oy, ox, tb * Pl::TB,
+                        (nb - tb * Pl::NCB) * Pl::CB);
+                };
+                if constexpr (Pl::DBUF) {
+                    // block nb + 1 loads while block nb computes
+                    Patch pa, pb;
+                    load_block(pa, 0);
+#pragma unroll 1
+                    for (int nb = 0; nb < NB; nb += 2) {
+                        if (nb + 1 < NB) load_block(pb, nb + 1);
+                        run_block<A, W, BIP, K, CW>(
+                            pa, blk(nb), nq, nb,
+                            nb + 1 < NB ? blk(nb + 1) : qsrc, f, row);
+                        if (nb + 1 < NB) {
+                            if (nb + 2 < NB) load_block(pa, nb + 2);
+                            run_block<A, W, BIP, K, CW>(
+                                pb, blk(nb + 1), nq, nb + 1,
+                                nb + 2 < NB ? blk(nb + 2) : qsrc, f, row);
                         }
+                    }
+                } else {
+                    Patch pa;
+#pragma unroll 1
+                    for (int nb = 0; nb < NB; ++nb) {
+                        load_block(pa, nb);
+                        run_block<A, W, BIP, K, CW>(
+                            pa, blk(nb), nq, nb,
+                            nb + 1 < NB ? blk(nb + 1) : qsrc, f, row);
                     }
                 }
                 wave_lds_sync();
@@ -399,10 +495,10 @@ using PixKernelFn = void (*)(const uint32_t*, const uint32_t*, int32_t*,
                              PixArgs);
 
 // Kernel for a supported (A, W, bipolar, K, S, CW) or nullptr; also reports
-// the output channels per filter slice (ocb), taps per slice (ts) and taps
-// per tap block (tb).
+// its plan: output channels per filter slice (ocb), taps per slice (ts),
+// taps and words per plane of a reduction block (tb, cb).
 PixKernelFn pick(int a, int w, bool b, int k, int s, int cw, int* ocb,
-                 int* ts, int* tb);
+                 int* ts, int* tb, int* cb);
 
 }  // namespace pix
 }  // namespace bs

@@ -193,7 +193,7 @@ def test_describe_names_the_kernel_each_mode_picks(lib):
     p = params(n=64, h=56, w=56, c=64, oc=64)
     try:
         assert bs.bs_conv2d_describe(p).startswith(
-            "conv_pix_kernel<A=2,W=1,unipolar,K=3,S=1,CW=2> patch=9taps "
+            "conv_pix_kernel<A=2,W=1,unipolar,K=3,S=1,CW=2> patch=9taps x 2words "
             "slice=1ch x 9taps")
         bs.bs_set_kernel_mode(2)
         assert bs.bs_conv2d_describe(p).startswith(

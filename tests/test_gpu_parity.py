@@ -323,6 +323,31 @@ def test_conv_wide_runs(oracle, shape, run):
         bs.bs_set_units_per_wave(0)
 
 
+# 1x1 layers and dense rows too wide for one patch: the reduction is split
+# into blocks of 8 or 16 words per plane (double-buffered patch blocks).
+@pytest.mark.parametrize("m,n,k", [(64, 8, 4096), (100, 20, 2048),
+                                   (130, 12, 1024), (70, 36, 4096)])
+@pytest.mark.parametrize("abits,wbits,bip", [(2, 2, False), (1, 1, True),
+                                             (2, 1, False), (3, 3, False)])
+def test_dense_word_blocks(oracle, m, n, k, abits, wbits, bip):
+    say("dense word blocks", m, n, k, abits, wbits, bip)
+    rng = np.random.default_rng(m * 31 + n + k + abits)
+    a = rng.integers(0, 1 << abits, size=(m, k), dtype=np.uint8)
+    w = rng.integers(0, 1 << wbits, size=(n, k), dtype=np.uint8)
+    ap, wp = oracle.pack(a, abits), oracle.pack(w, wbits)
+    want = oracle.dense(ap, wp, m, n, k, abits, wbits, int(bip))
+    g = Guarded(m * n, torch.int32, SENT32)
+    bs.bs_set_kernel_mode(3)
+    try:
+        bs.bs_dense(m, n, k, abits, wbits, int(bip), dev(ap.view(np.int32)),
+                    dev(wp.view(np.int32)), g.t)
+    finally:
+        bs.bs_set_kernel_mode(0)
+    torch.cuda.synchronize()
+    assert np.array_equal(g.t.cpu().numpy().reshape(m, n), want)
+    g.check_guards()
+
+
 def test_conv_deterministic(oracle):
     args = (2, 14, 14, 64, 64, 3, 3, 1, 1, 1, 1, 2, 1, False)
     a = run_conv(oracle, *args, seed=5)
