@@ -41,7 +41,11 @@ CONV_SOURCES = ["paper_1810_11066_amd/csrc/bs_internal.h",
                 "paper_1810_11066_amd/csrc/conv.hip",
                 "paper_1810_11066_amd/csrc/conv_fast.h",
                 "paper_1810_11066_amd/csrc/conv_pix.h",
-                "paper_1810_11066_amd/csrc/conv_pix.hip"]
+                "paper_1810_11066_amd/csrc/conv_pix.hip",
+                "paper_1810_11066_amd/csrc/conv_pix_a1.hip",
+                "paper_1810_11066_amd/csrc/conv_pix_a2.hip",
+                "paper_1810_11066_amd/csrc/conv_pix_a3.hip",
+                "paper_1810_11066_amd/csrc/conv_pix_a4.hip"]
 
 
 def popcount_roofline_tops(abits: int, wbits: int) -> float:
@@ -293,6 +297,10 @@ def main() -> int:
                     help="workload: 2 (default) is the headline ResNet-18 "
                          "layer-2 A2W1 line; 1, 3, 4, 5 print one line per "
                          "case of that workload")
+    ap.add_argument("--sweep", action="store_true",
+                    help="bit-width sweep A1-4 x W1-4 on ResNet-18 layer 9 "
+                         "(batch 128): one line per pair, then a summary "
+                         "line with the time ratios the paper reports")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -311,16 +319,30 @@ def main() -> int:
     torch.cuda.set_device(0)
     bs.load_library()
 
-    if args.config != 2:
-        cases = {1: lambda: [wl.config1()], 3: lambda: [wl.config3()],
-                 4: wl.config4, 5: wl.config5}[args.config]()
+    if args.sweep or args.config != 2:
+        if args.sweep:
+            cases = wl.bitwidth_sweep()
+        else:
+            cases = {1: lambda: [wl.config1()], 3: lambda: [wl.config3()],
+                     4: wl.config4, 5: wl.config5}[args.config]()
+        times = {}
         for case in cases:
             sets, step, _, _, describe, _ = prepare(case, args.sets, bs,
                                                     torch, np)
             m = measure(step, describe, args.steps, args.warmup, torch)
+            times[(case.abits, case.wbits)] = m.main_ms
             print(json.dumps(case_line(case, m, args)), flush=True)
             del sets
             torch.cuda.empty_cache()
+        if args.sweep:
+            # the paper's limit study quotes W1A1 against W4A4 and W2A2
+            # against W1A4 (activation width A, weight width W)
+            print(json.dumps({
+                "sweep": "resnet18_L9_b128 conv kernel time ratios",
+                "A4W4_over_A1W1": round(times[(4, 4)] / times[(1, 1)], 2),
+                "A4W1_over_A2W2": round(times[(4, 1)] / times[(2, 2)], 3),
+                "kernel_ms": {"A%dW%d" % k: round(v, 5)
+                              for k, v in sorted(times.items())}}))
         return 0
 
     case = wl.config2(batch=args.batch)

@@ -141,8 +141,7 @@ bool conv_has_fast_path(const ConvShape& s) {
 namespace {
 
 // Pixels-on-lanes kernel for this shape, or nullptr.
-pix::PixKernelFn pix_kernel_for(const ConvShape& s, int* ocb, int* ts,
-                                int* tb, int* cb) {
+pix::PixKernelFn pix_kernel_for(const ConvShape& s, pix::PlanInfo* info) {
     const int64_t cw = (s.c + 31) / 32;
     if (s.abits > 4 || s.wbits > 4) return nullptr;
     if (s.kh != s.kw || s.sh != s.sw) return nullptr;
@@ -153,8 +152,7 @@ pix::PixKernelFn pix_kernel_for(const ConvShape& s, int* ocb, int* ts,
     if (npix >= INT32_MAX || units >= INT32_MAX / 2) return nullptr;
     // the kernel addresses activation words with 32-bit offsets
     if ((int64_t)s.n * s.h * s.w * s.abits * cw >= INT32_MAX) return nullptr;
-    return pix::pick(s.abits, s.wbits, s.bipolar_w, s.kh, s.sh, (int)cw, ocb,
-                     ts, tb, cb);
+    return pix::pick(s.abits, s.wbits, s.bipolar_w, s.kh, s.sh, (int)cw, info);
 }
 
 // Compute units of the current device (cached per device).
@@ -280,10 +278,10 @@ enum class Family { kPixels, kChannels, kGeneric };
 // The kernel family a call takes: mode 0 tries pixels-on-lanes, then
 // channels-on-lanes, then generic; 3 and 2 try only their own family before
 // generic; 1 is generic only.
-Family choose(const ConvShape& s, int mode, pix::PixKernelFn* pfn, int* ocb,
-              int* ts, int* tb, int* cb) {
+Family choose(const ConvShape& s, int mode, pix::PixKernelFn* pfn,
+              pix::PlanInfo* info) {
     if (mode == 0 || mode == 3) {
-        if ((*pfn = pix_kernel_for(s, ocb, ts, tb, cb)) != nullptr)
+        if ((*pfn = pix_kernel_for(s, info)) != nullptr)
             return Family::kPixels;
     }
     if ((mode == 0 || mode == 2) && conv_has_fast_path(s))
@@ -298,10 +296,10 @@ hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
                        const ConvOptions& opt, hipStream_t st) {
     const int mode = opt.mode;
     pix::PixKernelFn pfn = nullptr;
-    int ocb = 1, ts = 1, tb = 1, cb = 1;
+    pix::PlanInfo info{};
     dim3 grid;
     size_t lds = 0;
-    switch (choose(s, mode, &pfn, &ocb, &ts, &tb, &cb)) {
+    switch (choose(s, mode, &pfn, &info)) {
         case Family::kPixels: {
             pix::PixArgs g;
             plan_pix(s, pfn, opt.units_per_wave, &g, &grid, &lds);
@@ -333,12 +331,12 @@ int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
                   size_t len) {
     const int mode = opt.mode;
     pix::PixKernelFn pfn = nullptr;
-    int ocb = 1, ts = 1, tb = 1, cb = 1;
+    pix::PlanInfo info{};
     dim3 grid;
     size_t lds = 0;
     const int cw = (s.c + 31) / 32;
     const char* enc = s.bipolar_w ? "bipolar" : "unipolar";
-    switch (choose(s, mode, &pfn, &ocb, &ts, &tb, &cb)) {
+    switch (choose(s, mode, &pfn, &info)) {
         case Family::kPixels: {
             pix::PixArgs g;
             plan_pix(s, pfn, opt.units_per_wave, &g, &grid, &lds);
@@ -347,9 +345,9 @@ int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
                             "patch=%dtaps x %dwords slice=%dch x %dtaps "
                             "grid=%u block=%d lds=%zu units=%d "
                             "units_per_wave=%d",
-                            s.abits, s.wbits, enc, s.kh, s.sh, cw, tb, cb,
-                            ocb, ts, grid.x, pix::kBlock, lds, g.units,
-                            g.per_wave);
+                            s.abits, s.wbits, enc, s.kh, s.sh, cw, info.tb,
+                            info.cb, info.ocb, info.ts, grid.x, pix::kBlock,
+                            lds, g.units, g.per_wave);
         }
         case Family::kChannels: {
             FastArgs g;

@@ -100,7 +100,11 @@ template <int A, int W, int K, int CW>
 struct Plan {
     static constexpr int kMaxPatchWords = 72;
     static constexpr int KK = K * K;
-    static constexpr int TB = KK * A * CW <= kMaxPatchWords ? KK
+    // one tap's filter words must fit a slice, else taps go one at a time
+    // and the words of each plane are split as well
+    static constexpr bool kWideTap = W * CW > kSliceWords;
+    static constexpr int TB = kWideTap ? 1
+                            : KK * A * CW <= kMaxPatchWords ? KK
                             : K * A * CW <= kMaxPatchWords ? K : 1;
     // words per plane in a block: all of them, or the largest power of two
     // whose patch and one-tap slice stay small
@@ -109,7 +113,8 @@ struct Plan {
         while (cb > 1 && (A * cb > 32 || W * cb > kSliceWords)) cb >>= 1;
         return cb;
     }
-    static constexpr int CB = TB * A * CW <= kMaxPatchWords ? CW : cb_split();
+    static constexpr int CB =
+        !kWideTap && TB * A * CW <= kMaxPatchWords ? CW : cb_split();
     static constexpr int NCB = CW / CB;                 // word chunks
     static constexpr int NB = KK / TB * NCB;            // reduction blocks
     static constexpr int PB = TB * A * CB;              // patch words / block
@@ -494,11 +499,82 @@ void conv_pix_kernel(
 using PixKernelFn = void (*)(const uint32_t*, const uint32_t*, int32_t*,
                              PixArgs);
 
-// Kernel for a supported (A, W, bipolar, K, S, CW) or nullptr; also reports
-// its plan: output channels per filter slice (ocb), taps per slice (ts),
-// taps and words per plane of a reduction block (tb, cb).
-PixKernelFn pick(int a, int w, bool b, int k, int s, int cw, int* ocb,
-                 int* ts, int* tb, int* cb);
+// Plan of a kernel as the host reports it.
+struct PlanInfo {
+    int ocb, ts, tb, cb;
+};
+
+// Kernel for a supported (A, W, bipolar, K, S, CW) or nullptr, with its plan
+// (output channels per filter slice, taps per slice, taps and words per
+// plane of a reduction block).  pick_a<A> is defined for A = 1..4 in
+// conv_pix_a<A>.hip, so the specialisations compile in parallel.
+PixKernelFn pick(int a, int w, bool b, int k, int s, int cw, PlanInfo* info);
+template <int A>
+PixKernelFn pick_a(int w, bool b, int k, int s, int cw, PlanInfo* info);
+template <> PixKernelFn pick_a<1>(int, bool, int, int, int, PlanInfo*);
+template <> PixKernelFn pick_a<2>(int, bool, int, int, int, PlanInfo*);
+template <> PixKernelFn pick_a<3>(int, bool, int, int, int, PlanInfo*);
+template <> PixKernelFn pick_a<4>(int, bool, int, int, int, PlanInfo*);
+
+// Specialisations for activation width A (included by conv_pix_a<A>.hip).
+template <int A, int W, bool B, int K, int S, int CW>
+PixKernelFn pick_kscw(PlanInfo* info) {
+    using Pl = Plan<A, W, K, CW>;
+    if constexpr (!Pl::kFits) {
+        return nullptr;
+    } else {
+        info->ocb = Pl::OCB;
+        info->ts = Pl::TS;
+        info->tb = Pl::TB;
+        info->cb = Pl::CB;
+        return conv_pix_kernel<A, W, B, K, S, CW>;
+    }
+}
+
+// Words per plane: 1..16 for 3x3 windows; 1x1 windows (and dense, a 1x1
+// conv) up to 128 words = 4096 input channels.
+template <int A, int W, bool B, int K, int S>
+PixKernelFn pick_cw(int cw, PlanInfo* info) {
+    switch (cw) {
+        case 1: return pick_kscw<A, W, B, K, S, 1>(info);
+        case 2: return pick_kscw<A, W, B, K, S, 2>(info);
+        case 4: return pick_kscw<A, W, B, K, S, 4>(info);
+        case 8: return pick_kscw<A, W, B, K, S, 8>(info);
+        case 16: return pick_kscw<A, W, B, K, S, 16>(info);
+        default: break;
+    }
+    if constexpr (K == 1) {
+        switch (cw) {
+            case 32: return pick_kscw<A, W, B, K, S, 32>(info);
+            case 64: return pick_kscw<A, W, B, K, S, 64>(info);
+            case 128: return pick_kscw<A, W, B, K, S, 128>(info);
+            default: break;
+        }
+    }
+    return nullptr;
+}
+
+template <int A, int W, bool B>
+PixKernelFn pick_ks(int k, int s, int cw, PlanInfo* info) {
+    if (k == 1) return s == 1 ? pick_cw<A, W, B, 1, 1>(cw, info)
+                              : pick_cw<A, W, B, 1, 2>(cw, info);
+    if (k == 3) return s == 1 ? pick_cw<A, W, B, 3, 1>(cw, info)
+                              : pick_cw<A, W, B, 3, 2>(cw, info);
+    return nullptr;
+}
+
+// Every weight width 1..4 with unipolar weights; bipolar weights at W = 1.
+template <int A>
+PixKernelFn pick_for_a(int w, bool b, int k, int s, int cw, PlanInfo* info) {
+    if (b) return w == 1 ? pick_ks<A, 1, true>(k, s, cw, info) : nullptr;
+    switch (w) {
+        case 1: return pick_ks<A, 1, false>(k, s, cw, info);
+        case 2: return pick_ks<A, 2, false>(k, s, cw, info);
+        case 3: return pick_ks<A, 3, false>(k, s, cw, info);
+        case 4: return pick_ks<A, 4, false>(k, s, cw, info);
+        default: return nullptr;
+    }
+}
 
 }  // namespace pix
 }  // namespace bs

@@ -1,0 +1,13 @@
+// Pixels-on-lanes conv specialisations for 2-bit activations.
+#include "conv_pix.h"
+
+namespace bs {
+namespace pix {
+
+template <>
+PixKernelFn pick_a<2>(int w, bool b, int k, int s, int cw, PlanInfo* info) {
+    return pick_for_a<2>(w, b, k, s, cw, info);
+}
+
+}  // namespace pix
+}  // namespace bs

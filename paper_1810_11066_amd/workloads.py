@@ -182,3 +182,17 @@ def config5(batch: int = 128) -> List[ConvCase]:
         out.append(ConvCase("a3w3_" + tag, batch, hw, hw, c, oc, k, s, p,
                             3, 3, seed=seed_for(5, 2 * sub + 1)))
     return out
+
+
+def bitwidth_sweep(batch: int = 128) -> List[ConvCase]:
+    """The limit study of Sec. 6.2.2 on ResNet-18 layer 9 (Table 1: 14x14,
+    256 -> 256 channels, 3x3, stride 1, pad 1): every activation width 1..4
+    with every unipolar weight width 1..4, codes uniform over their range."""
+    out = []
+    for abits in range(1, 5):
+        for wbits in range(1, 5):
+            out.append(ConvCase(
+                "resnet18_L9_b%d_A%dW%d" % (batch, abits, wbits), batch, 14,
+                14, 256, 256, 3, 1, 1, abits, wbits,
+                seed=seed_for(6, 10 * abits + wbits)))
+    return out

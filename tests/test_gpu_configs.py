@@ -150,3 +150,9 @@ def test_config4_resnet18_layer(oracle, case):
 def test_config5_bipolar_a3w3(oracle, case):
     say(case.name)
     check_sampled(oracle, case)
+
+
+@pytest.mark.parametrize("case", wl.bitwidth_sweep(), ids=lambda c: c.name)
+def test_bitwidth_sweep_layer9(oracle, case):
+    say(case.name)
+    check_sampled(oracle, case, n_random=4096)
