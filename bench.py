@@ -280,6 +280,77 @@ def case_line(case, m, args):
     }
 
 
+INT8_MFMA_PEAK_TOPS = 5000.0   # dense int8 MFMA, MI355X
+
+
+def int8_baseline_lines(args, bs, torch, np, wl) -> int:
+    """The int8 matrix-core comparison (a baseline, not the bitserial path):
+    config 2 as im2col + int8 GEMM, config 3 as one int8 GEMM, each timed
+    with per-launch events and checked equal to the bitserial result."""
+    from paper_1810_11066_amd import int8_baseline as ib
+
+    def timed(fn, steps):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True),
+               torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for e in ev:
+            e[0].record()
+            fn()
+            e[1].record()
+        torch.cuda.synchronize()
+        return sum(a.elapsed_time(b) for a, b in ev) / steps
+
+    ok_all = True
+    for case in (wl.config2(), wl.config3()):
+        dense = isinstance(case, wl.DenseCase)
+        sets, step, params, w_packed, describe, _ = prepare(case, 1, bs,
+                                                            torch, np)
+        m = measure(step, describe, args.steps, args.warmup, torch)
+        x = torch.from_numpy(case.activations()).cuda()
+        wq = torch.from_numpy(case.weights()).cuda()
+        x8, w8 = x.to(torch.int8), wq.to(torch.int8)
+        if dense:
+            wt = w8.t().contiguous()
+            gemm_ms = timed(lambda: torch._int_mm(x8, wt), args.steps)
+            im2col_ms = 0.0
+            ref = ib.dense_int8(x, wq)
+        else:
+            k = case.k
+            cols = ib.im2col_nhwc(x8, k, case.stride, case.pad).contiguous()
+            wt = w8.reshape(case.oc, -1).t().contiguous()
+            im2col_ms = timed(lambda: ib.im2col_nhwc(
+                x8, k, case.stride, case.pad).contiguous(), args.steps)
+            gemm_ms = timed(lambda: torch._int_mm(cols, wt), args.steps)
+            ref = ib.conv2d_int8(x, wq, case.stride, case.pad)
+        step(0)
+        torch.cuda.synchronize()
+        same = bool(torch.equal(ref.reshape(-1), sets[0][2].reshape(-1)))
+        ok_all &= same
+        ops = 2 * case.macs
+        print(json.dumps({
+            "baseline": ib.LABEL,
+            "workload": case.name,
+            "int8_gemm_ms": round(gemm_ms, 5),
+            "int8_im2col_ms": round(im2col_ms, 5),
+            "int8_total_ms": round(gemm_ms + im2col_ms, 5),
+            "int8_gemm_tops": round(ops / (gemm_ms * 1e-3) / 1e12, 1),
+            "int8_gemm_frac_of_mfma_peak": round(
+                ops / (gemm_ms * 1e-3) / 1e12 / INT8_MFMA_PEAK_TOPS, 4),
+            "bitserial_kernel_ms": round(m.main_ms, 5),
+            "bitserial_step_ms": round(m.ms_step, 5),
+            "bitserial_kernel_tops": round(ops / (m.main_ms * 1e-3) / 1e12,
+                                           1),
+            "int8_gemm_over_bitserial_kernel_time": round(
+                gemm_ms / m.main_ms, 3),
+            "outputs_equal": same,
+        }), flush=True)
+        del sets
+        torch.cuda.empty_cache()
+    return 0 if ok_all else 1
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -297,6 +368,10 @@ def main() -> int:
                     help="workload: 2 (default) is the headline ResNet-18 "
                          "layer-2 A2W1 line; 1, 3, 4, 5 print one line per "
                          "case of that workload")
+    ap.add_argument("--int8-baseline", action="store_true",
+                    help="time the labelled int8 matrix-core baseline "
+                         "(im2col + int8 GEMM) on configs 2 and 3 next to "
+                         "the bitserial kernels, checking equal outputs")
     ap.add_argument("--sweep", action="store_true",
                     help="bit-width sweep A1-4 x W1-4 on ResNet-18 layer 9 "
                          "(batch 128): one line per pair, then a summary "
@@ -318,6 +393,9 @@ def main() -> int:
         return 1
     torch.cuda.set_device(0)
     bs.load_library()
+
+    if args.int8_baseline:
+        return int8_baseline_lines(args, bs, torch, np, wl)
 
     if args.sweep or args.config != 2:
         if args.sweep:

@@ -269,3 +269,22 @@ def test_fullsize_layer_shapes(oracle, case):
                                            case.wenc == wl.BIPOLAR),
                           case.stride, case.pad)
     assert np.array_equal(got.astype(np.int64), want)
+
+
+def test_int8_baseline_matches_oracle(oracle):
+    # the labelled int8 comparison path (im2col + integer GEMM) computes the
+    # same exact integers; checked here with torch's CPU integer GEMM
+    import torch
+    from paper_1810_11066_amd import int8_baseline as ib
+    rng = np.random.default_rng(77)
+    for (n, h, w, c, oc, k, s, p, ab, wb) in [(2, 9, 7, 64, 24, 3, 2, 1, 2, 1),
+                                              (1, 6, 6, 96, 16, 3, 1, 1, 3, 3),
+                                              (1, 5, 8, 64, 8, 1, 1, 0, 4, 2)]:
+        a = rng.integers(0, 1 << ab, size=(n, h, w, c), dtype=np.uint8)
+        wq = rng.integers(0, 1 << wb, size=(oc, k, k, c), dtype=np.uint8)
+        got = ib.conv2d_int8(torch.from_numpy(a), torch.from_numpy(wq), s,
+                             p).numpy()
+        want = oracle.conv2d(oracle.conv_params(n, h, w, c, oc, k, k, s, p,
+                                                ab, wb),
+                             oracle.pack(a, ab), oracle.pack(wq, wb))
+        assert np.array_equal(got, want)
