@@ -120,6 +120,25 @@ bs_status bs_conv2d(const bs_conv2d_params *p, const uint32_t *act_packed,
                     const uint32_t *w_packed, int32_t *out,
                     bs_stream_t stream);
 
+/* Bitserial conv2d whose result is requantized and bit-packed as the next
+ * layer's activations (layer chaining, toward the end-to-end low-precision
+ * inference of Sec. 7): the int32 result v of bs_conv2d for each output is
+ * converted to float32, quantized as bs_quantize does (unipolar,
+ * q = clamp(round_half_even(fl32(v * out_scale)), 0, 2^out_bits - 1)) and
+ * packed as bs_pack does, along the output channels:
+ *   out_packed: [n][oh][ow][out_bits][ceil(oc/32)] uint32, tail bits zero.
+ * Equals bs_conv2d followed by bs_quantize_pack of its output converted to
+ * float32 (round to nearest even; exact while |v| <= 2^24), without ever
+ * writing the int32 result.  Device pointers as in bs_conv2d; out_packed
+ * must not alias the inputs.
+ * Errors: as bs_conv2d; BS_ERR_INVALID_ARG for out_bits outside 1..8 or a
+ * non-finite or non-positive out_scale. */
+bs_status bs_conv2d_requant(const bs_conv2d_params *p,
+                            const uint32_t *act_packed,
+                            const uint32_t *w_packed, float out_scale,
+                            int out_bits, uint32_t *out_packed,
+                            bs_stream_t stream);
+
 /* Describes, as text, the kernel and launch configuration that bs_conv2d
  * would use for p under the calling thread's kernel mode (template
  * parameters, grid, block, LDS bytes).  Writes at most len bytes including

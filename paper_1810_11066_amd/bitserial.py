@@ -37,7 +37,8 @@ UNIPOLAR = 0
 BIPOLAR = 1
 
 EXPORTED = ("bs_packed_words", "bs_quantize", "bs_pack", "bs_quantize_pack",
-            "bs_conv2d_out_shape", "bs_conv2d", "bs_conv2d_describe",
+            "bs_conv2d_out_shape", "bs_conv2d", "bs_conv2d_requant",
+            "bs_conv2d_describe",
             "bs_dense", "bs_status_string",
             "bs_last_error", "bs_set_kernel_mode", "bs_set_units_per_wave",
             "bs_abi_version")
@@ -82,6 +83,8 @@ def load_library():
                                          ctypes.POINTER(ctypes.c_int32),
                                          ctypes.POINTER(ctypes.c_int32)]),
             "bs_conv2d": (ci, [ctypes.POINTER(ConvParams), P, P, P, P]),
+            "bs_conv2d_requant": (ci, [ctypes.POINTER(ConvParams), P, P, cf,
+                                       ci, P, P]),
             "bs_conv2d_describe": (ci, [ctypes.POINTER(ConvParams),
                                         ctypes.c_char_p, ctypes.c_int32]),
             "bs_dense": (ci, [i64, i64, i64, ci, ci, ci, P, P, P, P]),
@@ -163,6 +166,37 @@ def bs_conv2d_out_shape(p: ConvParams):
                                               ctypes.byref(oh),
                                               ctypes.byref(ow)))
     return oh.value, ow.value
+
+
+def bs_conv2d_requant(p: ConvParams, act_packed: torch.Tensor,
+                      w_packed: torch.Tensor, out_scale: float, out_bits: int,
+                      out_packed: torch.Tensor, stream=None) -> None:
+    """bs_conv2d with its result requantized to out_bits and bit-packed as
+    [n][oh][ow][out_bits][ceil(oc/32)] words (the next layer's input)."""
+    lib = load_library()
+    oh, ow = bs_conv2d_out_shape(p)
+    cw = words(p.c)
+    _check(lib.bs_conv2d_requant(
+        ctypes.byref(p),
+        _dev(act_packed, "act_packed", torch.int32,
+             p.n * p.h * p.w * p.abits * cw),
+        _dev(w_packed, "w_packed", torch.int32,
+             p.oc * p.kh * p.kw * p.wbits * cw),
+        float(out_scale), int(out_bits),
+        _dev(out_packed, "out_packed", torch.int32,
+             p.n * oh * ow * out_bits * words(p.oc)),
+        _stream(stream)))
+
+
+def conv2d_requant(spec: "Conv2dSpec", act_packed: torch.Tensor,
+                   w_packed: torch.Tensor, out_scale: float,
+                   out_bits: int) -> torch.Tensor:
+    p = spec.params()
+    oh, ow = bs_conv2d_out_shape(p)
+    out = torch.empty((p.n, oh, ow, out_bits, words(p.oc)), dtype=torch.int32,
+                      device=act_packed.device)
+    bs_conv2d_requant(p, act_packed, w_packed, out_scale, out_bits, out)
+    return out
 
 
 def bs_conv2d_describe(p: ConvParams) -> str:

@@ -118,7 +118,7 @@ bs_status check_conv(const bs_conv2d_params* p, bs::ConvShape* s) {
 
 extern "C" {
 
-int bs_abi_version(void) { return 101; }
+int bs_abi_version(void) { return 102; }
 
 int64_t bs_packed_words(int64_t k) { return k <= 0 ? 0 : (k + 31) / 32; }
 
@@ -225,6 +225,31 @@ bs_status bs_conv2d(const bs_conv2d_params* p, const uint32_t* act_packed,
     return from_hip(bs::launch_conv(s, act_packed, w_packed, out,
                                     g_conv_opt, (hipStream_t)stream),
                     "bs_conv2d launch");
+}
+
+bs_status bs_conv2d_requant(const bs_conv2d_params* p,
+                            const uint32_t* act_packed,
+                            const uint32_t* w_packed, float out_scale,
+                            int out_bits, uint32_t* out_packed,
+                            bs_stream_t stream) {
+    bs_status st;
+    if ((st = check_ptr(act_packed, "act_packed")) != BS_OK) return st;
+    if ((st = check_ptr(w_packed, "w_packed")) != BS_OK) return st;
+    if ((st = check_ptr(out_packed, "out_packed")) != BS_OK) return st;
+    if ((st = check_bits(out_bits, "out_bits")) != BS_OK) return st;
+    if ((st = check_scale_enc(out_scale, out_bits, BS_UNIPOLAR)) != BS_OK)
+        return st;
+    bs::ConvShape s;
+    if ((st = check_conv(p, &s)) != BS_OK) return st;
+    if ((int64_t)s.n * s.oh * s.ow * ((s.oc + 31) / 32) >= INT32_MAX)
+        return fail(BS_ERR_UNSUPPORTED, "output too large");
+    bs::Requant rq;
+    rq.scale = out_scale;
+    rq.bits = out_bits;
+    return from_hip(bs::launch_conv_requant(s, act_packed, w_packed,
+                                            out_packed, rq, g_conv_opt,
+                                            (hipStream_t)stream),
+                    "bs_conv2d_requant launch");
 }
 
 bs_status bs_conv2d_describe(const bs_conv2d_params* p, char* buf,

@@ -28,6 +28,27 @@ struct FastDiv {
     }
 };
 
+// One quantizer code (the reading of the quantization operator used
+// throughout): round-half-to-even of a single binary32 product, clamped to
+// [0, qmax] with NaN sent to 0.  Bipolar: 1 iff x >= 0.  (A lone multiply
+// followed by rint leaves nothing to contract into an FMA.)
+template <bool BIP>
+__device__ __forceinline__ uint32_t quant_code(float x, float scale,
+                                               float qmax) {
+    if (BIP) return x >= 0.0f ? 1u : 0u;
+    float r = __builtin_rintf(x * scale);
+    r = r > 0.0f ? r : 0.0f;   // negative, -0 and NaN -> 0
+    r = r < qmax ? r : qmax;   // saturate (+inf included)
+    return (uint32_t)r;
+}
+
+// Bits b of the four bytes of v (bit b of byte k -> bit k of the result).
+__device__ __forceinline__ uint32_t nibble_of(uint32_t v, int b) {
+    uint32_t x = (v >> b) & 0x01010101u;
+    x = (x | (x >> 7)) & 0x00030003u;   // bits 0,1 and 16,17
+    return (x | (x >> 14)) & 0xFu;      // bits 0..3
+}
+
 // ---- launchers (each returns hipSuccess or the launch error) -------------
 
 hipError_t launch_quantize(const float* x, uint8_t* q, int64_t n, float scale,
@@ -61,6 +82,19 @@ struct ConvOptions {
 hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
                        const uint32_t* wts, int32_t* out,
                        const ConvOptions& opt, hipStream_t st);
+
+// Requantized output of a conv: codes of out_bits bits (quant_code of the
+// int32 result converted to float32, times out_scale), bit-packed along the
+// output channels as [n][oh][ow][out_bits][ceil(oc / 32)] uint32 words.
+struct Requant {
+    float scale;
+    int bits;       // 1..8
+};
+
+hipError_t launch_conv_requant(const ConvShape& s, const uint32_t* act,
+                               const uint32_t* wts, uint32_t* out,
+                               const Requant& rq, const ConvOptions& opt,
+                               hipStream_t st);
 
 // Writes the kernel and launch configuration launch_conv would use for this
 // shape and mode into buf (snprintf semantics); returns the snprintf result.

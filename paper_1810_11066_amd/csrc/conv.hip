@@ -56,41 +56,86 @@ struct GenericArgs {
     FastDiv div_oc, div_ow, div_oh;
 };
 
+// One output of the convolution, plain loops (Eq. 2 per tap and word).
+__device__ __forceinline__ uint32_t generic_output(
+    const ConvShape& s, const uint32_t* __restrict__ act,
+    const uint32_t* __restrict__ wts, int cw, uint32_t img, uint32_t oy,
+    uint32_t ox, uint32_t o) {
+    uint32_t sum = 0;
+    for (int r = 0; r < s.kh; ++r) {
+        const int iy = (int)oy * s.sh - s.ph + r;
+        if (iy < 0 || iy >= s.h) continue;          // zero padding
+        for (int c = 0; c < s.kw; ++c) {
+            const int ix = (int)ox * s.sw - s.pw + c;
+            if (ix < 0 || ix >= s.w) continue;      // zero padding
+            const uint32_t* ap =
+                act + (((int64_t)img * s.h + iy) * s.w + ix) *
+                          (int64_t)s.abits * cw;
+            const uint32_t* wp =
+                wts + (((int64_t)o * s.kh + r) * s.kw + c) *
+                          (int64_t)s.wbits * cw;
+            for (int t = 0; t < cw; ++t) {
+                for (int i = 0; i < s.abits; ++i) {
+                    const uint32_t a = ap[i * cw + t];
+                    for (int j = 0; j < s.wbits; ++j) {
+                        const uint32_t w = wp[j * cw + t];
+                        uint32_t term = __builtin_popcount(a & w);
+                        if (s.bipolar_w) term -= __builtin_popcount(a & ~w);
+                        sum += term << (i + j);
+                    }
+                }
+            }
+        }
+    }
+    return sum;
+}
+
 __global__ __launch_bounds__(kBlock) void conv_generic_kernel(GenericArgs g) {
     const ConvShape& s = g.s;
-    const int cw = g.cw;
     for (uint32_t f = blockIdx.x * kBlock + threadIdx.x; f < g.total;
          f += gridDim.x * kBlock) {
         const uint32_t pix = g.div_oc.div(f), o = f - pix * (uint32_t)s.oc;
         const uint32_t rowi = g.div_ow.div(pix), ox = pix - rowi * (uint32_t)s.ow;
         const uint32_t img = g.div_oh.div(rowi), oy = rowi - img * (uint32_t)s.oh;
-        uint32_t sum = 0;
-        for (int r = 0; r < s.kh; ++r) {
-            const int iy = (int)oy * s.sh - s.ph + r;
-            if (iy < 0 || iy >= s.h) continue;          // zero padding
-            for (int c = 0; c < s.kw; ++c) {
-                const int ix = (int)ox * s.sw - s.pw + c;
-                if (ix < 0 || ix >= s.w) continue;      // zero padding
-                const uint32_t* ap =
-                    g.act + (((int64_t)img * s.h + iy) * s.w + ix) *
-                                (int64_t)s.abits * cw;
-                const uint32_t* wp =
-                    g.wts + (((int64_t)o * s.kh + r) * s.kw + c) *
-                                (int64_t)s.wbits * cw;
-                for (int t = 0; t < cw; ++t) {
-                    for (int i = 0; i < s.abits; ++i) {
-                        const uint32_t a = ap[i * cw + t];
-                        for (int j = 0; j < s.wbits; ++j) {
-                            const uint32_t w = wp[j * cw + t];
-                            uint32_t term = __builtin_popcount(a & w);
-                            if (s.bipolar_w) term -= __builtin_popcount(a & ~w);
-                            sum += term << (i + j);
-                        }
-                    }
-                }
-            }
+        g.out[f] = (int32_t)generic_output(s, g.act, g.wts, g.cw, img, oy, ox,
+                                           o);
+    }
+}
+
+// Requantized, bit-packed output, plain loops: one thread per (pixel, word
+// of 32 output channels).
+struct GenericRequantArgs {
+    const uint32_t* act;
+    const uint32_t* wts;
+    uint32_t* out;
+    ConvShape s;
+    int32_t cw;
+    int32_t words;        // ceil(oc / 32)
+    uint32_t total;       // npix * words, < 2^31
+    float scale, qmax;
+    int32_t bits;
+    FastDiv div_words, div_ow, div_oh;
+};
+
+__global__ __launch_bounds__(kBlock) void conv_generic_requant_kernel(
+    GenericRequantArgs g) {
+    const ConvShape& s = g.s;
+    for (uint32_t f = blockIdx.x * kBlock + threadIdx.x; f < g.total;
+         f += gridDim.x * kBlock) {
+        const uint32_t pix = g.div_words.div(f), w = f - pix * (uint32_t)g.words;
+        const uint32_t rowi = g.div_ow.div(pix), ox = pix - rowi * (uint32_t)s.ow;
+        const uint32_t img = g.div_oh.div(rowi), oy = rowi - img * (uint32_t)s.oh;
+        uint32_t word[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        const int c1 = min(32, s.oc - 32 * (int)w);
+        for (int c = 0; c < c1; ++c) {
+            const uint32_t v = generic_output(s, g.act, g.wts, g.cw, img, oy,
+                                              ox, 32 * w + c);
+            const uint32_t code =
+                quant_code<false>((float)(int32_t)v, g.scale, g.qmax);
+            for (int b = 0; b < g.bits; ++b) word[b] |= ((code >> b) & 1u) << c;
         }
-        g.out[f] = (int32_t)sum;
+        uint32_t* dst = g.out + (size_t)pix * (uint32_t)(g.bits * g.words) + w;
+        for (int b = 0; b < g.bits; ++b) dst[(size_t)b * g.words] = word[b];
     }
 }
 
@@ -141,7 +186,8 @@ bool conv_has_fast_path(const ConvShape& s) {
 namespace {
 
 // Pixels-on-lanes kernel for this shape, or nullptr.
-pix::PixKernelFn pix_kernel_for(const ConvShape& s, pix::PlanInfo* info) {
+pix::PixKernelFn pix_kernel_for(const ConvShape& s, bool req,
+                                pix::PlanInfo* info) {
     const int64_t cw = (s.c + 31) / 32;
     if (s.abits > 4 || s.wbits > 4) return nullptr;
     if (s.kh != s.kw || s.sh != s.sw) return nullptr;
@@ -152,7 +198,8 @@ pix::PixKernelFn pix_kernel_for(const ConvShape& s, pix::PlanInfo* info) {
     if (npix >= INT32_MAX || units >= INT32_MAX / 2) return nullptr;
     // the kernel addresses activation words with 32-bit offsets
     if ((int64_t)s.n * s.h * s.w * s.abits * cw >= INT32_MAX) return nullptr;
-    return pix::pick(s.abits, s.wbits, s.bipolar_w, s.kh, s.sh, (int)cw, info);
+    return pix::pick(s.abits, s.wbits, s.bipolar_w, s.kh, s.sh, (int)cw, req,
+                     info);
 }
 
 // Compute units of the current device (cached per device).
@@ -199,18 +246,26 @@ int resident_blocks(pix::PixKernelFn fn, size_t lds) {
 // (at most `resident` blocks per CU), adjusted upwards while that lowers the
 // busiest CU's load (blocks per CU x L), so that CUs end together.
 void plan_pix(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
-              pix::PixArgs* g, dim3* grid, size_t* lds) {
+              const Requant* rq, pix::PixArgs* g, dim3* grid, size_t* lds) {
     g->h = s.h; g->w = s.w; g->oh = s.oh; g->ow = s.ow;
     g->ph = s.ph; g->pw = s.pw;
     g->oc = s.oc;
     g->npix = s.n * s.oh * s.ow;
     g->quads = s.oc / 4;
+    // a packed output word covers 32 channels (8 quads) of one pixel, so
+    // requantizing kernels take whole words
+    g->unit_quads = rq ? 8 : 1;
+    g->group_units = (g->quads + g->unit_quads - 1) / g->unit_quads;
+    g->out_scale = rq ? rq->scale : 0.0f;
+    g->out_bits = rq ? rq->bits : 0;
+    g->out_qmax = rq ? (float)((1 << rq->bits) - 1) : 0.0f;
+    g->out_words = (s.oc + 31) / 32;
     const int64_t groups = ((int64_t)g->npix + 63) / 64;
-    const int64_t units = groups * g->quads;
+    const int64_t units = groups * g->group_units;
     g->units = (int32_t)units;
     g->div_ow.init((uint32_t)s.ow);
     g->div_oh.init((uint32_t)s.oh);
-    g->div_quads.init((uint32_t)g->quads);
+    g->div_units.init((uint32_t)g->group_units);
     *lds = (size_t)pix::kWavesPerBlock * pix::kTileWords * 4;
     const int64_t cus = device_cus();
     const int64_t slots = cus * resident_blocks(fn, *lds);   // blocks
@@ -281,7 +336,7 @@ enum class Family { kPixels, kChannels, kGeneric };
 Family choose(const ConvShape& s, int mode, pix::PixKernelFn* pfn,
               pix::PlanInfo* info) {
     if (mode == 0 || mode == 3) {
-        if ((*pfn = pix_kernel_for(s, info)) != nullptr)
+        if ((*pfn = pix_kernel_for(s, false, info)) != nullptr)
             return Family::kPixels;
     }
     if ((mode == 0 || mode == 2) && conv_has_fast_path(s))
@@ -302,7 +357,7 @@ hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
     switch (choose(s, mode, &pfn, &info)) {
         case Family::kPixels: {
             pix::PixArgs g;
-            plan_pix(s, pfn, opt.units_per_wave, &g, &grid, &lds);
+            plan_pix(s, pfn, opt.units_per_wave, nullptr, &g, &grid, &lds);
             void* args[] = {&act, &wts, &out, &g};
             return hipLaunchKernel((const void*)pfn, grid, dim3(pix::kBlock),
                                    args, lds, st);
@@ -327,6 +382,46 @@ hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
     }
 }
 
+hipError_t launch_conv_requant(const ConvShape& s, const uint32_t* act,
+                               const uint32_t* wts, uint32_t* out,
+                               const Requant& rq, const ConvOptions& opt,
+                               hipStream_t st) {
+    // the pixels-on-lanes kernel (modes 0 and 3), else plain loops
+    pix::PlanInfo info{};
+    pix::PixKernelFn pfn = nullptr;
+    if (opt.mode == 0 || opt.mode == 3) pfn = pix_kernel_for(s, true, &info);
+    if (pfn) {
+        pix::PixArgs g;
+        dim3 grid;
+        size_t lds = 0;
+        // the run-length override counts packed words (8 quads) here
+        plan_pix(s, pfn, opt.units_per_wave, &rq, &g, &grid, &lds);
+        int32_t* o = reinterpret_cast<int32_t*>(out);
+        void* args[] = {&act, &wts, &o, &g};
+        return hipLaunchKernel((const void*)pfn, grid, dim3(pix::kBlock),
+                               args, lds, st);
+    }
+    GenericRequantArgs g;
+    g.act = act;
+    g.wts = wts;
+    g.out = out;
+    g.s = s;
+    g.cw = (s.c + 31) / 32;
+    g.words = (s.oc + 31) / 32;
+    g.total = (uint32_t)((int64_t)s.n * s.oh * s.ow * g.words);
+    g.scale = rq.scale;
+    g.qmax = (float)((1 << rq.bits) - 1);
+    g.bits = rq.bits;
+    g.div_words.init((uint32_t)g.words);
+    g.div_ow.init((uint32_t)s.ow);
+    g.div_oh.init((uint32_t)s.oh);
+    int64_t blocks = ((int64_t)g.total + kBlock - 1) / kBlock;
+    if (blocks > 65535) blocks = 65535;
+    if (blocks < 1) blocks = 1;
+    conv_generic_requant_kernel<<<(uint32_t)blocks, kBlock, 0, st>>>(g);
+    return hipGetLastError();
+}
+
 int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
                   size_t len) {
     const int mode = opt.mode;
@@ -339,7 +434,7 @@ int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
     switch (choose(s, mode, &pfn, &info)) {
         case Family::kPixels: {
             pix::PixArgs g;
-            plan_pix(s, pfn, opt.units_per_wave, &g, &grid, &lds);
+            plan_pix(s, pfn, opt.units_per_wave, nullptr, &g, &grid, &lds);
             return snprintf(buf, len,
                             "conv_pix_kernel<A=%d,W=%d,%s,K=%d,S=%d,CW=%d> "
                             "patch=%dtaps x %dwords slice=%dch x %dtaps "

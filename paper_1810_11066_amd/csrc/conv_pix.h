@@ -52,9 +52,15 @@ struct PixArgs {
     int32_t oc;            // output channels, a multiple of 4
     int32_t npix;          // n * oh * ow
     int32_t quads;         // oc / 4
-    int32_t units;         // ceil(npix / 64) * quads, < 2^31
+    int32_t unit_quads;    // quads per unit: 1 (int32 out), 8 (packed out)
+    int32_t group_units;   // units per 64-pixel group: ceil(quads / unit_quads)
+    int32_t units;         // ceil(npix / 64) * group_units, < 2^31
     int32_t per_wave;      // units per wave (the last waves may get fewer)
-    FastDiv div_ow, div_oh, div_quads;
+    // requantized output (packed kernels only)
+    float out_scale, out_qmax;
+    int32_t out_bits;      // 1..8
+    int32_t out_words;     // ceil(oc / 32): words per plane of a pixel
+    FastDiv div_ow, div_oh, div_units;
 };
 
 __device__ __forceinline__ void bcnt_acc(uint32_t& acc, uint32_t x) {
@@ -158,6 +164,38 @@ __device__ __forceinline__ void load_slice(
                     s.w[((o * Pl::TS + tt) * W + j) * Pl::CB + c] =
                         src[o * Pl::FW + (tt * W + j) * CW + c];
 }
+
+// Requantized, bit-packed output of one pixel: the codes of up to 32
+// consecutive output channels gathered bit by bit into one word per plane
+// (channel c of the word -> bit c, LSB first), stored when complete.
+struct PackedOut {
+    uint32_t word[8];
+
+    __device__ __forceinline__ void clear() {
+#pragma unroll
+        for (int b = 0; b < 8; ++b) word[b] = 0;
+    }
+    // codes of 4 consecutive channels starting at bit `pos` (a multiple of 4)
+    __device__ __forceinline__ void add4(const uint32_t (&val)[4],
+                                         const PixArgs& g, int pos) {
+        uint32_t bytes = 0;
+#pragma unroll
+        for (int o = 0; o < 4; ++o)
+            bytes |= quant_code<false>((float)(int32_t)val[o], g.out_scale,
+                                       g.out_qmax) << (8 * o);
+#pragma unroll
+        for (int b = 0; b < 8; ++b)
+            if (b < g.out_bits) word[b] |= nibble_of(bytes, b) << pos;
+    }
+    __device__ __forceinline__ void store(int32_t* __restrict__ out,
+                                          const PixArgs& g, int pix, int w) {
+        uint32_t* dst = reinterpret_cast<uint32_t*>(out) +
+                        (size_t)pix * (uint32_t)(g.out_bits * g.out_words) + w;
+#pragma unroll
+        for (int b = 0; b < 8; ++b)
+            if (b < g.out_bits) dst[(size_t)b * g.out_words] = word[b];
+    }
+};
 
 // Output tile staging.  With pixels on lanes, the NHWC output of one output
 // channel is 4 bytes per lane at a stride of oc * 4 bytes -- one memory
@@ -375,8 +413,9 @@ __device__ __forceinline__ void run_block(
 }
 
 // A, W: bit-widths; BIP: bipolar weights; K: square kernel size; S: stride;
-// CW: words per bit-plane.
-template <int A, int W, bool BIP, int K, int S, int CW>
+// CW: words per bit-plane; REQ: requantize and bit-pack the output (out then
+// holds [npix][out_bits][out_words] uint32 words) instead of storing int32.
+template <int A, int W, bool BIP, int K, int S, int CW, bool REQ>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_num_sgpr(80)))
 void conv_pix_kernel(
     const uint32_t* __restrict__ act, const uint32_t* __restrict__ wts,
@@ -395,9 +434,11 @@ void conv_pix_kernel(
     gu32* gw = (gu32*)(wts);
 
     while (u < u_end) {
-        const int grp = (int)g.div_quads.div((uint32_t)u);
-        const int q0 = u - grp * g.quads;
-        const int q1 = min(g.quads, q0 + (u_end - u));
+        const int grp = (int)g.div_units.div((uint32_t)u);
+        const int w0 = u - grp * g.group_units;            // first unit
+        const int w1 = min(g.group_units, w0 + (u_end - u));
+        const int q0 = w0 * g.unit_quads;
+        const int q1 = min(g.quads, w1 * g.unit_quads);
         const int pix0 = grp * 64;
 
         // this lane's output pixel (the last pixel stands in past the end)
@@ -422,22 +463,34 @@ void conv_pix_kernel(
             const int nq = q1 - q0;
             int chunk_base = 4 * q0;   // first channel held in the tile
             int held = 0;              // quads held in the tile
+            PackedOut po;
+            po.clear();
             for (int qi = 0; qi < nq; ++qi) {
                 uint32_t val[4];
                 gu32* q = src + (size_t)qi * 4 * FW;
                 compute_quad<A, W, BIP, K, CW>(
                     patch, sa, q, qi + 1 < nq ? q + 4 * FW : src, f, val);
+                if constexpr (REQ) {
+                    // a packed word holds 8 quads; runs start on a word
+                    const int qg = q0 + qi;
+                    po.add4(val, g, 4 * (qg & 7));
+                    if ((qg & 7) == 7 || qi + 1 == nq) {
+                        if (p < g.npix) po.store(out, g, p, qg >> 3);
+                        po.clear();
+                    }
+                } else {
 #pragma unroll
-                for (int o = 0; o < 4; ++o)
-                    tile[lane * kTileStride + held * 4 + o] = val[o];
-                ++held;
-                if (held == kChunk / 4 || qi + 1 == nq) {
-                    wave_lds_sync();
-                    flush_tile(tile, out, pix0, g.npix, g.oc, chunk_base,
-                               held * 4, lane);
-                    wave_lds_sync();
-                    chunk_base += held * 4;
-                    held = 0;
+                    for (int o = 0; o < 4; ++o)
+                        tile[lane * kTileStride + held * 4 + o] = val[o];
+                    ++held;
+                    if (held == kChunk / 4 || qi + 1 == nq) {
+                        wave_lds_sync();
+                        flush_tile(tile, out, pix0, g.npix, g.oc, chunk_base,
+                                   held * 4, lane);
+                        wave_lds_sync();
+                        chunk_base += held * 4;
+                        held = 0;
+                    }
                 }
             }
         } else {
@@ -445,6 +498,8 @@ void conv_pix_kernel(
             // channels; partial sums of later blocks are added in the tile
             using Patch = uint32_t[Pl::TB][A][Pl::CB];
             uint32_t* row = tile + lane * kTileStride;
+            PackedOut po;
+            po.clear();
             for (int sub = q0; sub < q1; sub += kChunk / 4) {
                 const int nq = min(kChunk / 4, q1 - sub);
                 gu32* qsrc = gw + (size_t)(4 * sub) * FW;
@@ -486,13 +541,28 @@ void conv_pix_kernel(
                             nb + 1 < NB ? blk(nb + 1) : qsrc, f, row);
                     }
                 }
-                wave_lds_sync();
-                flush_tile(tile, out, pix0, g.npix, g.oc, 4 * sub, nq * 4,
-                           lane);
-                wave_lds_sync();
+                if constexpr (REQ) {
+                    // the lane's own tile row: 4 quads of a packed word
+                    for (int qi = 0; qi < nq; ++qi) {
+                        const int qg = sub + qi;
+                        uint32_t val[4];
+#pragma unroll
+                        for (int o = 0; o < 4; ++o) val[o] = row[qi * 4 + o];
+                        po.add4(val, g, 4 * (qg & 7));
+                        if ((qg & 7) == 7 || qg + 1 == q1) {
+                            if (p < g.npix) po.store(out, g, p, qg >> 3);
+                            po.clear();
+                        }
+                    }
+                } else {
+                    wave_lds_sync();
+                    flush_tile(tile, out, pix0, g.npix, g.oc, 4 * sub, nq * 4,
+                               lane);
+                    wave_lds_sync();
+                }
             }
         }
-        u += q1 - q0;
+        u += w1 - w0;
     }
 }
 
@@ -504,21 +574,23 @@ struct PlanInfo {
     int ocb, ts, tb, cb;
 };
 
-// Kernel for a supported (A, W, bipolar, K, S, CW) or nullptr, with its plan
-// (output channels per filter slice, taps per slice, taps and words per
-// plane of a reduction block).  pick_a<A> is defined for A = 1..4 in
-// conv_pix_a<A>.hip, so the specialisations compile in parallel.
-PixKernelFn pick(int a, int w, bool b, int k, int s, int cw, PlanInfo* info);
+// Kernel for a supported (A, W, bipolar, K, S, CW, requantized output) or
+// nullptr, with its plan (output channels per filter slice, taps per slice,
+// taps and words per plane of a reduction block).  pick_a<A> is defined for
+// A = 1..4 in conv_pix_a<A>.hip, so the specialisations compile in parallel.
+PixKernelFn pick(int a, int w, bool b, int k, int s, int cw, bool req,
+                 PlanInfo* info);
 template <int A>
-PixKernelFn pick_a(int w, bool b, int k, int s, int cw, PlanInfo* info);
-template <> PixKernelFn pick_a<1>(int, bool, int, int, int, PlanInfo*);
-template <> PixKernelFn pick_a<2>(int, bool, int, int, int, PlanInfo*);
-template <> PixKernelFn pick_a<3>(int, bool, int, int, int, PlanInfo*);
-template <> PixKernelFn pick_a<4>(int, bool, int, int, int, PlanInfo*);
+PixKernelFn pick_a(int w, bool b, int k, int s, int cw, bool req,
+                   PlanInfo* info);
+template <> PixKernelFn pick_a<1>(int, bool, int, int, int, bool, PlanInfo*);
+template <> PixKernelFn pick_a<2>(int, bool, int, int, int, bool, PlanInfo*);
+template <> PixKernelFn pick_a<3>(int, bool, int, int, int, bool, PlanInfo*);
+template <> PixKernelFn pick_a<4>(int, bool, int, int, int, bool, PlanInfo*);
 
 // Specialisations for activation width A (included by conv_pix_a<A>.hip).
 template <int A, int W, bool B, int K, int S, int CW>
-PixKernelFn pick_kscw(PlanInfo* info) {
+PixKernelFn pick_kscw(bool req, PlanInfo* info) {
     using Pl = Plan<A, W, K, CW>;
     if constexpr (!Pl::kFits) {
         return nullptr;
@@ -527,27 +599,28 @@ PixKernelFn pick_kscw(PlanInfo* info) {
         info->ts = Pl::TS;
         info->tb = Pl::TB;
         info->cb = Pl::CB;
-        return conv_pix_kernel<A, W, B, K, S, CW>;
+        return req ? conv_pix_kernel<A, W, B, K, S, CW, true>
+                   : conv_pix_kernel<A, W, B, K, S, CW, false>;
     }
 }
 
 // Words per plane: 1..16 for 3x3 windows; 1x1 windows (and dense, a 1x1
 // conv) up to 128 words = 4096 input channels.
 template <int A, int W, bool B, int K, int S>
-PixKernelFn pick_cw(int cw, PlanInfo* info) {
+PixKernelFn pick_cw(int cw, bool req, PlanInfo* info) {
     switch (cw) {
-        case 1: return pick_kscw<A, W, B, K, S, 1>(info);
-        case 2: return pick_kscw<A, W, B, K, S, 2>(info);
-        case 4: return pick_kscw<A, W, B, K, S, 4>(info);
-        case 8: return pick_kscw<A, W, B, K, S, 8>(info);
-        case 16: return pick_kscw<A, W, B, K, S, 16>(info);
+        case 1: return pick_kscw<A, W, B, K, S, 1>(req, info);
+        case 2: return pick_kscw<A, W, B, K, S, 2>(req, info);
+        case 4: return pick_kscw<A, W, B, K, S, 4>(req, info);
+        case 8: return pick_kscw<A, W, B, K, S, 8>(req, info);
+        case 16: return pick_kscw<A, W, B, K, S, 16>(req, info);
         default: break;
     }
     if constexpr (K == 1) {
         switch (cw) {
-            case 32: return pick_kscw<A, W, B, K, S, 32>(info);
-            case 64: return pick_kscw<A, W, B, K, S, 64>(info);
-            case 128: return pick_kscw<A, W, B, K, S, 128>(info);
+            case 32: return pick_kscw<A, W, B, K, S, 32>(req, info);
+            case 64: return pick_kscw<A, W, B, K, S, 64>(req, info);
+            case 128: return pick_kscw<A, W, B, K, S, 128>(req, info);
             default: break;
         }
     }
@@ -555,23 +628,24 @@ PixKernelFn pick_cw(int cw, PlanInfo* info) {
 }
 
 template <int A, int W, bool B>
-PixKernelFn pick_ks(int k, int s, int cw, PlanInfo* info) {
-    if (k == 1) return s == 1 ? pick_cw<A, W, B, 1, 1>(cw, info)
-                              : pick_cw<A, W, B, 1, 2>(cw, info);
-    if (k == 3) return s == 1 ? pick_cw<A, W, B, 3, 1>(cw, info)
-                              : pick_cw<A, W, B, 3, 2>(cw, info);
+PixKernelFn pick_ks(int k, int s, int cw, bool req, PlanInfo* info) {
+    if (k == 1) return s == 1 ? pick_cw<A, W, B, 1, 1>(cw, req, info)
+                              : pick_cw<A, W, B, 1, 2>(cw, req, info);
+    if (k == 3) return s == 1 ? pick_cw<A, W, B, 3, 1>(cw, req, info)
+                              : pick_cw<A, W, B, 3, 2>(cw, req, info);
     return nullptr;
 }
 
 // Every weight width 1..4 with unipolar weights; bipolar weights at W = 1.
 template <int A>
-PixKernelFn pick_for_a(int w, bool b, int k, int s, int cw, PlanInfo* info) {
-    if (b) return w == 1 ? pick_ks<A, 1, true>(k, s, cw, info) : nullptr;
+PixKernelFn pick_for_a(int w, bool b, int k, int s, int cw, bool req,
+                       PlanInfo* info) {
+    if (b) return w == 1 ? pick_ks<A, 1, true>(k, s, cw, req, info) : nullptr;
     switch (w) {
-        case 1: return pick_ks<A, 1, false>(k, s, cw, info);
-        case 2: return pick_ks<A, 2, false>(k, s, cw, info);
-        case 3: return pick_ks<A, 3, false>(k, s, cw, info);
-        case 4: return pick_ks<A, 4, false>(k, s, cw, info);
+        case 1: return pick_ks<A, 1, false>(k, s, cw, req, info);
+        case 2: return pick_ks<A, 2, false>(k, s, cw, req, info);
+        case 3: return pick_ks<A, 3, false>(k, s, cw, req, info);
+        case 4: return pick_ks<A, 4, false>(k, s, cw, req, info);
         default: return nullptr;
     }
 }

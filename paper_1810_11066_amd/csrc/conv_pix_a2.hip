@@ -5,8 +5,9 @@ namespace bs {
 namespace pix {
 
 template <>
-PixKernelFn pick_a<2>(int w, bool b, int k, int s, int cw, PlanInfo* info) {
-    return pick_for_a<2>(w, b, k, s, cw, info);
+PixKernelFn pick_a<2>(int w, bool b, int k, int s, int cw, bool req,
+                      PlanInfo* info) {
+    return pick_for_a<2>(w, b, k, s, cw, req, info);
 }
 
 }  // namespace pix

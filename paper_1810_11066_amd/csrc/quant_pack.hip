@@ -19,16 +19,9 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kMaxBlocks = 8192;
 
-// One quantizer code: round-half-to-even of a single binary32 product,
-// clamped to [0, qmax] with NaN sent to 0.  Bipolar: 1 iff x >= 0.
-// (A lone multiply followed by rint leaves nothing to contract into an FMA.)
 template <bool BIP>
 __device__ __forceinline__ uint32_t code_of(float x, float scale, float qmax) {
-    if (BIP) return x >= 0.0f ? 1u : 0u;
-    float r = __builtin_rintf(x * scale);
-    r = r > 0.0f ? r : 0.0f;   // negative, -0 and NaN -> 0
-    r = r < qmax ? r : qmax;   // saturate (+inf included)
-    return (uint32_t)r;
+    return quant_code<BIP>(x, scale, qmax);
 }
 
 template <bool BIP>
@@ -65,17 +58,6 @@ __global__ __launch_bounds__(kBlock) void quantize_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// pack, k % 32 == 0: one thread per 32-element group (= one output word per
-// plane).  The group's 32 bytes are two 16-byte loads; consecutive threads
-// read consecutive 32-byte chunks.  Plane b of four bytes v is gathered in
-// registers: the bits sit at 0, 8, 16, 24 after (v >> b) & 0x01010101 and two
-// shift-or steps fold them into the low nibble.
-__device__ __forceinline__ uint32_t nibble_of(uint32_t v, int b) {
-    uint32_t x = (v >> b) & 0x01010101u;
-    x = (x | (x >> 7)) & 0x00030003u;   // bits 0,1 and 16,17
-    return (x | (x >> 14)) & 0xFu;      // bits 0..3
-}
-
 // Cross-lane OR with a DPP lane permutation (all source lanes are inside the
 // 8-lane group, so every lane reads a defined value).
 constexpr int kDppQuadXor1 = 0xB1;     // quad_perm [1,0,3,2]: lane ^ 1

@@ -41,7 +41,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_words(lib):
-    assert lib.bs_abi_version() == 101
+    assert lib.bs_abi_version() == 102
     for k, w in [(0, 0), (1, 1), (31, 1), (32, 1), (33, 2), (4096, 128)]:
         assert lib.bs_packed_words(k) == w
 
@@ -221,3 +221,23 @@ def test_describe_validation_and_truncation(lib):
                                   0) == bs.BS_ERR_INVALID_ARG
     assert lib.bs_conv2d_describe(ctypes.byref(params(kh=0)), buf,
                                   8) == bs.BS_ERR_INVALID_ARG
+
+
+def test_requant_validation(lib):
+    r = lib.bs_conv2d_requant
+    p = params()
+    assert r(ctypes.byref(p), FAKE, FAKE, 0.5, 0, FAKE,
+             STREAM) == bs.BS_ERR_INVALID_ARG
+    assert r(ctypes.byref(p), FAKE, FAKE, 0.5, 9, FAKE,
+             STREAM) == bs.BS_ERR_INVALID_ARG
+    for scale in (0.0, -2.0, float("inf"), float("nan")):
+        assert r(ctypes.byref(p), FAKE, FAKE, scale, 2, FAKE,
+                 STREAM) == bs.BS_ERR_INVALID_ARG
+    assert r(ctypes.byref(p), FAKE, FAKE, 0.5, 2, NULL,
+             STREAM) == bs.BS_ERR_INVALID_ARG
+    assert r(ctypes.byref(p), FAKE, MISALIGNED, 0.5, 2, FAKE,
+             STREAM) == bs.BS_ERR_INVALID_ARG
+    assert r(ctypes.byref(params(aenc=1)), FAKE, FAKE, 0.5, 2, FAKE,
+             STREAM) == bs.BS_ERR_UNSUPPORTED
+    assert r(ctypes.byref(params(abits=8, wbits=8, c=4000)), FAKE, FAKE, 0.5,
+             2, FAKE, STREAM) == bs.BS_ERR_OVERFLOW

@@ -377,6 +377,79 @@ def test_dense_random(oracle, seed):
     g.check_guards()
 
 
+# ------------------------------------------- requantized (chained) output --
+
+def run_requant(oracle, n, h, w, c, oc, k, s, pad, abits, wbits, bip, scale,
+                obits, seed, mode=0, run=0):
+    rng = np.random.default_rng(seed)
+    a = rng.integers(0, 1 << abits, size=(n, h, w, c), dtype=np.uint8)
+    wq = rng.integers(0, 1 << wbits, size=(oc, k, k, c), dtype=np.uint8)
+    ap, wp = oracle.pack(a, abits), oracle.pack(wq, wbits)
+    conv = oracle.conv2d(oracle.conv_params(n, h, w, c, oc, k, k, s, pad,
+                                            abits, wbits, wenc=int(bip)),
+                         ap, wp)
+    # the next layer's input: quantize the float32 values, pack over channels
+    want = oracle.pack(oracle.quantize(conv.astype(np.float32), scale, obits),
+                       obits)
+    p = bs.ConvParams(n, h, w, c, oc, k, k, s, s, pad, pad, abits, wbits, 0,
+                      int(bip))
+    g = Guarded(want.size, torch.int32, SENT32)
+    bs.bs_set_kernel_mode(mode)
+    bs.bs_set_units_per_wave(run)
+    try:
+        bs.bs_conv2d_requant(p, dev(ap.view(np.int32)), dev(wp.view(np.int32)),
+                             scale, obits, g.t)
+    finally:
+        bs.bs_set_kernel_mode(0)
+        bs.bs_set_units_per_wave(0)
+    torch.cuda.synchronize()
+    assert np.array_equal(as_words(g.t).reshape(want.shape), want)
+    g.check_guards()
+
+
+REQUANT_SHAPES = [
+    # n, h, w, c, oc, k, s, pad
+    (2, 9, 11, 64, 64, 3, 1, 1),
+    (1, 10, 9, 32, 36, 3, 1, 1),      # a partial last word (4 channels)
+    (2, 8, 7, 64, 96, 3, 2, 1),
+    (1, 12, 12, 128, 40, 1, 1, 0),
+    (2, 6, 7, 256, 64, 3, 1, 1),      # row blocks: partial sums in the tile
+    (1, 5, 5, 512, 32, 3, 2, 1),      # tap blocks
+    (1, 7, 6, 64, 70, 3, 1, 1),       # oc % 4 != 0: plain-loop kernel
+]
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("shape", REQUANT_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("abits,wbits,bip,obits", [
+    (2, 1, False, 2), (1, 1, True, 1), (2, 2, False, 3), (3, 3, False, 8)])
+def test_conv_requant(oracle, shape, abits, wbits, bip, obits, mode):
+    n, h, w, c, oc, k, s, pad = shape
+    say("conv requant", shape, abits, wbits, bip, obits, "mode", mode)
+    # a scale that spreads the results over the output codes
+    scale = ((1 << obits) - 1) / (0.5 * k * k * c * ((1 << abits) - 1) + 1)
+    run_requant(oracle, n, h, w, c, oc, k, s, pad, abits, wbits, bip, scale,
+                obits, seed=hash((shape, abits, obits)) % 10000, mode=mode)
+
+
+@pytest.mark.parametrize("run", [1, 2, 3, 100000])
+@pytest.mark.parametrize("shape", REQUANT_SHAPES[:3] + REQUANT_SHAPES[4:5],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_conv_requant_runs(oracle, shape, run):
+    n, h, w, c, oc, k, s, pad = shape
+    say("conv requant runs", shape, run)
+    run_requant(oracle, n, h, w, c, oc, k, s, pad, 2, 1, False, 0.01, 2,
+                seed=run + 3 * oc, mode=3, run=run)
+
+
+def test_conv_requant_special_scales(oracle):
+    # saturation (every result at the top code), everything rounding to 0,
+    # and ties: a scale of 0.5 puts odd results exactly halfway
+    for scale in (1e6, 1e-9, 0.5):
+        run_requant(oracle, 2, 9, 11, 64, 64, 3, 1, 1, 2, 1, False, scale, 2,
+                    seed=17)
+
+
 # ------------------------------------------------- int8 comparison baseline --
 
 def test_int8_baseline_equals_bitserial(oracle):
