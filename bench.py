@@ -283,6 +283,82 @@ def case_line(case, m, args):
 INT8_MFMA_PEAK_TOPS = 5000.0   # dense int8 MFMA, MI355X
 
 
+def chain_line(args, bs, torch, np, wl, batch=128, abits=2, wbits=1) -> int:
+    """ResNet-18's 3x3 conv path chained on the GPU: the float32 input is
+    quantized and packed once, every conv but the last writes the next
+    layer's packed codes (bs_conv2d_requant), the last writes int32."""
+    layers = wl.resnet18_chain(abits, wbits)
+    stream = torch.cuda.current_stream()
+    x = torch.from_numpy(wl.normal_floats((batch, 56, 56, 64),
+                                          wl.seed_for(7))).cuda()
+    packed_in = torch.empty((batch * 56 * 56, abits, bs.words(64)),
+                            dtype=torch.int32, device="cuda")
+    specs, wts, outs = [], [], []
+    for L in layers:
+        spec = bs.Conv2dSpec(batch, L.h, L.w, L.c, L.oc, L.k, L.k, L.stride,
+                             L.pad, abits, wbits)
+        p = spec.params()
+        oh, ow = bs.bs_conv2d_out_shape(p)
+        wts.append(bs.pack(torch.from_numpy(L.weights(wbits)).cuda(), wbits))
+        if L.out_scale is None:
+            outs.append(torch.empty((batch, oh, ow, L.oc), dtype=torch.int32,
+                                    device="cuda"))
+        else:
+            outs.append(torch.empty((batch, oh, ow, abits, bs.words(L.oc)),
+                                    dtype=torch.int32, device="cuda"))
+        specs.append(p)
+    macs = sum(batch * ((L.h + 2 * L.pad - L.k) // L.stride + 1) ** 2 *
+               L.oc * L.k * L.k * L.c for L in layers)
+
+    def run(ev=None):
+        bs.bs_quantize_pack(x, packed_in, batch * 56 * 56, 64, 1.0, abits,
+                            bs.UNIPOLAR, stream)
+        src = packed_in
+        for i, L in enumerate(layers):
+            if ev is not None:
+                ev[i][0].record(stream)
+            if L.out_scale is None:
+                bs.bs_conv2d(specs[i], src, wts[i], outs[i], stream)
+            else:
+                bs.bs_conv2d_requant(specs[i], src, wts[i], L.out_scale,
+                                     abits, outs[i], stream)
+            if ev is not None:
+                ev[i][1].record(stream)
+            src = outs[i]
+
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        run()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    ev = [[(torch.cuda.Event(enable_timing=True),
+            torch.cuda.Event(enable_timing=True)) for _ in layers]
+          for _ in range(args.steps)]
+    for r in range(args.steps):
+        run(ev[r])
+    torch.cuda.synchronize()
+    per = [sum(ev[r][i][0].elapsed_time(ev[r][i][1])
+               for r in range(args.steps)) / args.steps
+           for i in range(len(layers))]
+    print(json.dumps({
+        "chain": "resnet18 3x3 conv path, batch %d, A%dW%d, layers chained "
+                 "by bs_conv2d_requant" % (batch, abits, wbits),
+        "layers": len(layers),
+        "ms_per_pass": round(ms, 4),
+        "effective_tops": round(2 * macs / (ms * 1e-3) / 1e12, 1),
+        "frac_of_roofline": round(2 * macs / (ms * 1e-3) / 1e12 /
+                                  popcount_roofline_tops(abits, wbits), 4),
+        "layer_ms": {L.name: round(t, 4) for L, t in zip(layers, per)},
+    }))
+    return 0
+
+
 def int8_baseline_lines(args, bs, torch, np, wl) -> int:
     """The int8 matrix-core comparison (a baseline, not the bitserial path):
     config 2 as im2col + int8 GEMM, config 3 as one int8 GEMM, each timed
@@ -372,6 +448,11 @@ def main() -> int:
                     help="time the labelled int8 matrix-core baseline "
                          "(im2col + int8 GEMM) on configs 2 and 3 next to "
                          "the bitserial kernels, checking equal outputs")
+    ap.add_argument("--chain", action="store_true",
+                    help="the 16 3x3 convs of ResNet-18 (batch 128, A2W1) "
+                         "chained with bs_conv2d_requant: quantize+pack of "
+                         "the float input, 15 requantizing convs, one int32 "
+                         "conv; one line with the total and per-layer times")
     ap.add_argument("--sweep", action="store_true",
                     help="bit-width sweep A1-4 x W1-4 on ResNet-18 layer 9 "
                          "(batch 128): one line per pair, then a summary "
@@ -396,6 +477,8 @@ def main() -> int:
 
     if args.int8_baseline:
         return int8_baseline_lines(args, bs, torch, np, wl)
+    if args.chain:
+        return chain_line(args, bs, torch, np, wl)
 
     if args.sweep or args.config != 2:
         if args.sweep:

@@ -252,9 +252,9 @@ void plan_pix(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
     g->oc = s.oc;
     g->npix = s.n * s.oh * s.ow;
     g->quads = s.oc / 4;
-    // a packed output word covers 32 channels (8 quads) of one pixel, so
-    // requantizing kernels take whole words
-    g->unit_quads = rq ? 8 : 1;
+    // requantizing kernels store packed bytes (8 channels = 2 quads of one
+    // pixel), so their units are whole bytes
+    g->unit_quads = rq ? 2 : 1;
     g->group_units = (g->quads + g->unit_quads - 1) / g->unit_quads;
     g->out_scale = rq ? rq->scale : 0.0f;
     g->out_bits = rq ? rq->bits : 0;
@@ -394,7 +394,7 @@ hipError_t launch_conv_requant(const ConvShape& s, const uint32_t* act,
         pix::PixArgs g;
         dim3 grid;
         size_t lds = 0;
-        // the run-length override counts packed words (8 quads) here
+        // the run-length override counts packed bytes (2 quads) here
         plan_pix(s, pfn, opt.units_per_wave, &rq, &g, &grid, &lds);
         int32_t* o = reinterpret_cast<int32_t*>(out);
         void* args[] = {&act, &wts, &o, &g};

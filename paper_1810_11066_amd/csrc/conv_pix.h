@@ -52,7 +52,7 @@ struct PixArgs {
     int32_t oc;            // output channels, a multiple of 4
     int32_t npix;          // n * oh * ow
     int32_t quads;         // oc / 4
-    int32_t unit_quads;    // quads per unit: 1 (int32 out), 8 (packed out)
+    int32_t unit_quads;    // quads per unit: 1 (int32 out), 2 (packed out)
     int32_t group_units;   // units per 64-pixel group: ceil(quads / unit_quads)
     int32_t units;         // ceil(npix / 64) * group_units, < 2^31
     int32_t per_wave;      // units per wave (the last waves may get fewer)
@@ -165,35 +165,52 @@ __device__ __forceinline__ void load_slice(
                         src[o * Pl::FW + (tt * W + j) * CW + c];
 }
 
-// Requantized, bit-packed output of one pixel: the codes of up to 32
-// consecutive output channels gathered bit by bit into one word per plane
-// (channel c of the word -> bit c, LSB first), stored when complete.
+// Requantized, bit-packed output of one pixel: the codes of 8 consecutive
+// output channels (2 quads) gathered bit by bit into one byte per plane
+// (channel c of the byte -> bit c, LSB first; bytes of a word are
+// little-endian, so byte k of word w holds channels 32 w + 8 k ..), stored
+// as bytes -- 8-channel pieces let a wave's run end on any second quad
+// without sharing a store with its neighbour.
 struct PackedOut {
-    uint32_t word[8];
+    uint32_t codes[2];   // the codes of each quad, one byte per channel
 
-    __device__ __forceinline__ void clear() {
-#pragma unroll
-        for (int b = 0; b < 8; ++b) word[b] = 0;
-    }
-    // codes of 4 consecutive channels starting at bit `pos` (a multiple of 4)
+    __device__ __forceinline__ void clear() { codes[0] = codes[1] = 0; }
+    // codes of the 4 channels of quad `half` (0 or 1) of the byte: the int32
+    // results are exact in float32 (far below 2^24) and never NaN, so the
+    // clamp of the quantizer is one v_med3
     __device__ __forceinline__ void add4(const uint32_t (&val)[4],
-                                         const PixArgs& g, int pos) {
+                                         const PixArgs& g, int half) {
         uint32_t bytes = 0;
 #pragma unroll
-        for (int o = 0; o < 4; ++o)
-            bytes |= quant_code<false>((float)(int32_t)val[o], g.out_scale,
-                                       g.out_qmax) << (8 * o);
-#pragma unroll
-        for (int b = 0; b < 8; ++b)
-            if (b < g.out_bits) word[b] |= nibble_of(bytes, b) << pos;
+        for (int o = 0; o < 4; ++o) {
+            const float r =
+                __builtin_rintf((float)(int32_t)val[o] * g.out_scale);
+            bytes |= (uint32_t)__builtin_amdgcn_fmed3f(r, 0.0f, g.out_qmax)
+                     << (8 * o);
+        }
+        // (selects, not an indexed store: a runtime index into a register
+        // array would go through scratch memory)
+        codes[0] = half ? codes[0] : bytes;
+        codes[1] = half ? bytes : codes[1];
     }
+    // the byte of channels [8 k8, 8 k8 + 8) of pixel pix, every plane; the
+    // byte of the last channels also zeroes the rest of its word (the tail
+    // bits of the packed layout)
     __device__ __forceinline__ void store(int32_t* __restrict__ out,
-                                          const PixArgs& g, int pix, int w) {
-        uint32_t* dst = reinterpret_cast<uint32_t*>(out) +
-                        (size_t)pix * (uint32_t)(g.out_bits * g.out_words) + w;
+                                          const PixArgs& g, int pix, int k8) {
+        uint8_t* dst = reinterpret_cast<uint8_t*>(out) +
+                       (size_t)pix * (uint32_t)(4 * g.out_bits * g.out_words) +
+                       (uint32_t)k8;
+        const int last = (g.oc + 7) / 8 - 1;
+        const int pad = k8 == last ? 3 - (k8 & 3) : 0;
 #pragma unroll
         for (int b = 0; b < 8; ++b)
-            if (b < g.out_bits) dst[(size_t)b * g.out_words] = word[b];
+            if (b < g.out_bits) {
+                uint8_t* d = dst + (size_t)b * (uint32_t)(4 * g.out_words);
+                d[0] = (uint8_t)(nibble_of(codes[0], b) |
+                                 nibble_of(codes[1], b) << 4);
+                for (int z = 1; z <= pad; ++z) d[z] = 0;
+            }
     }
 };
 
@@ -471,11 +488,11 @@ void conv_pix_kernel(
                 compute_quad<A, W, BIP, K, CW>(
                     patch, sa, q, qi + 1 < nq ? q + 4 * FW : src, f, val);
                 if constexpr (REQ) {
-                    // a packed word holds 8 quads; runs start on a word
+                    // a packed byte holds 2 quads; runs start on a byte
                     const int qg = q0 + qi;
-                    po.add4(val, g, 4 * (qg & 7));
-                    if ((qg & 7) == 7 || qi + 1 == nq) {
-                        if (p < g.npix) po.store(out, g, p, qg >> 3);
+                    po.add4(val, g, qg & 1);
+                    if ((qg & 1) == 1 || qi + 1 == nq) {
+                        if (p < g.npix) po.store(out, g, p, qg >> 1);
                         po.clear();
                     }
                 } else {
@@ -542,15 +559,15 @@ void conv_pix_kernel(
                     }
                 }
                 if constexpr (REQ) {
-                    // the lane's own tile row: 4 quads of a packed word
+                    // the lane's own tile row, 2 quads per packed byte
                     for (int qi = 0; qi < nq; ++qi) {
                         const int qg = sub + qi;
                         uint32_t val[4];
 #pragma unroll
                         for (int o = 0; o < 4; ++o) val[o] = row[qi * 4 + o];
-                        po.add4(val, g, 4 * (qg & 7));
-                        if ((qg & 7) == 7 || qg + 1 == q1) {
-                            if (p < g.npix) po.store(out, g, p, qg >> 3);
+                        po.add4(val, g, qg & 1);
+                        if ((qg & 1) == 1 || qg + 1 == q1) {
+                            if (p < g.npix) po.store(out, g, p, qg >> 1);
                             po.clear();
                         }
                     }

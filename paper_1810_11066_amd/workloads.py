@@ -196,3 +196,45 @@ def bitwidth_sweep(batch: int = 128) -> List[ConvCase]:
                 14, 256, 256, 3, 1, 1, abits, wbits,
                 seed=seed_for(6, 10 * abits + wbits)))
     return out
+
+
+@dataclass
+class ChainLayer:
+    """One conv of a chained network: input shape, filters, next-layer
+    requantization scale (None for the last layer, which keeps int32)."""
+    name: str
+    h: int
+    w: int
+    c: int
+    oc: int
+    k: int
+    stride: int
+    pad: int
+    seed: int
+    out_scale: Optional[float] = None
+
+    def weights(self, wbits: int) -> np.ndarray:
+        return uniform_codes((self.oc, self.k, self.k, self.c), wbits,
+                             self.seed + 1)
+
+
+def resnet18_chain(abits: int = 2, wbits: int = 1) -> List[ChainLayer]:
+    """The 16 3x3 convs of ResNet-18 after conv1 (Table 1 layers 2, 4, 6, 7,
+    9, 10, 12 with their multiplicities 4, 1, 3, 1, 3, 1, 3), chained without
+    the residual adds and the 1x1 shortcut convs.  Each layer's output is
+    requantized to abits-bit codes with a scale that maps twice the mean
+    result of uniform codes, (2^A - 1)/2 * (2^W - 1)/2 * 9 C, to the top
+    code; the last layer keeps its int32 output."""
+    stages = [(2, 56, 64, 64, 1, 4), (4, 56, 64, 128, 2, 1),
+              (6, 28, 128, 128, 1, 3), (7, 28, 128, 256, 2, 1),
+              (9, 14, 256, 256, 1, 3), (10, 14, 256, 512, 2, 1),
+              (12, 7, 512, 512, 1, 3)]
+    out = []
+    for (layer, hw, c, oc, s, reps) in stages:
+        for r in range(reps):
+            mean = ((1 << abits) - 1) / 2 * ((1 << wbits) - 1) / 2 * 9 * c
+            out.append(ChainLayer("L%d.%d" % (layer, r), hw, hw, c, oc, 3, s,
+                                  1, seed_for(7, 10 * len(out)),
+                                  ((1 << abits) - 1) / (2 * mean)))
+    out[-1].out_scale = None
+    return out

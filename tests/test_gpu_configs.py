@@ -156,3 +156,35 @@ def test_config5_bipolar_a3w3(oracle, case):
 def test_bitwidth_sweep_layer9(oracle, case):
     say(case.name)
     check_sampled(oracle, case, n_random=4096)
+
+
+def test_resnet18_chain_batch2(oracle):
+    # the 16 chained 3x3 convs (bs_conv2d_requant between layers) on two
+    # images, against the oracle's conv -> quantize(float32) -> pack per layer
+    batch, abits, wbits = 2, 2, 1
+    layers = wl.resnet18_chain(abits, wbits)
+    x = wl.normal_floats((batch, 56, 56, 64), wl.seed_for(7))
+    cur_dev = bs.quantize_pack(dev(x), 1.0, abits)
+    cur = oracle.pack(oracle.quantize(x, 1.0, abits), abits)
+    torch.cuda.synchronize()
+    assert np.array_equal(words_np(cur_dev).reshape(cur.shape), cur)
+    for L in layers:
+        say("chain", L.name)
+        wq = L.weights(wbits)
+        w_dev = bs.pack(dev(wq), wbits)
+        spec = bs.Conv2dSpec(batch, L.h, L.w, L.c, L.oc, L.k, L.k, L.stride,
+                             L.pad, abits, wbits)
+        conv = oracle.conv2d(oracle.conv_params(batch, L.h, L.w, L.c, L.oc,
+                                                L.k, L.k, L.stride, L.pad,
+                                                abits, wbits),
+                             cur, oracle.pack(wq, wbits))
+        if L.out_scale is None:
+            got = bs.conv2d(spec, cur_dev, w_dev).cpu().numpy()
+            assert np.array_equal(got, conv)
+        else:
+            cur = oracle.pack(oracle.quantize(conv.astype(np.float32),
+                                              L.out_scale, abits), abits)
+            cur_dev = bs.conv2d_requant(spec, cur_dev, w_dev, L.out_scale,
+                                        abits)
+            torch.cuda.synchronize()
+            assert np.array_equal(words_np(cur_dev).reshape(cur.shape), cur)
