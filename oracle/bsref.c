@@ -40,12 +40,15 @@ int bsref_quantize(const float *x, uint8_t *q, int64_t n, float scale,
         return BSREF_EINVAL;
     if (!isfinite(scale) || !(scale > 0.0f))
         return BSREF_EINVAL;
-    if (enc != BSREF_UNIPOLAR && enc != BSREF_BIPOLAR)
+    if (enc != BSREF_UNIPOLAR && enc != BSREF_BIPOLAR && enc != BSREF_SIGNED)
         return BSREF_EINVAL;
     if (enc == BSREF_BIPOLAR && bits != 1)
         return BSREF_EINVAL;
+    if (enc == BSREF_SIGNED && bits < 2)
+        return BSREF_EINVAL;
 
     const int qmax = (1 << bits) - 1;
+    const int smin = -(1 << (bits - 1)), smax = (1 << (bits - 1)) - 1;
     for (int64_t i = 0; i < n; ++i) {
         if (enc == BSREF_BIPOLAR) {
             /* sign of the datum: +1 (bit 1) for x >= 0, -1 (bit 0) otherwise */
@@ -54,6 +57,19 @@ int bsref_quantize(const float *x, uint8_t *q, int64_t n, float scale,
         }
         float product = x[i] * scale;   /* one binary32 multiply */
         float r = rintf(product);       /* ties to even (default mode) */
+        if (enc == BSREF_SIGNED) {
+            int v;
+            if (r != r)                 /* NaN */
+                v = 0;
+            else if (r <= (float)smin)  /* saturate both ends */
+                v = smin;
+            else if (r >= (float)smax)
+                v = smax;
+            else
+                v = (int)r;
+            q[i] = (uint8_t)((unsigned)v & (unsigned)qmax);  /* two's complement */
+            continue;
+        }
         uint8_t v;
         if (!(r > 0.0f))                /* negative, zero or NaN */
             v = 0;
@@ -95,6 +111,45 @@ int bsref_pack(const uint8_t *q, uint32_t *packed, int64_t rows, int64_t k,
     return BSREF_OK;
 }
 
+int bsref_pack_ex(const uint8_t *q, uint32_t *packed, int64_t outer,
+                  int64_t k, int64_t inner, int bits, int layout)
+{
+    if (!q || !packed || outer < 0 || inner < 1 || k < 1 || bits < 1 ||
+        bits > 8)
+        return BSREF_EINVAL;
+    if (layout != BSREF_LAYOUT_MBK && layout != BSREF_LAYOUT_MKB &&
+        layout != BSREF_LAYOUT_BMK)
+        return BSREF_EINVAL;
+    const int64_t kw = words_for(k);
+    const int64_t rows = outer * inner;
+    for (int64_t o = 0; o < outer; ++o) {
+        for (int64_t i = 0; i < inner; ++i) {
+            const int64_t r = o * inner + i;
+            for (int b = 0; b < bits; ++b) {
+                for (int64_t t = 0; t < kw; ++t) {
+                    uint32_t word = 0;
+                    for (int u = 0; u < 32; ++u) {
+                        int64_t e = 32 * t + u;
+                        if (e < k) {
+                            uint8_t v = q[(o * k + e) * inner + i];
+                            word |= (((uint32_t)v >> b) & 1u) << u;
+                        }
+                    }
+                    int64_t at;
+                    if (layout == BSREF_LAYOUT_MBK)
+                        at = (r * bits + b) * kw + t;
+                    else if (layout == BSREF_LAYOUT_MKB)
+                        at = (r * kw + t) * bits + b;
+                    else
+                        at = ((int64_t)b * rows + r) * kw + t;
+                    packed[at] = word;
+                }
+            }
+        }
+    }
+    return BSREF_OK;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Decoding of packed elements back to integer values.                        */
 /* ------------------------------------------------------------------------ */
@@ -105,26 +160,34 @@ static int plane_bit(const uint32_t *vec, int64_t kw, int plane, int64_t c)
     return (int)((vec[plane * kw + c / 32] >> (c % 32)) & 1u);
 }
 
-/* unipolar activation value: sum_i 2^i a_i */
-static int64_t act_value(const uint32_t *vec, int64_t kw, int abits, int64_t c)
+/* integer value of element c of a [bits][kw] packed vector:
+ *   unipolar  sum_j 2^j b_j
+ *   bipolar   sum_j 2^j (2 b_j - 1)       (Sec. 2.2: bit 1 -> +1, 0 -> -1)
+ *   signed    two's complement: the top plane weighs -2^(bits-1)
+ *             (Sec. 2.2: binary dot products weighted by their sign) */
+static int64_t code_value(const uint32_t *vec, int64_t kw, int bits, int enc,
+                          int64_t c)
 {
     int64_t v = 0;
-    for (int i = 0; i < abits; ++i)
-        v += (int64_t)plane_bit(vec, kw, i, c) << i;
-    return v;
-}
-
-/* weight value: sum_j 2^j w_j (unipolar) or sum_j 2^j (2 w_j - 1) (bipolar) */
-static int64_t weight_value(const uint32_t *vec, int64_t kw, int wbits,
-                            int enc, int64_t c)
-{
-    int64_t v = 0;
-    for (int j = 0; j < wbits; ++j) {
+    for (int j = 0; j < bits; ++j) {
         int64_t bit = plane_bit(vec, kw, j, c);
-        int64_t level = (enc == BSREF_BIPOLAR) ? (2 * bit - 1) : bit;
+        int64_t level;
+        if (enc == BSREF_BIPOLAR)
+            level = 2 * bit - 1;
+        else if (enc == BSREF_SIGNED && j == bits - 1)
+            level = -bit;
+        else
+            level = bit;
         v += level * ((int64_t)1 << j);
     }
     return v;
+}
+
+static int valid_enc(int enc, int bits)
+{
+    if (enc == BSREF_UNIPOLAR || enc == BSREF_BIPOLAR)
+        return 1;
+    return enc == BSREF_SIGNED && bits >= 2;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -155,9 +218,7 @@ static int check_conv(const bsref_conv2d_params *p, int32_t *oh, int32_t *ow)
         return BSREF_EINVAL;
     if (p->abits < 1 || p->abits > 8 || p->wbits < 1 || p->wbits > 8)
         return BSREF_EINVAL;
-    if (p->aenc != BSREF_UNIPOLAR)
-        return BSREF_EINVAL;
-    if (p->wenc != BSREF_UNIPOLAR && p->wenc != BSREF_BIPOLAR)
+    if (!valid_enc(p->aenc, p->abits) || !valid_enc(p->wenc, p->wbits))
         return BSREF_EINVAL;
     return bsref_conv2d_out_shape(p, oh, ow);
 }
@@ -182,8 +243,8 @@ static int64_t conv_point(const bsref_conv2d_params *p, const uint32_t *act,
             const uint32_t *wvec =
                 wts + ((o * p->kh + r) * p->kw + s) * p->wbits * cw;
             for (int64_t c = 0; c < p->c; ++c)
-                sum += act_value(avec, cw, p->abits, c) *
-                       weight_value(wvec, cw, p->wbits, p->wenc, c);
+                sum += code_value(avec, cw, p->abits, p->aenc, c) *
+                       code_value(wvec, cw, p->wbits, p->wenc, c);
         }
     }
     return sum;
@@ -250,14 +311,15 @@ int bsref_conv2d_at(const bsref_conv2d_params *p, const uint32_t *act,
 /* ------------------------------------------------------------------------ */
 /* Dense (Sec. 3.2, Sec. 6.2.1): out[m][n] = sum_k a(m,k) w(n,k).             */
 /* ------------------------------------------------------------------------ */
-int bsref_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,
-                int wenc, const uint32_t *a, const uint32_t *w, int32_t *out)
+int bsref_dense_ex(int64_t m, int64_t n, int64_t k, int abits, int aenc,
+                   int wbits, int wenc, const uint32_t *a, const uint32_t *w,
+                   int32_t *out)
 {
     if (!a || !w || !out || m < 1 || n < 1 || k < 1)
         return BSREF_EINVAL;
     if (abits < 1 || abits > 8 || wbits < 1 || wbits > 8)
         return BSREF_EINVAL;
-    if (wenc != BSREF_UNIPOLAR && wenc != BSREF_BIPOLAR)
+    if (!valid_enc(aenc, abits) || !valid_enc(wenc, wbits))
         return BSREF_EINVAL;
     const int64_t kw = words_for(k);
     int bad = 0;
@@ -268,12 +330,19 @@ int bsref_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,
             const uint32_t *wvec = w + j * wbits * kw;
             int64_t sum = 0;
             for (int64_t c = 0; c < k; ++c)
-                sum += act_value(avec, kw, abits, c) *
-                       weight_value(wvec, kw, wbits, wenc, c);
+                sum += code_value(avec, kw, abits, aenc, c) *
+                       code_value(wvec, kw, wbits, wenc, c);
             if (sum > INT32_MAX || sum < INT32_MIN)
                 bad = 1;
             out[i * n + j] = (int32_t)sum;
         }
     }
     return bad ? BSREF_ERANGE : BSREF_OK;
+}
+
+int bsref_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,
+                int wenc, const uint32_t *a, const uint32_t *w, int32_t *out)
+{
+    return bsref_dense_ex(m, n, k, abits, BSREF_UNIPOLAR, wbits, wenc, a, w,
+                          out);
 }

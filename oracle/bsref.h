@@ -28,13 +28,23 @@ extern "C" {
 
 #define BSREF_UNIPOLAR 0
 #define BSREF_BIPOLAR 1
+#define BSREF_SIGNED 2
+
+/* Packed layouts (Sec. 3.1, bitpacking operator): where the bit axis B sits
+ * relative to the row axis M and the packed reduction axis K'. */
+#define BSREF_LAYOUT_MBK 0   /* [rows][bits][words] */
+#define BSREF_LAYOUT_MKB 1   /* [rows][words][bits] */
+#define BSREF_LAYOUT_BMK 2   /* [bits][rows][words] */
 
 /* Quantization of float data to k bits (Sec. 3.1; contribution list, Sec. 1).
  * The paper names the operator but prints no formula.  Reading used here:
  *   unipolar: q = clamp(round_half_even(fl32(x * scale)), 0, 2^bits - 1),
  *             NaN -> 0, +inf -> 2^bits - 1, -inf -> 0, denormals kept;
  *   bipolar (bits == 1 only): q = 1 if x >= 0 (so -0.0 -> 1) else 0, NaN -> 0;
- *             bit 1 encodes +1 and bit 0 encodes -1 (Sec. 2.2, bipolar format).
+ *             bit 1 encodes +1 and bit 0 encodes -1 (Sec. 2.2, bipolar format);
+ *   signed (bits >= 2): v = clamp(round_half_even(fl32(x * scale)),
+ *             -2^(bits-1), 2^(bits-1) - 1), NaN -> 0, stored as the low `bits`
+ *             bits of v in two's complement (Sec. 2.2, signed data).
  * x: [n] float32, q: [n] uint8.  scale must be finite and > 0. */
 int bsref_quantize(const float *x, uint8_t *q, int64_t n, float scale,
                    int bits, int enc);
@@ -46,15 +56,27 @@ int bsref_quantize(const float *x, uint8_t *q, int64_t n, float scale,
 int bsref_pack(const uint8_t *q, uint32_t *packed, int64_t rows, int64_t k,
                int bits);
 
+/* General bit packing (Sec. 3.1): the input is viewed as [outer][k][inner]
+ * with the reduction axis k at stride `inner` (inner = 1 is bsref_pack's
+ * [rows][k]; NCHW activations are outer = n, k = c, inner = h*w, and OIHW
+ * filters outer = oc, k = c, inner = kh*kw).  Row r = o*inner + i of the packed
+ * tensor holds the k elements q[o][.][i]; the bit axis sits where `layout`
+ * says (BSREF_LAYOUT_*).  Word and bit order as in bsref_pack. */
+int bsref_pack_ex(const uint8_t *q, uint32_t *packed, int64_t outer,
+                  int64_t k, int64_t inner, int bits, int layout);
+
 /* Bitserial 2-D convolution, NHWC activations, OHWI filters (Sec. 3.2).
  * The bitserial form (Eq. 1, Eq. 2) reaches exactly the integer convolution of
  * the quantized values, so this oracle computes that convolution as written:
- * decode each packed element to its integer value and sum products.
- *   activation value  a = sum_i 2^i a_i                     (unipolar only)
- *   weight value      w = sum_j 2^j w_j                     (unipolar)
- *                     w = sum_j 2^j (2 w_j - 1)             (bipolar weights)
- *   out[n][oh][ow][o] = sum over in-range taps (kh,kw) and channels c of a*w,
- * taps that fall in the zero padding contribute nothing.
+ * decode each packed element to its integer value and sum products.  The same
+ * decoding applies to activations (aenc) and weights (wenc), with b_j the bit
+ * of plane j and B the bit-width:
+ *   unipolar  v = sum_j 2^j b_j
+ *   bipolar   v = sum_j 2^j (2 b_j - 1)        (B = 1: bit 1 -> +1, 0 -> -1)
+ *   signed    v = sum_{j<B-1} 2^j b_j - 2^(B-1) b_{B-1}   (B >= 2)
+ *   out[n][oh][ow][o] = sum over in-range taps (kh,kw) and channels c of a*w;
+ * taps that fall in the padding contribute nothing (zero padding of the value
+ * tensor, also for bipolar activations).
  * act: [n][h][w][abits][ceil(c/32)], wts: [oc][kh][kw][wbits][ceil(c/32)],
  * out: [n][oh][ow][oc] int32 with oh = (h + 2 pad_h - kh) / stride_h + 1. */
 typedef struct {
@@ -80,6 +102,10 @@ int bsref_conv2d_at(const bsref_conv2d_params *p, const uint32_t *act,
  * a: [m][abits][ceil(k/32)], w: [n][wbits][ceil(k/32)], out: [m][n] int32. */
 int bsref_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,
                 int wenc, const uint32_t *a, const uint32_t *w, int32_t *out);
+/* The same with an activation encoding as well. */
+int bsref_dense_ex(int64_t m, int64_t n, int64_t k, int abits, int aenc,
+                   int wbits, int wenc, const uint32_t *a, const uint32_t *w,
+                   int32_t *out);
 
 /* Number of host threads the oracle's parallel loops use. */
 int bsref_threads(void);

@@ -11,9 +11,14 @@ documented in ``bsref.h``; the paper passages they follow are:
 * ``quantize``  -- quantization of float data to k bits (Sec. 3.1)
 * ``pack``      -- bit-plane split and packing into uint32 words (Sec. 2.2,
   Sec. 3.1, layout MBK')
+* ``pack_ex``   -- the same with any reduction-axis stride and bit-axis
+  position (MBK', MK'B, BMK'; Sec. 3.1)
 * ``conv2d``    -- bitserial conv2d, NHWC / OHWI (Sec. 3.2; Eq. 1, Eq. 2 reach
   exactly the integer convolution, which is what the oracle evaluates)
 * ``dense``     -- bitserial dense / matmul (Sec. 3.2, Sec. 6.2.1)
+
+Encodings (Sec. 2.2): unipolar codes, bipolar (+-1) codes and signed (two's
+complement) codes, for activations and weights alike.
 """
 from __future__ import annotations
 
@@ -30,6 +35,11 @@ _LIB_PATH = os.path.join(_HERE, "libbsref.so")
 
 UNIPOLAR = 0
 BIPOLAR = 1
+SIGNED = 2
+
+LAYOUT_MBK = 0
+LAYOUT_MKB = 1
+LAYOUT_BMK = 2
 
 _lock = threading.Lock()
 _lib = None
@@ -68,6 +78,7 @@ def _load():
         ci = ctypes.c_int
         lib.bsref_quantize.argtypes = [P, P, i64, ctypes.c_float, ci, ci]
         lib.bsref_pack.argtypes = [P, P, i64, i64, ci]
+        lib.bsref_pack_ex.argtypes = [P, P, i64, i64, i64, ci, ci]
         lib.bsref_conv2d_out_shape.argtypes = [
             ctypes.POINTER(ConvParams), ctypes.POINTER(ctypes.c_int32),
             ctypes.POINTER(ctypes.c_int32)]
@@ -75,9 +86,10 @@ def _load():
         lib.bsref_conv2d_at.argtypes = [ctypes.POINTER(ConvParams), P, P, P,
                                         i64, P]
         lib.bsref_dense.argtypes = [i64, i64, i64, ci, ci, ci, P, P, P]
-        for fn in ("bsref_quantize", "bsref_pack", "bsref_conv2d_out_shape",
-                   "bsref_conv2d", "bsref_conv2d_at", "bsref_dense",
-                   "bsref_threads"):
+        lib.bsref_dense_ex.argtypes = [i64, i64, i64, ci, ci, ci, ci, P, P, P]
+        for fn in ("bsref_quantize", "bsref_pack", "bsref_pack_ex",
+                   "bsref_conv2d_out_shape", "bsref_conv2d", "bsref_conv2d_at",
+                   "bsref_dense", "bsref_dense_ex", "bsref_threads"):
             getattr(lib, fn).restype = ci
         _lib = lib
         return lib
@@ -120,6 +132,26 @@ def pack(q: np.ndarray, bits: int):
     out = np.empty(q.shape[:-1] + (bits, words(k)), dtype=np.uint32)
     _check(_load().bsref_pack(_ptr(q), _ptr(out), rows, k, bits),
            "bsref_pack")
+    return out
+
+
+def pack_ex(q: np.ndarray, bits: int, axis: int = -1,
+            layout: int = LAYOUT_MBK):
+    """Pack along ``axis`` of q (any rank).  The packed rows are the other
+    axes in order (the leading ones, then the trailing ones); the result is
+    [rows][bits][words] (MBK'), [rows][words][bits] (MK'B) or
+    [bits][rows][words] (BMK'), rows flattened."""
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    axis = axis % q.ndim
+    k = q.shape[axis]
+    outer = int(np.prod(q.shape[:axis], dtype=np.int64))
+    inner = int(np.prod(q.shape[axis + 1:], dtype=np.int64))
+    rows, kw = outer * inner, words(k)
+    shape = {LAYOUT_MBK: (rows, bits, kw), LAYOUT_MKB: (rows, kw, bits),
+             LAYOUT_BMK: (bits, rows, kw)}[layout]
+    out = np.empty(shape, dtype=np.uint32)
+    _check(_load().bsref_pack_ex(_ptr(q), _ptr(out), outer, k, inner, bits,
+                                 layout), "bsref_pack_ex")
     return out
 
 
@@ -172,12 +204,12 @@ def conv2d_at(p: ConvParams, act: np.ndarray, wts: np.ndarray,
 
 
 def dense(a: np.ndarray, w: np.ndarray, m: int, n: int, k: int, abits: int,
-          wbits: int, wenc: int = UNIPOLAR) -> np.ndarray:
+          wbits: int, wenc: int = UNIPOLAR, aenc: int = UNIPOLAR) -> np.ndarray:
     a = np.ascontiguousarray(a, dtype=np.uint32)
     w = np.ascontiguousarray(w, dtype=np.uint32)
     if a.size != m * abits * words(k) or w.size != n * wbits * words(k):
         raise ValueError("packed operand size mismatch")
     out = np.empty((m, n), dtype=np.int32)
-    _check(_load().bsref_dense(m, n, k, abits, wbits, wenc, _ptr(a), _ptr(w),
-                               _ptr(out)), "bsref_dense")
+    _check(_load().bsref_dense_ex(m, n, k, abits, aenc, wbits, wenc, _ptr(a),
+                                  _ptr(w), _ptr(out)), "bsref_dense_ex")
     return out

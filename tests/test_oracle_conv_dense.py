@@ -187,8 +187,9 @@ def test_conv_rejects(oracle):
               pad_h=1, pad_w=1, abits=2, wbits=1, aenc=0, wenc=0)
     a = np.zeros((1, 4, 4, 2, 1), np.uint32)
     w = np.zeros((2, 3, 3, 1, 1), np.uint32)
-    for bad in (dict(abits=0), dict(wbits=9), dict(aenc=1), dict(stride_h=0),
-                dict(pad_w=-1), dict(kh=7, pad_h=0), dict(wenc=2)):
+    for bad in (dict(abits=0), dict(wbits=9), dict(aenc=3), dict(stride_h=0),
+                dict(pad_w=-1), dict(kh=7, pad_h=0), dict(wenc=2),
+                dict(aenc=2, abits=1), dict(wenc=-1)):
         p = oracle.ConvParams(**{**ok, **bad})
         with pytest.raises((oracle.OracleError, ValueError)):
             oracle.conv2d(p, a, w)
