@@ -45,7 +45,12 @@ CONV_SOURCES = ["paper_1810_11066_amd/csrc/bs_internal.h",
                 "paper_1810_11066_amd/csrc/conv_pix_a1.hip",
                 "paper_1810_11066_amd/csrc/conv_pix_a2.hip",
                 "paper_1810_11066_amd/csrc/conv_pix_a3.hip",
-                "paper_1810_11066_amd/csrc/conv_pix_a4.hip"]
+                "paper_1810_11066_amd/csrc/conv_pix_a4.hip",
+                "paper_1810_11066_amd/csrc/conv_pix_s1.hip",
+                "paper_1810_11066_amd/csrc/conv_pix_s2.hip",
+                "paper_1810_11066_amd/csrc/conv_pix_s3.hip",
+                "paper_1810_11066_amd/csrc/conv_pix_s4.hip",
+                "paper_1810_11066_amd/csrc/conv_pix_b.hip"]
 
 
 def popcount_roofline_tops(abits: int, wbits: int) -> float:
@@ -145,7 +150,8 @@ def prepare(case, n_sets, bs, torch, np):
     else:
         params = bs.Conv2dSpec(case.n, case.h, case.w, case.c, case.oc,
                                case.k, case.k, case.stride, case.pad,
-                               case.abits, case.wbits, case.wenc).params()
+                               case.abits, case.wbits, case.wenc,
+                               case.aenc).params()
         oh, ow = bs.bs_conv2d_out_shape(params)
         out_shape = (case.n, oh, ow, case.oc)
     quantized = (not dense) and case.act_scale is not None
@@ -165,7 +171,7 @@ def prepare(case, n_sets, bs, torch, np):
             ev[0].record(stream)
         if quantized:
             bs.bs_quantize_pack(x, packed, rows, k, case.act_scale, abits,
-                                bs.UNIPOLAR, stream)
+                                case.aenc, stream)
         else:
             bs.bs_pack(x, packed, rows, k, abits, stream)
         if ev is not None:
@@ -231,6 +237,9 @@ def case_bytes(case):
     return src + packed, packed + wbytes + out
 
 
+ENC_NAMES = ("unipolar", "bipolar", "signed")
+
+
 def case_line(case, m, args):
     """One JSON result object for a workload other than the headline one."""
     from paper_1810_11066_amd import workloads as wl
@@ -266,8 +275,8 @@ def case_line(case, m, args):
                    "(activations) + " + ("bs_dense" if dense
                                          else "bs_conv2d"),
                    "abits": case.abits, "wbits": case.wbits,
-                   "encoding": "bipolar" if getattr(case, "wenc", 0)
-                   else "unipolar"},
+                   "encoding": ENC_NAMES[getattr(case, "wenc", 0)],
+                   "act_encoding": ENC_NAMES[getattr(case, "aenc", 0)]},
         "roofline": roof,
         "pack_roofline": {
             "bound": "hbm",
@@ -453,6 +462,10 @@ def main() -> int:
                          "chained with bs_conv2d_requant: quantize+pack of "
                          "the float input, 15 requantizing convs, one int32 "
                          "conv; one line with the total and per-layer times")
+    ap.add_argument("--encodings", action="store_true",
+                    help="config 5's shapes with +-1 activations and weights "
+                         "(XNOR), signed A3W3, and unipolar A2 x signed W2: "
+                         "one line per case")
     ap.add_argument("--sweep", action="store_true",
                     help="bit-width sweep A1-4 x W1-4 on ResNet-18 layer 9 "
                          "(batch 128): one line per pair, then a summary "
@@ -480,9 +493,11 @@ def main() -> int:
     if args.chain:
         return chain_line(args, bs, torch, np, wl)
 
-    if args.sweep or args.config != 2:
+    if args.sweep or args.encodings or args.config != 2:
         if args.sweep:
             cases = wl.bitwidth_sweep()
+        elif args.encodings:
+            cases = wl.encodings()
         else:
             cases = {1: lambda: [wl.config1()], 3: lambda: [wl.config3()],
                      4: wl.config4, 5: wl.config5}[args.config]()

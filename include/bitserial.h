@@ -44,9 +44,23 @@ typedef enum {
     BS_ERR_HIP = 4          /* the HIP runtime refused the launch */
 } bs_status;
 
-/* Encoding of 1-bit planes (Sec. 2.2): unipolar {0,1}, or bipolar where bit 1
- * stands for +1 and bit 0 for -1. */
-typedef enum { BS_UNIPOLAR = 0, BS_BIPOLAR = 1 } bs_encoding;
+/* Encoding of the codes (Sec. 2.2), with b_j the bit of plane j of a B-bit code:
+ *   BS_UNIPOLAR  value sum_j 2^j b_j;
+ *   BS_BIPOLAR   value sum_j 2^j (2 b_j - 1): a 1-bit plane stands for +1
+ *                (bit 1) or -1 (bit 0), the form whose products the paper
+ *                computes with XNOR;
+ *   BS_SIGNED    two's complement (B >= 2): the top plane weighs -2^(B-1),
+ *                i.e. every binary dot product is weighted by the sign of its
+ *                planes. */
+typedef enum { BS_UNIPOLAR = 0, BS_BIPOLAR = 1, BS_SIGNED = 2 } bs_encoding;
+
+/* Position of the bit axis B in a packed tensor of rows M and packed
+ * reduction axis K' (Sec. 3.1, bitpacking operator): */
+typedef enum {
+    BS_LAYOUT_MBK = 0,   /* [rows][bits][words]  (what conv and dense read) */
+    BS_LAYOUT_MKB = 1,   /* [rows][words][bits]  (bits innermost) */
+    BS_LAYOUT_BMK = 2    /* [bits][rows][words]  (bits outermost) */
+} bs_layout;
 
 /* A hipStream_t, kept opaque so this header does not need HIP headers. */
 typedef void *bs_stream_t;
@@ -79,6 +93,25 @@ bs_status bs_quantize(const float *x, uint8_t *q, int64_t n, float scale,
 bs_status bs_pack(const uint8_t *q, uint32_t *packed, int64_t rows, int64_t k,
                   int bits, bs_stream_t stream);
 
+/* General bit packing (Sec. 3.1: the caller chooses the reduction axis and
+ * where the bit axis goes).  q is viewed as [outer][k][inner] uint8 codes
+ * (device): the reduction axis k has stride `inner`.  Packed row
+ * r = o * inner + i holds the k codes q[o][.][i]; words and bits as in bs_pack,
+ * in the given layout:
+ *   BS_LAYOUT_MBK  packed[r][b][t]        (inner = 1: exactly bs_pack)
+ *   BS_LAYOUT_MKB  packed[r][t][b]
+ *   BS_LAYOUT_BMK  packed[b][r][t]        with t < ceil(k/32), b < bits.
+ * NCHW activations packed with outer = n, k = c, inner = h*w give the packed
+ * NHWC tensor bs_conv2d reads; OIHW filters (outer = oc, k = c,
+ * inner = kh*kw) give the packed OHWI filters.  packed (device) is fully
+ * overwritten, tail bits 0.
+ * Errors: BS_ERR_INVALID_ARG for NULL/misaligned pointers, outer < 0, k < 1,
+ * inner < 1, bits outside 1..8, an unknown layout; BS_ERR_UNSUPPORTED beyond
+ * 2^40 codes. */
+bs_status bs_pack_ex(const uint8_t *q, uint32_t *packed, int64_t outer,
+                     int64_t k, int64_t inner, int bits, bs_layout layout,
+                     bs_stream_t stream);
+
 /* Fused quantize + pack: identical output to bs_quantize followed by bs_pack
  * on the same [rows][k] float32 tensor, without the uint8 intermediate.
  * Errors: as bs_quantize and bs_pack. */
@@ -87,29 +120,33 @@ bs_status bs_quantize_pack(const float *x, uint32_t *packed, int64_t rows,
                            bs_stream_t stream);
 
 /* Bitserial 2-D convolution (Sec. 3.2; NHWC data, direct convolution without
- * an im2col copy).  Activations must be unipolar; filters may be unipolar or
- * bipolar.  Zero padding: taps outside the input contribute nothing.
+ * an im2col copy).  Activations and filters each take any bs_encoding.
  *   act_packed: [n][h][w][abits][ceil(c/32)] uint32 (bs_pack of NHWC codes)
  *   w_packed:   [oc][kh][kw][wbits][ceil(c/32)] uint32 (bs_pack of OHWI codes)
  *   out:        [n][oh][ow][oc] int32, oh = (h + 2 pad_h - kh) / stride_h + 1,
  *               ow likewise; every element is written.
- *   out[n][y][x][o] = sum over in-range taps (r,s), planes i<abits, j<wbits of
- *     2^(i+j) * sum_t f(a_i[t], w_j[t]),  f = popcount(a AND w) (unipolar) or
- *     popcount(a AND w) - popcount(a AND NOT w) (bipolar weights),
- *   which equals the integer convolution of the codes with weight values
- *   sum_j 2^j w_j (unipolar) or sum_j 2^j (2 w_j - 1) (bipolar).
+ *   out[n][y][x][o] = sum over in-range taps (r,s) and channels c of
+ *     value(a) * value(w), the values of the codes under aenc and wenc:
+ *     the integer convolution of the decoded tensors with zero padding (a
+ *     padded position is 0, also for bipolar activations, so it contributes
+ *     nothing).  Unipolar data is Eq. 2,
+ *     sum_{i,j} 2^(i+j) sum_t popcount(a_i[t] AND w_j[t]); bipolar operands
+ *     add popcount corrections (for +-1 data the sum over a tap's c channels
+ *     is c - 2 popcount(a XOR w), the XNOR form); signed operands weight
+ *     each plane pair by the sign of its planes.
  * Errors: BS_ERR_INVALID_ARG (NULL/misaligned pointers, non-positive sizes,
- * bit-widths outside 1..8, stride < 1, pad < 0, oh or ow < 1);
- * BS_ERR_UNSUPPORTED (bipolar activations, or sizes beyond the 2^31 pixel /
- * 2^31 word-index range); BS_ERR_OVERFLOW when
- * (2^abits - 1)(2^wbits - 1) kh kw c > 2^31 - 1. */
+ * bit-widths outside 1..8, an unknown encoding, signed data with fewer than
+ * 2 bits, stride < 1, pad < 0, oh or ow < 1); BS_ERR_UNSUPPORTED (sizes
+ * beyond the 2^31 pixel / 2^31 word-index range); BS_ERR_OVERFLOW when
+ * max|a| max|w| kh kw c > 2^31 - 1, with max|v| = 2^bits - 1 for unipolar
+ * and bipolar codes and 2^(bits-1) for signed ones. */
 typedef struct {
     int32_t n, h, w, c;       /* NHWC activations */
     int32_t oc, kh, kw;       /* OHWI filters: oc filters of kh x kw x c */
     int32_t stride_h, stride_w;
     int32_t pad_h, pad_w;
     int32_t abits, wbits;     /* 1..8 */
-    int32_t aenc, wenc;       /* bs_encoding; aenc must be BS_UNIPOLAR */
+    int32_t aenc, wenc;       /* bs_encoding of activations and filters */
 } bs_conv2d_params;
 
 /* Output height/width of a conv; BS_ERR_INVALID_ARG if either would be < 1. */
@@ -153,11 +190,19 @@ bs_status bs_conv2d_describe(const bs_conv2d_params *p, char *buf,
 /* Bitserial dense / matrix multiply (Sec. 3.2; evaluated in Sec. 6.2.1):
  *   a_packed: [m][abits][ceil(k/32)], w_packed: [n][wbits][ceil(k/32)] uint32
  *   (each output neuron's weights contiguous along the reduction axis),
- *   out: [m][n] int32, out[r][o] = sum_{i,j} 2^(i+j) sum_t f(a_i[t], w_j[t]).
- * Errors: as bs_conv2d, with the overflow bound (2^abits-1)(2^wbits-1) k. */
+ *   out: [m][n] int32, out[r][o] = sum_k value(a[r][k]) * value(w[o][k]),
+ *   unipolar activations, weights under wenc (as bs_conv2d).
+ * Errors: as bs_conv2d, with the overflow bound max|a| max|w| k. */
 bs_status bs_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,
                    bs_encoding wenc, const uint32_t *a_packed,
                    const uint32_t *w_packed, int32_t *out, bs_stream_t stream);
+
+/* bs_dense with an activation encoding as well (bipolar +-1 activations,
+ * signed activations).  Layouts, results and errors as bs_dense. */
+bs_status bs_dense_ex(int64_t m, int64_t n, int64_t k, int abits,
+                      bs_encoding aenc, int wbits, bs_encoding wenc,
+                      const uint32_t *a_packed, const uint32_t *w_packed,
+                      int32_t *out, bs_stream_t stream);
 
 /* Static description of a status code. */
 const char *bs_status_string(bs_status s);

@@ -35,11 +35,17 @@ BS_ERR_HIP = 4
 
 UNIPOLAR = 0
 BIPOLAR = 1
+SIGNED = 2
 
-EXPORTED = ("bs_packed_words", "bs_quantize", "bs_pack", "bs_quantize_pack",
+LAYOUT_MBK = 0
+LAYOUT_MKB = 1
+LAYOUT_BMK = 2
+
+EXPORTED = ("bs_packed_words", "bs_quantize", "bs_pack", "bs_pack_ex",
+            "bs_quantize_pack",
             "bs_conv2d_out_shape", "bs_conv2d", "bs_conv2d_requant",
             "bs_conv2d_describe",
-            "bs_dense", "bs_status_string",
+            "bs_dense", "bs_dense_ex", "bs_status_string",
             "bs_last_error", "bs_set_kernel_mode", "bs_set_units_per_wave",
             "bs_abi_version")
 
@@ -78,6 +84,7 @@ def load_library():
             "bs_packed_words": (i64, [i64]),
             "bs_quantize": (ci, [P, P, i64, cf, ci, ci, P]),
             "bs_pack": (ci, [P, P, i64, i64, ci, P]),
+            "bs_pack_ex": (ci, [P, P, i64, i64, i64, ci, ci, P]),
             "bs_quantize_pack": (ci, [P, P, i64, i64, cf, ci, ci, P]),
             "bs_conv2d_out_shape": (ci, [ctypes.POINTER(ConvParams),
                                          ctypes.POINTER(ctypes.c_int32),
@@ -88,6 +95,7 @@ def load_library():
             "bs_conv2d_describe": (ci, [ctypes.POINTER(ConvParams),
                                         ctypes.c_char_p, ctypes.c_int32]),
             "bs_dense": (ci, [i64, i64, i64, ci, ci, ci, P, P, P, P]),
+            "bs_dense_ex": (ci, [i64, i64, i64, ci, ci, ci, ci, P, P, P, P]),
             "bs_status_string": (ctypes.c_char_p, [ci]),
             "bs_last_error": (ctypes.c_char_p, []),
             "bs_set_kernel_mode": (ci, [ci]),
@@ -232,6 +240,25 @@ def bs_dense(m: int, n: int, k: int, abits: int, wbits: int, wenc: int,
         _dev(out, "out", torch.int32, m * n), _stream(stream)))
 
 
+def bs_dense_ex(m: int, n: int, k: int, abits: int, aenc: int, wbits: int,
+                wenc: int, a_packed: torch.Tensor, w_packed: torch.Tensor,
+                out: torch.Tensor, stream=None) -> None:
+    _check(load_library().bs_dense_ex(
+        m, n, k, int(abits), int(aenc), int(wbits), int(wenc),
+        _dev(a_packed, "a_packed", torch.int32, m * abits * words(k)),
+        _dev(w_packed, "w_packed", torch.int32, n * wbits * words(k)),
+        _dev(out, "out", torch.int32, m * n), _stream(stream)))
+
+
+def bs_pack_ex(q: torch.Tensor, packed: torch.Tensor, outer: int, k: int,
+               inner: int, bits: int, layout: int = LAYOUT_MBK,
+               stream=None) -> None:
+    _check(load_library().bs_pack_ex(
+        _dev(q, "q", torch.uint8, outer * k * inner),
+        _dev(packed, "packed", torch.int32, outer * inner * bits * words(k)),
+        outer, k, inner, int(bits), int(layout), _stream(stream)))
+
+
 def bs_set_kernel_mode(mode: int) -> None:
     _check(load_library().bs_set_kernel_mode(int(mode)))
 
@@ -264,11 +291,12 @@ class Conv2dSpec:
     abits: int = 1
     wbits: int = 1
     wenc: int = UNIPOLAR
+    aenc: int = UNIPOLAR
 
     def params(self) -> ConvParams:
         return ConvParams(self.n, self.h, self.w, self.c, self.oc, self.kh,
                           self.kw, self.stride, self.stride, self.pad,
-                          self.pad, self.abits, self.wbits, UNIPOLAR,
+                          self.pad, self.abits, self.wbits, self.aenc,
                           self.wenc)
 
 
@@ -285,6 +313,25 @@ def pack(q: torch.Tensor, bits: int) -> torch.Tensor:
     out = torch.empty(tuple(q.shape[:-1]) + (bits, words(k)),
                       dtype=torch.int32, device=q.device)
     bs_pack(q, out, rows, k, bits)
+    return out
+
+
+def pack_ex(q: torch.Tensor, bits: int, axis: int = -1,
+            layout: int = LAYOUT_MBK) -> torch.Tensor:
+    """Pack q (any rank, uint8) along ``axis``; the packed rows are the
+    other axes in order.  Returns [rows][bits][words] (MBK'),
+    [rows][words][bits] (MK'B) or [bits][rows][words] (BMK') int32 words."""
+    axis = axis % q.dim()
+    k = q.shape[axis]
+    outer = 1
+    for d in q.shape[:axis]:
+        outer *= d
+    inner = q.numel() // (outer * k)
+    rows, kw = outer * inner, words(k)
+    shape = {LAYOUT_MBK: (rows, bits, kw), LAYOUT_MKB: (rows, kw, bits),
+             LAYOUT_BMK: (bits, rows, kw)}[layout]
+    out = torch.empty(shape, dtype=torch.int32, device=q.device)
+    bs_pack_ex(q, out, outer, k, inner, bits, layout)
     return out
 
 
@@ -309,7 +356,12 @@ def conv2d(spec: Conv2dSpec, act_packed: torch.Tensor,
 
 
 def dense(a_packed: torch.Tensor, w_packed: torch.Tensor, m: int, n: int,
-          k: int, abits: int, wbits: int, wenc: int = UNIPOLAR):
+          k: int, abits: int, wbits: int, wenc: int = UNIPOLAR,
+          aenc: int = UNIPOLAR):
     out = torch.empty((m, n), dtype=torch.int32, device=a_packed.device)
-    bs_dense(m, n, k, abits, wbits, wenc, a_packed, w_packed, out)
+    if aenc == UNIPOLAR:
+        bs_dense(m, n, k, abits, wbits, wenc, a_packed, w_packed, out)
+    else:
+        bs_dense_ex(m, n, k, abits, aenc, wbits, wenc, a_packed, w_packed,
+                    out)
     return out

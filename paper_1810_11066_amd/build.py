@@ -29,7 +29,9 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["api.hip", "quant_pack.hip", "conv.hip", "conv_fast_a1.hip",
            "conv_fast_a2.hip", "conv_fast_a3.hip", "conv_fast_a4.hip",
            "conv_pix.hip", "conv_pix_a1.hip", "conv_pix_a2.hip",
-           "conv_pix_a3.hip", "conv_pix_a4.hip"]
+           "conv_pix_a3.hip", "conv_pix_a4.hip", "conv_pix_s1.hip",
+           "conv_pix_s2.hip", "conv_pix_s3.hip", "conv_pix_s4.hip",
+           "conv_pix_b.hip"]
 
 CFLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

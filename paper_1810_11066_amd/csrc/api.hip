@@ -48,25 +48,45 @@ bs_status check_bits(int bits, const char* name) {
     return BS_OK;
 }
 
+// An encoding of conv/dense operands: signed (two's complement) data needs a
+// sign plane and at least one magnitude plane.
+bs_status check_enc(int enc, int bits, const char* name) {
+    if (enc != BS_UNIPOLAR && enc != BS_BIPOLAR && enc != BS_SIGNED)
+        return fail(BS_ERR_INVALID_ARG, "unknown %s encoding %d", name, enc);
+    if (enc == BS_SIGNED && bits < 2)
+        return fail(BS_ERR_INVALID_ARG, "signed %s need >= 2 bits", name);
+    return BS_OK;
+}
+
 bs_status check_scale_enc(float scale, int bits, bs_encoding enc) {
     if (!isfinite(scale) || !(scale > 0.0f))
         return fail(BS_ERR_INVALID_ARG, "scale must be finite and > 0");
-    if (enc != BS_UNIPOLAR && enc != BS_BIPOLAR)
-        return fail(BS_ERR_INVALID_ARG, "unknown encoding %d", (int)enc);
+    bs_status st;
+    if ((st = check_enc((int)enc, bits, "quantization")) != BS_OK) return st;
     if (enc == BS_BIPOLAR && bits != 1)
         return fail(BS_ERR_INVALID_ARG,
                     "bipolar quantization is 1-bit (bits = %d)", bits);
     return BS_OK;
 }
 
-// (2^a - 1)(2^w - 1) * taps * c must fit int32 for the exact result to.
-bs_status check_overflow(int abits, int wbits, int64_t taps, int64_t c) {
-    unsigned __int128 bound = (unsigned __int128)((1u << abits) - 1) *
-                              ((1u << wbits) - 1) * (uint64_t)taps *
+// Largest magnitude a value of `bits` bits takes under an encoding:
+// unipolar 2^bits - 1, bipolar |2u - (2^bits - 1)| <= 2^bits - 1, signed
+// 2^(bits-1) (the most negative value).
+uint64_t max_abs(int enc, int bits) {
+    return enc == BS_SIGNED ? (1ull << (bits - 1)) : (1ull << bits) - 1;
+}
+
+// max|a| * max|w| * taps * c must fit int32 for the exact result to.
+bs_status check_overflow(int abits, int aenc, int wbits, int wenc,
+                         int64_t taps, int64_t c) {
+    unsigned __int128 bound = (unsigned __int128)max_abs(aenc, abits) *
+                              max_abs(wenc, wbits) * (uint64_t)taps *
                               (uint64_t)c;
     if (bound > (unsigned __int128)INT32_MAX)
         return fail(BS_ERR_OVERFLOW,
-                    "(2^%d-1)(2^%d-1)*%lld*%lld exceeds int32", abits, wbits,
+                    "%llu*%llu*%lld*%lld exceeds int32",
+                    (unsigned long long)max_abs(aenc, abits),
+                    (unsigned long long)max_abs(wenc, wbits),
                     (long long)taps, (long long)c);
     return BS_OK;
 }
@@ -84,18 +104,14 @@ bs_status check_conv(const bs_conv2d_params* p, bs::ConvShape* s) {
     bs_status st;
     if ((st = check_bits(p->abits, "abits")) != BS_OK) return st;
     if ((st = check_bits(p->wbits, "wbits")) != BS_OK) return st;
-    if (p->aenc != BS_UNIPOLAR && p->aenc != BS_BIPOLAR)
-        return fail(BS_ERR_INVALID_ARG, "unknown activation encoding");
-    if (p->wenc != BS_UNIPOLAR && p->wenc != BS_BIPOLAR)
-        return fail(BS_ERR_INVALID_ARG, "unknown weight encoding");
+    if ((st = check_enc(p->aenc, p->abits, "activation")) != BS_OK) return st;
+    if ((st = check_enc(p->wenc, p->wbits, "weight")) != BS_OK) return st;
     const int64_t eh = (int64_t)p->h + 2 * (int64_t)p->pad_h - p->kh;
     const int64_t ew = (int64_t)p->w + 2 * (int64_t)p->pad_w - p->kw;
     if (eh < 0 || ew < 0)
         return fail(BS_ERR_INVALID_ARG, "kernel larger than padded input");
-    if (p->aenc != BS_UNIPOLAR)
-        return fail(BS_ERR_UNSUPPORTED, "bipolar activations are not supported");
-    if ((st = check_overflow(p->abits, p->wbits, (int64_t)p->kh * p->kw,
-                             p->c)) != BS_OK)
+    if ((st = check_overflow(p->abits, p->aenc, p->wbits, p->wenc,
+                             (int64_t)p->kh * p->kw, p->c)) != BS_OK)
         return st;
     const int64_t oh = eh / p->stride_h + 1, ow = ew / p->stride_w + 1;
     const int64_t pixels = (int64_t)p->n * oh * ow;
@@ -110,6 +126,7 @@ bs_status check_conv(const bs_conv2d_params* p, bs::ConvShape* s) {
     s->ph = p->pad_h; s->pw = p->pad_w;
     s->oh = (int32_t)oh; s->ow = (int32_t)ow;
     s->abits = p->abits; s->wbits = p->wbits;
+    s->aenc = p->aenc; s->wenc = p->wenc;
     s->bipolar_w = p->wenc == BS_BIPOLAR;
     return BS_OK;
 }
@@ -118,7 +135,7 @@ bs_status check_conv(const bs_conv2d_params* p, bs::ConvShape* s) {
 
 extern "C" {
 
-int bs_abi_version(void) { return 102; }
+int bs_abi_version(void) { return 103; }
 
 int64_t bs_packed_words(int64_t k) { return k <= 0 ? 0 : (k + 31) / 32; }
 
@@ -157,8 +174,7 @@ bs_status bs_quantize(const float* x, uint8_t* q, int64_t n, float scale,
     if ((st = check_bits(bits, "bits")) != BS_OK) return st;
     if ((st = check_scale_enc(scale, bits, enc)) != BS_OK) return st;
     if (n == 0) return ok();
-    return from_hip(bs::launch_quantize(x, q, n, scale, bits,
-                                        enc == BS_BIPOLAR,
+    return from_hip(bs::launch_quantize(x, q, n, scale, bits, (int)enc,
                                         (hipStream_t)stream),
                     "bs_quantize launch");
 }
@@ -179,6 +195,28 @@ bs_status bs_pack(const uint8_t* q, uint32_t* packed, int64_t rows, int64_t k,
                     "bs_pack launch");
 }
 
+bs_status bs_pack_ex(const uint8_t* q, uint32_t* packed, int64_t outer,
+                     int64_t k, int64_t inner, int bits, bs_layout layout,
+                     bs_stream_t stream) {
+    bs_status st;
+    if ((st = check_ptr(q, "q")) != BS_OK) return st;
+    if ((st = check_ptr(packed, "packed")) != BS_OK) return st;
+    if (outer < 0) return fail(BS_ERR_INVALID_ARG, "outer < 0");
+    if (k < 1) return fail(BS_ERR_INVALID_ARG, "k < 1");
+    if (inner < 1) return fail(BS_ERR_INVALID_ARG, "inner < 1");
+    if ((st = check_bits(bits, "bits")) != BS_OK) return st;
+    if (layout != BS_LAYOUT_MBK && layout != BS_LAYOUT_MKB &&
+        layout != BS_LAYOUT_BMK)
+        return fail(BS_ERR_INVALID_ARG, "unknown layout %d", (int)layout);
+    if (k > ((int64_t)1 << 40) || inner > ((int64_t)1 << 40) / k ||
+        outer > ((int64_t)1 << 40) / (k * inner))
+        return fail(BS_ERR_UNSUPPORTED, "tensor too large");
+    if (outer == 0) return ok();
+    return from_hip(bs::launch_pack_ex(q, packed, outer, k, inner, bits,
+                                       (int)layout, (hipStream_t)stream),
+                    "bs_pack_ex launch");
+}
+
 bs_status bs_quantize_pack(const float* x, uint32_t* packed, int64_t rows,
                            int64_t k, float scale, int bits, bs_encoding enc,
                            bs_stream_t stream) {
@@ -193,8 +231,7 @@ bs_status bs_quantize_pack(const float* x, uint32_t* packed, int64_t rows,
         return fail(BS_ERR_UNSUPPORTED, "tensor too large");
     if (rows == 0) return ok();
     return from_hip(bs::launch_quantize_pack(x, packed, rows, k, scale, bits,
-                                             enc == BS_BIPOLAR,
-                                             (hipStream_t)stream),
+                                             (int)enc, (hipStream_t)stream),
                     "bs_quantize_pack launch");
 }
 
@@ -263,9 +300,10 @@ bs_status bs_conv2d_describe(const bs_conv2d_params* p, char* buf,
     return ok();
 }
 
-bs_status bs_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,
-                   bs_encoding wenc, const uint32_t* a_packed,
-                   const uint32_t* w_packed, int32_t* out, bs_stream_t stream) {
+bs_status bs_dense_ex(int64_t m, int64_t n, int64_t k, int abits,
+                      bs_encoding aenc, int wbits, bs_encoding wenc,
+                      const uint32_t* a_packed, const uint32_t* w_packed,
+                      int32_t* out, bs_stream_t stream) {
     bs_status st;
     if ((st = check_ptr(a_packed, "a_packed")) != BS_OK) return st;
     if ((st = check_ptr(w_packed, "w_packed")) != BS_OK) return st;
@@ -278,13 +316,20 @@ bs_status bs_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,
     bs_conv2d_params p;
     p.n = 1; p.h = 1; p.w = (int32_t)m; p.c = (int32_t)k; p.oc = (int32_t)n;
     p.kh = 1; p.kw = 1; p.stride_h = 1; p.stride_w = 1; p.pad_h = 0;
-    p.pad_w = 0; p.abits = abits; p.wbits = wbits; p.aenc = BS_UNIPOLAR;
+    p.pad_w = 0; p.abits = abits; p.wbits = wbits; p.aenc = aenc;
     p.wenc = wenc;
     bs::ConvShape s;
     if ((st = check_conv(&p, &s)) != BS_OK) return st;
     return from_hip(bs::launch_conv(s, a_packed, w_packed, out, g_conv_opt,
                                     (hipStream_t)stream),
                     "bs_dense launch");
+}
+
+bs_status bs_dense(int64_t m, int64_t n, int64_t k, int abits, int wbits,
+                   bs_encoding wenc, const uint32_t* a_packed,
+                   const uint32_t* w_packed, int32_t* out, bs_stream_t stream) {
+    return bs_dense_ex(m, n, k, abits, BS_UNIPOLAR, wbits, wenc, a_packed,
+                       w_packed, out, stream);
 }
 
 }  // extern "C"

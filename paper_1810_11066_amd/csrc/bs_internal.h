@@ -42,6 +42,30 @@ __device__ __forceinline__ uint32_t quant_code(float x, float scale,
     return (uint32_t)r;
 }
 
+// Signed (two's complement) code: round-half-to-even of the binary32
+// product clamped to [-(hmax + 1), hmax] with NaN sent to 0, returned as its
+// low bits (hmax = 2^(bits-1) - 1).
+__device__ __forceinline__ uint32_t quant_code_signed(float x, float scale,
+                                                      float hmax) {
+    float r = __builtin_rintf(x * scale);
+    r = r == r ? r : 0.0f;                 // NaN -> 0
+    r = r > -hmax - 1.0f ? r : -hmax - 1.0f;
+    r = r < hmax ? r : hmax;               // saturate (+-inf included)
+    return (uint32_t)(int32_t)r & (uint32_t)(2.0f * hmax + 1.0f);
+}
+
+// Operand encodings (the values of bs_encoding).
+constexpr int kUnipolar = 0, kBipolar = 1, kSigned = 2;
+
+// Code of one value under encoding ENC; qmax is 2^bits - 1 for unipolar
+// codes and 2^(bits-1) - 1 for signed ones (bipolar ignores it).
+template <int ENC>
+__device__ __forceinline__ uint32_t quant_code_enc(float x, float scale,
+                                                   float qmax) {
+    if constexpr (ENC == kSigned) return quant_code_signed(x, scale, qmax);
+    else return quant_code<ENC == kBipolar>(x, scale, qmax);
+}
+
 // Bits b of the four bytes of v (bit b of byte k -> bit k of the result).
 __device__ __forceinline__ uint32_t nibble_of(uint32_t v, int b) {
     uint32_t x = (v >> b) & 0x01010101u;
@@ -51,22 +75,33 @@ __device__ __forceinline__ uint32_t nibble_of(uint32_t v, int b) {
 
 // ---- launchers (each returns hipSuccess or the launch error) -------------
 
+// enc: kUnipolar, kBipolar or kSigned
 hipError_t launch_quantize(const float* x, uint8_t* q, int64_t n, float scale,
-                           int bits, bool bipolar, hipStream_t st);
+                           int bits, int enc, hipStream_t st);
 
 hipError_t launch_pack(const uint8_t* q, uint32_t* packed, int64_t rows,
                        int64_t k, int bits, hipStream_t st);
 
+// Packed layouts (the values of bs_layout).
+constexpr int kLayoutMBK = 0, kLayoutMKB = 1, kLayoutBMK = 2;
+
+// q viewed as [outer][k][inner], packed along k into the given layout with
+// rows o * inner + i.
+hipError_t launch_pack_ex(const uint8_t* q, uint32_t* packed, int64_t outer,
+                          int64_t k, int64_t inner, int bits, int layout,
+                          hipStream_t st);
+
 hipError_t launch_quantize_pack(const float* x, uint32_t* packed,
                                 int64_t rows, int64_t k, float scale, int bits,
-                                bool bipolar, hipStream_t st);
+                                int enc, hipStream_t st);
 
 // Geometry of a convolution as the kernels see it; dense is the 1x1 case
 // with n = 1, h = 1, w = m.
 struct ConvShape {
     int32_t n, h, w, c, oc, kh, kw, sh, sw, ph, pw, oh, ow;
     int32_t abits, wbits;
-    bool bipolar_w;
+    int32_t aenc, wenc;   // kUnipolar, kBipolar, kSigned
+    bool bipolar_w;       // wenc == kBipolar
 };
 
 // Kernel selection for a conv call.  mode 0: the fastest applicable kernel;

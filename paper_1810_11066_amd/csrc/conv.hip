@@ -56,12 +56,22 @@ struct GenericArgs {
     FastDiv div_oc, div_ow, div_oh;
 };
 
-// One output of the convolution, plain loops (Eq. 2 per tap and word).
+// One output of the convolution, plain loops over in-range taps and words.
+// With u the plain binary value sum_j +-2^j b_j of a code (the top plane of
+// signed data negative) every encoding is affine in u: value = alpha u + beta
+// with (alpha, beta) = (1, 0) for unipolar and signed codes and
+// (2, -(2^B - 1)) for bipolar ones.  Over the in-range taps
+//   sum value(a) value(w) = aa aw S + aa bw SA + ba aw SW + ba bw N
+// where S = sum_{i,j} +-2^(i+j) popcount(a_i AND w_j) (Eq. 2 with the sign of
+// each plane pair), SA and SW the plane-weighted popcounts of the activation
+// and weight words, and N the number of in-range channel values.  All sums
+// wrap in uint32; the host's overflow bound makes the result exact.
 __device__ __forceinline__ uint32_t generic_output(
     const ConvShape& s, const uint32_t* __restrict__ act,
     const uint32_t* __restrict__ wts, int cw, uint32_t img, uint32_t oy,
     uint32_t ox, uint32_t o) {
-    uint32_t sum = 0;
+    const bool sa_neg = s.aenc == kSigned, sw_neg = s.wenc == kSigned;
+    uint32_t sum = 0, sa = 0, sw = 0, nval = 0;
     for (int r = 0; r < s.kh; ++r) {
         const int iy = (int)oy * s.sh - s.ph + r;
         if (iy < 0 || iy >= s.h) continue;          // zero padding
@@ -74,20 +84,35 @@ __device__ __forceinline__ uint32_t generic_output(
             const uint32_t* wp =
                 wts + (((int64_t)o * s.kh + r) * s.kw + c) *
                           (int64_t)s.wbits * cw;
+            nval += (uint32_t)s.c;
             for (int t = 0; t < cw; ++t) {
                 for (int i = 0; i < s.abits; ++i) {
                     const uint32_t a = ap[i * cw + t];
+                    const bool ni = sa_neg && i == s.abits - 1;
+                    const uint32_t pa = (uint32_t)__builtin_popcount(a) << i;
+                    sa += ni ? 0u - pa : pa;
                     for (int j = 0; j < s.wbits; ++j) {
                         const uint32_t w = wp[j * cw + t];
-                        uint32_t term = __builtin_popcount(a & w);
-                        if (s.bipolar_w) term -= __builtin_popcount(a & ~w);
-                        sum += term << (i + j);
+                        const bool nj = sw_neg && j == s.wbits - 1;
+                        const uint32_t term =
+                            (uint32_t)__builtin_popcount(a & w) << (i + j);
+                        sum += ni != nj ? 0u - term : term;
                     }
+                }
+                for (int j = 0; j < s.wbits; ++j) {
+                    const bool nj = sw_neg && j == s.wbits - 1;
+                    const uint32_t pw =
+                        (uint32_t)__builtin_popcount(wp[j * cw + t]) << j;
+                    sw += nj ? 0u - pw : pw;
                 }
             }
         }
     }
-    return sum;
+    const uint32_t aa = s.aenc == kBipolar ? 2u : 1u;
+    const uint32_t ba = s.aenc == kBipolar ? 0u - ((1u << s.abits) - 1) : 0u;
+    const uint32_t aw = s.wenc == kBipolar ? 2u : 1u;
+    const uint32_t bw = s.wenc == kBipolar ? 0u - ((1u << s.wbits) - 1) : 0u;
+    return aa * aw * sum + aa * bw * sa + ba * aw * sw + ba * bw * nval;
 }
 
 __global__ __launch_bounds__(kBlock) void conv_generic_kernel(GenericArgs g) {
@@ -167,6 +192,8 @@ bool conv_has_fast_path(const ConvShape& s) {
     const int64_t cw = (s.c + 31) / 32;
     const int p = pick_group_pixels(s.ow);
     if (s.abits > 4 || s.wbits > 4) return false;
+    // unipolar activations with unipolar or bipolar filters only
+    if (s.aenc != kUnipolar || s.wenc == kSigned) return false;
     if (s.kh != s.kw || (s.kh != 1 && s.kh != 3)) return false;
     if (s.sh != s.sw || (s.sh != 1 && s.sh != 2)) return false;
     if (cw % 2 != 0) return false;
@@ -198,8 +225,8 @@ pix::PixKernelFn pix_kernel_for(const ConvShape& s, bool req,
     if (npix >= INT32_MAX || units >= INT32_MAX / 2) return nullptr;
     // the kernel addresses activation words with 32-bit offsets
     if ((int64_t)s.n * s.h * s.w * s.abits * cw >= INT32_MAX) return nullptr;
-    return pix::pick(s.abits, s.wbits, s.bipolar_w, s.kh, s.sh, (int)cw, req,
-                     info);
+    return pix::pick(s.abits, s.wbits, s.aenc, s.wenc, s.kh, s.sh, (int)cw,
+                     req, info);
 }
 
 // Compute units of the current device (cached per device).
@@ -249,6 +276,7 @@ void plan_pix(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
               const Requant* rq, pix::PixArgs* g, dim3* grid, size_t* lds) {
     g->h = s.h; g->w = s.w; g->oh = s.oh; g->ow = s.ow;
     g->ph = s.ph; g->pw = s.pw;
+    g->c = s.c;
     g->oc = s.oc;
     g->npix = s.n * s.oh * s.ow;
     g->quads = s.oc / 4;
@@ -430,17 +458,29 @@ int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
     dim3 grid;
     size_t lds = 0;
     const int cw = (s.c + 31) / 32;
-    const char* enc = s.bipolar_w ? "bipolar" : "unipolar";
+    static const char* const names[3] = {"unipolar", "bipolar", "signed"};
+    char enc[48];
+    if (s.aenc == kUnipolar)
+        snprintf(enc, sizeof(enc), "%s", names[s.wenc]);
+    else
+        snprintf(enc, sizeof(enc), "%s x %s", names[s.aenc], names[s.wenc]);
     switch (choose(s, mode, &pfn, &info)) {
         case Family::kPixels: {
             pix::PixArgs g;
             plan_pix(s, pfn, opt.units_per_wave, nullptr, &g, &grid, &lds);
+            // the encodings the specialisation was compiled for
+            char kenc[48];
+            if (info.enc / 3 == kUnipolar)
+                snprintf(kenc, sizeof(kenc), "%s", names[info.enc % 3]);
+            else
+                snprintf(kenc, sizeof(kenc), "%s x %s", names[info.enc / 3],
+                         names[info.enc % 3]);
             return snprintf(buf, len,
                             "conv_pix_kernel<A=%d,W=%d,%s,K=%d,S=%d,CW=%d> "
                             "patch=%dtaps x %dwords slice=%dch x %dtaps "
                             "grid=%u block=%d lds=%zu units=%d "
                             "units_per_wave=%d",
-                            s.abits, s.wbits, enc, s.kh, s.sh, cw, info.tb,
+                            s.abits, s.wbits, kenc, s.kh, s.sh, cw, info.tb,
                             info.cb, info.ocb, info.ts, grid.x, pix::kBlock,
                             lds, g.units, g.per_wave);
         }

@@ -47,6 +47,31 @@ constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / 64;
 constexpr int kSliceWords = 24;     // filter words per SGPR slice
 
+// Operand encodings of a specialisation: E = 3 * (activation encoding) +
+// (weight encoding), each kUnipolar, kBipolar or kSigned.
+//
+// Every encoding is affine in the plain binary value u of a code (the sum of
+// its planes' +-2^j, the top plane of signed data negative): value =
+// alpha u + beta, (alpha, beta) = (1, 0) unipolar or signed, (2, -(2^B - 1))
+// bipolar.  Over the in-range taps of a window
+//   sum value(a) value(w) = aa aw S + aa bw SA + ba aw SW + ba bw N,
+// S = sum_{i,j} +-2^(i+j) popcount(a_i AND w_j) (the inner loop, plane pairs
+// of opposite sign in separate accumulators), SA and SW the plane-weighted
+// popcounts of the window's activation and (in-range) filter words, N the
+// number of in-range channel values.  SA and N are per lane; SW depends on
+// the lane's in-range taps and the channel: the scalar unit counts the bits
+// of each tap's filter words from the SGPR slice, and one v_dot2_u32_u16 per
+// pair of taps weighs them by the lane's in-range flags.
+template <int E>
+struct Enc {
+    static constexpr int AE = E / 3, WE = E % 3;
+    static constexpr bool kSignedPairs = AE == kSigned || WE == kSigned;
+    // the sign of plane pair (i, j) of an A x W product
+    static constexpr bool neg(int i, int j, int A, int W) {
+        return (AE == kSigned && i == A - 1) != (WE == kSigned && j == W - 1);
+    }
+};
+
 struct PixArgs {
     int32_t h, w, oh, ow, ph, pw;
     int32_t oc;            // output channels, a multiple of 4
@@ -61,6 +86,7 @@ struct PixArgs {
     int32_t out_bits;      // 1..8
     int32_t out_words;     // ceil(oc / 32): words per plane of a pixel
     FastDiv div_ow, div_oh, div_units;
+    int32_t c;             // input channels (+-1 activations only)
 };
 
 __device__ __forceinline__ void bcnt_acc(uint32_t& acc, uint32_t x) {
@@ -84,6 +110,7 @@ __device__ __forceinline__ void wait_scalar_loads() {
 }
 
 typedef const uint32_t __attribute__((address_space(1))) gu32;
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 
 // Static plan of a specialisation.
 //
@@ -132,6 +159,7 @@ struct Plan {
         BW <= kSliceWords ? TB
         : (TB % 3 == 0 && 3 * W * CB <= kSliceWords) ? 3 : 1;
     static constexpr int NP = TB / TS;                  // slices per block
+    static constexpr int NPAIR = (TS + 1) / 2;          // tap pairs / slice
     static constexpr int SW = OCB * TS * W * CB;        // words per slice
     static constexpr int STEPS = 4 / OCB * NP;          // slices per quad
     static constexpr bool kFits = TS * W * CB <= kSliceWords &&
@@ -254,25 +282,34 @@ __device__ __forceinline__ void flush_tile(
 // or block's first slice; callers with nothing left pass any valid slice
 // address, so the load never needs a branch or a null check).  `patch` holds
 // the block's TB taps x A planes x CB words.
-template <int A, int W, bool BIP, int K, int CW>
+template <int A, int W, int E, int K, int CW>
 __device__ __forceinline__ void compute_quad(
     const uint32_t (&patch)[Plan<A, W, K, CW>::TB][A][Plan<A, W, K, CW>::CB],
-    uint32_t sa, gu32* src, gu32* next, Slice<Plan<A, W, K, CW>::SW> (&f)[2],
+    uint32_t lc,
+    const uint32_t (&tv)[Plan<A, W, K, CW>::NP][Plan<A, W, K, CW>::NPAIR],
+    gu32* src, gu32* next, Slice<Plan<A, W, K, CW>::SW> (&f)[2],
     uint32_t (&val)[4]) {
     using Pl = Plan<A, W, K, CW>;
+    using En = Enc<E>;
+    static_assert(En::AE != kBipolar || (A == 1 && W == 1),
+                  "+-1 activations are specialised for A == W == 1");
     constexpr int NS = A + W - 1;
+    constexpr int NA = En::kSignedPairs ? 2 * NS : NS;   // accumulators
     constexpr int OCB = Pl::OCB, TS = Pl::TS, NP = Pl::NP, CB = Pl::CB;
     constexpr int FW = Pl::FW, TSW = TS * W * CW;
 #pragma unroll
     for (int b = 0; b < 4 / OCB; ++b) {
-        uint32_t acc[2][OCB][NS];
-        bool fresh[2][OCB][NS];
+        uint32_t acc[2][OCB][NA];
+        bool fresh[2][OCB][NA];
+        uint32_t corr[OCB];   // SW: in-range filter popcounts (bipolar acts)
+#pragma unroll
+        for (int o = 0; o < OCB; ++o) corr[o] = 0;
 #pragma unroll
         for (int h = 0; h < 2; ++h)
 #pragma unroll
             for (int o = 0; o < OCB; ++o)
 #pragma unroll
-                for (int s = 0; s < NS; ++s) fresh[h][o][s] = true;
+                for (int s = 0; s < NA; ++s) fresh[h][o][s] = true;
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
             const int st = b * NP + p;
@@ -285,6 +322,29 @@ __device__ __forceinline__ void compute_quad(
                 load_slice<A, W, K, CW>(f[0], next);
             }
             __builtin_amdgcn_sched_barrier(0);
+            if constexpr (En::AE == kBipolar) {
+                // W == 1: per tap, the bits of its CB filter words (uniform,
+                // on the scalar unit); taps 2m and 2m+1 of the slice share
+                // one dot2 with the lane's flags
+#pragma unroll
+                for (int o = 0; o < OCB; ++o)
+#pragma unroll
+                    for (int m = 0; m < Pl::NPAIR; ++m) {
+                        uint32_t lo = 0, hi = 0;
+#pragma unroll
+                        for (int c = 0; c < CB; ++c) {
+                            lo += __builtin_popcount(
+                                f[st & 1].w[(o * TS + 2 * m) * CB + c]);
+                            if (2 * m + 1 < TS)
+                                hi += __builtin_popcount(
+                                    f[st & 1].w[(o * TS + 2 * m + 1) * CB + c]);
+                        }
+                        corr[o] = __builtin_amdgcn_udot2(
+                            __builtin_bit_cast(u16x2, tv[p][m]),
+                            __builtin_bit_cast(u16x2, lo | hi << 16), corr[o],
+                            false);
+                    }
+            }
 #pragma unroll
             for (int tt = 0; tt < TS; ++tt)
 #pragma unroll
@@ -297,14 +357,16 @@ __device__ __forceinline__ void compute_quad(
                             for (int o = 0; o < OCB; ++o) {
                                 const int t = p * TS + tt;
                                 const int h = (t * CB + c) & 1;
+                                const int s =
+                                    i + j + (En::neg(i, j, A, W) ? NS : 0);
                                 const uint32_t x =
                                     patch[t][i][c] &
                                     f[st & 1].w[((o * TS + tt) * W + j) * CB + c];
-                                if (fresh[h][o][i + j]) {
-                                    bcnt_first(acc[h][o][i + j], x);
-                                    fresh[h][o][i + j] = false;
+                                if (fresh[h][o][s]) {
+                                    bcnt_first(acc[h][o][s], x);
+                                    fresh[h][o][s] = false;
                                 } else {
-                                    bcnt_acc(acc[h][o][i + j], x);
+                                    bcnt_acc(acc[h][o][s], x);
                                 }
                             }
             __builtin_amdgcn_sched_barrier(0);
@@ -313,13 +375,21 @@ __device__ __forceinline__ void compute_quad(
         for (int o = 0; o < OCB; ++o) {
             uint32_t v = 0;
 #pragma unroll
-            for (int s = 0; s < NS; ++s) {
+            for (int s = 0; s < NA; ++s) {
                 const uint32_t a0 = fresh[0][o][s] ? 0u : acc[0][o][s];
                 const uint32_t a1 = fresh[1][o][s] ? 0u : acc[1][o][s];
-                v += (a0 + a1) << s;
+                if (s < NS) v += (a0 + a1) << s;
+                else v -= (a0 + a1) << (s - NS);
             }
-            // bipolar weight value 2w - (2^W - 1): 2*sum - (2^W - 1)*sum(a)
-            if (BIP) v = 2u * v - (uint32_t)((1 << W) - 1) * sa;
+            if constexpr (En::AE == kBipolar) {
+                // +-1 activations (A == W == 1): bipolar filters give
+                // 4 S - 2 SW + (N - 2 SA), unipolar ones 2 S - SW
+                if constexpr (En::WE == kBipolar) v = 4u * v - 2u * corr[o] + lc;
+                else v = 2u * v - corr[o];
+            } else if constexpr (En::WE == kBipolar) {
+                // bipolar weight value 2w - (2^W - 1): 2 S - (2^W - 1) SA
+                v = 2u * v - (uint32_t)((1 << W) - 1) * lc;
+            }
             val[b * OCB + o] = v;
         }
     }
@@ -376,8 +446,9 @@ __device__ __forceinline__ void load_patch(
     }
 }
 
-// Bipolar correction term of a block: sum_i 2^i popcount(a_i) over its words.
-template <int A, int TB, int CB>
+// SA of a block: sum_i +-2^i popcount(a_i) over its words (the top plane of
+// signed activations negative).
+template <int A, int TB, int CB, bool SGN>
 __device__ __forceinline__ uint32_t patch_sum(
     const uint32_t (&patch)[TB][A][CB]) {
     uint32_t sa = 0;
@@ -386,9 +457,58 @@ __device__ __forceinline__ uint32_t patch_sum(
 #pragma unroll
         for (int i = 0; i < A; ++i)
 #pragma unroll
-            for (int c = 0; c < CB; ++c)
-                sa += (uint32_t)__builtin_popcount(patch[tt][i][c]) << i;
+            for (int c = 0; c < CB; ++c) {
+                const uint32_t x = (uint32_t)__builtin_popcount(patch[tt][i][c])
+                                   << i;
+                sa += SGN && i == A - 1 ? 0u - x : x;
+            }
     return sa;
+}
+
+// Per-lane constants of reduction block nb (taps t0 = (nb / NCB) TB ..): the
+// in-range flags of its taps as u16 pairs per slice (bipolar activations),
+// and the lane constant lc the epilogue adds: SA for bipolar filters, N - 2 SA
+// for +-1 data, 0 otherwise.
+template <int A, int W, int E, int K, int S, int CW>
+__device__ __forceinline__ uint32_t block_consts(
+    const uint32_t (&patch)[Plan<A, W, K, CW>::TB][A][Plan<A, W, K, CW>::CB],
+    uint32_t (&tv)[Plan<A, W, K, CW>::NP][Plan<A, W, K, CW>::NPAIR],
+    const PixArgs& g, int oy, int ox, int nb) {
+    using Pl = Plan<A, W, K, CW>;
+    using En = Enc<E>;
+    const uint32_t sa =
+        En::WE == kBipolar
+            ? patch_sum<A, Pl::TB, Pl::CB, En::AE == kSigned>(patch) : 0u;
+    if constexpr (En::AE == kBipolar) {
+        const int tb = nb / Pl::NCB, cb = nb - tb * Pl::NCB;
+        const int t0 = tb * Pl::TB;
+        uint32_t nv = 0;
+#pragma unroll
+        for (int p = 0; p < Pl::NP; ++p)
+#pragma unroll
+            for (int m = 0; m < Pl::NPAIR; ++m) {
+                uint32_t flag[2] = {0, 0};
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    if (2 * m + e >= Pl::TS) continue;
+                    const int t = t0 + p * Pl::TS + 2 * m + e;
+                    const int r = t / K, q = t - r * K;
+                    const int iy = oy * S - g.ph + r, ix = ox * S - g.pw + q;
+                    flag[e] = (unsigned)iy < (unsigned)g.h &&
+                              (unsigned)ix < (unsigned)g.w;
+                }
+                tv[p][m] = flag[0] | flag[1] << 16;
+                nv += flag[0] + flag[1];
+            }
+        if constexpr (En::WE == kBipolar) {
+            // channels of the block's words
+            const int ch = min(32 * Pl::CB, g.c - 32 * Pl::CB * cb);
+            return nv * (uint32_t)ch - 2u * sa;
+        }
+        return 0u;
+    } else {
+        return sa;
+    }
 }
 
 // Offset of reduction block nb's words inside a filter.
@@ -403,20 +523,23 @@ __device__ __forceinline__ int block_offset(int nb) {
 // (nb == 0) or added to (nb > 0) the lane's tile row.  On exit f[0] is
 // receiving `next_block` (the next block's first slice, or any valid slice
 // address when there is none).
-template <int A, int W, bool BIP, int K, int CW>
+template <int A, int W, int E, int K, int S, int CW>
 __device__ __forceinline__ void run_block(
     const uint32_t (&patch)[Plan<A, W, K, CW>::TB][A][Plan<A, W, K, CW>::CB],
     gu32* src, int nq, int nb, gu32* next_block,
-    Slice<Plan<A, W, K, CW>::SW> (&f)[2], uint32_t* row) {
+    Slice<Plan<A, W, K, CW>::SW> (&f)[2], uint32_t* row, const PixArgs& g,
+    int oy, int ox) {
     using Pl = Plan<A, W, K, CW>;
-    const uint32_t sa =
-        BIP ? patch_sum<A, Pl::TB, Pl::CB>(patch) : 0u;
+    uint32_t tv[Pl::NP][Pl::NPAIR];
+    const uint32_t lc =
+        block_consts<A, W, E, K, S, CW>(patch, tv, g, oy, ox, nb);
 #pragma unroll 1
     for (int qi = 0; qi < nq; ++qi) {
         uint32_t val[4];
         gu32* q = src + (size_t)qi * 4 * Pl::FW;
-        compute_quad<A, W, BIP, K, CW>(
-            patch, sa, q, qi + 1 < nq ? q + 4 * Pl::FW : next_block, f, val);
+        compute_quad<A, W, E, K, CW>(
+            patch, lc, tv, q, qi + 1 < nq ? q + 4 * Pl::FW : next_block, f,
+            val);
         // only this lane touches its tile row until the flush
         uint32_t* t = row + qi * 4;
         if (nb == 0) {
@@ -429,10 +552,11 @@ __device__ __forceinline__ void run_block(
     }
 }
 
-// A, W: bit-widths; BIP: bipolar weights; K: square kernel size; S: stride;
-// CW: words per bit-plane; REQ: requantize and bit-pack the output (out then
-// holds [npix][out_bits][out_words] uint32 words) instead of storing int32.
-template <int A, int W, bool BIP, int K, int S, int CW, bool REQ>
+// A, W: bit-widths; E: operand encodings (Enc); K: square kernel size;
+// S: stride; CW: words per bit-plane; REQ: requantize and bit-pack the output
+// (out then holds [npix][out_bits][out_words] uint32 words) instead of
+// storing int32.
+template <int A, int W, int E, int K, int S, int CW, bool REQ>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_num_sgpr(80)))
 void conv_pix_kernel(
     const uint32_t* __restrict__ act, const uint32_t* __restrict__ wts,
@@ -472,8 +596,9 @@ void conv_pix_kernel(
             uint32_t patch[Pl::TB][A][CW];
             load_patch<A, K, S, CW, Pl::TB, CW>(patch, act, g, img, oy, ox, 0,
                                                0);
-            const uint32_t sa =
-                BIP ? patch_sum<A, Pl::TB, CW>(patch) : 0u;
+            uint32_t tv[Pl::NP][Pl::NPAIR];
+            const uint32_t lc =
+                block_consts<A, W, E, K, S, CW>(patch, tv, g, oy, ox, 0);
             gu32* src = gw + (size_t)(4 * q0) * FW;
             Slice<Pl::SW> f[2];
             load_slice<A, W, K, CW>(f[0], src);
@@ -485,8 +610,8 @@ void conv_pix_kernel(
             for (int qi = 0; qi < nq; ++qi) {
                 uint32_t val[4];
                 gu32* q = src + (size_t)qi * 4 * FW;
-                compute_quad<A, W, BIP, K, CW>(
-                    patch, sa, q, qi + 1 < nq ? q + 4 * FW : src, f, val);
+                compute_quad<A, W, E, K, CW>(
+                    patch, lc, tv, q, qi + 1 < nq ? q + 4 * FW : src, f, val);
                 if constexpr (REQ) {
                     // a packed byte holds 2 quads; runs start on a byte
                     const int qg = q0 + qi;
@@ -538,14 +663,16 @@ void conv_pix_kernel(
 #pragma unroll 1
                     for (int nb = 0; nb < NB; nb += 2) {
                         if (nb + 1 < NB) load_block(pb, nb + 1);
-                        run_block<A, W, BIP, K, CW>(
+                        run_block<A, W, E, K, S, CW>(
                             pa, blk(nb), nq, nb,
-                            nb + 1 < NB ? blk(nb + 1) : qsrc, f, row);
+                            nb + 1 < NB ? blk(nb + 1) : qsrc, f, row, g, oy,
+                            ox);
                         if (nb + 1 < NB) {
                             if (nb + 2 < NB) load_block(pa, nb + 2);
-                            run_block<A, W, BIP, K, CW>(
+                            run_block<A, W, E, K, S, CW>(
                                 pb, blk(nb + 1), nq, nb + 1,
-                                nb + 2 < NB ? blk(nb + 2) : qsrc, f, row);
+                                nb + 2 < NB ? blk(nb + 2) : qsrc, f, row, g,
+                                oy, ox);
                         }
                     }
                 } else {
@@ -553,9 +680,10 @@ void conv_pix_kernel(
 #pragma unroll 1
                     for (int nb = 0; nb < NB; ++nb) {
                         load_block(pa, nb);
-                        run_block<A, W, BIP, K, CW>(
+                        run_block<A, W, E, K, S, CW>(
                             pa, blk(nb), nq, nb,
-                            nb + 1 < NB ? blk(nb + 1) : qsrc, f, row);
+                            nb + 1 < NB ? blk(nb + 1) : qsrc, f, row, g, oy,
+                            ox);
                     }
                 }
                 if constexpr (REQ) {
@@ -589,13 +717,21 @@ using PixKernelFn = void (*)(const uint32_t*, const uint32_t*, int32_t*,
 // Plan of a kernel as the host reports it.
 struct PlanInfo {
     int ocb, ts, tb, cb;
+    int enc;    // E of the specialisation: 3 * activation + weight encoding
 };
 
-// Kernel for a supported (A, W, bipolar, K, S, CW, requantized output) or
+// Kernel for a supported (A, W, encodings, K, S, CW, requantized output) or
 // nullptr, with its plan (output channels per filter slice, taps per slice,
-// taps and words per plane of a reduction block).  pick_a<A> is defined for
-// A = 1..4 in conv_pix_a<A>.hip, so the specialisations compile in parallel.
-PixKernelFn pick(int a, int w, bool b, int k, int s, int cw, bool req,
+// taps and words per plane of a reduction block).  ae / we are the operand
+// encodings (kUnipolar, kBipolar, kSigned).  The specialisations are spread
+// over several sources so that they compile in parallel:
+//   conv_pix_a<A>.hip  unipolar activations, unipolar or bipolar filters
+//                      (W = 1..4 / W = 1), int32 or requantized output;
+//   conv_pix_s<A>.hip  signed filters W = 2..4 with unipolar activations,
+//                      and signed activations with signed filters of the
+//                      same width, int32 output;
+//   conv_pix_b.hip     +-1 activations with 1-bit filters, int32 output.
+PixKernelFn pick(int a, int w, int ae, int we, int k, int s, int cw, bool req,
                  PlanInfo* info);
 template <int A>
 PixKernelFn pick_a(int w, bool b, int k, int s, int cw, bool req,
@@ -604,9 +740,18 @@ template <> PixKernelFn pick_a<1>(int, bool, int, int, int, bool, PlanInfo*);
 template <> PixKernelFn pick_a<2>(int, bool, int, int, int, bool, PlanInfo*);
 template <> PixKernelFn pick_a<3>(int, bool, int, int, int, bool, PlanInfo*);
 template <> PixKernelFn pick_a<4>(int, bool, int, int, int, bool, PlanInfo*);
+template <int A>
+PixKernelFn pick_signed(int w, int ae, int we, int k, int s, int cw,
+                        PlanInfo* info);
+template <> PixKernelFn pick_signed<1>(int, int, int, int, int, int, PlanInfo*);
+template <> PixKernelFn pick_signed<2>(int, int, int, int, int, int, PlanInfo*);
+template <> PixKernelFn pick_signed<3>(int, int, int, int, int, int, PlanInfo*);
+template <> PixKernelFn pick_signed<4>(int, int, int, int, int, int, PlanInfo*);
+PixKernelFn pick_bipolar_act(int we, int k, int s, int cw, PlanInfo* info);
 
-// Specialisations for activation width A (included by conv_pix_a<A>.hip).
-template <int A, int W, bool B, int K, int S, int CW>
+// Specialisations (included by the sources above).  Requantizing variants
+// exist for unipolar activations with unipolar or bipolar filters only.
+template <int A, int W, int E, int K, int S, int CW>
 PixKernelFn pick_kscw(bool req, PlanInfo* info) {
     using Pl = Plan<A, W, K, CW>;
     if constexpr (!Pl::kFits) {
@@ -616,53 +761,82 @@ PixKernelFn pick_kscw(bool req, PlanInfo* info) {
         info->ts = Pl::TS;
         info->tb = Pl::TB;
         info->cb = Pl::CB;
-        return req ? conv_pix_kernel<A, W, B, K, S, CW, true>
-                   : conv_pix_kernel<A, W, B, K, S, CW, false>;
+        info->enc = E;
+        if constexpr (E == 3 * kUnipolar + kUnipolar ||
+                      E == 3 * kUnipolar + kBipolar)
+            return req ? conv_pix_kernel<A, W, E, K, S, CW, true>
+                       : conv_pix_kernel<A, W, E, K, S, CW, false>;
+        else
+            return req ? nullptr : conv_pix_kernel<A, W, E, K, S, CW, false>;
     }
 }
 
 // Words per plane: 1..16 for 3x3 windows; 1x1 windows (and dense, a 1x1
 // conv) up to 128 words = 4096 input channels.
-template <int A, int W, bool B, int K, int S>
+template <int A, int W, int E, int K, int S>
 PixKernelFn pick_cw(int cw, bool req, PlanInfo* info) {
     switch (cw) {
-        case 1: return pick_kscw<A, W, B, K, S, 1>(req, info);
-        case 2: return pick_kscw<A, W, B, K, S, 2>(req, info);
-        case 4: return pick_kscw<A, W, B, K, S, 4>(req, info);
-        case 8: return pick_kscw<A, W, B, K, S, 8>(req, info);
-        case 16: return pick_kscw<A, W, B, K, S, 16>(req, info);
+        case 1: return pick_kscw<A, W, E, K, S, 1>(req, info);
+        case 2: return pick_kscw<A, W, E, K, S, 2>(req, info);
+        case 4: return pick_kscw<A, W, E, K, S, 4>(req, info);
+        case 8: return pick_kscw<A, W, E, K, S, 8>(req, info);
+        case 16: return pick_kscw<A, W, E, K, S, 16>(req, info);
         default: break;
     }
     if constexpr (K == 1) {
         switch (cw) {
-            case 32: return pick_kscw<A, W, B, K, S, 32>(req, info);
-            case 64: return pick_kscw<A, W, B, K, S, 64>(req, info);
-            case 128: return pick_kscw<A, W, B, K, S, 128>(req, info);
+            case 32: return pick_kscw<A, W, E, K, S, 32>(req, info);
+            case 64: return pick_kscw<A, W, E, K, S, 64>(req, info);
+            case 128: return pick_kscw<A, W, E, K, S, 128>(req, info);
             default: break;
         }
     }
     return nullptr;
 }
 
-template <int A, int W, bool B>
+template <int A, int W, int E>
 PixKernelFn pick_ks(int k, int s, int cw, bool req, PlanInfo* info) {
-    if (k == 1) return s == 1 ? pick_cw<A, W, B, 1, 1>(cw, req, info)
-                              : pick_cw<A, W, B, 1, 2>(cw, req, info);
-    if (k == 3) return s == 1 ? pick_cw<A, W, B, 3, 1>(cw, req, info)
-                              : pick_cw<A, W, B, 3, 2>(cw, req, info);
+    if (k == 1) return s == 1 ? pick_cw<A, W, E, 1, 1>(cw, req, info)
+                              : pick_cw<A, W, E, 1, 2>(cw, req, info);
+    if (k == 3) return s == 1 ? pick_cw<A, W, E, 3, 1>(cw, req, info)
+                              : pick_cw<A, W, E, 3, 2>(cw, req, info);
     return nullptr;
 }
 
-// Every weight width 1..4 with unipolar weights; bipolar weights at W = 1.
+// Unipolar activations: every weight width 1..4 with unipolar weights;
+// bipolar weights at W = 1.
 template <int A>
 PixKernelFn pick_for_a(int w, bool b, int k, int s, int cw, bool req,
                        PlanInfo* info) {
-    if (b) return w == 1 ? pick_ks<A, 1, true>(k, s, cw, req, info) : nullptr;
+    constexpr int UU = 3 * kUnipolar + kUnipolar, UB = 3 * kUnipolar + kBipolar;
+    if (b) return w == 1 ? pick_ks<A, 1, UB>(k, s, cw, req, info) : nullptr;
     switch (w) {
-        case 1: return pick_ks<A, 1, false>(k, s, cw, req, info);
-        case 2: return pick_ks<A, 2, false>(k, s, cw, req, info);
-        case 3: return pick_ks<A, 3, false>(k, s, cw, req, info);
-        case 4: return pick_ks<A, 4, false>(k, s, cw, req, info);
+        case 1: return pick_ks<A, 1, UU>(k, s, cw, req, info);
+        case 2: return pick_ks<A, 2, UU>(k, s, cw, req, info);
+        case 3: return pick_ks<A, 3, UU>(k, s, cw, req, info);
+        case 4: return pick_ks<A, 4, UU>(k, s, cw, req, info);
+        default: return nullptr;
+    }
+}
+
+// Signed filters of width 2..4 with unipolar activations; signed
+// activations with signed filters of the same width.
+template <int A>
+PixKernelFn pick_signed_for_a(int w, int ae, int we, int k, int s, int cw,
+                              PlanInfo* info) {
+    constexpr int US = 3 * kUnipolar + kSigned, SS = 3 * kSigned + kSigned;
+    if (we != kSigned) return nullptr;
+    if (ae == kSigned) {
+        if constexpr (A >= 2)
+            return w == A ? pick_ks<A, A, SS>(k, s, cw, false, info) : nullptr;
+        else
+            return nullptr;
+    }
+    if (ae != kUnipolar) return nullptr;
+    switch (w) {
+        case 2: return pick_ks<A, 2, US>(k, s, cw, false, info);
+        case 3: return pick_ks<A, 3, US>(k, s, cw, false, info);
+        case 4: return pick_ks<A, 4, US>(k, s, cw, false, info);
         default: return nullptr;
     }
 }

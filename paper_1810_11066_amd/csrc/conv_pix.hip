@@ -1,12 +1,28 @@
-// Dispatch to the pixels-on-lanes conv specialisations (conv_pix_a<A>.hip).
+// Dispatch to the pixels-on-lanes conv specialisations (conv_pix_a<A>.hip,
+// conv_pix_s<A>.hip, conv_pix_b.hip).
 #include "conv_pix.h"
 
 namespace bs {
 namespace pix {
 
-PixKernelFn pick(int a, int w, bool b, int k, int s, int cw, bool req,
+PixKernelFn pick(int a, int w, int ae, int we, int k, int s, int cw, bool req,
                  PlanInfo* info) {
     if (s != 1 && s != 2) return nullptr;
+    if (ae == kBipolar) {
+        if (a != 1 || w != 1 || we == kSigned || req) return nullptr;
+        return pick_bipolar_act(we, k, s, cw, info);
+    }
+    if (we == kSigned || ae == kSigned) {
+        if (req) return nullptr;
+        switch (a) {
+            case 1: return pick_signed<1>(w, ae, we, k, s, cw, info);
+            case 2: return pick_signed<2>(w, ae, we, k, s, cw, info);
+            case 3: return pick_signed<3>(w, ae, we, k, s, cw, info);
+            case 4: return pick_signed<4>(w, ae, we, k, s, cw, info);
+            default: return nullptr;
+        }
+    }
+    const bool b = we == kBipolar;
     switch (a) {
         case 1: return pick_a<1>(w, b, k, s, cw, req, info);
         case 2: return pick_a<2>(w, b, k, s, cw, req, info);

@@ -19,23 +19,24 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kMaxBlocks = 8192;
 
-template <bool BIP>
+// ENC: kUnipolar, kBipolar or kSigned (qmax as for quant_code_enc)
+template <int ENC>
 __device__ __forceinline__ uint32_t code_of(float x, float scale, float qmax) {
-    return quant_code<BIP>(x, scale, qmax);
+    return quant_code_enc<ENC>(x, scale, qmax);
 }
 
-template <bool BIP>
+template <int ENC>
 __device__ __forceinline__ uint32_t codes4(float4 f, float scale, float qmax) {
-    return code_of<BIP>(f.x, scale, qmax) |
-           (code_of<BIP>(f.y, scale, qmax) << 8) |
-           (code_of<BIP>(f.z, scale, qmax) << 16) |
-           (code_of<BIP>(f.w, scale, qmax) << 24);
+    return code_of<ENC>(f.x, scale, qmax) |
+           (code_of<ENC>(f.y, scale, qmax) << 8) |
+           (code_of<ENC>(f.z, scale, qmax) << 16) |
+           (code_of<ENC>(f.w, scale, qmax) << 24);
 }
 
 // ---------------------------------------------------------------------------
 // quantize: 16 elements per thread per step (four 16-byte loads, one 16-byte
 // store); the n % 16 tail is done one element per thread.
-template <bool BIP>
+template <int ENC>
 __global__ __launch_bounds__(kBlock) void quantize_kernel(
     const float* __restrict__ x, uint8_t* __restrict__ q, int64_t n,
     float scale, float qmax) {
@@ -47,14 +48,14 @@ __global__ __launch_bounds__(kBlock) void quantize_kernel(
     for (int64_t v = tid; v < nvec; v += nthr) {
         float4 f0 = xv[4 * v + 0], f1 = xv[4 * v + 1];
         float4 f2 = xv[4 * v + 2], f3 = xv[4 * v + 3];
-        qv[v] = make_uint4(codes4<BIP>(f0, scale, qmax),
-                           codes4<BIP>(f1, scale, qmax),
-                           codes4<BIP>(f2, scale, qmax),
-                           codes4<BIP>(f3, scale, qmax));
+        qv[v] = make_uint4(codes4<ENC>(f0, scale, qmax),
+                           codes4<ENC>(f1, scale, qmax),
+                           codes4<ENC>(f2, scale, qmax),
+                           codes4<ENC>(f3, scale, qmax));
     }
     const int64_t tail = nvec << 4;
     if (tid < n - tail)
-        q[tail + tid] = (uint8_t)code_of<BIP>(x[tail + tid], scale, qmax);
+        q[tail + tid] = (uint8_t)code_of<ENC>(x[tail + tid], scale, qmax);
 }
 
 // ---------------------------------------------------------------------------
@@ -139,7 +140,7 @@ __global__ __launch_bounds__(kBlock) void pack_dpp_kernel(
 // is then exactly the two packed words 2c, 2c+1 of plane b (bit l <- lane l),
 // so no per-lane bit shuffling is needed.  Used for the uint8 input when k is
 // not a multiple of 32 and for the float input whenever k is not.
-template <bool FROM_FLOAT, bool BIP>
+template <bool FROM_FLOAT, int ENC>
 __global__ __launch_bounds__(kBlock) void pack_ballot_kernel(
     const void* __restrict__ src, uint32_t* __restrict__ packed, int64_t rows,
     int64_t k, int bits, float scale, float qmax) {
@@ -155,7 +156,7 @@ __global__ __launch_bounds__(kBlock) void pack_ballot_kernel(
         uint32_t code = 0;
         if (e < k) {
             if (FROM_FLOAT)
-                code = code_of<BIP>(
+                code = code_of<ENC>(
                     static_cast<const float*>(src)[row * k + e], scale, qmax);
             else
                 code = static_cast<const uint8_t*>(src)[row * k + e];
@@ -178,7 +179,7 @@ __global__ __launch_bounds__(kBlock) void pack_ballot_kernel(
 // quantizes its 4 values, places their plane-b bits at 4 (lane % 8), and
 // three DPP ORs combine the group.  Lane 8m + i keeps word 8 j + m when
 // j == i; a ds_bpermute per plane then moves word w to lane w.
-template <int A, bool BIP>
+template <int A, int ENC>
 __global__ __launch_bounds__(kBlock) void quantize_pack_dpp_kernel(
     const float* __restrict__ x, uint32_t* __restrict__ packed,
     uint32_t nwords, FastDiv kwdiv, float scale, float qmax) {
@@ -203,7 +204,7 @@ __global__ __launch_bounds__(kBlock) void quantize_pack_dpp_kernel(
         for (int b = 0; b < A; ++b) keep[b] = 0;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const uint32_t c4 = codes4<BIP>(f[j], scale, qmax);
+            const uint32_t c4 = codes4<ENC>(f[j], scale, qmax);
 #pragma unroll
             for (int b = 0; b < A; ++b) {
                 uint32_t h = nibble_of(c4, b) << (4 * (lane & 7));
@@ -227,6 +228,63 @@ __global__ __launch_bounds__(kBlock) void quantize_pack_dpp_kernel(
     }
 }
 
+// ---------------------------------------------------------------------------
+// pack_ex: the codes viewed as [outer][k][inner], the reduction axis k at
+// stride `inner` (NCHW activations, OIHW filters).  A thread builds word t of
+// every plane for V consecutive rows i0 .. i0+V-1 of one outer index: for
+// each of the word's 32 elements it makes one V-byte load (neighbouring
+// threads take neighbouring rows, so a load instruction reads one contiguous
+// span), then moves every bit into place with an extract and a shift-or.
+// The words are stored where the layout puts them.
+template <int V>
+__global__ __launch_bounds__(kBlock) void pack_strided_kernel(
+    const uint8_t* __restrict__ q, uint32_t* __restrict__ packed,
+    int64_t outer, int64_t k, int64_t inner, int bits, int layout) {
+    const int64_t kw = (k + 31) >> 5;
+    const int64_t iv = inner / V;            // V divides inner (host)
+    const int64_t total = outer * kw * iv;
+    const int64_t rows = outer * inner;
+    for (int64_t f = (int64_t)blockIdx.x * kBlock + threadIdx.x; f < total;
+         f += (int64_t)gridDim.x * kBlock) {
+        const int64_t ig = f % iv, rest = f / iv;
+        const int64_t t = rest % kw, o = rest / kw;
+        const int64_t i0 = ig * V;
+        const int64_t left = k - 32 * t;
+        const int u_end = left < 32 ? (int)left : 32;
+        const uint8_t* src = q + (o * k + 32 * t) * inner + i0;
+        uint32_t word[V][8];
+#pragma unroll
+        for (int v = 0; v < V; ++v)
+#pragma unroll
+            for (int b = 0; b < 8; ++b) word[v][b] = 0;
+        for (int u = 0; u < u_end; ++u) {
+            uint32_t x;
+            if constexpr (V == 4)
+                x = *reinterpret_cast<const uint32_t*>(src + (int64_t)u * inner);
+            else
+                x = src[(int64_t)u * inner];
+#pragma unroll
+            for (int v = 0; v < V; ++v)
+#pragma unroll
+                for (int b = 0; b < 8; ++b)
+                    if (b < bits) word[v][b] |= ((x >> (8 * v + b)) & 1u) << u;
+        }
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            const int64_t r = o * inner + i0 + v;
+#pragma unroll
+            for (int b = 0; b < 8; ++b) {
+                if (b >= bits) continue;
+                int64_t at;
+                if (layout == kLayoutMBK) at = (r * bits + b) * kw + t;
+                else if (layout == kLayoutMKB) at = (r * kw + t) * bits + b;
+                else at = ((int64_t)b * rows + r) * kw + t;
+                packed[at] = word[v][b];
+            }
+        }
+    }
+}
+
 int grid_for(int64_t work_items, int per_block) {
     int64_t b = (work_items + per_block - 1) / per_block;
     if (b < 1) b = 1;
@@ -243,12 +301,12 @@ hipError_t launch_pack32(const uint8_t* q, uint32_t* packed, uint32_t nwords,
     return hipGetLastError();
 }
 
-template <int A, bool BIP>
+template <int A, int ENC>
 hipError_t launch_qpack(const float* x, uint32_t* packed, uint32_t nwords,
                         const FastDiv& d, float scale, float qmax,
                         hipStream_t st) {
     // 64 words per wave, 4 waves per block
-    quantize_pack_dpp_kernel<A, BIP>
+    quantize_pack_dpp_kernel<A, ENC>
         <<<grid_for(nwords, 256), kBlock, 0, st>>>(x, packed, nwords, d,
                                                     scale, qmax);
     return hipGetLastError();
@@ -256,14 +314,23 @@ hipError_t launch_qpack(const float* x, uint32_t* packed, uint32_t nwords,
 
 }  // namespace
 
+// qmax of an encoding: the top unipolar code, the top signed value
+static float enc_qmax(int bits, int enc) {
+    return enc == kSigned ? (float)((1 << (bits - 1)) - 1)
+                          : (float)((1 << bits) - 1);
+}
+
 hipError_t launch_quantize(const float* x, uint8_t* q, int64_t n, float scale,
-                           int bits, bool bipolar, hipStream_t st) {
-    const float qmax = (float)((1 << bits) - 1);
+                           int bits, int enc, hipStream_t st) {
+    const float qmax = enc_qmax(bits, enc);
     const int grid = grid_for((n >> 4) + 1, kBlock);
-    if (bipolar)
-        quantize_kernel<true><<<grid, kBlock, 0, st>>>(x, q, n, scale, qmax);
+    if (enc == kBipolar)
+        quantize_kernel<kBipolar><<<grid, kBlock, 0, st>>>(x, q, n, scale, qmax);
+    else if (enc == kSigned)
+        quantize_kernel<kSigned><<<grid, kBlock, 0, st>>>(x, q, n, scale, qmax);
     else
-        quantize_kernel<false><<<grid, kBlock, 0, st>>>(x, q, n, scale, qmax);
+        quantize_kernel<kUnipolar><<<grid, kBlock, 0, st>>>(x, q, n, scale,
+                                                           qmax);
     return hipGetLastError();
 }
 
@@ -286,40 +353,71 @@ hipError_t launch_pack(const uint8_t* q, uint32_t* packed, int64_t rows,
         }
     }
     const int64_t waves = rows * ((k + 63) / 64);
-    pack_ballot_kernel<false, false><<<grid_for(waves, 4), kBlock, 0, st>>>(
+    pack_ballot_kernel<false, kUnipolar><<<grid_for(waves, 4), kBlock, 0, st>>>(
         q, packed, rows, k, bits, 0.0f, 0.0f);
     return hipGetLastError();
 }
 
-hipError_t launch_quantize_pack(const float* x, uint32_t* packed,
-                                int64_t rows, int64_t k, float scale, int bits,
-                                bool bipolar, hipStream_t st) {
-    const float qmax = (float)((1 << bits) - 1);
+hipError_t launch_pack_ex(const uint8_t* q, uint32_t* packed, int64_t outer,
+                          int64_t k, int64_t inner, int bits, int layout,
+                          hipStream_t st) {
+    if (inner == 1 && layout == kLayoutMBK)
+        return launch_pack(q, packed, outer, k, bits, st);
+    const int64_t kw = (k + 31) / 32;
+    if (inner % 4 == 0) {
+        const int grid = grid_for(outer * kw * (inner / 4), kBlock);
+        pack_strided_kernel<4><<<grid, kBlock, 0, st>>>(q, packed, outer, k,
+                                                        inner, bits, layout);
+    } else {
+        const int grid = grid_for(outer * kw * inner, kBlock);
+        pack_strided_kernel<1><<<grid, kBlock, 0, st>>>(q, packed, outer, k,
+                                                        inner, bits, layout);
+    }
+    return hipGetLastError();
+}
+
+namespace {
+
+template <int ENC>
+hipError_t quantize_pack_enc(const float* x, uint32_t* packed, int64_t rows,
+                             int64_t k, float scale, int bits, float qmax,
+                             hipStream_t st) {
     const int64_t nwords = rows * ((k + 31) / 32);
     if (k % 32 == 0 && nwords < (int64_t)INT32_MAX - 64) {
         FastDiv d;
         d.init((uint32_t)(k / 32));
-        if (bipolar) return launch_qpack<1, true>(x, packed, (uint32_t)nwords,
-                                                  d, scale, qmax, st);
+        const uint32_t nw = (uint32_t)nwords;
         switch (bits) {
-            case 1: return launch_qpack<1, false>(x, packed, (uint32_t)nwords, d, scale, qmax, st);
-            case 2: return launch_qpack<2, false>(x, packed, (uint32_t)nwords, d, scale, qmax, st);
-            case 3: return launch_qpack<3, false>(x, packed, (uint32_t)nwords, d, scale, qmax, st);
-            case 4: return launch_qpack<4, false>(x, packed, (uint32_t)nwords, d, scale, qmax, st);
-            case 5: return launch_qpack<5, false>(x, packed, (uint32_t)nwords, d, scale, qmax, st);
-            case 6: return launch_qpack<6, false>(x, packed, (uint32_t)nwords, d, scale, qmax, st);
-            case 7: return launch_qpack<7, false>(x, packed, (uint32_t)nwords, d, scale, qmax, st);
-            default: return launch_qpack<8, false>(x, packed, (uint32_t)nwords, d, scale, qmax, st);
+            case 1: return launch_qpack<1, ENC>(x, packed, nw, d, scale, qmax, st);
+            case 2: return launch_qpack<2, ENC>(x, packed, nw, d, scale, qmax, st);
+            case 3: return launch_qpack<3, ENC>(x, packed, nw, d, scale, qmax, st);
+            case 4: return launch_qpack<4, ENC>(x, packed, nw, d, scale, qmax, st);
+            case 5: return launch_qpack<5, ENC>(x, packed, nw, d, scale, qmax, st);
+            case 6: return launch_qpack<6, ENC>(x, packed, nw, d, scale, qmax, st);
+            case 7: return launch_qpack<7, ENC>(x, packed, nw, d, scale, qmax, st);
+            default: return launch_qpack<8, ENC>(x, packed, nw, d, scale, qmax, st);
         }
     }
     const int64_t waves = rows * ((k + 63) / 64);
-    if (bipolar)
-        pack_ballot_kernel<true, true><<<grid_for(waves, 4), kBlock, 0, st>>>(
-            x, packed, rows, k, bits, scale, qmax);
-    else
-        pack_ballot_kernel<true, false><<<grid_for(waves, 4), kBlock, 0, st>>>(
-            x, packed, rows, k, bits, scale, qmax);
+    pack_ballot_kernel<true, ENC><<<grid_for(waves, 4), kBlock, 0, st>>>(
+        x, packed, rows, k, bits, scale, qmax);
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_quantize_pack(const float* x, uint32_t* packed,
+                                int64_t rows, int64_t k, float scale, int bits,
+                                int enc, hipStream_t st) {
+    const float qmax = enc_qmax(bits, enc);
+    if (enc == kBipolar)
+        return quantize_pack_enc<kBipolar>(x, packed, rows, k, scale, 1, qmax,
+                                           st);
+    if (enc == kSigned)
+        return quantize_pack_enc<kSigned>(x, packed, rows, k, scale, bits,
+                                          qmax, st);
+    return quantize_pack_enc<kUnipolar>(x, packed, rows, k, scale, bits, qmax,
+                                        st);
 }
 
 }  // namespace bs

@@ -22,6 +22,7 @@ import numpy as np
 
 UNIPOLAR = 0
 BIPOLAR = 1
+SIGNED = 2
 
 SEED_BASE = 1810 * 100
 
@@ -72,6 +73,9 @@ class ConvCase:
     act_scale: Optional[float] = None
     # bipolar weights arrive as float +-1 and go through the bipolar quantizer
     weights_from_signs: bool = False
+    # encoding of the activation codes (quantized with it when act_scale is
+    # set); the codes are drawn uniformly over their 2^abits patterns
+    aenc: int = UNIPOLAR
 
     @property
     def oh(self) -> int:
@@ -181,6 +185,32 @@ def config5(batch: int = 128) -> List[ConvCase]:
                             weights_from_signs=True))
         out.append(ConvCase("a3w3_" + tag, batch, hw, hw, c, oc, k, s, p,
                             3, 3, seed=seed_for(5, 2 * sub + 1)))
+    return out
+
+
+def encodings(batch: int = 128) -> List[ConvCase]:
+    """Config 5's shapes (3x3 stride-2 conv 128x28x28x128 -> 256, 1x1 conv
+    128x14x14x256 -> 512 at stride 2 and 1) with the other encodings of
+    Sec. 2.2: +-1 activations and +-1 weights (the XNOR case; activations
+    N(0,1) floats binarized by sign per call, weights float signs), signed
+    3-bit activations and weights (N(0,1) activations quantized per call at
+    scale 2, weight codes uniform over the 3-bit two's complement range), and
+    unipolar 2-bit activations with signed 2-bit weights."""
+    out = []
+    for sub, (hw, c, oc, k, s, p) in enumerate([
+            (28, 128, 256, 3, 2, 1), (14, 256, 512, 1, 2, 0),
+            (14, 256, 512, 1, 1, 0)]):
+        tag = "%dx%dx%dx%d_%dx%d_s%d" % (batch, hw, hw, c, k, k, s)
+        out.append(ConvCase("a1w1xnor_" + tag, batch, hw, hw, c, oc, k, s, p,
+                            1, 1, wenc=BIPOLAR, aenc=BIPOLAR,
+                            seed=seed_for(7, 3 * sub), act_scale=1.0,
+                            weights_from_signs=True))
+        out.append(ConvCase("a3w3signed_" + tag, batch, hw, hw, c, oc, k, s,
+                            p, 3, 3, wenc=SIGNED, aenc=SIGNED,
+                            seed=seed_for(7, 3 * sub + 1), act_scale=2.0))
+        out.append(ConvCase("a2uw2s_" + tag, batch, hw, hw, c, oc, k, s, p,
+                            2, 2, wenc=SIGNED, aenc=UNIPOLAR,
+                            seed=seed_for(7, 3 * sub + 2), act_scale=1.5))
     return out
 
 

@@ -41,7 +41,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_words(lib):
-    assert lib.bs_abi_version() == 102
+    assert lib.bs_abi_version() == 103
     for k, w in [(0, 0), (1, 1), (31, 1), (32, 1), (33, 2), (4096, 128)]:
         assert lib.bs_packed_words(k) == w
 
@@ -65,6 +65,10 @@ def test_quantize_validation(lib):
         assert q(FAKE, FAKE, 8, scale, 2, 0, STREAM) == bs.BS_ERR_INVALID_ARG
     assert q(FAKE, FAKE, 8, 1.0, 2, 1, STREAM) == bs.BS_ERR_INVALID_ARG
     assert q(FAKE, FAKE, 8, 1.0, 1, 7, STREAM) == bs.BS_ERR_INVALID_ARG
+    # signed codes need a sign plane and a magnitude plane
+    assert q(FAKE, FAKE, 8, 1.0, 1, 2, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert b"signed" in lib.bs_last_error()
+    assert q(FAKE, FAKE, 0, 1.0, 2, 2, STREAM) == bs.BS_OK
 
 
 def test_empty_is_ok_without_launch(lib):
@@ -85,6 +89,24 @@ def test_pack_validation(lib):
     qp = lib.bs_quantize_pack
     assert qp(FAKE, FAKE, 4, 64, 1.0, 2, 1, STREAM) == bs.BS_ERR_INVALID_ARG
     assert qp(FAKE, FAKE, 4, 64, 0.0, 2, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert qp(FAKE, FAKE, 4, 64, 1.0, 1, 2, STREAM) == bs.BS_ERR_INVALID_ARG
+
+
+def test_pack_ex_validation(lib):
+    p = lib.bs_pack_ex
+    assert p(NULL, FAKE, 2, 64, 9, 2, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert p(FAKE, MISALIGNED, 2, 64, 9, 2, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert p(FAKE, FAKE, -1, 64, 9, 2, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert p(FAKE, FAKE, 2, 0, 9, 2, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert p(FAKE, FAKE, 2, 64, 0, 2, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+    assert p(FAKE, FAKE, 2, 64, 9, 9, 0, STREAM) == bs.BS_ERR_INVALID_ARG
+    for layout in (-1, 3):
+        assert p(FAKE, FAKE, 2, 64, 9, 2, layout,
+                 STREAM) == bs.BS_ERR_INVALID_ARG
+    assert b"layout" in lib.bs_last_error()
+    assert p(FAKE, FAKE, 1 << 30, 1 << 20, 1 << 10, 2, 0,
+             STREAM) == bs.BS_ERR_UNSUPPORTED
+    assert p(FAKE, FAKE, 0, 64, 9, 2, 1, STREAM) == bs.BS_OK   # nothing to do
 
 
 def params(**kw):
@@ -106,7 +128,9 @@ def params(**kw):
     (dict(wbits=9), bs.BS_ERR_INVALID_ARG),
     (dict(wenc=2), bs.BS_ERR_INVALID_ARG),
     (dict(kh=11, pad_h=1), bs.BS_ERR_INVALID_ARG),     # oh < 1
-    (dict(aenc=1), bs.BS_ERR_UNSUPPORTED),             # bipolar activations
+    (dict(aenc=3), bs.BS_ERR_INVALID_ARG),             # unknown encoding
+    (dict(aenc=2, abits=1), bs.BS_ERR_INVALID_ARG),    # signed needs 2 bits
+    (dict(wenc=-1), bs.BS_ERR_INVALID_ARG),
     (dict(abits=8, wbits=8, c=(1 << 31) // (255 * 255 * 9) + 1),
      bs.BS_ERR_OVERFLOW),
 ])
@@ -136,6 +160,36 @@ def test_overflow_guard_boundary(lib):
     k = (2 ** 31 - 1) // (255 * 255) + 1
     assert lib.bs_dense(4, 4, k, 8, 8, 0, FAKE, FAKE, FAKE,
                         STREAM) == bs.BS_ERR_OVERFLOW
+
+
+def test_overflow_guard_encodings(lib):
+    """The bound uses the largest magnitude of each encoding: 2^(B-1) for
+    signed codes, 2^B - 1 for unipolar and bipolar ones (checked on the host
+    through bs_conv2d_describe, which launches nothing)."""
+    buf = ctypes.create_string_buffer(256)
+    d = lib.bs_conv2d_describe
+    uni = (2 ** 31 - 1) // (255 * 255 * 9)
+    sgn = (2 ** 31 - 1) // (128 * 128 * 9)
+    ok = params(abits=8, wbits=8, aenc=2, wenc=2, c=uni + 1)
+    assert d(ctypes.byref(ok), buf, 256) == bs.BS_OK
+    bad = params(abits=8, wbits=8, aenc=2, wenc=2, c=sgn + 1)
+    assert d(ctypes.byref(bad), buf, 256) == bs.BS_ERR_OVERFLOW
+    bip = params(abits=8, wbits=8, aenc=1, wenc=1, c=uni + 1)
+    assert d(ctypes.byref(bip), buf, 256) == bs.BS_ERR_OVERFLOW
+    assert lib.bs_dense_ex(4, 4, (2 ** 31 - 1) // (128 * 255) + 1, 8, 2, 8, 0,
+                           FAKE, FAKE, FAKE, STREAM) == bs.BS_ERR_OVERFLOW
+
+
+def test_dense_ex_validation(lib):
+    d = lib.bs_dense_ex
+    assert d(4, 4, 64, 1, 2, 2, 0, FAKE, FAKE, FAKE,
+             STREAM) == bs.BS_ERR_INVALID_ARG        # 1-bit signed
+    assert d(4, 4, 64, 2, 5, 2, 0, FAKE, FAKE, FAKE,
+             STREAM) == bs.BS_ERR_INVALID_ARG        # unknown encoding
+    assert d(4, 4, 64, 2, 0, 2, 0, NULL, FAKE, FAKE,
+             STREAM) == bs.BS_ERR_INVALID_ARG
+    assert d(0, 4, 64, 1, 1, 1, 1, FAKE, FAKE, FAKE,
+             STREAM) == bs.BS_ERR_INVALID_ARG
 
 
 def test_dense_validation(lib):
@@ -211,6 +265,43 @@ def test_describe_names_the_kernel_each_mode_picks(lib):
         "conv_generic_kernel")
 
 
+ENC = ("unipolar", "bipolar", "signed")
+
+
+@pytest.mark.parametrize("aenc", [0, 1, 2])
+@pytest.mark.parametrize("wenc", [0, 1, 2])
+@pytest.mark.parametrize("bits", [1, 2, 3])
+def test_describe_kernel_encodings_match_the_call(lib, aenc, wenc, bits):
+    """Whatever kernel serves a call was compiled for the call's encodings:
+    a pixels-on-lanes specialisation names its own (activation x weight)
+    encodings, which must be the requested ones (host-only planning)."""
+    abits = 1 if aenc == 1 else max(bits, 2 if aenc == 2 else 1)
+    wbits = 1 if wenc == 1 else max(bits, 2 if wenc == 2 else 1)
+    for a_, w_ in ((abits, wbits), (abits, abits)):
+        if (aenc == 1 and a_ != 1) or (wenc == 1 and w_ != 1) or \
+                (wenc == 2 and w_ < 2):
+            continue
+        d = bs.bs_conv2d_describe(params(abits=a_, wbits=w_, aenc=aenc,
+                                         wenc=wenc))
+        if not d.startswith("conv_pix_kernel"):
+            continue
+        kenc = d.split(",")[2]
+        want = ENC[wenc] if aenc == 0 else "%s x %s" % (ENC[aenc], ENC[wenc])
+        assert kenc == want, d
+
+
+def test_describe_pixel_kernel_serves_new_encodings(lib):
+    for kw in (dict(abits=1, wbits=1, aenc=1, wenc=1),     # XNOR
+               dict(abits=1, wbits=1, aenc=1, wenc=0),
+               dict(abits=2, wbits=2, aenc=0, wenc=2),
+               dict(abits=3, wbits=3, aenc=2, wenc=2)):
+        d = bs.bs_conv2d_describe(params(**kw))
+        assert d.startswith("conv_pix_kernel"), (kw, d)
+    # signed activations with unipolar weights: no specialisation, plain loops
+    d = bs.bs_conv2d_describe(params(abits=2, wbits=2, aenc=2, wenc=0))
+    assert d.startswith("conv_generic_kernel"), d
+
+
 def test_describe_validation_and_truncation(lib):
     buf = ctypes.create_string_buffer(8)
     assert lib.bs_conv2d_describe(ctypes.byref(params()), buf, 8) == bs.BS_OK
@@ -237,7 +328,7 @@ def test_requant_validation(lib):
              STREAM) == bs.BS_ERR_INVALID_ARG
     assert r(ctypes.byref(p), FAKE, MISALIGNED, 0.5, 2, FAKE,
              STREAM) == bs.BS_ERR_INVALID_ARG
-    assert r(ctypes.byref(params(aenc=1)), FAKE, FAKE, 0.5, 2, FAKE,
-             STREAM) == bs.BS_ERR_UNSUPPORTED
+    assert r(ctypes.byref(params(aenc=3)), FAKE, FAKE, 0.5, 2, FAKE,
+             STREAM) == bs.BS_ERR_INVALID_ARG
     assert r(ctypes.byref(params(abits=8, wbits=8, c=4000)), FAKE, FAKE, 0.5,
              2, FAKE, STREAM) == bs.BS_ERR_OVERFLOW

@@ -41,8 +41,9 @@ def prepare(oracle, case: wl.ConvCase):
     x = case.activations()
     wsrc = case.weights()
     if case.act_scale is not None:
-        a_codes = oracle.quantize(x, case.act_scale, case.abits)
-        a_dev = bs.quantize_pack(dev(x), case.act_scale, case.abits)
+        a_codes = oracle.quantize(x, case.act_scale, case.abits, case.aenc)
+        a_dev = bs.quantize_pack(dev(x), case.act_scale, case.abits,
+                                 case.aenc)
     else:
         a_codes = x
         a_dev = bs.pack(dev(x), case.abits)
@@ -63,13 +64,14 @@ def prepare(oracle, case: wl.ConvCase):
 def spec_of(case):
     return bs.Conv2dSpec(case.n, case.h, case.w, case.c, case.oc, case.k,
                          case.k, case.stride, case.pad, case.abits,
-                         case.wbits, case.wenc)
+                         case.wbits, case.wenc, case.aenc)
 
 
 def oracle_params(oracle, case):
     return oracle.conv_params(case.n, case.h, case.w, case.c, case.oc,
                               case.k, case.k, case.stride, case.pad,
-                              case.abits, case.wbits, wenc=case.wenc)
+                              case.abits, case.wbits, aenc=case.aenc,
+                              wenc=case.wenc)
 
 
 def check_full(oracle, case):
@@ -148,6 +150,12 @@ def test_config4_resnet18_layer(oracle, case):
 
 @pytest.mark.parametrize("case", wl.config5(), ids=lambda c: c.name)
 def test_config5_bipolar_a3w3(oracle, case):
+    say(case.name)
+    check_sampled(oracle, case)
+
+
+@pytest.mark.parametrize("case", wl.encodings(), ids=lambda c: c.name)
+def test_encodings_xnor_signed(oracle, case):
     say(case.name)
     check_sampled(oracle, case)
 
