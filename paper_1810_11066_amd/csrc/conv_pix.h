@@ -62,10 +62,17 @@ constexpr int kSliceWords = 24;     // filter words per SGPR slice
 // the lane's in-range taps and the channel: the scalar unit counts the bits
 // of each tap's filter words from the SGPR slice, and one v_dot2_u32_u16 per
 // pair of taps weighs them by the lane's in-range flags.
+//
+// +-1 data on both sides (the XNOR case) takes the paper's form instead:
+// per in-range tap the product is c - 2 popcount(a XOR w), so the inner loop
+// counts the bits of (a XOR w) AND keep, keep being the lane's all-ones /
+// all-zeros in-range mask of the tap -- one v_bitop3_b32 and one v_bcnt per
+// word, the cost of the unipolar loop -- and the epilogue is N - 2 D.
 template <int E>
 struct Enc {
     static constexpr int AE = E / 3, WE = E % 3;
     static constexpr bool kSignedPairs = AE == kSigned || WE == kSigned;
+    static constexpr bool kXnor = AE == kBipolar && WE == kBipolar;
     // the sign of plane pair (i, j) of an A x W product
     static constexpr bool neg(int i, int j, int A, int W) {
         return (AE == kSigned && i == A - 1) != (WE == kSigned && j == W - 1);
@@ -168,6 +175,31 @@ struct Plan {
     static_assert(STEPS % 2 == 0, "slice buffers alternate within a quad");
     static_assert(CB == CW || TB == 1, "word chunks only with one tap");
 };
+
+// Per-lane tap data of a reduction block (+-1 activations only): the
+// in-range mask of each tap (XNOR) or the in-range flags of tap pairs of
+// each slice as u16 pairs (unipolar filters).
+template <int A, int W, int K, int CW>
+struct TapInfo {
+    using Pl = Plan<A, W, K, CW>;
+    uint32_t keep[Pl::TB];
+    uint32_t pairs[Pl::NP][Pl::NPAIR];
+};
+
+// (a XOR w) AND keep in one v_bitop3_b32.  The function is symmetric in a
+// and w, so with the mask as the middle operand its truth table (bits 3 and
+// 6: a != w with keep set) reads the same whichever of the outer operands
+// supplies the high index bit.
+__device__ __forceinline__ uint32_t xor_keep(uint32_t a, uint32_t keep,
+                                             uint32_t w) {
+    return __builtin_amdgcn_bitop3_b32(a, keep, w, 0x48);
+}
+
+// Bits set in two consecutive filter words of an SGPR slice (uniform: one
+// s_bcnt1_i32_b64 on the aligned register pair).
+__device__ __forceinline__ uint32_t popcount2(uint32_t lo, uint32_t hi) {
+    return (uint32_t)__builtin_popcountll((uint64_t)hi << 32 | lo);
+}
 
 template <int SW>
 struct Slice {
@@ -285,10 +317,8 @@ __device__ __forceinline__ void flush_tile(
 template <int A, int W, int E, int K, int CW>
 __device__ __forceinline__ void compute_quad(
     const uint32_t (&patch)[Plan<A, W, K, CW>::TB][A][Plan<A, W, K, CW>::CB],
-    uint32_t lc,
-    const uint32_t (&tv)[Plan<A, W, K, CW>::NP][Plan<A, W, K, CW>::NPAIR],
-    gu32* src, gu32* next, Slice<Plan<A, W, K, CW>::SW> (&f)[2],
-    uint32_t (&val)[4]) {
+    uint32_t lc, const TapInfo<A, W, K, CW>& tv, gu32* src, gu32* next,
+    Slice<Plan<A, W, K, CW>::SW> (&f)[2], uint32_t (&val)[4]) {
     using Pl = Plan<A, W, K, CW>;
     using En = Enc<E>;
     static_assert(En::AE != kBipolar || (A == 1 && W == 1),
@@ -322,27 +352,30 @@ __device__ __forceinline__ void compute_quad(
                 load_slice<A, W, K, CW>(f[0], next);
             }
             __builtin_amdgcn_sched_barrier(0);
-            if constexpr (En::AE == kBipolar) {
+            if constexpr (En::AE == kBipolar && !En::kXnor) {
                 // W == 1: per tap, the bits of its CB filter words (uniform,
-                // on the scalar unit); taps 2m and 2m+1 of the slice share
-                // one dot2 with the lane's flags
+                // on the scalar unit, two words per count); taps 2m and
+                // 2m+1 of the slice share one dot2 with the lane's flags
 #pragma unroll
                 for (int o = 0; o < OCB; ++o)
 #pragma unroll
                     for (int m = 0; m < Pl::NPAIR; ++m) {
-                        uint32_t lo = 0, hi = 0;
+                        uint32_t cnt[2] = {0, 0};
 #pragma unroll
-                        for (int c = 0; c < CB; ++c) {
-                            lo += __builtin_popcount(
-                                f[st & 1].w[(o * TS + 2 * m) * CB + c]);
-                            if (2 * m + 1 < TS)
-                                hi += __builtin_popcount(
-                                    f[st & 1].w[(o * TS + 2 * m + 1) * CB + c]);
+                        for (int e = 0; e < 2; ++e) {
+                            if (2 * m + e >= TS) continue;
+                            const uint32_t* wt =
+                                &f[st & 1].w[(o * TS + 2 * m + e) * CB];
+#pragma unroll
+                            for (int c = 0; c + 1 < CB; c += 2)
+                                cnt[e] += popcount2(wt[c], wt[c + 1]);
+                            if (CB & 1)
+                                cnt[e] += __builtin_popcount(wt[CB - 1]);
                         }
                         corr[o] = __builtin_amdgcn_udot2(
-                            __builtin_bit_cast(u16x2, tv[p][m]),
-                            __builtin_bit_cast(u16x2, lo | hi << 16), corr[o],
-                            false);
+                            __builtin_bit_cast(u16x2, tv.pairs[p][m]),
+                            __builtin_bit_cast(u16x2, cnt[0] | cnt[1] << 16),
+                            corr[o], false);
                     }
             }
 #pragma unroll
@@ -359,9 +392,12 @@ __device__ __forceinline__ void compute_quad(
                                 const int h = (t * CB + c) & 1;
                                 const int s =
                                     i + j + (En::neg(i, j, A, W) ? NS : 0);
-                                const uint32_t x =
-                                    patch[t][i][c] &
+                                const uint32_t wv =
                                     f[st & 1].w[((o * TS + tt) * W + j) * CB + c];
+                                const uint32_t x =
+                                    En::kXnor
+                                        ? xor_keep(patch[t][i][c], tv.keep[t], wv)
+                                        : patch[t][i][c] & wv;
                                 if (fresh[h][o][s]) {
                                     bcnt_first(acc[h][o][s], x);
                                     fresh[h][o][s] = false;
@@ -381,11 +417,12 @@ __device__ __forceinline__ void compute_quad(
                 if (s < NS) v += (a0 + a1) << s;
                 else v -= (a0 + a1) << (s - NS);
             }
-            if constexpr (En::AE == kBipolar) {
-                // +-1 activations (A == W == 1): bipolar filters give
-                // 4 S - 2 SW + (N - 2 SA), unipolar ones 2 S - SW
-                if constexpr (En::WE == kBipolar) v = 4u * v - 2u * corr[o] + lc;
-                else v = 2u * v - corr[o];
+            if constexpr (En::kXnor) {
+                // v counts the in-range disagreements D: N - 2 D
+                v = lc - 2u * v;
+            } else if constexpr (En::AE == kBipolar) {
+                // +-1 activations, unipolar 1-bit filters: 2 S - SW
+                v = 2u * v - corr[o];
             } else if constexpr (En::WE == kBipolar) {
                 // bipolar weight value 2w - (2^W - 1): 2 S - (2^W - 1) SA
                 v = 2u * v - (uint32_t)((1 << W) - 1) * lc;
@@ -466,19 +503,15 @@ __device__ __forceinline__ uint32_t patch_sum(
 }
 
 // Per-lane constants of reduction block nb (taps t0 = (nb / NCB) TB ..): the
-// in-range flags of its taps as u16 pairs per slice (bipolar activations),
-// and the lane constant lc the epilogue adds: SA for bipolar filters, N - 2 SA
-// for +-1 data, 0 otherwise.
+// tap data of +-1 activations (TapInfo), and the lane constant lc the
+// epilogue adds: SA for bipolar filters of unipolar or signed activations,
+// N (in-range channel values of the block) for +-1 data, 0 otherwise.
 template <int A, int W, int E, int K, int S, int CW>
 __device__ __forceinline__ uint32_t block_consts(
     const uint32_t (&patch)[Plan<A, W, K, CW>::TB][A][Plan<A, W, K, CW>::CB],
-    uint32_t (&tv)[Plan<A, W, K, CW>::NP][Plan<A, W, K, CW>::NPAIR],
-    const PixArgs& g, int oy, int ox, int nb) {
+    TapInfo<A, W, K, CW>& tv, const PixArgs& g, int oy, int ox, int nb) {
     using Pl = Plan<A, W, K, CW>;
     using En = Enc<E>;
-    const uint32_t sa =
-        En::WE == kBipolar
-            ? patch_sum<A, Pl::TB, Pl::CB, En::AE == kSigned>(patch) : 0u;
     if constexpr (En::AE == kBipolar) {
         const int tb = nb / Pl::NCB, cb = nb - tb * Pl::NCB;
         const int t0 = tb * Pl::TB;
@@ -490,24 +523,28 @@ __device__ __forceinline__ uint32_t block_consts(
                 uint32_t flag[2] = {0, 0};
 #pragma unroll
                 for (int e = 0; e < 2; ++e) {
+                    const int tt = p * Pl::TS + 2 * m + e;
                     if (2 * m + e >= Pl::TS) continue;
-                    const int t = t0 + p * Pl::TS + 2 * m + e;
+                    const int t = t0 + tt;
                     const int r = t / K, q = t - r * K;
                     const int iy = oy * S - g.ph + r, ix = ox * S - g.pw + q;
                     flag[e] = (unsigned)iy < (unsigned)g.h &&
                               (unsigned)ix < (unsigned)g.w;
+                    tv.keep[tt] = 0u - flag[e];
                 }
-                tv[p][m] = flag[0] | flag[1] << 16;
+                tv.pairs[p][m] = flag[0] | flag[1] << 16;
                 nv += flag[0] + flag[1];
             }
-        if constexpr (En::WE == kBipolar) {
+        if constexpr (En::kXnor) {
             // channels of the block's words
             const int ch = min(32 * Pl::CB, g.c - 32 * Pl::CB * cb);
-            return nv * (uint32_t)ch - 2u * sa;
+            return nv * (uint32_t)ch;
         }
         return 0u;
+    } else if constexpr (En::WE == kBipolar) {
+        return patch_sum<A, Pl::TB, Pl::CB, En::AE == kSigned>(patch);
     } else {
-        return sa;
+        return 0u;
     }
 }
 
@@ -530,7 +567,7 @@ __device__ __forceinline__ void run_block(
     Slice<Plan<A, W, K, CW>::SW> (&f)[2], uint32_t* row, const PixArgs& g,
     int oy, int ox) {
     using Pl = Plan<A, W, K, CW>;
-    uint32_t tv[Pl::NP][Pl::NPAIR];
+    TapInfo<A, W, K, CW> tv;
     const uint32_t lc =
         block_consts<A, W, E, K, S, CW>(patch, tv, g, oy, ox, nb);
 #pragma unroll 1
@@ -596,7 +633,7 @@ void conv_pix_kernel(
             uint32_t patch[Pl::TB][A][CW];
             load_patch<A, K, S, CW, Pl::TB, CW>(patch, act, g, img, oy, ox, 0,
                                                0);
-            uint32_t tv[Pl::NP][Pl::NPAIR];
+            TapInfo<A, W, K, CW> tv;
             const uint32_t lc =
                 block_consts<A, W, E, K, S, CW>(patch, tv, g, oy, ox, 0);
             gu32* src = gw + (size_t)(4 * q0) * FW;
