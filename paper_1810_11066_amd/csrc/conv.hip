@@ -212,6 +212,27 @@ bool conv_has_fast_path(const ConvShape& s) {
 
 namespace {
 
+// Images per launch of the pixels-on-lanes kernel: all of them, or as many
+// as keep the packed activations and the int32 output (not the packed
+// output of a requantizing call) within the kernel's 32-bit buffer offsets
+// and its unit counts within int32; 0 when one image is already too large.
+int64_t pix_images_per_launch(const ConvShape& s, bool req) {
+    const int64_t cw = (s.c + 31) / 32;
+    const int64_t act_img = (int64_t)s.h * s.w * s.abits * cw * 4;
+    const int64_t pix_img = (int64_t)s.oh * s.ow;
+    const int64_t out_img = req ? 0 : pix_img * s.oc * 4;
+    const int64_t lim = pix::kMaxBufferBytes;
+    int64_t n = s.n;
+    if (act_img > 0) n = n < lim / act_img ? n : lim / act_img;
+    if (out_img > 0) n = n < lim / out_img ? n : lim / out_img;
+    // npix < 2^31 and units = ceil(npix / 64) * (oc / 4) < 2^30
+    const int64_t by_pix = (INT32_MAX - 64) / pix_img;
+    n = n < by_pix ? n : by_pix;
+    while (n > 0 && ((n * pix_img + 63) / 64) * (s.oc / 4) >= INT32_MAX / 2)
+        n = n / 2;
+    return n;
+}
+
 // Pixels-on-lanes kernel for this shape, or nullptr.
 pix::PixKernelFn pix_kernel_for(const ConvShape& s, bool req,
                                 pix::PlanInfo* info) {
@@ -220,11 +241,7 @@ pix::PixKernelFn pix_kernel_for(const ConvShape& s, bool req,
     if (s.kh != s.kw || s.sh != s.sw) return nullptr;
     // output tiles are written in 16-byte quads of channels
     if (s.oc % 4 != 0) return nullptr;
-    const int64_t npix = (int64_t)s.n * s.oh * s.ow;
-    const int64_t units = (npix + 63) / 64 * (s.oc / 4);
-    if (npix >= INT32_MAX || units >= INT32_MAX / 2) return nullptr;
-    // the kernel addresses activation words with 32-bit offsets
-    if ((int64_t)s.n * s.h * s.w * s.abits * cw >= INT32_MAX) return nullptr;
+    if (pix_images_per_launch(s, req) < 1) return nullptr;
     return pix::pick(s.abits, s.wbits, s.aenc, s.wenc, s.kh, s.sh, (int)cw,
                      req, info);
 }
@@ -294,6 +311,9 @@ void plan_pix(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
     g->div_ow.init((uint32_t)s.ow);
     g->div_oh.init((uint32_t)s.oh);
     g->div_units.init((uint32_t)g->group_units);
+    // within kMaxBufferBytes (pix_images_per_launch)
+    g->act_bytes = (int32_t)((int64_t)s.n * s.h * s.w * s.abits *
+                             ((s.c + 31) / 32) * 4);
     *lds = (size_t)pix::kWavesPerBlock * pix::kTileWords * 4;
     const int64_t cus = device_cus();
     const int64_t slots = cus * resident_blocks(fn, *lds);   // blocks
@@ -356,6 +376,35 @@ void plan_generic(const ConvShape& s, const uint32_t* act, const uint32_t* wts,
     *grid = dim3((uint32_t)blocks);
 }
 
+// Launches the pixels-on-lanes kernel fn over the batch, in chunks of
+// pix_images_per_launch images (a single launch unless the tensors pass
+// 2 GB).  rq: requantized, bit-packed output (out holds uint32 words).
+hipError_t launch_pix(const ConvShape& s, pix::PixKernelFn fn,
+                      const uint32_t* act, const uint32_t* wts, int32_t* out,
+                      int forced_run, const Requant* rq, hipStream_t st) {
+    const int64_t per = pix_images_per_launch(s, rq != nullptr);
+    const int64_t cw = (s.c + 31) / 32;
+    const int64_t act_img = (int64_t)s.h * s.w * s.abits * cw;
+    const int64_t out_img =
+        rq ? (int64_t)s.oh * s.ow * rq->bits * ((s.oc + 31) / 32)
+           : (int64_t)s.oh * s.ow * s.oc;
+    for (int64_t n0 = 0; n0 < s.n; n0 += per) {
+        ConvShape c = s;
+        c.n = (int32_t)(s.n - n0 < per ? s.n - n0 : per);
+        pix::PixArgs g;
+        dim3 grid;
+        size_t lds = 0;
+        plan_pix(c, fn, forced_run, rq, &g, &grid, &lds);
+        const uint32_t* a = act + n0 * act_img;
+        int32_t* o = out + n0 * out_img;
+        void* args[] = {&a, &wts, &o, &g};
+        const hipError_t e = hipLaunchKernel((const void*)fn, grid,
+                                             dim3(pix::kBlock), args, lds, st);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 enum class Family { kPixels, kChannels, kGeneric };
 
 // The kernel family a call takes: mode 0 tries pixels-on-lanes, then
@@ -383,13 +432,9 @@ hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
     dim3 grid;
     size_t lds = 0;
     switch (choose(s, mode, &pfn, &info)) {
-        case Family::kPixels: {
-            pix::PixArgs g;
-            plan_pix(s, pfn, opt.units_per_wave, nullptr, &g, &grid, &lds);
-            void* args[] = {&act, &wts, &out, &g};
-            return hipLaunchKernel((const void*)pfn, grid, dim3(pix::kBlock),
-                                   args, lds, st);
-        }
+        case Family::kPixels:
+            return launch_pix(s, pfn, act, wts, out, opt.units_per_wave,
+                              nullptr, st);
         case Family::kChannels: {
             FastArgs g;
             plan_fast(s, &g, &grid, &lds);
@@ -419,15 +464,9 @@ hipError_t launch_conv_requant(const ConvShape& s, const uint32_t* act,
     pix::PixKernelFn pfn = nullptr;
     if (opt.mode == 0 || opt.mode == 3) pfn = pix_kernel_for(s, true, &info);
     if (pfn) {
-        pix::PixArgs g;
-        dim3 grid;
-        size_t lds = 0;
         // the run-length override counts packed bytes (2 quads) here
-        plan_pix(s, pfn, opt.units_per_wave, &rq, &g, &grid, &lds);
-        int32_t* o = reinterpret_cast<int32_t*>(out);
-        void* args[] = {&act, &wts, &o, &g};
-        return hipLaunchKernel((const void*)pfn, grid, dim3(pix::kBlock),
-                               args, lds, st);
+        return launch_pix(s, pfn, act, wts, reinterpret_cast<int32_t*>(out),
+                          opt.units_per_wave, &rq, st);
     }
     GenericRequantArgs g;
     g.act = act;
@@ -466,8 +505,13 @@ int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
         snprintf(enc, sizeof(enc), "%s x %s", names[s.aenc], names[s.wenc]);
     switch (choose(s, mode, &pfn, &info)) {
         case Family::kPixels: {
+            // the plan of the first launch (of `launches` image chunks)
+            const int64_t per = pix_images_per_launch(s, false);
+            ConvShape c = s;
+            c.n = (int32_t)(s.n < per ? s.n : per);
             pix::PixArgs g;
-            plan_pix(s, pfn, opt.units_per_wave, nullptr, &g, &grid, &lds);
+            plan_pix(c, pfn, opt.units_per_wave, nullptr, &g, &grid, &lds);
+            const int64_t launches = (s.n + per - 1) / per;
             // the encodings the specialisation was compiled for
             char kenc[48];
             if (info.enc / 3 == kUnipolar)
@@ -479,10 +523,11 @@ int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
                             "conv_pix_kernel<A=%d,W=%d,%s,K=%d,S=%d,CW=%d> "
                             "patch=%dtaps x %dwords slice=%dch x %dtaps "
                             "grid=%u block=%d lds=%zu units=%d "
-                            "units_per_wave=%d",
+                            "units_per_wave=%d%s",
                             s.abits, s.wbits, kenc, s.kh, s.sh, cw, info.tb,
                             info.cb, info.ocb, info.ts, grid.x, pix::kBlock,
-                            lds, g.units, g.per_wave);
+                            lds, g.units, g.per_wave,
+                            launches > 1 ? " (per launch; batch split)" : "");
         }
         case Family::kChannels: {
             FastArgs g;

@@ -94,6 +94,7 @@ struct PixArgs {
     int32_t out_words;     // ceil(oc / 32): words per plane of a pixel
     FastDiv div_ow, div_oh, div_units;
     int32_t c;             // input channels (+-1 activations only)
+    int32_t act_bytes;     // size of the packed activations, bytes
 };
 
 __device__ __forceinline__ void bcnt_acc(uint32_t& acc, uint32_t x) {
@@ -283,25 +284,64 @@ constexpr int kChunk = 16;                 // output channels per LDS tile
 constexpr int kTileStride = kChunk + 1;    // words per pixel row (padded)
 constexpr int kTileWords = 64 * kTileStride;
 
-__device__ __forceinline__ void flush_tile(
-    const uint32_t* __restrict__ tile, int32_t* __restrict__ out,
-    int pix0, int npix, int oc_total, int oc_base, int nch, int lane) {
-    // nch in {4, 8, 12, 16}: lpp = nch / 4 lanes per pixel, lpp rounds of
-    // 64 (pixel, quad) entries.  e / lpp for e < 256 is (e * m) >> 16 with
-    // m = ceil(2^16 / lpp): the error e (m lpp - 2^16) / (lpp 2^16) stays
-    // below 1/lpp - frac(e / lpp) for every such e.
-    const int lpp = nch >> 2;
-    const uint32_t m = lpp == 1 ? 65536u : lpp == 2 ? 32768u
-                     : lpp == 3 ? 21846u : 16384u;
-    for (int r = 0; r < lpp; ++r) {
-        const uint32_t e = (uint32_t)(r * 64 + lane);
-        const int px = (int)((e * m) >> 16);
-        const int q = (int)e - px * lpp;
-        if (pix0 + px < npix) {
-            const uint32_t* t = tile + px * kTileStride + 4 * q;
-            *reinterpret_cast<uint4*>(
-                out + (int64_t)(pix0 + px) * oc_total + oc_base + 4 * q) =
-                make_uint4(t[0], t[1], t[2], t[3]);
+// Buffer resource of the packed activations.  They are read through raw
+// buffer loads: a load at an offset past the buffer's size returns zeros, so
+// a tap in the padding only needs the offset kOutOfRange -- no address
+// arithmetic per tap and no masking of the loaded words.  The host keeps the
+// activations below kMaxBufferBytes, so that offset plus any instruction
+// offset stays out of range.  (Results leave through global stores: a wide
+// buffer store whose scalar offset is a register has been seen to lose its
+// data when the next instruction overwrote the data registers, a wait the
+// compiler does not insert for that form.)
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr uint32_t kOutOfRange = 0x80000000u;
+constexpr int64_t kMaxBufferBytes = (int64_t)kOutOfRange - 65536;
+constexpr int kRsrcWord3 = 0x00020000;   // 32-bit data format (gfx9 family)
+
+__device__ __forceinline__ Rsrc make_rsrc(const void* p, int32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0,
+                                             bytes, kRsrcWord3);
+}
+
+// Where a lane's 16-byte pieces of a tile flush go.  Round r (0..3) of a
+// flush moves the tile entries of pixel 16 r + lane / 4, quad lane % 4.
+// off0 is the byte offset of round 0's piece for the group's first channel;
+// round r adds 64 r oc bytes (16 pixel rows) and a chunk its first channel,
+// both uniform, to the base address (a scalar base plus a 32-bit lane
+// offset).  Only the group holding the last pixel needs per-round checks.
+// The host keeps the output below kMaxBufferBytes.
+struct FlushMap {
+    uint32_t off0;
+    int pix0, npix, oc;
+
+    __device__ __forceinline__ void init(int pix0_, int npix_, int oc_,
+                                         int lane) {
+        pix0 = pix0_;
+        npix = npix_;
+        oc = oc_;
+        off0 = ((uint32_t)(pix0 + (lane >> 2)) * (uint32_t)oc +
+                4u * (lane & 3)) * 4u;
+    }
+};
+
+// Writes channels [oc_base, oc_base + nch) of the group's 64 pixels from the
+// wave's tile (nch in {4, 8, 12, 16}: quads lane % 4 < nch / 4 take part).
+__device__ __forceinline__ void flush_tile(const uint32_t* __restrict__ tile,
+                                           int32_t* __restrict__ out,
+                                           const FlushMap& fm, int oc_base,
+                                           int nch, int lane) {
+    const uint32_t rstep = 64u * (uint32_t)fm.oc;    // bytes per round
+    const bool full = fm.pix0 + 64 <= fm.npix;       // uniform
+    if ((lane & 3) < (nch >> 2)) {
+        const uint32_t* t = tile + (lane >> 2) * kTileStride + 4 * (lane & 3);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t* e = t + 16 * r * kTileStride;
+            char* base = reinterpret_cast<char*>(out) + 4 * oc_base +
+                         (size_t)(r * rstep);
+            if (full || fm.pix0 + 16 * r + (lane >> 2) < fm.npix)
+                *reinterpret_cast<uint4*>(base + fm.off0) =
+                    make_uint4(e[0], e[1], e[2], e[3]);
         }
     }
 }
@@ -432,53 +472,58 @@ __device__ __forceinline__ void compute_quad(
     }
 }
 
+// The lane's input window: byte offset of its top-left input pixel
+// (iy0, ix0) -- wrapped modulo 2^32 when that pixel lies in the padding; only
+// in-range taps use it, and for those the sum is the true offset -- and the
+// window's origin.
+struct Window {
+    uint32_t base;
+    int iy0, ix0;
+};
+
 // Loads the lane's input words of one reduction block: taps [t0, t0 + TB)
 // of the window and words [c0, c0 + CB) of each of the A planes (zero for
-// taps in the padding).
-template <int A, int K, int S, int CW, int TB, int CB>
-__device__ __forceinline__ void load_patch(
-    uint32_t (&patch)[TB][A][CB], const uint32_t* __restrict__ act,
-    const PixArgs& g, uint32_t img, int oy, int ox, int t0, int c0) {
-    constexpr int PW = A * CW;           // words per packed input pixel
+// taps in the padding: their offset is out of the buffer's range).
+template <int A, int K, int CW, int TB, int CB>
+__device__ __forceinline__ void load_patch(uint32_t (&patch)[TB][A][CB],
+                                           Rsrc act, const PixArgs& g,
+                                           const Window& win, int t0, int c0) {
+    constexpr uint32_t PWB = 4 * A * CW;     // bytes per packed input pixel
+    const uint32_t rowb = (uint32_t)g.w * PWB;
 #pragma unroll
     for (int tt = 0; tt < TB; ++tt) {
         const int t = t0 + tt;
         const int r = t / K, s = t - r * K;
-        const int iy = oy * S - g.ph + r;
-        const int ix = ox * S - g.pw + s;
-        const bool in = (unsigned)iy < (unsigned)g.h &&
-                        (unsigned)ix < (unsigned)g.w;
-        // 32-bit word offsets: the host keeps the activations below 2^31
-        // words; a padded tap reads pixel 0 and is masked below
-        const uint32_t pix =
-            in ? ((uint32_t)img * (uint32_t)g.h + (uint32_t)iy) *
-                         (uint32_t)g.w + (uint32_t)ix
-               : 0u;
-        const uint32_t keep = in ? 0xFFFFFFFFu : 0u;
+        const bool in = (unsigned)(win.iy0 + r) < (unsigned)g.h &&
+                        (unsigned)(win.ix0 + s) < (unsigned)g.w;
+        const uint32_t off =
+            (in ? win.base + (uint32_t)r * rowb + (uint32_t)s * PWB
+                : kOutOfRange) + 4u * (uint32_t)c0;
 #pragma unroll
         for (int i = 0; i < A; ++i) {
-            const uint32_t* src =
-                act + (size_t)(pix * (uint32_t)PW + (uint32_t)(i * CW + c0));
-            uint32_t wv[CB];
+            const uint32_t o = off + 4u * (uint32_t)(i * CW);
             if constexpr (CB % 4 == 0) {
 #pragma unroll
                 for (int k = 0; k < CB; k += 4) {
-                    const uint4 x = *reinterpret_cast<const uint4*>(src + k);
-                    wv[k] = x.x; wv[k + 1] = x.y;
-                    wv[k + 2] = x.z; wv[k + 3] = x.w;
+                    const auto x = __builtin_amdgcn_raw_buffer_load_b128(
+                        act, o + 4u * k, 0, 0);
+                    patch[tt][i][k] = x[0]; patch[tt][i][k + 1] = x[1];
+                    patch[tt][i][k + 2] = x[2]; patch[tt][i][k + 3] = x[3];
                 }
             } else if constexpr (CB % 2 == 0) {
 #pragma unroll
                 for (int k = 0; k < CB; k += 2) {
-                    const uint2 x = *reinterpret_cast<const uint2*>(src + k);
-                    wv[k] = x.x; wv[k + 1] = x.y;
+                    const auto x = __builtin_amdgcn_raw_buffer_load_b64(
+                        act, o + 4u * k, 0, 0);
+                    patch[tt][i][k] = x[0]; patch[tt][i][k + 1] = x[1];
                 }
             } else {
 #pragma unroll
-                for (int k = 0; k < CB; ++k) wv[k] = src[k];
+                for (int k = 0; k < CB; ++k)
+                    patch[tt][i][k] =
+                        __builtin_amdgcn_raw_buffer_load_b32(act, o + 4u * k,
+                                                             0, 0);
             }
-#pragma unroll
-            for (int c = 0; c < CB; ++c) patch[tt][i][c] = wv[c] & keep;
         }
     }
 }
@@ -610,6 +655,7 @@ void conv_pix_kernel(
     extern __shared__ uint32_t lds[];
     uint32_t* tile = lds + (threadIdx.x >> 6) * kTileWords;
     gu32* gw = (gu32*)(wts);
+    const Rsrc ract = make_rsrc(act, g.act_bytes);
 
     while (u < u_end) {
         const int grp = (int)g.div_units.div((uint32_t)u);
@@ -626,13 +672,19 @@ void conv_pix_kernel(
         const int ox = (int)(pc - rowi * (uint32_t)g.ow);
         const uint32_t img = g.div_oh.div(rowi);
         const int oy = (int)(rowi - img * (uint32_t)g.oh);
+        Window win;
+        win.iy0 = oy * S - g.ph;
+        win.ix0 = ox * S - g.pw;
+        win.base = ((img * (uint32_t)g.h + (uint32_t)win.iy0) * (uint32_t)g.w +
+                    (uint32_t)win.ix0) * (uint32_t)(4 * A * CW);
+        FlushMap fm;
+        if constexpr (!REQ) fm.init(pix0, g.npix, g.oc, lane);
 
         if constexpr (NB == 1) {
             // whole patch: one pass over the segment's quads, the slice
             // pipeline running across tile flushes
             uint32_t patch[Pl::TB][A][CW];
-            load_patch<A, K, S, CW, Pl::TB, CW>(patch, act, g, img, oy, ox, 0,
-                                               0);
+            load_patch<A, K, CW, Pl::TB, CW>(patch, ract, g, win, 0, 0);
             TapInfo<A, W, K, CW> tv;
             const uint32_t lc =
                 block_consts<A, W, E, K, S, CW>(patch, tv, g, oy, ox, 0);
@@ -664,8 +716,8 @@ void conv_pix_kernel(
                     ++held;
                     if (held == kChunk / 4 || qi + 1 == nq) {
                         wave_lds_sync();
-                        flush_tile(tile, out, pix0, g.npix, g.oc, chunk_base,
-                                   held * 4, lane);
+                        flush_tile(tile, out, fm, chunk_base, held * 4,
+                                   lane);
                         wave_lds_sync();
                         chunk_base += held * 4;
                         held = 0;
@@ -689,8 +741,8 @@ void conv_pix_kernel(
                 };
                 auto load_block = [&](Patch& pt, int nb) {
                     const int tb = nb / Pl::NCB;
-                    load_patch<A, K, S, CW, Pl::TB, Pl::CB>(
-                        pt, act, g, img, oy, ox, tb * Pl::TB,
+                    load_patch<A, K, CW, Pl::TB, Pl::CB>(
+                        pt, ract, g, win, tb * Pl::TB,
                         (nb - tb * Pl::NCB) * Pl::CB);
                 };
                 if constexpr (Pl::DBUF) {
@@ -738,8 +790,7 @@ void conv_pix_kernel(
                     }
                 } else {
                     wave_lds_sync();
-                    flush_tile(tile, out, pix0, g.npix, g.oc, 4 * sub, nq * 4,
-                               lane);
+                    flush_tile(tile, out, fm, 4 * sub, nq * 4, lane);
                     wave_lds_sync();
                 }
             }

@@ -234,6 +234,20 @@ def test_units_per_wave(lib):
         assert lib.bs_set_units_per_wave(0) == bs.BS_OK
 
 
+def test_describe_batch_split(lib):
+    # the pixel kernel addresses its tensors with 32-bit offsets: an int32
+    # output past 2 GB (128 x 56 x 56 x 1344) is split into image chunks of
+    # 127 and 1 (2^31 - 64 KiB / 16.9 MB per image), one below stays whole
+    big = params(n=128, h=56, w=56, c=32, oc=1344, kh=1, kw=1, pad_h=0,
+                 pad_w=0, abits=1, wbits=1)
+    d = bs.bs_conv2d_describe(big)
+    assert d.startswith("conv_pix_kernel") and "batch split" in d
+    assert "units=%d " % (127 * 56 * 56 // 64 * 1344 // 4) in d
+    small = params(n=126, h=56, w=56, c=32, oc=1344, kh=1, kw=1, pad_h=0,
+                   pad_w=0, abits=1, wbits=1)
+    assert "batch split" not in bs.bs_conv2d_describe(small)
+
+
 def test_binding_refuses_cpu_tensors():
     import torch
     x = torch.zeros(16, dtype=torch.float32)

@@ -472,3 +472,37 @@ def test_int8_baseline_equals_bitserial(oracle):
     got = bs.dense(bs.pack(dev(a), 2), bs.pack(dev(wd), 2), m, nn, k, 2, 2)
     torch.cuda.synchronize()
     assert torch.equal(base, got)
+
+
+# ------------------------------------------------ batch split past 2 GB --
+
+def test_conv_batch_split_over_2gb(oracle):
+    # an int32 output of 2.16 GB is more than one launch of the pixel kernel
+    # addresses (32-bit offsets): the batch is split into image chunks.  The
+    # chunk boundary (127 images, then 1) is checked against the oracle on
+    # whole images and against the generic kernel everywhere.
+    n, h, w, c, oc = 128, 56, 56, 32, 1344
+    say("conv batch split", n, h, w, c, oc)
+    rng = np.random.default_rng(2048)
+    a = rng.integers(0, 2, size=(n, h, w, c), dtype=np.uint8)
+    wq = rng.integers(0, 2, size=(oc, 1, 1, c), dtype=np.uint8)
+    ap, wp = oracle.pack(a, 1), oracle.pack(wq, 1)
+    spec = bs.Conv2dSpec(n, h, w, c, oc, 1, 1, 1, 0, 1, 1)
+    assert "batch split" in bs.bs_conv2d_describe(spec.params())
+    a_dev, w_dev = dev(ap.view(np.int32)), dev(wp.view(np.int32))
+    out = bs.conv2d(spec, a_dev, w_dev)
+    bs.bs_set_kernel_mode(1)
+    try:
+        ref = bs.conv2d(spec, a_dev, w_dev)
+    finally:
+        bs.bs_set_kernel_mode(0)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
+    del ref
+    per_image = h * w * oc
+    idx = np.concatenate([np.arange(125 * per_image, n * per_image),
+                          rng.integers(0, n * per_image, 65536)])
+    got = out.view(-1)[torch.from_numpy(idx).cuda()].cpu().numpy()
+    want = oracle.conv2d_at(oracle.conv_params(n, h, w, c, oc, 1, 1, 1, 0, 1,
+                                               1), ap, wp, idx)
+    assert np.array_equal(got, want)
