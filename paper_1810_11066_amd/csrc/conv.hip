@@ -261,8 +261,9 @@ int device_cus() {
 }
 
 // Resident blocks of fn per CU (register, LDS and wave-slot limits), cached
-// per kernel and device.  The pixel kernels stay within 80 SGPRs, where the
-// runtime's count agrees with the hardware.
+// per kernel and device.  The runtime counts SGPRs the way the compiler does,
+// which overstates residency above 80 SGPRs; the pixel kernels use up to 96,
+// where the hardware holds pix::kWavesPerSimd waves per SIMD.
 int resident_blocks(pix::PixKernelFn fn, size_t lds) {
     struct Entry { pix::PixKernelFn fn; int dev; size_t lds; int blocks; };
     static std::mutex mu;
@@ -279,6 +280,9 @@ int resident_blocks(pix::PixKernelFn fn, size_t lds) {
             &blocks, (const void*)fn, pix::kBlock, lds) != hipSuccess ||
         blocks < 1)
         return 1;
+    // 4 SIMDs per CU
+    const int cap = 4 * pix::kWavesPerSimd / pix::kWavesPerBlock;
+    if (blocks > cap) blocks = cap;
     std::lock_guard<std::mutex> lock(mu);
     cache.push_back({fn, dev, lds, blocks});
     return blocks;

@@ -32,10 +32,12 @@
 //
 // Occupancy.  The hardware reserves more SGPRs per wave than the compiler's
 // count: measured on gfx950, 8 waves fit on a SIMD up to 80 SGPRs, 7 up to
-// 96 and 6 above.  The kernel is therefore compiled for at most 80 SGPRs
+// 96 and 6 above.  The kernel is compiled for at most kMaxSgprs = 96 SGPRs
 // (the slice bound keeps the channel loop within that; what does not fit is
-// spilled to VGPR lanes in the per-group code), and the host's occupancy
-// query, which counts the way the compiler does, is then exact.
+// spilled to VGPR lanes in the per-group code), and the host caps the
+// occupancy query, which counts the way the compiler does, at
+// kWavesPerSimd = 7 waves per SIMD.  At 80 SGPRs (8 waves) the spills of the
+// per-group code cost more than the eighth wave gains.
 #pragma once
 
 #include "bs_internal.h"
@@ -45,6 +47,7 @@ namespace pix {
 
 constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / 64;
+constexpr int kWavesPerSimd = 7;    // resident at up to 96 SGPRs per wave
 constexpr int kSliceWords = 24;     // filter words per SGPR slice
 
 // Operand encodings of a specialisation: E = 3 * (activation encoding) +
@@ -639,7 +642,7 @@ __device__ __forceinline__ void run_block(
 // (out then holds [npix][out_bits][out_words] uint32 words) instead of
 // storing int32.
 template <int A, int W, int E, int K, int S, int CW, bool REQ>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_num_sgpr(80)))
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_num_sgpr(96)))
 void conv_pix_kernel(
     const uint32_t* __restrict__ act, const uint32_t* __restrict__ wts,
     int32_t* __restrict__ out, PixArgs g) {
