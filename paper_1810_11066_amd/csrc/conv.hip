@@ -318,6 +318,7 @@ void plan_pix(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
     // within kMaxBufferBytes (pix_images_per_launch)
     g->act_bytes = (int32_t)((int64_t)s.n * s.h * s.w * s.abits *
                              ((s.c + 31) / 32) * 4);
+    g->out_bytes = rq ? 0 : (int32_t)((int64_t)g->npix * s.oc * 4);
     *lds = (size_t)pix::kWavesPerBlock * pix::kTileWords * 4;
     const int64_t cus = device_cus();
     const int64_t slots = cus * resident_blocks(fn, *lds);   // blocks
@@ -332,7 +333,18 @@ void plan_pix(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
     int64_t best = lmin;
     for (int64_t l = lmin + 1; l <= 2 * lmin; ++l)
         if (load(l) < load(best)) best = l;
-    if (forced_run > 0) best = forced_run < units ? forced_run : units;
+    // 1x1 layers with few word pairs per result (A W words <= 16) are bound
+    // by their int32 stores, not by the vector ALUs: runs of one tile chunk
+    // of quads make every flush write whole 64-byte pieces of the pixel
+    // rows (a run boundary inside a chunk leaves pieces of 16-48 bytes, which
+    // the memory system handles at a fraction of the rate), however many
+    // rounds of waves that takes.  Measured on the ResNet-18 1x1 layers:
+    // 5-20 % faster than the balanced single-round plan.
+    const int64_t cw = (s.c + 31) / 32;
+    if (!rq && s.kh == 1 && s.abits * s.wbits * cw <= 16)
+        best = pix::kChunk / 4;
+    if (forced_run > 0) best = forced_run;
+    if (best > units) best = units;
     g->per_wave = (int32_t)best;
     const int64_t waves = (units + best - 1) / best;
     *grid = dim3((uint32_t)((waves + wpb - 1) / wpb));

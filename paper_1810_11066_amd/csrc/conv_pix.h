@@ -98,6 +98,7 @@ struct PixArgs {
     FastDiv div_ow, div_oh, div_units;
     int32_t c;             // input channels (+-1 activations only)
     int32_t act_bytes;     // size of the packed activations, bytes
+    int32_t out_bytes;     // size of the int32 output, bytes (0: packed out)
 };
 
 __device__ __forceinline__ void bcnt_acc(uint32_t& acc, uint32_t x) {
@@ -287,15 +288,18 @@ constexpr int kChunk = 16;                 // output channels per LDS tile
 constexpr int kTileStride = kChunk + 1;    // words per pixel row (padded)
 constexpr int kTileWords = 64 * kTileStride;
 
-// Buffer resource of the packed activations.  They are read through raw
-// buffer loads: a load at an offset past the buffer's size returns zeros, so
-// a tap in the padding only needs the offset kOutOfRange -- no address
-// arithmetic per tap and no masking of the loaded words.  The host keeps the
-// activations below kMaxBufferBytes, so that offset plus any instruction
-// offset stays out of range.  (Results leave through global stores: a wide
-// buffer store whose scalar offset is a register has been seen to lose its
-// data when the next instruction overwrote the data registers, a wait the
-// compiler does not insert for that form.)
+// Buffer resources.  Activations are read and int32 results written
+// through raw buffer instructions: an access at an offset past the buffer's
+// size reads zeros or is dropped.  A tap in the padding therefore only needs
+// the offset kOutOfRange -- no address arithmetic per tap, no masking of the
+// loaded words -- and so does a store for a pixel past the end, which keeps
+// the stores of a flush unconditional (a fixed number of memory operations
+// after a prefetch, which the compiler's wait counts rely on).  The host
+// keeps both tensors below kMaxBufferBytes, so that kOutOfRange plus any
+// instruction offset stays out of range.  The scalar offset of every store
+// is the constant 0: a wide buffer store whose scalar offset is a register
+// has been seen to lose its data when the next instruction overwrote the
+// data registers, a wait the compiler only inserts for the constant form.
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 constexpr uint32_t kOutOfRange = 0x80000000u;
 constexpr int64_t kMaxBufferBytes = (int64_t)kOutOfRange - 65536;
@@ -306,13 +310,17 @@ __device__ __forceinline__ Rsrc make_rsrc(const void* p, int32_t bytes) {
                                              bytes, kRsrcWord3);
 }
 
-// Where a lane's 16-byte pieces of a tile flush go.  Round r (0..3) of a
-// flush moves the tile entries of pixel 16 r + lane / 4, quad lane % 4.
-// off0 is the byte offset of round 0's piece for the group's first channel;
-// round r adds 64 r oc bytes (16 pixel rows) and a chunk its first channel,
-// both uniform, to the base address (a scalar base plus a 32-bit lane
-// offset).  Only the group holding the last pixel needs per-round checks.
-// The host keeps the output below kMaxBufferBytes.
+// Where a lane's 16-byte pieces of a tile flush go.  A flush moves the
+// tile's 64 pixels x kChunk channels in kFlushRounds rounds: in round r lane
+// l stores quad l % kFlushRounds of pixel r * 64 / kFlushRounds +
+// l / kFlushRounds (kChunk / 4 lanes per pixel, so a round writes runs of
+// 4 kChunk contiguous bytes).  off0 is the byte offset of round 0's piece for
+// the group's first channel; round r adds (64 / kFlushRounds) r oc 4 bytes
+// and a chunk its first channel.  Only the group holding the last pixel
+// needs per-round checks.
+constexpr int kFlushRounds = kChunk / 4;
+constexpr int kFlushPixels = 64 / kFlushRounds;    // pixels per round
+
 struct FlushMap {
     uint32_t off0;
     int pix0, npix, oc;
@@ -322,30 +330,30 @@ struct FlushMap {
         pix0 = pix0_;
         npix = npix_;
         oc = oc_;
-        off0 = ((uint32_t)(pix0 + (lane >> 2)) * (uint32_t)oc +
-                4u * (lane & 3)) * 4u;
+        off0 = ((uint32_t)(pix0 + lane / kFlushRounds) * (uint32_t)oc +
+                4u * (uint32_t)(lane % kFlushRounds)) * 4u;
     }
 };
 
 // Writes channels [oc_base, oc_base + nch) of the group's 64 pixels from the
-// wave's tile (nch in {4, 8, 12, 16}: quads lane % 4 < nch / 4 take part).
+// wave's tile (nch a multiple of 4 up to kChunk: the lanes of quads below
+// nch / 4 take part, the others store out of range).
 __device__ __forceinline__ void flush_tile(const uint32_t* __restrict__ tile,
-                                           int32_t* __restrict__ out,
-                                           const FlushMap& fm, int oc_base,
-                                           int nch, int lane) {
-    const uint32_t rstep = 64u * (uint32_t)fm.oc;    // bytes per round
-    const bool full = fm.pix0 + 64 <= fm.npix;       // uniform
-    if ((lane & 3) < (nch >> 2)) {
-        const uint32_t* t = tile + (lane >> 2) * kTileStride + 4 * (lane & 3);
+                                           Rsrc out, const FlushMap& fm,
+                                           int oc_base, int nch, int lane) {
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const uint32_t rstep = 4u * kFlushPixels * (uint32_t)fm.oc;  // per round
+    const int q = lane % kFlushRounds, pr = lane / kFlushRounds;
+    const bool qin = q < (nch >> 2);
+    const uint32_t o0 = fm.off0 + 4u * (uint32_t)oc_base;
+    const uint32_t* t = tile + pr * kTileStride + 4 * q;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const uint32_t* e = t + 16 * r * kTileStride;
-            char* base = reinterpret_cast<char*>(out) + 4 * oc_base +
-                         (size_t)(r * rstep);
-            if (full || fm.pix0 + 16 * r + (lane >> 2) < fm.npix)
-                *reinterpret_cast<uint4*>(base + fm.off0) =
-                    make_uint4(e[0], e[1], e[2], e[3]);
-        }
+    for (int r = 0; r < kFlushRounds; ++r) {
+        const uint32_t* e = t + kFlushPixels * r * kTileStride;
+        const u32x4 v = {e[0], e[1], e[2], e[3]};
+        const bool in = qin && fm.pix0 + kFlushPixels * r + pr < fm.npix;
+        __builtin_amdgcn_raw_buffer_store_b128(
+            v, out, in ? o0 + (uint32_t)r * rstep : kOutOfRange, 0, 0);
     }
 }
 
@@ -637,6 +645,18 @@ __device__ __forceinline__ void run_block(
     }
 }
 
+// One group visit of a wave: units [w0, w1) of a 64-pixel group, i.e.
+// quads [q0, q1) of its output channels, and the lane's pixel p = pix0 +
+// lane at (oy, ox) with its input window and flush offsets.
+struct Visit {
+    int w0, w1, q0, q1, pix0, p, ox, oy;
+    Window win;
+    FlushMap fm;
+};
+
+// Patches of at most this many words are requested a visit ahead.
+constexpr int kAheadWords = 16;
+
 // A, W: bit-widths; E: operand encodings (Enc); K: square kernel size;
 // S: stride; CW: words per bit-plane; REQ: requantize and bit-pack the output
 // (out then holds [npix][out_bits][out_words] uint32 words) instead of
@@ -659,44 +679,74 @@ void conv_pix_kernel(
     uint32_t* tile = lds + (threadIdx.x >> 6) * kTileWords;
     gu32* gw = (gu32*)(wts);
     const Rsrc ract = make_rsrc(act, g.act_bytes);
+    const Rsrc rout = make_rsrc(out, g.out_bytes);
 
-    while (u < u_end) {
-        const int grp = (int)g.div_units.div((uint32_t)u);
-        const int w0 = u - grp * g.group_units;            // first unit
-        const int w1 = min(g.group_units, w0 + (u_end - u));
-        const int q0 = w0 * g.unit_quads;
-        const int q1 = min(g.quads, w1 * g.unit_quads);
-        const int pix0 = grp * 64;
-
+    // one group visit: the run's units in the current 64-pixel group
+    auto visit_at = [&](int u0) {
+        Visit v;
+        const int grp = (int)g.div_units.div((uint32_t)u0);
+        v.w0 = u0 - grp * g.group_units;                     // first unit
+        v.w1 = min(g.group_units, v.w0 + (u_end - u0));
+        v.q0 = v.w0 * g.unit_quads;
+        v.q1 = min(g.quads, v.w1 * g.unit_quads);
+        v.pix0 = grp * 64;
         // this lane's output pixel (the last pixel stands in past the end)
-        const int p = pix0 + lane;
-        const uint32_t pc = (uint32_t)(p < g.npix ? p : g.npix - 1);
+        v.p = v.pix0 + lane;
+        const uint32_t pc = (uint32_t)(v.p < g.npix ? v.p : g.npix - 1);
         const uint32_t rowi = g.div_ow.div(pc);
-        const int ox = (int)(pc - rowi * (uint32_t)g.ow);
+        v.ox = (int)(pc - rowi * (uint32_t)g.ow);
         const uint32_t img = g.div_oh.div(rowi);
-        const int oy = (int)(rowi - img * (uint32_t)g.oh);
-        Window win;
-        win.iy0 = oy * S - g.ph;
-        win.ix0 = ox * S - g.pw;
-        win.base = ((img * (uint32_t)g.h + (uint32_t)win.iy0) * (uint32_t)g.w +
-                    (uint32_t)win.ix0) * (uint32_t)(4 * A * CW);
-        FlushMap fm;
-        if constexpr (!REQ) fm.init(pix0, g.npix, g.oc, lane);
+        v.oy = (int)(rowi - img * (uint32_t)g.oh);
+        v.win.iy0 = v.oy * S - g.ph;
+        v.win.ix0 = v.ox * S - g.pw;
+        v.win.base = ((img * (uint32_t)g.h + (uint32_t)v.win.iy0) *
+                          (uint32_t)g.w + (uint32_t)v.win.ix0) *
+                     (uint32_t)(4 * A * CW);
+        if constexpr (!REQ) v.fm.init(v.pix0, g.npix, g.oc, lane);
+        return v;
+    };
 
-        if constexpr (NB == 1) {
-            // whole patch: one pass over the segment's quads, the slice
-            // pipeline running across tile flushes
-            uint32_t patch[Pl::TB][A][CW];
-            load_patch<A, K, CW, Pl::TB, CW>(patch, ract, g, win, 0, 0);
+    if constexpr (NB == 1) {
+        // whole patch: one pass over each visit's quads, the slice pipeline
+        // running across tile flushes.  With a small patch the next visit's
+        // words are requested before this visit's last stores: vmcnt counts
+        // loads and stores in order, so a load issued after them would wait
+        // for their completion (and the HBM-bound 1x1 layers would stall).
+        constexpr bool kAhead = Pl::PB <= kAheadWords;
+        if (u >= u_end) return;
+        Visit v = visit_at(u);
+        uint32_t patch[Pl::TB][A][CW];
+        load_patch<A, K, CW, Pl::TB, CW>(patch, ract, g, v.win, 0, 0);
+        if constexpr (kAhead && !REQ) {
+            // an empty flush (every store out of range): the loop is then
+            // entered, as it is re-entered, with the patch load followed by
+            // one flush's stores, so the wait for the patch can leave those
+            // in flight
+            flush_tile(tile, rout, v.fm, 0, 0, lane);
+        }
+        while (true) {
+            if constexpr (kAhead) {
+                // take the patch words here, outside the channel loop: the
+                // wait for them is then placed here and counts past the
+                // stores that followed their load (a first use inside the
+                // loop gets a full wait in front of it instead)
+#pragma unroll
+                for (int t = 0; t < Pl::TB; ++t)
+#pragma unroll
+                    for (int i = 0; i < A; ++i)
+#pragma unroll
+                        for (int c = 0; c < CW; ++c)
+                            asm volatile("" ::"v"(patch[t][i][c]));
+            }
             TapInfo<A, W, K, CW> tv;
             const uint32_t lc =
-                block_consts<A, W, E, K, S, CW>(patch, tv, g, oy, ox, 0);
-            gu32* src = gw + (size_t)(4 * q0) * FW;
+                block_consts<A, W, E, K, S, CW>(patch, tv, g, v.oy, v.ox, 0);
+            gu32* src = gw + (size_t)(4 * v.q0) * FW;
             Slice<Pl::SW> f[2];
             load_slice<A, W, K, CW>(f[0], src);
-            const int nq = q1 - q0;
-            int chunk_base = 4 * q0;   // first channel held in the tile
-            int held = 0;              // quads held in the tile
+            const int nq = v.q1 - v.q0;
+            int chunk_base = 4 * v.q0;   // first channel held in the tile
+            int held = 0;                // quads held in the tile
             PackedOut po;
             po.clear();
             for (int qi = 0; qi < nq; ++qi) {
@@ -706,10 +756,10 @@ void conv_pix_kernel(
                     patch, lc, tv, q, qi + 1 < nq ? q + 4 * FW : src, f, val);
                 if constexpr (REQ) {
                     // a packed byte holds 2 quads; runs start on a byte
-                    const int qg = q0 + qi;
+                    const int qg = v.q0 + qi;
                     po.add4(val, g, qg & 1);
-                    if ((qg & 1) == 1 || qi + 1 == nq) {
-                        if (p < g.npix) po.store(out, g, p, qg >> 1);
+                    if ((qg & 1) == 1 && qi + 1 < nq) {
+                        if (v.p < g.npix) po.store(out, g, v.p, qg >> 1);
                         po.clear();
                     }
                 } else {
@@ -717,9 +767,9 @@ void conv_pix_kernel(
                     for (int o = 0; o < 4; ++o)
                         tile[lane * kTileStride + held * 4 + o] = val[o];
                     ++held;
-                    if (held == kChunk / 4 || qi + 1 == nq) {
+                    if (held == kChunk / 4 && qi + 1 < nq) {
                         wave_lds_sync();
-                        flush_tile(tile, out, fm, chunk_base, held * 4,
+                        flush_tile(tile, rout, v.fm, chunk_base, held * 4,
                                    lane);
                         wave_lds_sync();
                         chunk_base += held * 4;
@@ -727,7 +777,44 @@ void conv_pix_kernel(
                     }
                 }
             }
-        } else {
+            u += v.w1 - v.w0;
+            const bool more = u < u_end;
+            Visit nv;
+            uint32_t pn[Pl::TB][A][CW];
+            if constexpr (kAhead) {
+                if (more) {
+                    nv = visit_at(u);
+                    load_patch<A, K, CW, Pl::TB, CW>(pn, ract, g, nv.win, 0,
+                                                     0);
+                }
+            }
+            // the visit's last byte or tile chunk
+            if constexpr (REQ) {
+                if (v.p < g.npix) po.store(out, g, v.p, (v.q1 - 1) >> 1);
+            } else {
+                wave_lds_sync();
+                flush_tile(tile, rout, v.fm, chunk_base, held * 4, lane);
+                wave_lds_sync();
+            }
+            if (!more) break;
+            if constexpr (kAhead) {
+                v = nv;
+#pragma unroll
+                for (int t = 0; t < Pl::TB; ++t)
+#pragma unroll
+                    for (int i = 0; i < A; ++i)
+#pragma unroll
+                        for (int c = 0; c < CW; ++c) patch[t][i][c] = pn[t][i][c];
+            } else {
+                v = visit_at(u);
+                load_patch<A, K, CW, Pl::TB, CW>(patch, ract, g, v.win, 0, 0);
+            }
+        }
+    } else {
+      while (u < u_end) {
+        const Visit v = visit_at(u);
+        const int q0 = v.q0, q1 = v.q1, p = v.p;
+        {
             // reduction blocks outermost, per tile chunk of up to kChunk
             // channels; partial sums of later blocks are added in the tile
             using Patch = uint32_t[Pl::TB][A][Pl::CB];
@@ -745,7 +832,7 @@ void conv_pix_kernel(
                 auto load_block = [&](Patch& pt, int nb) {
                     const int tb = nb / Pl::NCB;
                     load_patch<A, K, CW, Pl::TB, Pl::CB>(
-                        pt, ract, g, win, tb * Pl::TB,
+                        pt, ract, g, v.win, tb * Pl::TB,
                         (nb - tb * Pl::NCB) * Pl::CB);
                 };
                 if constexpr (Pl::DBUF) {
@@ -757,14 +844,14 @@ void conv_pix_kernel(
                         if (nb + 1 < NB) load_block(pb, nb + 1);
                         run_block<A, W, E, K, S, CW>(
                             pa, blk(nb), nq, nb,
-                            nb + 1 < NB ? blk(nb + 1) : qsrc, f, row, g, oy,
-                            ox);
+                            nb + 1 < NB ? blk(nb + 1) : qsrc, f, row, g, v.oy,
+                            v.ox);
                         if (nb + 1 < NB) {
                             if (nb + 2 < NB) load_block(pa, nb + 2);
                             run_block<A, W, E, K, S, CW>(
                                 pb, blk(nb + 1), nq, nb + 1,
                                 nb + 2 < NB ? blk(nb + 2) : qsrc, f, row, g,
-                                oy, ox);
+                                v.oy, v.ox);
                         }
                     }
                 } else {
@@ -774,8 +861,8 @@ void conv_pix_kernel(
                         load_block(pa, nb);
                         run_block<A, W, E, K, S, CW>(
                             pa, blk(nb), nq, nb,
-                            nb + 1 < NB ? blk(nb + 1) : qsrc, f, row, g, oy,
-                            ox);
+                            nb + 1 < NB ? blk(nb + 1) : qsrc, f, row, g, v.oy,
+                            v.ox);
                     }
                 }
                 if constexpr (REQ) {
@@ -793,12 +880,13 @@ void conv_pix_kernel(
                     }
                 } else {
                     wave_lds_sync();
-                    flush_tile(tile, out, fm, 4 * sub, nq * 4, lane);
+                    flush_tile(tile, rout, v.fm, 4 * sub, nq * 4, lane);
                     wave_lds_sync();
                 }
             }
         }
-        u += w1 - w0;
+        u += v.w1 - v.w0;
+      }
     }
 }
 

@@ -234,6 +234,24 @@ def test_units_per_wave(lib):
         assert lib.bs_set_units_per_wave(0) == bs.BS_OK
 
 
+def test_describe_store_bound_1x1_runs(lib):
+    # 1x1 layers with A*W*words <= 16 run one tile chunk (4 quads) per wave;
+    # others keep the balanced plan (not 4 here: 50176 units on the CPU's
+    # stand-in of one block per CU)
+    import re
+
+    def run_of(p):
+        return int(re.search(r"units_per_wave=(\d+)",
+                             bs.bs_conv2d_describe(p)).group(1))
+
+    l3 = params(n=128, h=56, w=56, c=64, oc=64, kh=1, kw=1, pad_h=0, pad_w=0)
+    assert run_of(l3) == 4
+    a3w3 = params(n=128, h=14, w=14, c=256, oc=512, kh=1, kw=1, pad_h=0,
+                  pad_w=0, abits=3, wbits=3)
+    assert run_of(a3w3) != 4
+    assert run_of(params(n=64, h=56, w=56, c=64, oc=64)) != 4
+
+
 def test_describe_batch_split(lib):
     # the pixel kernel addresses its tensors with 32-bit offsets: an int32
     # output past 2 GB (128 x 56 x 56 x 1344) is split into image chunks of
