@@ -314,24 +314,20 @@ __device__ __forceinline__ Rsrc make_rsrc(const void* p, int32_t bytes) {
 // tile's 64 pixels x kChunk channels in kFlushRounds rounds: in round r lane
 // l stores quad l % kFlushRounds of pixel r * 64 / kFlushRounds +
 // l / kFlushRounds (kChunk / 4 lanes per pixel, so a round writes runs of
-// 4 kChunk contiguous bytes).  off0 is the byte offset of round 0's piece for
-// the group's first channel; round r adds (64 / kFlushRounds) r oc 4 bytes
-// and a chunk its first channel.  Only the group holding the last pixel
-// needs per-round checks.
+// 4 kChunk contiguous bytes).  Round r's byte offset is that of round 0 plus
+// (64 / kFlushRounds) r oc 4; the lane's part is recomputed per flush rather
+// than held across the channel loop, where registers are scarce.  Only the
+// group holding the last pixel needs per-round checks.
 constexpr int kFlushRounds = kChunk / 4;
 constexpr int kFlushPixels = 64 / kFlushRounds;    // pixels per round
 
 struct FlushMap {
-    uint32_t off0;
-    int pix0, npix, oc;
+    int pix0, npix, oc;    // uniform
 
-    __device__ __forceinline__ void init(int pix0_, int npix_, int oc_,
-                                         int lane) {
+    __device__ __forceinline__ void init(int pix0_, int npix_, int oc_) {
         pix0 = pix0_;
         npix = npix_;
         oc = oc_;
-        off0 = ((uint32_t)(pix0 + lane / kFlushRounds) * (uint32_t)oc +
-                4u * (uint32_t)(lane % kFlushRounds)) * 4u;
     }
 };
 
@@ -345,7 +341,8 @@ __device__ __forceinline__ void flush_tile(const uint32_t* __restrict__ tile,
     const uint32_t rstep = 4u * kFlushPixels * (uint32_t)fm.oc;  // per round
     const int q = lane % kFlushRounds, pr = lane / kFlushRounds;
     const bool qin = q < (nch >> 2);
-    const uint32_t o0 = fm.off0 + 4u * (uint32_t)oc_base;
+    const uint32_t o0 = ((uint32_t)(fm.pix0 + pr) * (uint32_t)fm.oc +
+                         (uint32_t)(oc_base + 4 * q)) * 4u;
     const uint32_t* t = tile + pr * kTileStride + 4 * q;
 #pragma unroll
     for (int r = 0; r < kFlushRounds; ++r) {
@@ -354,6 +351,9 @@ __device__ __forceinline__ void flush_tile(const uint32_t* __restrict__ tile,
         const bool in = qin && fm.pix0 + kFlushPixels * r + pr < fm.npix;
         __builtin_amdgcn_raw_buffer_store_b128(
             v, out, in ? o0 + (uint32_t)r * rstep : kOutOfRange, 0, 0);
+        // one round's data in registers at a time: the flush runs while the
+        // whole input patch is held
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -702,7 +702,7 @@ void conv_pix_kernel(
         v.win.base = ((img * (uint32_t)g.h + (uint32_t)v.win.iy0) *
                           (uint32_t)g.w + (uint32_t)v.win.ix0) *
                      (uint32_t)(4 * A * CW);
-        if constexpr (!REQ) v.fm.init(v.pix0, g.npix, g.oc, lane);
+        if constexpr (!REQ) v.fm.init(v.pix0, g.npix, g.oc);
         return v;
     };
 
