@@ -333,7 +333,10 @@ struct FlushMap {
 
 // Writes channels [oc_base, oc_base + nch) of the group's 64 pixels from the
 // wave's tile (nch a multiple of 4 up to kChunk: the lanes of quads below
-// nch / 4 take part, the others store out of range).
+// nch / 4 take part, the others store out of range).  SERIAL: one round's
+// data in registers at a time, for flushes that run while a large input
+// patch is held.
+template <bool SERIAL>
 __device__ __forceinline__ void flush_tile(const uint32_t* __restrict__ tile,
                                            Rsrc out, const FlushMap& fm,
                                            int oc_base, int nch, int lane) {
@@ -351,9 +354,7 @@ __device__ __forceinline__ void flush_tile(const uint32_t* __restrict__ tile,
         const bool in = qin && fm.pix0 + kFlushPixels * r + pr < fm.npix;
         __builtin_amdgcn_raw_buffer_store_b128(
             v, out, in ? o0 + (uint32_t)r * rstep : kOutOfRange, 0, 0);
-        // one round's data in registers at a time: the flush runs while the
-        // whole input patch is held
-        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (SERIAL) __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -661,8 +662,26 @@ constexpr int kAheadWords = 16;
 // S: stride; CW: words per bit-plane; REQ: requantize and bit-pack the output
 // (out then holds [npix][out_bits][out_words] uint32 words) instead of
 // storing int32.
+// Waves per SIMD the compiler must leave room for: kWavesPerSimd (72 VGPRs)
+// for the kernels that fit there without spilling -- at most 2 plane pairs
+// of unipolar activations (unipolar or bipolar filters), int32 output, and a
+// block patch of at most 48 words with its double buffer -- where a register
+// or two over 72 would cost a wave and change the launch plan (ResNet-18
+// layer 10: 73 VGPRs, 6 waves, 40.1 us; 72 VGPRs, 7 waves, 38.2 us); for the
+// others whatever their patch needs.
+template <int A, int W, int E, int K, int CW, bool REQ>
+constexpr int min_waves_per_simd() {
+    using Pl = Plan<A, W, K, CW>;
+    return !REQ && A * W <= 2 && E / 3 == kUnipolar && E % 3 != kSigned &&
+                   Pl::PB * (Pl::DBUF ? 2 : 1) <= 48
+               ? kWavesPerSimd
+               : 1;
+}
+
 template <int A, int W, int E, int K, int S, int CW, bool REQ>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_num_sgpr(96)))
+__global__ __launch_bounds__(kBlock) __attribute__((
+    amdgpu_num_sgpr(96),
+    amdgpu_waves_per_eu(min_waves_per_simd<A, W, E, K, CW, REQ>())))
 void conv_pix_kernel(
     const uint32_t* __restrict__ act, const uint32_t* __restrict__ wts,
     int32_t* __restrict__ out, PixArgs g) {
@@ -713,6 +732,9 @@ void conv_pix_kernel(
         // loads and stores in order, so a load issued after them would wait
         // for their completion (and the HBM-bound 1x1 layers would stall).
         constexpr bool kAhead = Pl::PB <= kAheadWords;
+        // flushes run while the patch is held: keep their registers few
+        // when the patch is large (all four rounds hoisted cost 4-9 VGPRs)
+        constexpr bool kSerialFlush = Pl::PB > 32;
         if (u >= u_end) return;
         Visit v = visit_at(u);
         uint32_t patch[Pl::TB][A][CW];
@@ -722,7 +744,7 @@ void conv_pix_kernel(
             // entered, as it is re-entered, with the patch load followed by
             // one flush's stores, so the wait for the patch can leave those
             // in flight
-            flush_tile(tile, rout, v.fm, 0, 0, lane);
+            flush_tile<kSerialFlush>(tile, rout, v.fm, 0, 0, lane);
         }
         while (true) {
             if constexpr (kAhead) {
@@ -769,8 +791,8 @@ void conv_pix_kernel(
                     ++held;
                     if (held == kChunk / 4 && qi + 1 < nq) {
                         wave_lds_sync();
-                        flush_tile(tile, rout, v.fm, chunk_base, held * 4,
-                                   lane);
+                        flush_tile<kSerialFlush>(tile, rout, v.fm,
+                                                 chunk_base, held * 4, lane);
                         wave_lds_sync();
                         chunk_base += held * 4;
                         held = 0;
@@ -793,7 +815,8 @@ void conv_pix_kernel(
                 if (v.p < g.npix) po.store(out, g, v.p, (v.q1 - 1) >> 1);
             } else {
                 wave_lds_sync();
-                flush_tile(tile, rout, v.fm, chunk_base, held * 4, lane);
+                flush_tile<kSerialFlush>(tile, rout, v.fm, chunk_base,
+                                         held * 4, lane);
                 wave_lds_sync();
             }
             if (!more) break;
@@ -880,7 +903,8 @@ void conv_pix_kernel(
                     }
                 } else {
                     wave_lds_sync();
-                    flush_tile(tile, rout, v.fm, 4 * sub, nq * 4, lane);
+                    flush_tile<false>(tile, rout, v.fm, 4 * sub, nq * 4,
+                                      lane);
                     wave_lds_sync();
                 }
             }
