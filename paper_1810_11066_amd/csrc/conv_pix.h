@@ -20,10 +20,11 @@
 // operand of v_and_b32.
 //
 // Inner loop: per (tap, plane pair, word) one v_and_b32 (SGPR x VGPR) and one
-// accumulating v_bcnt_u32_b32 into one of 2 (A+W-1) per-shift accumulators
-// (split by tap parity so consecutive popcounts are independent); the
-// shift-add (and bipolar correction, whose patch popcount sum is computed
-// once per group) runs once per output.
+// accumulating v_bcnt_u32_b32 into one of A+W-1 per-shift accumulators (5-7
+// resident waves hide the dependence of consecutive popcounts on one
+// accumulator; a second set split by tap parity cost registers and
+// epilogue adds); the shift-add (and bipolar correction, whose patch
+// popcount sum is computed once per group) runs once per output.
 //
 // Filter words stream through two SGPR slices of at most kSliceWords words
 // each: the slice for step s+1 is requested before step s computes, and the
@@ -381,17 +382,15 @@ __device__ __forceinline__ void compute_quad(
     constexpr int FW = Pl::FW, TSW = TS * W * CW;
 #pragma unroll
     for (int b = 0; b < 4 / OCB; ++b) {
-        uint32_t acc[2][OCB][NA];
-        bool fresh[2][OCB][NA];
+        uint32_t acc[OCB][NA];
+        bool fresh[OCB][NA];
         uint32_t corr[OCB];   // SW: in-range filter popcounts (bipolar acts)
 #pragma unroll
         for (int o = 0; o < OCB; ++o) corr[o] = 0;
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
+        for (int o = 0; o < OCB; ++o)
 #pragma unroll
-            for (int o = 0; o < OCB; ++o)
-#pragma unroll
-                for (int s = 0; s < NA; ++s) fresh[h][o][s] = true;
+            for (int s = 0; s < NA; ++s) fresh[o][s] = true;
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
             const int st = b * NP + p;
@@ -441,7 +440,6 @@ __device__ __forceinline__ void compute_quad(
 #pragma unroll
                             for (int o = 0; o < OCB; ++o) {
                                 const int t = p * TS + tt;
-                                const int h = (t * CB + c) & 1;
                                 const int s =
                                     i + j + (En::neg(i, j, A, W) ? NS : 0);
                                 const uint32_t wv =
@@ -450,11 +448,11 @@ __device__ __forceinline__ void compute_quad(
                                     En::kXnor
                                         ? xor_keep(patch[t][i][c], tv.keep[t], wv)
                                         : patch[t][i][c] & wv;
-                                if (fresh[h][o][s]) {
-                                    bcnt_first(acc[h][o][s], x);
-                                    fresh[h][o][s] = false;
+                                if (fresh[o][s]) {
+                                    bcnt_first(acc[o][s], x);
+                                    fresh[o][s] = false;
                                 } else {
-                                    bcnt_acc(acc[h][o][s], x);
+                                    bcnt_acc(acc[o][s], x);
                                 }
                             }
             __builtin_amdgcn_sched_barrier(0);
@@ -464,10 +462,9 @@ __device__ __forceinline__ void compute_quad(
             uint32_t v = 0;
 #pragma unroll
             for (int s = 0; s < NA; ++s) {
-                const uint32_t a0 = fresh[0][o][s] ? 0u : acc[0][o][s];
-                const uint32_t a1 = fresh[1][o][s] ? 0u : acc[1][o][s];
-                if (s < NS) v += (a0 + a1) << s;
-                else v -= (a0 + a1) << (s - NS);
+                const uint32_t a = fresh[o][s] ? 0u : acc[o][s];
+                if (s < NS) v += a << s;
+                else v -= a << (s - NS);
             }
             if constexpr (En::kXnor) {
                 // v counts the in-range disagreements D: N - 2 D
