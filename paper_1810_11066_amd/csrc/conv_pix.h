@@ -643,6 +643,20 @@ __device__ __forceinline__ void run_block(
     }
 }
 
+// Block index in the order of the work, XCD-major.  The dispatcher deals
+// blocks to the 8 XCDs round-robin (block b to XCD b % 8), and each XCD
+// has its own L2; numbering the blocks of XCD x consecutively (x * q +
+// min(x, r) + b / 8 for q = blocks / 8, r = blocks % 8, a bijection) gives
+// each XCD a contiguous range of pixel groups, so the input rows that
+// neighbouring groups share (the window's halo) are fetched into one L2.
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ int xcd_block() {
+    const int b = blockIdx.x, n = gridDim.x;
+    const int q = n / kXcds, r = n % kXcds, x = b % kXcds;
+    return x * q + min(x, r) + b / kXcds;
+}
+
 // One group visit of a wave: units [w0, w1) of a 64-pixel group, i.e.
 // quads [q0, q1) of its output channels, and the lane's pixel p = pix0 +
 // lane at (oy, ox) with its input window and flush offsets.
@@ -686,7 +700,7 @@ void conv_pix_kernel(
     constexpr int FW = Pl::FW, NB = Pl::NB;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(
-        (int)(blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)));
+        (int)(xcd_block() * kWavesPerBlock + (threadIdx.x >> 6)));
     // units [u, u_end) of this wave; per_wave * waves < 2^31 (host)
     int u = wave * g.per_wave;
     const int u_end = min(u + g.per_wave, g.units);
