@@ -7,12 +7,14 @@
 // wave takes one contiguous run of units, so a wave visits at most a few
 // groups and, inside a group, a contiguous range of output channels.  The
 // host sizes the runs so that the whole grid is resident at once and every
-// CU holds the same number of waves (no second round, no straggler CUs).
+// CU holds the same number of waves (no second round, no straggler CUs);
+// store-bound 1x1 layers instead run one 16-channel tile chunk per wave.
+// Blocks take their work in XCD-major order.
 //
 // Per group, each lane loads the packed words of its K x K input patch
-// (vector loads; consecutive lanes read consecutive pixels), zeroes the taps
-// in the padding, and keeps the patch in VGPRs for all the channels of its
-// run.  When the whole patch does not fit (wide layers), it is taken one tap
+// (raw buffer loads, consecutive lanes reading consecutive pixels; a tap in
+// the padding reads past the buffer and gets zeros) and keeps the patch in
+// VGPRs for all the channels of its run.  When the whole patch does not fit (wide layers), it is taken one tap
 // block at a time -- a filter row, or a single tap -- with tap blocks as the
 // outer loop and partial sums added into the LDS output tile.  Filter words
 // are the same for every lane, so they are read with scalar loads (a layer's
@@ -33,7 +35,7 @@
 //
 // Occupancy.  The hardware reserves more SGPRs per wave than the compiler's
 // count: measured on gfx950, 8 waves fit on a SIMD up to 80 SGPRs, 7 up to
-// 96 and 6 above.  The kernel is compiled for at most kMaxSgprs = 96 SGPRs
+// 96 and 6 above.  The kernel is compiled for at most 96 SGPRs
 // (the slice bound keeps the channel loop within that; what does not fit is
 // spilled to VGPR lanes in the per-group code), and the host caps the
 // occupancy query, which counts the way the compiler does, at
@@ -669,10 +671,6 @@ struct Visit {
 // Patches of at most this many words are requested a visit ahead.
 constexpr int kAheadWords = 16;
 
-// A, W: bit-widths; E: operand encodings (Enc); K: square kernel size;
-// S: stride; CW: words per bit-plane; REQ: requantize and bit-pack the output
-// (out then holds [npix][out_bits][out_words] uint32 words) instead of
-// storing int32.
 // Waves per SIMD the compiler must leave room for: kWavesPerSimd (72 VGPRs)
 // for the kernels that fit there without spilling -- at most 2 plane pairs
 // of unipolar activations (unipolar or bipolar filters), int32 output, and a
@@ -689,6 +687,10 @@ constexpr int min_waves_per_simd() {
                : 1;
 }
 
+// A, W: bit-widths; E: operand encodings (Enc); K: square kernel size;
+// S: stride; CW: words per bit-plane; REQ: requantize and bit-pack the output
+// (out then holds [npix][out_bits][out_words] uint32 words) instead of
+// storing int32.
 template <int A, int W, int E, int K, int S, int CW, bool REQ>
 __global__ __launch_bounds__(kBlock) __attribute__((
     amdgpu_num_sgpr(96),
@@ -845,14 +847,13 @@ void conv_pix_kernel(
             }
         }
     } else {
-      while (u < u_end) {
-        const Visit v = visit_at(u);
-        const int q0 = v.q0, q1 = v.q1, p = v.p;
-        {
-            // reduction blocks outermost, per tile chunk of up to kChunk
-            // channels; partial sums of later blocks are added in the tile
-            using Patch = uint32_t[Pl::TB][A][Pl::CB];
-            uint32_t* row = tile + lane * kTileStride;
+        // reduction blocks outermost, per tile chunk of up to kChunk
+        // channels; partial sums of later blocks are added in the tile
+        using Patch = uint32_t[Pl::TB][A][Pl::CB];
+        uint32_t* row = tile + lane * kTileStride;
+        while (u < u_end) {
+            const Visit v = visit_at(u);
+            const int q0 = v.q0, q1 = v.q1, p = v.p;
             PackedOut po;
             po.clear();
             for (int sub = q0; sub < q1; sub += kChunk / 4) {
@@ -919,9 +920,8 @@ void conv_pix_kernel(
                     wave_lds_sync();
                 }
             }
+            u += v.w1 - v.w0;
         }
-        u += v.w1 - v.w0;
-      }
     }
 }
 
