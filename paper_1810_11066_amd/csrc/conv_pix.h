@@ -784,7 +784,7 @@ void conv_pix_kernel(
             int held = 0;                // quads held in the tile
             PackedOut po;
             po.clear();
-            for (int qi = 0; qi < nq; ++qi) {
+            auto quad = [&](int qi) __attribute__((always_inline)) {
                 uint32_t val[4];
                 gu32* q = src + (size_t)qi * 4 * FW;
                 compute_quad<A, W, E, K, CW>(
@@ -811,7 +811,13 @@ void conv_pix_kernel(
                         held = 0;
                     }
                 }
-            }
+            };
+            // the visit's first quad outside the loop: its taps are used in
+            // load order, so each waits only for its own load, and the
+            // arithmetic starts while the later taps are still arriving (a
+            // first use inside the loop waits for the whole patch)
+            quad(0);
+            for (int qi = 1; qi < nq; ++qi) quad(qi);
             u += v.w1 - v.w0;
             const bool more = u < u_end;
             Visit nv;
