@@ -237,6 +237,22 @@ def case_bytes(case):
     return src + packed, packed + wbytes + out
 
 
+def sets_for(case, minimum: int) -> int:
+    """Rotated buffer sets for a case: at least `minimum`, and enough that
+    the sets together pass 512 MB (twice the 256 MB Infinity Cache), so
+    timed steps read their inputs from HBM; at most 256 (tiny workloads stay
+    cache-resident whatever the count)."""
+    from paper_1810_11066_amd import workloads as wl
+    if isinstance(case, wl.DenseCase):
+        out = case.m * case.n * 4
+    else:
+        out = case.n * case.oh * case.ow * case.oc * 4
+    pre_bytes, _ = case_bytes(case)
+    per_set = pre_bytes + out
+    need = -(-512 * 10**6 // per_set)
+    return max(minimum, min(256, need))
+
+
 ENC_NAMES = ("unipolar", "bipolar", "signed")
 
 
@@ -441,9 +457,15 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--batch", type=int, default=64)
+    ap.add_argument("--batch", type=int, default=None,
+                    help="images per call: config 2 (default 64) and "
+                         "configs 4, 5 and --encodings (default 128); "
+                         "config 4 at 16 is one GPU's share of a batch-128 "
+                         "run sharded over 8")
     ap.add_argument("--sets", type=int, default=6,
-                    help="input/output buffer sets rotated across steps")
+                    help="at least this many input/output buffer sets "
+                         "rotated across steps (more where needed to pass "
+                         "512 MB in all)")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="seconds of oracle time for cpu_baseline (0: skip)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -494,17 +516,19 @@ def main() -> int:
         return chain_line(args, bs, torch, np, wl)
 
     if args.sweep or args.encodings or args.config != 2:
+        b = {} if args.batch is None else {"batch": args.batch}
         if args.sweep:
             cases = wl.bitwidth_sweep()
         elif args.encodings:
-            cases = wl.encodings()
+            cases = wl.encodings(**b)
         else:
             cases = {1: lambda: [wl.config1()], 3: lambda: [wl.config3()],
-                     4: wl.config4, 5: wl.config5}[args.config]()
+                     4: lambda: wl.config4(**b),
+                     5: lambda: wl.config5(**b)}[args.config]()
         times = {}
         for case in cases:
-            sets, step, _, _, describe, _ = prepare(case, args.sets, bs,
-                                                    torch, np)
+            sets, step, _, _, describe, _ = prepare(
+                case, sets_for(case, args.sets), bs, torch, np)
             m = measure(step, describe, args.steps, args.warmup, torch)
             times[(case.abits, case.wbits)] = m.main_ms
             print(json.dumps(case_line(case, m, args)), flush=True)
@@ -521,9 +545,10 @@ def main() -> int:
                               for k, v in sorted(times.items())}}))
         return 0
 
-    case = wl.config2(batch=args.batch)
+    case = wl.config2(batch=args.batch or 64)
     rows, k = case.n * case.h * case.w, case.c
-    sets, step, params, w_packed, describe, _ = prepare(case, args.sets, bs,
+    n_sets = sets_for(case, args.sets)
+    sets, step, params, w_packed, describe, _ = prepare(case, n_sets, bs,
                                                         torch, np)
     m = measure(step, describe, args.steps, args.warmup, torch)
     stream = torch.cuda.current_stream()
@@ -562,7 +587,7 @@ def main() -> int:
             "pad": case.pad, "abits": case.abits, "wbits": case.wbits,
             "encoding": "unipolar", "output": "int32 NHWC",
             "per_step": "bs_pack(activations) + bs_conv2d",
-            "buffer_sets": args.sets,
+            "buffer_sets": n_sets,
         },
         "roofline": {
             "bound": "alu",

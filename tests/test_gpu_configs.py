@@ -148,6 +148,14 @@ def test_config4_resnet18_layer(oracle, case):
     check_sampled(oracle, case)
 
 
+@pytest.mark.parametrize("case", wl.config4(batch=16), ids=lambda c: c.name)
+def test_config4_one_gpu_share(oracle, case):
+    """Config 4 at batch 16, one GPU's share of the batch-128 run sharded
+    over 8 GPUs by images: the planner lays out the smaller grid."""
+    say(case.name)
+    check_sampled(oracle, case)
+
+
 @pytest.mark.parametrize("case", wl.config5(), ids=lambda c: c.name)
 def test_config5_bipolar_a3w3(oracle, case):
     say(case.name)
