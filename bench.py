@@ -59,11 +59,39 @@ def popcount_roofline_tops(abits: int, wbits: int) -> float:
     return 2 * binary_macs / (abits * wbits) / 1e12
 
 
+def strip_comments(src: str) -> str:
+    """C/C++ source without its comments, whitespace runs collapsed, so that
+    the hash below follows the code and not its documentation."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c in "\"'":                       # string or character literal
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_hash() -> str:
+    """Hash of the conv kernel sources' code (comments excluded): a recorded
+    counter figure stays valid while only comments change."""
     h = hashlib.sha256()
     for rel in CONV_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            h.update(strip_comments(f.read()).encode())
+            h.update(b"\0")
     return h.hexdigest()[:16]
 
 

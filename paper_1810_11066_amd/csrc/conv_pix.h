@@ -14,12 +14,14 @@
 // Per group, each lane loads the packed words of its K x K input patch
 // (raw buffer loads, consecutive lanes reading consecutive pixels; a tap in
 // the padding reads past the buffer and gets zeros) and keeps the patch in
-// VGPRs for all the channels of its run.  When the whole patch does not fit (wide layers), it is taken one tap
-// block at a time -- a filter row, or a single tap -- with tap blocks as the
-// outer loop and partial sums added into the LDS output tile.  Filter words
-// are the same for every lane, so they are read with scalar loads (a layer's
-// filters are small and stay in the scalar cache) and used as the SGPR
-// operand of v_and_b32.
+// VGPRs for all the channels of its run.  When the whole patch does not
+// fit (wide layers), it is taken one tap block at a time -- a filter row, or
+// a single tap -- with tap blocks as the outer loop and partial sums added
+// into the LDS output tile.  Filter words are the same for every lane, so
+// they are read with scalar loads and used as the SGPR operand of
+// v_and_b32 (the scalar cache holds a small layer's filters; for the large
+// ones, up to the 4 MB of a 4096 x 4096 dense layer, the kernel time was
+// measured not to depend on it).
 //
 // Inner loop: per (tap, plane pair, word) one v_and_b32 (SGPR x VGPR) and one
 // accumulating v_bcnt_u32_b32 into one of A+W-1 per-shift accumulators (5-7
@@ -35,7 +37,9 @@
 //
 // Occupancy.  The hardware reserves more SGPRs per wave than the compiler's
 // count: measured on gfx950, 8 waves fit on a SIMD up to 80 SGPRs, 7 up to
-// 96 and 6 above.  The kernel is compiled for at most 96 SGPRs
+// 96 and 6 above.  VGPRs come from 512 per lane in granules of 8 (64 -> 8
+// waves, 72 -> 7, 80 -> 6, 88-96 -> 5, up to 128 -> 4), as the occupancy
+// query counts them.  The kernel is compiled for at most 96 SGPRs
 // (the slice bound keeps the channel loop within that; what does not fit is
 // spilled to VGPR lanes in the per-group code), and the host caps the
 // occupancy query, which counts the way the compiler does, at
