@@ -21,7 +21,10 @@
  *    invalid call returns its status and enqueues nothing, so no output byte
  *    is written.  bs_last_error() then describes the problem.
  *  - An empty problem (n == 0 or rows == 0) is valid and enqueues nothing.
- *  - Outputs must not overlap inputs.
+ *  - An output must not share a byte with an input (inputs may alias each
+ *    other, e.g. one packed matrix as both operands of bs_dense): a call
+ *    whose output range, as its sizes define it, overlaps an input's returns
+ *    BS_ERR_INVALID_ARG.
  *  - Results are exact integers and do not depend on launch configuration;
  *    no kernel uses atomics, so repeated calls are bit-identical.
  *  - Thread safety: calls from several host threads are safe; the only
@@ -167,7 +170,7 @@ bs_status bs_conv2d(const bs_conv2d_params *p, const uint32_t *act_packed,
  * Equals bs_conv2d followed by bs_quantize_pack of its output converted to
  * float32 (round to nearest even; exact while |v| <= 2^24), without ever
  * writing the int32 result.  Device pointers as in bs_conv2d; out_packed
- * must not alias the inputs.
+ * must not overlap the inputs.
  * Errors: as bs_conv2d; BS_ERR_INVALID_ARG for out_bits outside 1..8 or a
  * non-finite or non-positive out_scale. */
 bs_status bs_conv2d_requant(const bs_conv2d_params *p,

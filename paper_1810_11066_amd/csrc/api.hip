@@ -42,6 +42,39 @@ bs_status check_ptr(const void* p, const char* name) {
     return BS_OK;
 }
 
+// An output must not share a byte with an input: the kernels read inputs
+// while other waves write outputs, in no fixed order.  Inputs may alias each
+// other (a product of a matrix with itself).  Sizes in bytes; empty ranges
+// never overlap.
+bs_status check_disjoint(const void* out, uint64_t out_bytes, const char* oname,
+                         const void* in, uint64_t in_bytes, const char* iname) {
+    const uintptr_t o = (uintptr_t)out, i = (uintptr_t)in;
+    if (out_bytes > 0 && in_bytes > 0 && o < i + in_bytes &&
+        i < o + out_bytes)
+        return fail(BS_ERR_INVALID_ARG, "%s overlaps %s", oname, iname);
+    return BS_OK;
+}
+
+uint64_t packed_bytes(int64_t rows, int bits, int64_t k) {
+    return (uint64_t)rows * (uint64_t)bits * (uint64_t)((k + 31) / 32) * 4u;
+}
+
+// The operands of a conv call must not overlap its output.
+bs_status check_conv_buffers(const bs::ConvShape& s, const void* act,
+                             const void* wts, const void* out,
+                             uint64_t out_bytes) {
+    const uint64_t cw = (uint64_t)((s.c + 31) / 32);
+    const uint64_t act_bytes =
+        (uint64_t)s.n * s.h * s.w * (uint64_t)s.abits * cw * 4u;
+    const uint64_t w_bytes =
+        (uint64_t)s.oc * s.kh * s.kw * (uint64_t)s.wbits * cw * 4u;
+    bs_status st;
+    if ((st = check_disjoint(out, out_bytes, "out", act, act_bytes,
+                             "act_packed")) != BS_OK)
+        return st;
+    return check_disjoint(out, out_bytes, "out", wts, w_bytes, "w_packed");
+}
+
 bs_status check_bits(int bits, const char* name) {
     if (bits < 1 || bits > 8)
         return fail(BS_ERR_INVALID_ARG, "%s = %d is outside 1..8", name, bits);
@@ -135,7 +168,7 @@ bs_status check_conv(const bs_conv2d_params* p, bs::ConvShape* s) {
 
 extern "C" {
 
-int bs_abi_version(void) { return 103; }
+int bs_abi_version(void) { return 104; }
 
 int64_t bs_packed_words(int64_t k) { return k <= 0 ? 0 : (k + 31) / 32; }
 
@@ -174,6 +207,9 @@ bs_status bs_quantize(const float* x, uint8_t* q, int64_t n, float scale,
     if ((st = check_bits(bits, "bits")) != BS_OK) return st;
     if ((st = check_scale_enc(scale, bits, enc)) != BS_OK) return st;
     if (n == 0) return ok();
+    if ((st = check_disjoint(q, (uint64_t)n, "q", x, (uint64_t)n * 4u,
+                             "x")) != BS_OK)
+        return st;
     return from_hip(bs::launch_quantize(x, q, n, scale, bits, (int)enc,
                                         (hipStream_t)stream),
                     "bs_quantize launch");
@@ -190,6 +226,9 @@ bs_status bs_pack(const uint8_t* q, uint32_t* packed, int64_t rows, int64_t k,
     if (rows > ((int64_t)1 << 40) / k)
         return fail(BS_ERR_UNSUPPORTED, "tensor too large");
     if (rows == 0) return ok();
+    if ((st = check_disjoint(packed, packed_bytes(rows, bits, k), "packed", q,
+                             (uint64_t)rows * (uint64_t)k, "q")) != BS_OK)
+        return st;
     return from_hip(bs::launch_pack(q, packed, rows, k, bits,
                                     (hipStream_t)stream),
                     "bs_pack launch");
@@ -212,6 +251,11 @@ bs_status bs_pack_ex(const uint8_t* q, uint32_t* packed, int64_t outer,
         outer > ((int64_t)1 << 40) / (k * inner))
         return fail(BS_ERR_UNSUPPORTED, "tensor too large");
     if (outer == 0) return ok();
+    if ((st = check_disjoint(packed, packed_bytes(outer * inner, bits, k),
+                             "packed", q,
+                             (uint64_t)outer * (uint64_t)k * (uint64_t)inner,
+                             "q")) != BS_OK)
+        return st;
     return from_hip(bs::launch_pack_ex(q, packed, outer, k, inner, bits,
                                        (int)layout, (hipStream_t)stream),
                     "bs_pack_ex launch");
@@ -230,6 +274,9 @@ bs_status bs_quantize_pack(const float* x, uint32_t* packed, int64_t rows,
     if (rows > ((int64_t)1 << 40) / k)
         return fail(BS_ERR_UNSUPPORTED, "tensor too large");
     if (rows == 0) return ok();
+    if ((st = check_disjoint(packed, packed_bytes(rows, bits, k), "packed", x,
+                             (uint64_t)rows * (uint64_t)k * 4u, "x")) != BS_OK)
+        return st;
     return from_hip(bs::launch_quantize_pack(x, packed, rows, k, scale, bits,
                                              (int)enc, (hipStream_t)stream),
                     "bs_quantize_pack launch");
@@ -259,6 +306,10 @@ bs_status bs_conv2d(const bs_conv2d_params* p, const uint32_t* act_packed,
     if ((st = check_ptr(out, "out")) != BS_OK) return st;
     bs::ConvShape s;
     if ((st = check_conv(p, &s)) != BS_OK) return st;
+    if ((st = check_conv_buffers(
+             s, act_packed, w_packed, out,
+             (uint64_t)s.n * s.oh * s.ow * (uint64_t)s.oc * 4u)) != BS_OK)
+        return st;
     return from_hip(bs::launch_conv(s, act_packed, w_packed, out,
                                     g_conv_opt, (hipStream_t)stream),
                     "bs_conv2d launch");
@@ -280,6 +331,11 @@ bs_status bs_conv2d_requant(const bs_conv2d_params* p,
     if ((st = check_conv(p, &s)) != BS_OK) return st;
     if ((int64_t)s.n * s.oh * s.ow * ((s.oc + 31) / 32) >= INT32_MAX)
         return fail(BS_ERR_UNSUPPORTED, "output too large");
+    if ((st = check_conv_buffers(
+             s, act_packed, w_packed, out_packed,
+             packed_bytes((int64_t)s.n * s.oh * s.ow, out_bits, s.oc))) !=
+        BS_OK)
+        return st;
     bs::Requant rq;
     rq.scale = out_scale;
     rq.bits = out_bits;
@@ -320,6 +376,9 @@ bs_status bs_dense_ex(int64_t m, int64_t n, int64_t k, int abits,
     p.wenc = wenc;
     bs::ConvShape s;
     if ((st = check_conv(&p, &s)) != BS_OK) return st;
+    if ((st = check_conv_buffers(s, a_packed, w_packed, out,
+                                 (uint64_t)m * (uint64_t)n * 4u)) != BS_OK)
+        return st;
     return from_hip(bs::launch_conv(s, a_packed, w_packed, out, g_conv_opt,
                                     (hipStream_t)stream),
                     "bs_dense launch");

@@ -41,7 +41,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_words(lib):
-    assert lib.bs_abi_version() == 103
+    assert lib.bs_abi_version() == 104
     for k, w in [(0, 0), (1, 1), (31, 1), (32, 1), (33, 2), (4096, 128)]:
         assert lib.bs_packed_words(k) == w
 
@@ -148,6 +148,41 @@ def test_conv_pointer_validation(lib):
                          STREAM) == bs.BS_ERR_INVALID_ARG
     assert lib.bs_conv2d(None, FAKE, FAKE, FAKE,
                          STREAM) == bs.BS_ERR_INVALID_ARG
+
+
+def at(offset):
+    """A fake device address `offset` bytes past FAKE (never dereferenced)."""
+    return ctypes.c_void_p(0x10000 + offset)
+
+
+FAR = ctypes.c_void_p(0x40000000)
+
+
+def test_output_overlapping_an_input_is_rejected(lib):
+    """An output sharing a byte with an input is an invalid argument, found
+    before anything is enqueued (fake pointers, nothing is launched)."""
+    E = bs.BS_ERR_INVALID_ARG
+    # 8 floats span 32 bytes; codes at byte 16 overlap them
+    assert lib.bs_quantize(FAKE, at(16), 8, 1.0, 2, 0, STREAM) == E
+    assert b"overlaps" in lib.bs_last_error()
+    assert lib.bs_pack(FAKE, at(16), 4, 64, 2, STREAM) == E
+    assert lib.bs_pack_ex(FAKE, at(16), 2, 64, 9, 2, 0, STREAM) == E
+    assert lib.bs_quantize_pack(FAKE, at(16), 4, 64, 1.0, 2, 0, STREAM) == E
+    # the output placed first, the input starting inside it
+    assert lib.bs_pack(at(16), FAKE, 4, 64, 2, STREAM) == E
+    p = params()                       # 1x8x8x64 A2 -> 8x8x64 int32
+    assert lib.bs_conv2d(ctypes.byref(p), FAKE, FAR, at(1008),
+                         STREAM) == E    # out from the last 16 of act's 1 KB
+    assert b"act_packed" in lib.bs_last_error()
+    assert lib.bs_conv2d(ctypes.byref(p), FAR, FAKE, at(4592),
+                         STREAM) == E    # ... of the filters' 4608 B
+    assert b"w_packed" in lib.bs_last_error()
+    assert lib.bs_conv2d_requant(ctypes.byref(p), FAKE, FAR, 0.5, 2, at(16),
+                                 STREAM) == E
+    assert lib.bs_dense(4, 4, 64, 2, 2, 0, FAKE, FAKE, at(16),
+                        STREAM) == E
+    assert lib.bs_dense_ex(4, 4, 64, 2, 0, 2, 0, FAR, FAKE, at(16),
+                           STREAM) == E
 
 
 def test_overflow_guard_boundary(lib):

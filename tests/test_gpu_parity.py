@@ -5,6 +5,8 @@ buffers pre-filled with a sentinel and flanked by guard bands, so a test also
 fails if a kernel leaves an element unwritten or writes past its output.
 Results are exact integers; the bar is equality.
 """
+import ctypes
+
 import numpy as np
 import pytest
 import torch
@@ -375,6 +377,58 @@ def test_dense_random(oracle, seed):
     torch.cuda.synchronize()
     assert np.array_equal(g.t.cpu().numpy().reshape(m, n), want)
     g.check_guards()
+
+
+def test_dense_operands_may_alias(oracle):
+    """A . A^T from one packed matrix passed as both operands: inputs may
+    alias each other (only an output overlapping an input is refused)."""
+    rng = np.random.default_rng(77)
+    m, k, bits = 96, 320, 2
+    say("dense alias", m, k, bits)
+    a = rng.integers(0, 1 << bits, size=(m, k), dtype=np.uint8)
+    ap = oracle.pack(a, bits)
+    want = oracle.dense(ap, ap, m, m, k, bits, bits, 0)
+    a_dev = dev(ap.view(np.int32))
+    out = torch.empty((m, m), dtype=torch.int32, device="cuda")
+    bs.bs_dense(m, m, k, bits, bits, 0, a_dev, a_dev, out)
+    torch.cuda.synchronize()
+    assert np.array_equal(out.cpu().numpy(), want)
+
+
+def test_conv_output_adjacent_and_overlapping(oracle):
+    """One allocation holding the packed input and, right after its last
+    byte, the output: a valid call.  With the output moved 16 bytes back
+    onto the input, the call is refused and writes nothing."""
+    rng = np.random.default_rng(78)
+    n, h, w, c, oc = 2, 9, 11, 64, 24
+    codes = rng.integers(0, 4, size=(n * h * w, c), dtype=np.uint8)
+    filt = rng.integers(0, 2, size=(oc * 9, c), dtype=np.uint8)
+    ap, wp = oracle.pack(codes, 2), oracle.pack(filt, 1)
+    spec = bs.Conv2dSpec(n, h, w, c, oc, 3, 3, 1, 1, 2, 1)
+    want = oracle.conv2d(oracle.conv_params(n, h, w, c, oc, 3, 3, 1, 1, 2, 1),
+                         ap, wp)
+    act_words = ap.size
+    out_elems = n * h * w * oc
+    say("conv adjacent", act_words, out_elems)
+    buf = torch.full((act_words + out_elems,), SENT32, dtype=torch.int32,
+                     device="cuda")
+    buf[:act_words] = dev(ap.view(np.int32).ravel())
+    w_dev = dev(wp.view(np.int32))
+    act = buf[:act_words]
+    out = buf[act_words:]
+    bs.bs_conv2d(spec.params(), act, w_dev, out)
+    torch.cuda.synchronize()
+    assert np.array_equal(out.cpu().numpy().reshape(want.shape), want)
+    assert np.array_equal(as_words(act).reshape(ap.shape), ap)
+    before = buf.clone()
+    lib = bs.load_library()
+    st = lib.bs_conv2d(ctypes.byref(spec.params()), act.data_ptr(),
+                       w_dev.data_ptr(), buf[act_words - 4:].data_ptr(),
+                       ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    assert st == bs.BS_ERR_INVALID_ARG
+    assert b"overlaps" in lib.bs_last_error()
+    torch.cuda.synchronize()
+    assert torch.equal(buf, before)
 
 
 # ------------------------------------------- requantized (chained) output --
