@@ -332,6 +332,39 @@ def test_describe_names_the_kernel_each_mode_picks(lib):
         "conv_generic_kernel")
 
 
+def test_error_string_and_kernel_mode_are_per_thread(lib):
+    """The library's only state (last error, kernel mode) is per host
+    thread: another thread's error and mode do not leak into this one."""
+    import threading
+    p = params(n=64, h=56, w=56, c=64, oc=64)
+    seen = {}
+    ready, resume = threading.Event(), threading.Event()
+
+    def worker():
+        bs.bs_set_kernel_mode(1)
+        seen["status"] = lib.bs_quantize(NULL, FAKE, 8, 1.0, 2, 0, STREAM)
+        seen["err"] = lib.bs_last_error()
+        ready.set()
+        resume.wait(30)
+        seen["err_after"] = lib.bs_last_error()
+        seen["desc"] = bs.bs_conv2d_describe(p)
+        bs.bs_set_kernel_mode(0)
+
+    t = threading.Thread(target=worker)
+    t.start()
+    try:
+        assert ready.wait(30)
+        assert lib.bs_set_units_per_wave(0) == bs.BS_OK   # clears this one
+        assert lib.bs_last_error() == b""
+        assert bs.bs_conv2d_describe(p).startswith("conv_pix_kernel")
+    finally:
+        resume.set()
+        t.join(30)
+    assert seen["status"] == bs.BS_ERR_INVALID_ARG
+    assert b"NULL" in seen["err"] and seen["err_after"] == seen["err"]
+    assert seen["desc"].startswith("conv_generic_kernel")
+
+
 ENC = ("unipolar", "bipolar", "signed")
 
 

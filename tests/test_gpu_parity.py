@@ -431,6 +431,62 @@ def test_conv_output_adjacent_and_overlapping(oracle):
     assert torch.equal(buf, before)
 
 
+def test_concurrent_threads_and_streams(oracle):
+    """Four host threads, each on its own stream (default priority) and in
+    its own kernel mode, pack and convolve different shapes at the same
+    time; every result equals the oracle's."""
+    import threading
+    # (n, h, w, c, oc, k, stride, pad, abits, wbits, bipolar w, kernel mode)
+    jobs = [(2, 14, 14, 64, 64, 3, 1, 1, 2, 1, False, 0),
+            (1, 9, 13, 96, 40, 3, 2, 1, 1, 1, True, 2),
+            (3, 7, 7, 128, 36, 1, 1, 0, 3, 2, False, 3),
+            (1, 6, 6, 32, 12, 3, 1, 1, 2, 2, False, 1)]
+    prepared = []
+    for i, (n, h, w, c, oc, k, st, pd, ab, wb, bip, mode) in enumerate(jobs):
+        rng = np.random.default_rng(900 + i)
+        codes = rng.integers(0, 1 << ab, size=(n, h, w, c), dtype=np.uint8)
+        filt = rng.integers(0, 1 << wb, size=(oc, k, k, c), dtype=np.uint8)
+        wenc = 1 if bip else 0
+        want = oracle.conv2d(
+            oracle.conv_params(n, h, w, c, oc, k, k, st, pd, ab, wb,
+                               wenc=wenc),
+            oracle.pack(codes.reshape(-1, c), ab),
+            oracle.pack(filt.reshape(-1, c), wb))
+        spec = bs.Conv2dSpec(n, h, w, c, oc, k, k, st, pd, ab, wb, wenc)
+        prepared.append((dev(codes), bs.pack(dev(filt.reshape(-1, c)), wb),
+                         spec, ab, mode, want))
+    torch.cuda.synchronize()
+    errors = []
+
+    def run(x, w_dev, spec, ab, mode, want):
+        try:
+            bs.bs_set_kernel_mode(mode)
+            stream = torch.cuda.Stream()
+            outs = []
+            with torch.cuda.stream(stream):
+                for _ in range(25):
+                    a_dev = bs.pack(x.view(-1, x.shape[-1]), ab)
+                    outs.append(bs.conv2d(spec, a_dev, w_dev))
+            stream.synchronize()
+            for o in outs:
+                if not np.array_equal(o.cpu().numpy(), want):
+                    errors.append("mode %d: result differs" % mode)
+                    break
+        except Exception as e:        # reported in the main thread
+            errors.append("mode %d: %r" % (mode, e))
+        finally:
+            bs.bs_set_kernel_mode(0)
+
+    say("concurrent", len(prepared), "threads")
+    threads = [threading.Thread(target=run, args=job) for job in prepared]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(120)
+    assert not any(t.is_alive() for t in threads)
+    assert errors == []
+
+
 # ------------------------------------------- requantized (chained) output --
 
 def run_requant(oracle, n, h, w, c, oc, k, s, pad, abits, wbits, bip, scale,
