@@ -32,6 +32,9 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "bsref.c")
 _LIB_PATH = os.path.join(_HERE, "libbsref.so")
+# BSREF_LIBRARY: load this build of bsref.c instead (the mutation tests point
+# it at deliberately broken copies, to show that the pins reject them)
+_OVERRIDE = os.environ.get("BSREF_LIBRARY")
 
 UNIPOLAR = 0
 BIPOLAR = 1
@@ -45,16 +48,23 @@ _lock = threading.Lock()
 _lib = None
 
 
+def compile_to(src: str, out: str) -> None:
+    """gcc command line of the oracle: plain C11 + OpenMP, IEEE float."""
+    cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
+           "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra",
+           src, "-o", out, "-lm"]
+    subprocess.run(cmd, check=True, cwd=os.path.dirname(src))
+
+
 def build(force: bool = True) -> str:
     """Compile ``libbsref.so`` with gcc (plain C11 + OpenMP).  Returns its path."""
+    if _OVERRIDE:
+        return _OVERRIDE
     if not force and os.path.exists(_LIB_PATH) and \
             os.path.getmtime(_LIB_PATH) >= os.path.getmtime(_SRC):
         return _LIB_PATH
     tmp = _LIB_PATH + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
-           "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra",
-           _SRC, "-o", tmp, "-lm"]
-    subprocess.run(cmd, check=True, cwd=_HERE)
+    compile_to(_SRC, tmp)
     os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
 
@@ -71,8 +81,7 @@ def _load():
     with _lock:
         if _lib is not None:
             return _lib
-        build(force=False)
-        lib = ctypes.CDLL(_LIB_PATH)
+        lib = ctypes.CDLL(build(force=False))
         P = ctypes.c_void_p
         i64 = ctypes.c_int64
         ci = ctypes.c_int
