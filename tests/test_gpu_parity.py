@@ -220,6 +220,48 @@ def test_conv_random_generic(oracle, seed):
     run_conv(oracle, *args, seed=seed, mode=1)
 
 
+def random_pixel_conv(rng):
+    """A random shape inside the pixels-on-lanes kernel's domain: A, W <= 4
+    (bipolar filters at W = 1), 1x1 or 3x3 windows, stride 1 or 2, padding
+    0-2, a word count per plane the kernel is specialised for with a random
+    tail, output channels a multiple of 4."""
+    k = int(rng.choice([1, 3]))
+    s = int(rng.choice([1, 2]))
+    pad = int(rng.integers(0, 3))
+    cw = int(rng.choice([1, 2, 4, 8, 16] + ([32] if k == 1 else [])))
+    c = int(rng.integers(32 * (cw - 1) + 1, 32 * cw + 1))
+    oc = 4 * int(rng.integers(1, 25))
+    n = int(rng.integers(1, 3))
+    h, w = int(rng.integers(1, 25)), int(rng.integers(1, 25))
+    h, w = max(h, k - 2 * pad), max(w, k - 2 * pad)
+    bipolar = bool(rng.integers(0, 2))
+    abits = int(rng.integers(1, 5))
+    wbits = 1 if bipolar else int(rng.integers(1, 5))
+    return (n, h, w, c, oc, k, k, s, s, pad, pad, abits, wbits, bipolar)
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_conv_random_pixel_domain(oracle, seed):
+    """Random shapes the pixel kernel takes (checked through the plan it
+    reports), each at a random run length so that group visits and tile
+    chunks break at varied places."""
+    rng = np.random.default_rng(5000 + seed)
+    args = random_pixel_conv(rng)
+    run = int(rng.choice([0, 1, 2, 3, 5, 7, 13]))
+    say("conv pixel domain", args, "run", run)
+    p = bs.ConvParams(*args[:13], 0, int(args[13]))
+    bs.bs_set_kernel_mode(3)
+    try:
+        assert bs.bs_conv2d_describe(p).startswith("conv_pix_kernel")
+    finally:
+        bs.bs_set_kernel_mode(0)
+    bs.bs_set_units_per_wave(run)
+    try:
+        run_conv(oracle, *args, seed=seed, mode=3)
+    finally:
+        bs.bs_set_units_per_wave(0)
+
+
 @pytest.mark.parametrize("mode", [0, 2, 3])
 @pytest.mark.parametrize("seed", range(40))
 def test_conv_random_fast(oracle, seed, mode):
