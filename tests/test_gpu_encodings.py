@@ -186,6 +186,33 @@ def test_conv_encodings_pixel(oracle, shape, enc):
                  expect_pix=True)
 
 
+@pytest.mark.parametrize("seed", range(40))
+def test_conv_encodings_pixel_random(oracle, seed):
+    """Random shapes inside the pixel kernel's domain with a random encoding
+    it serves (signed data, the XNOR case, +-1 activations with unipolar
+    filters) at a random run length; the plan must be the pixel kernel."""
+    rng = np.random.default_rng(7000 + seed)
+    abits, aenc, wbits, wenc = PIX_ENCODINGS[
+        int(rng.integers(0, len(PIX_ENCODINGS)))]
+    k, s, pad = int(rng.choice([1, 3])), int(rng.choice([1, 2])), \
+        int(rng.integers(0, 3))
+    cw = int(rng.choice([1, 2, 4, 8, 16] + ([32] if k == 1 else [])))
+    c = int(rng.integers(32 * (cw - 1) + 1, 32 * cw + 1))
+    oc = 4 * int(rng.integers(1, 25))
+    n = int(rng.integers(1, 3))
+    h = max(int(rng.integers(1, 25)), k - 2 * pad)
+    w = max(int(rng.integers(1, 25)), k - 2 * pad)
+    run = int(rng.choice([0, 1, 2, 3, 5, 7, 13]))
+    shape = (n, h, w, c, oc, k, s, pad)
+    say("conv enc pixel random", shape, (abits, aenc, wbits, wenc), "run", run)
+    bs.bs_set_units_per_wave(run)
+    try:
+        run_conv_enc(oracle, shape, abits, aenc, wbits, wenc, seed=seed,
+                     mode=3, expect_pix=True)
+    finally:
+        bs.bs_set_units_per_wave(0)
+
+
 @pytest.mark.parametrize("aenc", [0, 1, 2])
 @pytest.mark.parametrize("wenc", [0, 1, 2])
 @pytest.mark.parametrize("seed", range(4))
