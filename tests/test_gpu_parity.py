@@ -571,6 +571,70 @@ REQUANT_SHAPES = [
 ]
 
 
+@pytest.mark.parametrize("seed", range(30))
+def test_conv_requant_random(oracle, seed):
+    """Random pixel-domain shapes (output channels often not a multiple of
+    8, so the last packed byte is partial) with 1- to 8-bit requantized
+    output at a random run length; shapes are drawn where the plain conv's
+    plan is the pixel kernel, whose requantizing variant then runs."""
+    rng = np.random.default_rng(8000 + seed)
+    k, s, pad = int(rng.choice([1, 3])), int(rng.choice([1, 2])), \
+        int(rng.integers(0, 3))
+    cw = int(rng.choice([1, 2, 4, 8] + ([16] if k == 1 else [])))
+    c = int(rng.integers(32 * (cw - 1) + 1, 32 * cw + 1))
+    oc = 4 * int(rng.integers(1, 25))
+    n = int(rng.integers(1, 3))
+    h = max(int(rng.integers(1, 20)), k - 2 * pad)
+    w = max(int(rng.integers(1, 20)), k - 2 * pad)
+    bip = bool(rng.integers(0, 2))
+    abits = int(rng.integers(1, 5))
+    wbits = 1 if bip else int(rng.integers(1, 5))
+    obits = int(rng.integers(1, 9))
+    run = int(rng.choice([0, 1, 2, 3, 5, 7, 13]))
+    # a scale that spreads the results over the output codes
+    scale = ((1 << obits) - 1) / (0.5 * k * k * c * ((1 << abits) - 1) + 1)
+    p = bs.ConvParams(n, h, w, c, oc, k, k, s, s, pad, pad, abits, wbits, 0,
+                      int(bip))
+    bs.bs_set_kernel_mode(3)
+    try:
+        assert bs.bs_conv2d_describe(p).startswith("conv_pix_kernel")
+    finally:
+        bs.bs_set_kernel_mode(0)
+    say("conv requant random", (n, h, w, c, oc, k, s, pad), abits, wbits,
+        bip, obits, "run", run)
+    run_requant(oracle, n, h, w, c, oc, k, s, pad, abits, wbits, bip, scale,
+                obits, seed=seed, mode=0, run=run)
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_conv_channels_on_lanes_random(oracle, seed):
+    """Random shapes inside the channels-on-lanes kernel's domain (even word
+    counts per plane, any number of output channels); the plan must be
+    that kernel."""
+    rng = np.random.default_rng(9000 + seed)
+    k, s, pad = int(rng.choice([1, 3])), int(rng.choice([1, 2])), \
+        int(rng.integers(0, 3))
+    cw = int(rng.choice([2, 4, 8]))
+    c = int(rng.integers(32 * (cw - 1) + 1, 32 * cw + 1))
+    oc = int(rng.integers(1, 150))
+    n = int(rng.integers(1, 3))
+    h = max(int(rng.integers(1, 20)), k - 2 * pad)
+    w = max(int(rng.integers(1, 30)), k - 2 * pad)
+    bip = bool(rng.integers(0, 2))
+    abits = int(rng.integers(1, 5))
+    wbits = 1 if bip else int(rng.integers(1, 5))
+    p = bs.ConvParams(n, h, w, c, oc, k, k, s, s, pad, pad, abits, wbits, 0,
+                      int(bip))
+    bs.bs_set_kernel_mode(2)
+    try:
+        assert bs.bs_conv2d_describe(p).startswith("conv_ocl_kernel")
+    finally:
+        bs.bs_set_kernel_mode(0)
+    args = (n, h, w, c, oc, k, k, s, s, pad, pad, abits, wbits, bip)
+    say("conv channels-on-lanes random", args)
+    run_conv(oracle, *args, seed=seed, mode=2)
+
+
 @pytest.mark.parametrize("mode", [0, 1])
 @pytest.mark.parametrize("shape", REQUANT_SHAPES, ids=lambda s: "x".join(map(str, s)))
 @pytest.mark.parametrize("abits,wbits,bip,obits", [
