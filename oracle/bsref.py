@@ -32,8 +32,9 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "bsref.c")
 _LIB_PATH = os.path.join(_HERE, "libbsref.so")
-# BSREF_LIBRARY: load this build of bsref.c instead (the mutation tests point
-# it at deliberately broken copies, to show that the pins reject them)
+# BSREF_LIBRARY: load this compiled copy of bsref.c instead (the mutation
+# tests point it at deliberately broken copies, to show that the pins reject
+# them)
 _OVERRIDE = os.environ.get("BSREF_LIBRARY")
 
 UNIPOLAR = 0
