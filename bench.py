@@ -37,20 +37,9 @@ HBM_PEAK_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
 # sources of the conv kernels: a committed traffic figure is used only while
 # their hash matches the one recorded with it
-CONV_SOURCES = ["paper_1810_11066_amd/csrc/bs_internal.h",
-                "paper_1810_11066_amd/csrc/conv.hip",
-                "paper_1810_11066_amd/csrc/conv_fast.h",
-                "paper_1810_11066_amd/csrc/conv_pix.h",
-                "paper_1810_11066_amd/csrc/conv_pix.hip",
-                "paper_1810_11066_amd/csrc/conv_pix_a1.hip",
-                "paper_1810_11066_amd/csrc/conv_pix_a2.hip",
-                "paper_1810_11066_amd/csrc/conv_pix_a3.hip",
-                "paper_1810_11066_amd/csrc/conv_pix_a4.hip",
-                "paper_1810_11066_amd/csrc/conv_pix_s1.hip",
-                "paper_1810_11066_amd/csrc/conv_pix_s2.hip",
-                "paper_1810_11066_amd/csrc/conv_pix_s3.hip",
-                "paper_1810_11066_amd/csrc/conv_pix_s4.hip",
-                "paper_1810_11066_amd/csrc/conv_pix_b.hip"]
+CONV_SOURCES = ["paper_1810_11066_amd/csrc/" + f for f in (
+    "bs_internal.h", "conv.hip", "conv_fast.h", "conv_fast_inst.hip",
+    "conv_pix.h", "conv_pix.hip", "conv_pix_inst.hip")]
 
 
 def popcount_roofline_tops(abits: int, wbits: int) -> float:
@@ -109,6 +98,87 @@ def committed_traffic(workload: str):
     return float(m_val.group(1))
 
 
+def committed_kernel_trace(workload: str, ops: float, peak_tops: float):
+    """The conv kernel's average duration in the committed rocprofv3 kernel
+    trace of this workload, with the roofline fraction it gives, or None if
+    there is none or the kernel source changed since."""
+    path = os.path.join(PROFILES, "conv2d_%s_kernel_trace.md" % workload)
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_src = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
+    m_val = re.search(r"conv_kernel_avg_ns:\s*([0-9.eE+]+)", text)
+    if not m_src or not m_val or m_src.group(1) != kernel_source_hash():
+        return None
+    ns = float(m_val.group(1))
+    return {"kernel_ms": round(ns * 1e-6, 5),
+            "frac": round(ops / (ns * 1e-9) / 1e12 / peak_tops, 4),
+            "source": os.path.relpath(path, ROOT)}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), or '' if unknown."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
+
+
+def oracle_one_thread():
+    """The oracle on one host thread, on bounded samples of configs 1-3
+    (pack of the activations + conv / dense; about 2 s each)."""
+    from oracle import bsref
+    from paper_1810_11066_amd import workloads as wl
+    out = {}
+    bsref.set_threads(1)
+    try:
+        for name, case in (("config1", wl.config1()), ("config2", wl.config2()),
+                           ("config3", wl.config3())):
+            if isinstance(case, wl.DenseCase):
+                rows = 8
+                a = case.activations()[:rows]
+                wp = bsref.pack(case.weights(), case.wbits)
+                macs = rows * case.n * case.k
+
+                def run():
+                    ap = bsref.pack(a, case.abits)
+                    bsref.dense(ap, wp, rows, case.n, case.k, case.abits,
+                                case.wbits)
+                what = "%d of %d rows" % (rows, case.m)
+            else:
+                n_img = 1
+                a = case.activations()[:n_img]
+                wp = bsref.pack(case.weights(), case.wbits)
+                p = bsref.conv_params(n_img, case.h, case.w, case.c, case.oc,
+                                      case.k, case.k, case.stride, case.pad,
+                                      case.abits, case.wbits)
+                macs = n_img * case.oh * case.ow * case.oc * case.k ** 2 * \
+                    case.c
+
+                def run():
+                    bsref.conv2d(p, bsref.pack(a, case.abits), wp)
+                what = "%d of %d images" % (n_img, case.n)
+            reps, t0 = 0, time.perf_counter()
+            while True:
+                run()
+                reps += 1
+                el = time.perf_counter() - t0
+                if el >= 2.0:
+                    break
+            out[name] = {"value": round(2 * macs * reps / el / 1e9, 4),
+                         "unit": "GOPS",
+                         "sample": "%d x (pack + %s) of %s, %.1f s" % (
+                             reps, "dense" if "rows" in what else "conv",
+                             what, el)}
+    finally:
+        bsref.set_threads(os.cpu_count() or 1)
+    return out
+
+
 def cpu_baseline(case, a_host, w_host, gpu_out_fn, budget_s: float):
     """Time the oracle (pack + conv) on the first images of the batch until
     `budget_s` of wall time is spent; check the GPU output on that slice."""
@@ -130,14 +200,17 @@ def cpu_baseline(case, a_host, w_host, gpu_out_fn, budget_s: float):
         if el >= budget_s:
             break
     macs = n_img * case.oh * case.ow * case.oc * case.k * case.k * case.c
+    cores = bsref.threads()
     gpu = gpu_out_fn(n_img)
     return {
         "value": round(2 * macs * reps / el / 1e9, 3),
         "unit": "GOPS",
-        "cores": bsref.threads(),
+        "cores": cores,
         "kind": "oracle",
         "sample": "%d x (pack + conv) of the first %d of %d images, %.1f s"
                   % (reps, n_img, case.n, el),
+        "cpu_model": cpu_model(),
+        "one_thread": oracle_one_thread(),
     }, bool(np.array_equal(gpu, ref))
 
 
@@ -145,12 +218,14 @@ class Measured:
     """Times of one workload: the clean step, and per-launch kernel times."""
 
     def __init__(self, ms_step, host_ms, pre_ms, main_ms, describe,
-                 pre_b2b_ms):
+                 pre_b2b_ms, pre_ev_ms, main_ev_ms):
         self.ms_step = ms_step
         self.host_ms = host_ms
         self.pre_ms = pre_ms          # activation (quantize +) pack kernel
         self.pre_b2b_ms = pre_b2b_ms  # the same, back-to-back launches
         self.main_ms = main_ms        # conv / dense kernel
+        self.pre_ev_ms = pre_ev_ms    # event pairs recorded around launches
+        self.main_ev_ms = main_ev_ms
         self.describe = describe
 
 
@@ -195,10 +270,15 @@ def prepare(case, n_sets, bs, torch, np):
         sets.append((x, packed, out))
     torch.cuda.synchronize()
 
-    def step(i, ev=None, pack_only=False):
+    def step(i, ev=None, pack_only=False, dispatch_ev=None):
+        """One step on set i.  ev: three events recorded around the two
+        launches; dispatch_ev: two (start, stop) pairs the library attaches
+        to the pack and the conv dispatch themselves."""
         x, packed, out = sets[i % len(sets)]
         if ev is not None:
             ev[0].record(stream)
+        if dispatch_ev is not None:
+            bs.bs_set_timing_events(*dispatch_ev[0])
         if quantized:
             bs.bs_quantize_pack(x, packed, rows, k, case.act_scale, abits,
                                 case.aenc, stream)
@@ -208,11 +288,15 @@ def prepare(case, n_sets, bs, torch, np):
             return
         if ev is not None:
             ev[1].record(stream)
+        if dispatch_ev is not None:
+            bs.bs_set_timing_events(*dispatch_ev[1])
         if dense:
             bs.bs_dense(case.m, case.n, case.k, case.abits, case.wbits,
                         bs.UNIPOLAR, packed, w_packed, out, stream)
         else:
             bs.bs_conv2d(params, packed, w_packed, out, stream)
+        if dispatch_ev is not None:
+            bs.bs_set_timing_events(None, None)
         if ev is not None:
             ev[2].record(stream)
 
@@ -222,6 +306,11 @@ def prepare(case, n_sets, bs, torch, np):
             case.wbits).params())
     else:
         describe = bs.bs_conv2d_describe(params)
+    # initialisation: one step per set writes every packed and output buffer
+    # once, so that no buffer is first written inside a timed region
+    for i in range(n_sets):
+        step(i)
+    torch.cuda.synchronize()
     return sets, step, params, w_packed, describe, quantized
 
 
@@ -229,29 +318,45 @@ def measure(step, describe, steps, warmup, torch):
     """Clean timed region (one event pair around all steps), then the same
     steps again with an event pair around each launch for kernel times, then
     the pack launches alone, back to back under one event pair (an event
-    pair around a launch of a few microseconds adds about as much again)."""
+    pair around a launch of a few microseconds adds about as much again).
+
+    The start event is recorded behind the warmup steps while they are still
+    queued, with no synchronisation in between: the GPU goes from the last
+    warmup step straight into the first timed one, and the timed region
+    never waits for the host to enqueue its first launch."""
     stream = torch.cuda.current_stream()
-    for i in range(warmup):
-        step(i)
     torch.cuda.synchronize()
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
+    for i in range(warmup):
+        step(i)
     h0 = time.perf_counter()
     t_start.record(stream)
     for i in range(steps):
-        step(i)
+        step(warmup + i)
     t_end.record(stream)
     host_ms = (time.perf_counter() - h0) * 1e3 / steps
     torch.cuda.synchronize()
     ms_step = t_start.elapsed_time(t_end) / steps
-    # events between launches add gaps, so they stay out of the timed region
-    ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3))
-          for _ in range(steps)]
+    # kernel durations: events the runtime stamps with each dispatch's own
+    # start and end (the library launches through hipExtLaunchKernel while
+    # they are set), the figure a kernel trace reports
+    def mk():
+        return torch.cuda.Event(enable_timing=True)
+    dev = [((mk(), mk()), (mk(), mk())) for _ in range(steps)]
+    for i in range(steps):
+        step(i, dispatch_ev=dev[i])
+    torch.cuda.synchronize()
+    pre_ms = sum(d[0][0].elapsed_time(d[0][1]) for d in dev) / steps
+    main_ms = sum(d[1][0].elapsed_time(d[1][1]) for d in dev) / steps
+    # for comparison: event pairs recorded on the stream around each launch
+    # (they also count part of each launch's overhead)
+    ev = [tuple(mk() for _ in range(3)) for _ in range(steps)]
     for i in range(steps):
         step(i, ev[i])
     torch.cuda.synchronize()
-    pre_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
-    main_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / steps
+    pre_ev_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
+    main_ev_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / steps
     p_start = torch.cuda.Event(enable_timing=True)
     p_end = torch.cuda.Event(enable_timing=True)
     p_start.record(stream)
@@ -260,18 +365,22 @@ def measure(step, describe, steps, warmup, torch):
     p_end.record(stream)
     torch.cuda.synchronize()
     pre_b2b_ms = p_start.elapsed_time(p_end) / steps
-    return Measured(ms_step, host_ms, pre_ms, main_ms, describe, pre_b2b_ms)
+    return Measured(ms_step, host_ms, pre_ms, main_ms, describe, pre_b2b_ms,
+                    pre_ev_ms, main_ev_ms)
 
 
 def pack_roofline(nbytes, m):
-    """The activation (quantize +) pack kernel against the HBM peak, timed
-    by back-to-back launches; the per-launch event figure beside it."""
-    gbs = nbytes / (m.pre_b2b_ms * 1e-3) / 1e9
+    """The activation (quantize +) pack kernel against the HBM peak, timed by
+    dispatch-stamped events; back-to-back launches and event pairs around
+    each launch beside it."""
+    gbs = nbytes / (m.pre_ms * 1e-3) / 1e9
     return {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-            "bytes": nbytes, "kernel_ms": round(m.pre_b2b_ms, 5),
-            "timing": "back-to-back pack launches under one event pair",
-            "kernel_ms_per_launch_events": round(m.pre_ms, 5)}
+            "bytes": nbytes, "kernel_ms": round(m.pre_ms, 5),
+            "timing": "dispatch-stamped events (hipExtLaunchKernel) on each "
+                      "pack launch",
+            "kernel_ms_back_to_back": round(m.pre_b2b_ms, 5),
+            "kernel_ms_events_around_launch": round(m.pre_ev_ms, 5)}
 
 
 def case_bytes(case):
@@ -321,7 +430,8 @@ def case_line(case, m, args):
     bound = "alu" if t_alu >= t_hbm else "hbm"
     main_s = m.main_ms * 1e-3
     roof = {"bound": bound, "kernel": m.describe,
-            "kernel_ms": round(m.main_ms, 5)}
+            "kernel_ms": round(m.main_ms, 5),
+            "kernel_ms_events_around_launch": round(m.main_ev_ms, 5)}
     if bound == "alu":
         roof.update(achieved=round(ops / main_s / 1e12, 2),
                     peak=round(peak, 1), unit="TOPS (effective ops, "
@@ -645,8 +755,10 @@ def main() -> int:
             "traffic": committed_traffic(workload),
             "kernel": m.describe,
             "kernel_ms": round(m.main_ms, 5),
-            "timing": "per-launch HIP events on the launch stream, in a "
-                      "second pass over the same steps",
+            "timing": "dispatch-stamped events (hipExtLaunchKernel) on each "
+                      "conv launch, in a second pass over the same steps",
+            "kernel_ms_events_around_launch": round(m.main_ev_ms, 5),
+            "kernel_trace": committed_kernel_trace(workload, 2 * macs, peak),
         },
         "host_enqueue_ms_per_step": round(m.host_ms, 5),
         "pack_roofline": pack_roofline(pack_bytes, m),

@@ -28,7 +28,8 @@
  *  - Results are exact integers and do not depend on launch configuration;
  *    no kernel uses atomics, so repeated calls are bit-identical.
  *  - Thread safety: calls from several host threads are safe; the only
- *    library state is per thread (the error string and the kernel mode).
+ *    library state is per thread (the error string, the kernel mode, the
+ *    run-length override and the timing events).
  */
 #ifndef BITSERIAL_H
 #define BITSERIAL_H
@@ -233,6 +234,19 @@ bs_status bs_set_kernel_mode(int mode);
  * Results do not depend on it; it exists for tests of the run boundaries and
  * for tuning.  Errors: BS_ERR_INVALID_ARG for units < 0. */
 bs_status bs_set_units_per_wave(int units);
+
+/* Timing of the library's own kernels, for benchmarks.  Until cleared, every
+ * kernel the library launches for calls made on the calling host thread is
+ * launched with `start` and `stop` (hipEvent_t handles the caller created,
+ * e.g. with hipEventCreate) as the dispatch's start and stop events
+ * (hipExtLaunchKernel): the runtime stamps them with the dispatch's own
+ * start and end on the GPU, so hipEventElapsedTime(start, stop) after a call
+ * is its kernel's execution time -- the duration a kernel trace reports --
+ * without the gaps that events recorded between launches add.  A call that
+ * launches several kernels (a batch split into several launches) leaves the
+ * pair on its last kernel.  Either handle may be NULL; NULL, NULL clears.
+ * The library neither creates nor destroys the events.  Returns BS_OK. */
+bs_status bs_set_timing_events(void *start, void *stop);
 
 /* ABI version of this header (major * 100 + minor). */
 int bs_abi_version(void);

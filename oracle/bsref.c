@@ -28,6 +28,16 @@ int bsref_threads(void)
 #endif
 }
 
+int bsref_set_threads(int n)
+{
+    if (n < 1)
+        return BSREF_EINVAL;
+#ifdef _OPENMP
+    omp_set_num_threads(n);
+#endif
+    return BSREF_OK;
+}
+
 static int64_t words_for(int64_t k) { return (k + 31) / 32; }
 
 /* ------------------------------------------------------------------------ */

@@ -110,6 +110,10 @@ int bsref_dense_ex(int64_t m, int64_t n, int64_t k, int abits, int aenc,
 /* Number of host threads the oracle's parallel loops use. */
 int bsref_threads(void);
 
+/* Sets that number for later calls on the calling thread (n >= 1; the
+ * results do not depend on it).  Returns BSREF_EINVAL for n < 1. */
+int bsref_set_threads(int n);
+
 #ifdef __cplusplus
 }
 #endif

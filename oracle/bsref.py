@@ -99,7 +99,8 @@ def _load():
         lib.bsref_dense_ex.argtypes = [i64, i64, i64, ci, ci, ci, ci, P, P, P]
         for fn in ("bsref_quantize", "bsref_pack", "bsref_pack_ex",
                    "bsref_conv2d_out_shape", "bsref_conv2d", "bsref_conv2d_at",
-                   "bsref_dense", "bsref_dense_ex", "bsref_threads"):
+                   "bsref_dense", "bsref_dense_ex", "bsref_threads",
+                   "bsref_set_threads"):
             getattr(lib, fn).restype = ci
         _lib = lib
         return lib
@@ -120,6 +121,14 @@ def _ptr(a: np.ndarray):
 
 def threads() -> int:
     return _load().bsref_threads()
+
+
+def set_threads(n: int) -> None:
+    """Host threads for later oracle calls from this thread (timing only;
+    results do not depend on it)."""
+    lib = _load()
+    lib.bsref_set_threads.argtypes = [ctypes.c_int]
+    _check(lib.bsref_set_threads(n), "bsref_set_threads")
 
 
 def words(k: int) -> int:

@@ -47,7 +47,7 @@ EXPORTED = ("bs_packed_words", "bs_quantize", "bs_pack", "bs_pack_ex",
             "bs_conv2d_describe",
             "bs_dense", "bs_dense_ex", "bs_status_string",
             "bs_last_error", "bs_set_kernel_mode", "bs_set_units_per_wave",
-            "bs_abi_version")
+            "bs_set_timing_events", "bs_abi_version")
 
 
 class BitserialError(RuntimeError):
@@ -100,6 +100,7 @@ def load_library():
             "bs_last_error": (ctypes.c_char_p, []),
             "bs_set_kernel_mode": (ci, [ci]),
             "bs_set_units_per_wave": (ci, [ci]),
+            "bs_set_timing_events": (ci, [P, P]),
             "bs_abi_version": (ci, []),
         }
         for name, (res, args) in sig.items():
@@ -265,6 +266,23 @@ def bs_set_kernel_mode(mode: int) -> None:
 
 def bs_set_units_per_wave(units: int) -> None:
     _check(load_library().bs_set_units_per_wave(int(units)))
+
+
+def bs_set_timing_events(start=None, stop=None) -> None:
+    """Attach torch.cuda.Event start/stop (or None) to the library's later
+    kernel dispatches from this thread (bs_set_timing_events).  The events
+    are recorded once on the current stream first, so that their HIP events
+    exist; after a call, start.elapsed_time(stop) is its kernel's duration."""
+    handles = []
+    for e in (start, stop):
+        if e is None:
+            handles.append(None)
+            continue
+        if not isinstance(e, torch.cuda.Event):
+            raise TypeError("timing events must be torch.cuda.Event")
+        e.record(torch.cuda.current_stream())
+        handles.append(ctypes.c_void_p(e.cuda_event))
+    _check(load_library().bs_set_timing_events(*handles))
 
 
 def bs_packed_words(k: int) -> int:

@@ -2,8 +2,11 @@
 
     python -m paper_1810_11066_amd.build
 
-Every HIP source under csrc/ is compiled to an object in parallel, then linked
-into paper_1810_11066_amd/libbitserial.so.  Flags:
+Every compile unit below is compiled to an object in parallel, then linked
+into paper_1810_11066_amd/libbitserial.so.  The kernel instantiation sources
+(conv_fast_inst.hip, conv_pix_inst.hip) are compiled once per unit, each with
+its own -D selection, so that the specialisations compile in parallel.
+Flags:
   --offload-arch=gfx950          MI355X only
   -ffp-contract=off              the quantizer's product must stay a lone
                                  binary32 multiply (no FMA contraction)
@@ -26,12 +29,19 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libbitserial.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["api.hip", "quant_pack.hip", "conv.hip", "conv_fast_a1.hip",
-           "conv_fast_a2.hip", "conv_fast_a3.hip", "conv_fast_a4.hip",
-           "conv_pix.hip", "conv_pix_a1.hip", "conv_pix_a2.hip",
-           "conv_pix_a3.hip", "conv_pix_a4.hip", "conv_pix_s1.hip",
-           "conv_pix_s2.hip", "conv_pix_s3.hip", "conv_pix_s4.hip",
-           "conv_pix_b.hip"]
+# (source, object name, defines)
+UNITS = ([("api.hip", "api", ()), ("quant_pack.hip", "quant_pack", ()),
+          ("conv.hip", "conv", ()), ("conv_pix.hip", "conv_pix", ())] +
+         [("conv_fast_inst.hip", "conv_fast_a%d" % a, ("BS_A=%d" % a,))
+          for a in range(1, 5)] +
+         [("conv_pix_inst.hip", "conv_pix_a%d" % a,
+           ("BS_PIX_FAMILY=0", "BS_A=%d" % a)) for a in range(1, 5)] +
+         [("conv_pix_inst.hip", "conv_pix_s%d" % a,
+           ("BS_PIX_FAMILY=1", "BS_A=%d" % a)) for a in range(1, 5)] +
+         [("conv_pix_inst.hip", "conv_pix_b", ("BS_PIX_FAMILY=2",))])
+# every source file the library is built from (headers included)
+SOURCES = sorted({u[0] for u in UNITS} |
+                 {"bs_internal.h", "conv_fast.h", "conv_pix.h"})
 
 CFLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
@@ -55,10 +65,11 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
     returns its path."""
     extra = ["-D" + d for d in defines]
     with tempfile.TemporaryDirectory(prefix="bs_build_") as tmp:
-        objs = [os.path.join(tmp, s.replace(".hip", ".o")) for s in SOURCES]
-        with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-            list(ex.map(lambda a: _compile(a[0], a[1], extra),
-                        zip(SOURCES, objs)))
+        objs = [os.path.join(tmp, u[1] + ".o") for u in UNITS]
+        with cf.ThreadPoolExecutor(max_workers=min(8, len(UNITS))) as ex:
+            list(ex.map(lambda a: _compile(
+                a[0][0], a[1], extra + ["-D" + d for d in a[0][2]]),
+                zip(UNITS, objs)))
         out_tmp = out + ".tmp%d" % os.getpid()
         cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC"] + objs + \
               ["-o", out_tmp]

@@ -14,6 +14,7 @@ namespace {
 
 thread_local char g_err[512];
 thread_local bs::ConvOptions g_conv_opt;
+thread_local bs::TimingEvents g_timing;
 
 bs_status fail(bs_status st, const char* fmt, ...) {
     va_list ap;
@@ -166,9 +167,24 @@ bs_status check_conv(const bs_conv2d_params* p, bs::ConvShape* s) {
 
 }  // namespace
 
+namespace bs {
+
+TimingEvents& timing_events() { return g_timing; }
+
+hipError_t launch_kernel(const void* fn, dim3 grid, dim3 block, void** args,
+                         size_t lds, hipStream_t st) {
+    const TimingEvents& t = g_timing;
+    if (t.start || t.stop)
+        return hipExtLaunchKernel(fn, grid, block, args, lds, st, t.start,
+                                  t.stop, 0);
+    return hipLaunchKernel(fn, grid, block, args, lds, st);
+}
+
+}  // namespace bs
+
 extern "C" {
 
-int bs_abi_version(void) { return 104; }
+int bs_abi_version(void) { return 105; }
 
 int64_t bs_packed_words(int64_t k) { return k <= 0 ? 0 : (k + 31) / 32; }
 
@@ -195,6 +211,12 @@ bs_status bs_set_kernel_mode(int mode) {
 bs_status bs_set_units_per_wave(int units) {
     if (units < 0) return fail(BS_ERR_INVALID_ARG, "units per wave must be >= 0");
     g_conv_opt.units_per_wave = units;
+    return ok();
+}
+
+bs_status bs_set_timing_events(void* start, void* stop) {
+    g_timing.start = (hipEvent_t)start;
+    g_timing.stop = (hipEvent_t)stop;
     return ok();
 }
 

@@ -73,6 +73,34 @@ __device__ __forceinline__ uint32_t nibble_of(uint32_t v, int b) {
     return (x | (x >> 14)) & 0xFu;      // bits 0..3
 }
 
+// ---- kernel launch -------------------------------------------------------
+
+// The calling host thread's timing events (bs_set_timing_events); both
+// null unless a benchmark set them.
+struct TimingEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+TimingEvents& timing_events();
+
+// Launches fn.  With the thread's timing events set, the launch goes
+// through hipExtLaunchKernel, which has the runtime stamp the events with
+// this dispatch's own start and end.
+hipError_t launch_kernel(const void* fn, dim3 grid, dim3 block, void** args,
+                         size_t lds, hipStream_t st);
+
+template <typename T>
+struct Ident {
+    using type = T;
+};
+
+// Typed form: the arguments convert to the kernel's parameter types.
+template <typename... P>
+hipError_t launch(void (*fn)(P...), dim3 grid, dim3 block, size_t lds,
+                  hipStream_t st, typename Ident<P>::type... args) {
+    void* argv[] = {(void*)&args...};
+    return launch_kernel((const void*)fn, grid, block, argv, lds, st);
+}
+
 // ---- launchers (each returns hipSuccess or the launch error) -------------
 
 // enc: kUnipolar, kBipolar or kSigned

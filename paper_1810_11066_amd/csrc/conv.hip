@@ -413,9 +413,8 @@ hipError_t launch_pix(const ConvShape& s, pix::PixKernelFn fn,
         plan_pix(c, fn, forced_run, rq, &g, &grid, &lds);
         const uint32_t* a = act + n0 * act_img;
         int32_t* o = out + n0 * out_img;
-        void* args[] = {&a, &wts, &o, &g};
-        const hipError_t e = hipLaunchKernel((const void*)fn, grid,
-                                             dim3(pix::kBlock), args, lds, st);
+        const hipError_t e =
+            launch(fn, grid, dim3(pix::kBlock), lds, st, a, wts, o, g);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -457,16 +456,13 @@ hipError_t launch_conv(const ConvShape& s, const uint32_t* act,
             const KernelFn fn = pick_fast(s.abits, s.wbits, s.bipolar_w, s.kh,
                                           s.sh, pick_group_pixels(s.ow),
                                           g.cw);
-            void* args[] = {&act, &wts, &out, &g};
-            return hipLaunchKernel((const void*)fn, grid, dim3(kBlock), args,
-                                   lds, st);
+            return launch(fn, grid, dim3(kBlock), lds, st, act, wts, out, g);
         }
         case Family::kGeneric:
         default: {
             GenericArgs g;
             plan_generic(s, act, wts, out, &g, &grid);
-            conv_generic_kernel<<<grid, kBlock, 0, st>>>(g);
-            return hipGetLastError();
+            return launch(conv_generic_kernel, grid, dim3(kBlock), 0, st, g);
         }
     }
 }
@@ -501,8 +497,8 @@ hipError_t launch_conv_requant(const ConvShape& s, const uint32_t* act,
     int64_t blocks = ((int64_t)g.total + kBlock - 1) / kBlock;
     if (blocks > 65535) blocks = 65535;
     if (blocks < 1) blocks = 1;
-    conv_generic_requant_kernel<<<(uint32_t)blocks, kBlock, 0, st>>>(g);
-    return hipGetLastError();
+    return launch(conv_generic_requant_kernel, dim3((uint32_t)blocks),
+                  dim3(kBlock), 0, st, g);
 }
 
 int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,

@@ -333,7 +333,7 @@ using KernelFn = void (*)(const uint32_t*, const uint32_t*, int32_t*,
 // Kernel for (A, wbits, bipolar, kernel size, stride, group pixels, words
 // per plane); the word count is a compile-time constant when a
 // specialisation for it exists and a run-time argument otherwise.  Defined
-// for A = 1..4 in conv_fast_a<A>.hip.
+// for A = 1..4 by the compile units of conv_fast_inst.hip.
 template <int A>
 KernelFn pick_w(int w, bool b, int k, int s, int p, int cw);
 template <> KernelFn pick_w<1>(int w, bool b, int k, int s, int p, int cw);

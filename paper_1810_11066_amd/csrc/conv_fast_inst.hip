@@ -1,5 +1,15 @@
-// Specialisations of the fast bitserial conv kernel for 3-bit activations.
+// Specialisations of the channels-on-lanes conv kernel for BS_A-bit
+// activations (BS_A = 1..4).  The build compiles this source once per
+// activation width, each with its own -DBS_A, so that the widths compile in
+// parallel.
 #include "conv_fast.h"
+
+#ifndef BS_A
+#error "BS_A (activation bits, 1..4) must be defined"
+#endif
+#if BS_A < 1 || BS_A > 4
+#error "BS_A must be 1..4"
+#endif
 
 namespace bs {
 namespace fast {
@@ -47,12 +57,12 @@ KernelFn pick_b(bool b, int k, int s, int p, int cw) {
 }  // namespace
 
 template <>
-KernelFn pick_w<3>(int w, bool b, int k, int s, int p, int cw) {
+KernelFn pick_w<BS_A>(int w, bool b, int k, int s, int p, int cw) {
     switch (w) {
-        case 1: return pick_b<3, 1>(b, k, s, p, cw);
-        case 2: return pick_b<3, 2>(b, k, s, p, cw);
-        case 3: return pick_b<3, 3>(b, k, s, p, cw);
-        default: return pick_b<3, 4>(b, k, s, p, cw);
+        case 1: return pick_b<BS_A, 1>(b, k, s, p, cw);
+        case 2: return pick_b<BS_A, 2>(b, k, s, p, cw);
+        case 3: return pick_b<BS_A, 3>(b, k, s, p, cw);
+        default: return pick_b<BS_A, 4>(b, k, s, p, cw);
     }
 }
 

@@ -948,13 +948,14 @@ struct PlanInfo {
 // nullptr, with its plan (output channels per filter slice, taps per slice,
 // taps and words per plane of a reduction block).  ae / we are the operand
 // encodings (kUnipolar, kBipolar, kSigned).  The specialisations are spread
-// over several sources so that they compile in parallel:
-//   conv_pix_a<A>.hip  unipolar activations, unipolar or bipolar filters
+// over several compile units of conv_pix_inst.hip so that they compile in
+// parallel:
+//   pick_a<A>          unipolar activations, unipolar or bipolar filters
 //                      (W = 1..4 / W = 1), int32 or requantized output;
-//   conv_pix_s<A>.hip  signed filters W = 2..4 with unipolar activations,
+//   pick_signed<A>     signed filters W = 2..4 with unipolar activations,
 //                      and signed activations with signed filters of the
 //                      same width, int32 output;
-//   conv_pix_b.hip     +-1 activations with 1-bit filters, int32 output.
+//   pick_bipolar_act   +-1 activations with 1-bit filters, int32 output.
 PixKernelFn pick(int a, int w, int ae, int we, int k, int s, int cw, bool req,
                  PlanInfo* info);
 template <int A>

@@ -1,5 +1,5 @@
-// Dispatch to the pixels-on-lanes conv specialisations (conv_pix_a<A>.hip,
-// conv_pix_s<A>.hip, conv_pix_b.hip).
+// Dispatch to the pixels-on-lanes conv specialisations (the compile units of
+// conv_pix_inst.hip).
 #include "conv_pix.h"
 
 namespace bs {

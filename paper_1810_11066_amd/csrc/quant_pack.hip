@@ -318,9 +318,8 @@ template <int A>
 hipError_t launch_pack32(const uint8_t* q, uint32_t* packed, uint32_t nwords,
                          const FastDiv& d, hipStream_t st) {
     // 128 words per wave, 4 waves per block
-    pack_dpp_kernel<A><<<grid_for(nwords, 512), kBlock, 0, st>>>(q, packed,
-                                                                 nwords, d);
-    return hipGetLastError();
+    return launch(pack_dpp_kernel<A>, dim3(grid_for(nwords, 512)),
+                  dim3(kBlock), 0, st, q, packed, nwords, d);
 }
 
 template <int A, int ENC>
@@ -328,10 +327,9 @@ hipError_t launch_qpack(const float* x, uint32_t* packed, uint32_t nwords,
                         const FastDiv& d, float scale, float qmax,
                         hipStream_t st) {
     // 64 words per wave, 4 waves per block
-    quantize_pack_dpp_kernel<A, ENC>
-        <<<grid_for(nwords, 256), kBlock, 0, st>>>(x, packed, nwords, d,
-                                                    scale, qmax);
-    return hipGetLastError();
+    return launch(quantize_pack_dpp_kernel<A, ENC>,
+                  dim3(grid_for(nwords, 256)), dim3(kBlock), 0, st, x, packed,
+                  nwords, d, scale, qmax);
 }
 
 }  // namespace
@@ -345,15 +343,15 @@ static float enc_qmax(int bits, int enc) {
 hipError_t launch_quantize(const float* x, uint8_t* q, int64_t n, float scale,
                            int bits, int enc, hipStream_t st) {
     const float qmax = enc_qmax(bits, enc);
-    const int grid = grid_for((n >> 4) + 1, kBlock);
+    const dim3 grid(grid_for((n >> 4) + 1, kBlock));
     if (enc == kBipolar)
-        quantize_kernel<kBipolar><<<grid, kBlock, 0, st>>>(x, q, n, scale, qmax);
-    else if (enc == kSigned)
-        quantize_kernel<kSigned><<<grid, kBlock, 0, st>>>(x, q, n, scale, qmax);
-    else
-        quantize_kernel<kUnipolar><<<grid, kBlock, 0, st>>>(x, q, n, scale,
-                                                           qmax);
-    return hipGetLastError();
+        return launch(quantize_kernel<kBipolar>, grid, dim3(kBlock), 0, st, x,
+                      q, n, scale, qmax);
+    if (enc == kSigned)
+        return launch(quantize_kernel<kSigned>, grid, dim3(kBlock), 0, st, x,
+                      q, n, scale, qmax);
+    return launch(quantize_kernel<kUnipolar>, grid, dim3(kBlock), 0, st, x, q,
+                  n, scale, qmax);
 }
 
 hipError_t launch_pack(const uint8_t* q, uint32_t* packed, int64_t rows,
@@ -375,9 +373,9 @@ hipError_t launch_pack(const uint8_t* q, uint32_t* packed, int64_t rows,
         }
     }
     const int64_t waves = rows * ((k + 63) / 64);
-    pack_ballot_kernel<false, kUnipolar><<<grid_for(waves, 4), kBlock, 0, st>>>(
-        q, packed, rows, k, bits, 0.0f, 0.0f);
-    return hipGetLastError();
+    return launch(pack_ballot_kernel<false, kUnipolar>,
+                  dim3(grid_for(waves, 4)), dim3(kBlock), 0, st, q, packed,
+                  rows, k, bits, 0.0f, 0.0f);
 }
 
 hipError_t launch_pack_ex(const uint8_t* q, uint32_t* packed, int64_t outer,
@@ -386,16 +384,14 @@ hipError_t launch_pack_ex(const uint8_t* q, uint32_t* packed, int64_t outer,
     if (inner == 1 && layout == kLayoutMBK)
         return launch_pack(q, packed, outer, k, bits, st);
     const int64_t kw = (k + 31) / 32;
-    if (inner % 4 == 0) {
-        const int grid = grid_for(outer * kw * (inner / 4), kBlock);
-        pack_strided_kernel<4><<<grid, kBlock, 0, st>>>(q, packed, outer, k,
-                                                        inner, bits, layout);
-    } else {
-        const int grid = grid_for(outer * kw * inner, kBlock);
-        pack_strided_kernel<1><<<grid, kBlock, 0, st>>>(q, packed, outer, k,
-                                                        inner, bits, layout);
-    }
-    return hipGetLastError();
+    if (inner % 4 == 0)
+        return launch(pack_strided_kernel<4>,
+                      dim3(grid_for(outer * kw * (inner / 4), kBlock)),
+                      dim3(kBlock), 0, st, q, packed, outer, k, inner, bits,
+                      layout);
+    return launch(pack_strided_kernel<1>,
+                  dim3(grid_for(outer * kw * inner, kBlock)), dim3(kBlock), 0,
+                  st, q, packed, outer, k, inner, bits, layout);
 }
 
 namespace {
@@ -421,9 +417,8 @@ hipError_t quantize_pack_enc(const float* x, uint32_t* packed, int64_t rows,
         }
     }
     const int64_t waves = rows * ((k + 63) / 64);
-    pack_ballot_kernel<true, ENC><<<grid_for(waves, 4), kBlock, 0, st>>>(
-        x, packed, rows, k, bits, scale, qmax);
-    return hipGetLastError();
+    return launch(pack_ballot_kernel<true, ENC>, dim3(grid_for(waves, 4)),
+                  dim3(kBlock), 0, st, x, packed, rows, k, bits, scale, qmax);
 }
 
 }  // namespace

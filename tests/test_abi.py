@@ -41,9 +41,15 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_words(lib):
-    assert lib.bs_abi_version() == 104
+    assert lib.bs_abi_version() == 105
     for k, w in [(0, 0), (1, 1), (31, 1), (32, 1), (33, 2), (4096, 128)]:
         assert lib.bs_packed_words(k) == w
+
+
+def test_timing_events_set_and_clear(lib):
+    # host-side state only: nothing is launched, the handles are not touched
+    assert lib.bs_set_timing_events(FAKE, FAKE) == bs.BS_OK
+    assert lib.bs_set_timing_events(NULL, NULL) == bs.BS_OK
 
 
 def test_status_strings(lib):
