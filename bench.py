@@ -211,7 +211,7 @@ def cpu_baseline(case, a_host, w_host, gpu_out_fn, budget_s: float):
                   % (reps, n_img, case.n, el),
         "cpu_model": cpu_model(),
         "one_thread": oracle_one_thread(),
-    }, bool(np.array_equal(gpu, ref))
+    }, all(bool(np.array_equal(g, ref)) for g in gpu)
 
 
 class Measured:
@@ -229,14 +229,22 @@ class Measured:
         self.describe = describe
 
 
-def prepare(case, n_sets, bs, torch, np):
+def prepare(case, n_sets, bs, torch, np, fused=False):
     """Device buffers for `n_sets` rotated steps of a conv or dense case, and
     the per-step launch function.  Inputs are the workload's seeded host
     arrays (rolled along the batch axis for sets beyond the first); weights
-    are packed once, outside the timed steps."""
+    are packed once, outside the timed steps.
+
+    fused: the step is one call that bit-packs (and quantizes) the
+    activations inside the conv kernel (bs_conv2d_codes /
+    bs_quantize_conv2d) instead of bs_pack / bs_quantize_pack followed by
+    bs_conv2d; None is returned when the fused kernels do not cover the
+    case."""
     from paper_1810_11066_amd import workloads as wl
     stream = torch.cuda.current_stream()
     dense = isinstance(case, wl.DenseCase)
+    if dense and fused:
+        return None
     if dense:
         rows, k, abits = case.m, case.k, case.abits
     else:
@@ -270,55 +278,82 @@ def prepare(case, n_sets, bs, torch, np):
         sets.append((x, packed, out))
     torch.cuda.synchronize()
 
-    def step(i, ev=None, pack_only=False, dispatch_ev=None):
-        """One step on set i.  ev: three events recorded around the two
-        launches; dispatch_ev: two (start, stop) pairs the library attaches
-        to the pack and the conv dispatch themselves."""
-        x, packed, out = sets[i % len(sets)]
-        if ev is not None:
-            ev[0].record(stream)
-        if dispatch_ev is not None:
-            bs.bs_set_timing_events(*dispatch_ev[0])
+    def pack_launch(x, packed):
         if quantized:
             bs.bs_quantize_pack(x, packed, rows, k, case.act_scale, abits,
                                 case.aenc, stream)
         else:
             bs.bs_pack(x, packed, rows, k, abits, stream)
+
+    def main_launch(x, packed, out):
+        if dense:
+            bs.bs_dense(case.m, case.n, case.k, case.abits, case.wbits,
+                        bs.UNIPOLAR, packed, w_packed, out, stream)
+        elif fused and quantized:
+            bs.bs_quantize_conv2d(params, x, case.act_scale, w_packed, out,
+                                  stream)
+        elif fused:
+            bs.bs_conv2d_codes(params, x, w_packed, out, stream)
+        else:
+            bs.bs_conv2d(params, packed, w_packed, out, stream)
+
+    def step(i, ev=None, pack_only=False, dispatch_ev=None):
+        """One step on set i.  ev: three events recorded around the launches;
+        dispatch_ev: two (start, stop) pairs the library attaches to the pack
+        and the conv dispatch themselves.  pack_only: the standalone
+        activation pack alone (also for a fused step, as a reference)."""
+        x, packed, out = sets[i % len(sets)]
         if pack_only:
+            pack_launch(x, packed)
             return
+        if ev is not None:
+            ev[0].record(stream)
+        if not fused:
+            if dispatch_ev is not None:
+                bs.bs_set_timing_events(*dispatch_ev[0])
+            pack_launch(x, packed)
         if ev is not None:
             ev[1].record(stream)
         if dispatch_ev is not None:
             bs.bs_set_timing_events(*dispatch_ev[1])
-        if dense:
-            bs.bs_dense(case.m, case.n, case.k, case.abits, case.wbits,
-                        bs.UNIPOLAR, packed, w_packed, out, stream)
-        else:
-            bs.bs_conv2d(params, packed, w_packed, out, stream)
+        main_launch(x, packed, out)
         if dispatch_ev is not None:
             bs.bs_set_timing_events(None, None)
         if ev is not None:
             ev[2].record(stream)
 
+    step.fused = fused
+    if fused:
+        try:
+            step(0)
+        except bs.BitserialError as e:
+            if e.status == bs.BS_ERR_UNSUPPORTED:
+                return None
+            raise
     if dense:
         describe = bs.bs_conv2d_describe(bs.Conv2dSpec(
             1, 1, case.m, case.k, case.n, 1, 1, 1, 0, case.abits,
             case.wbits).params())
     else:
         describe = bs.bs_conv2d_describe(params)
+    if fused:
+        describe = ("staged activations (%s into LDS): " % (
+            "quantize + bit-pack" if quantized else "bit-pack") + describe)
     # initialisation: one step per set writes every packed and output buffer
     # once, so that no buffer is first written inside a timed region
     for i in range(n_sets):
         step(i)
+        if fused:
+            step(i, pack_only=True)
     torch.cuda.synchronize()
     return sets, step, params, w_packed, describe, quantized
 
 
 def measure(step, describe, steps, warmup, torch):
     """Clean timed region (one event pair around all steps), then the same
-    steps again with an event pair around each launch for kernel times, then
-    the pack launches alone, back to back under one event pair (an event
-    pair around a launch of a few microseconds adds about as much again).
+    steps again with dispatch-stamped events on each launch for kernel times
+    and once more with event pairs around each launch, then the activation
+    pack launches alone, back to back under one event pair.
 
     The start event is recorded behind the warmup steps while they are still
     queued, with no synchronisation in between: the GPU goes from the last
@@ -347,7 +382,8 @@ def measure(step, describe, steps, warmup, torch):
     for i in range(steps):
         step(i, dispatch_ev=dev[i])
     torch.cuda.synchronize()
-    pre_ms = sum(d[0][0].elapsed_time(d[0][1]) for d in dev) / steps
+    pre_ms = None if step.fused else \
+        sum(d[0][0].elapsed_time(d[0][1]) for d in dev) / steps
     main_ms = sum(d[1][0].elapsed_time(d[1][1]) for d in dev) / steps
     # for comparison: event pairs recorded on the stream around each launch
     # (they also count part of each launch's overhead)
@@ -355,7 +391,8 @@ def measure(step, describe, steps, warmup, torch):
     for i in range(steps):
         step(i, ev[i])
     torch.cuda.synchronize()
-    pre_ev_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
+    pre_ev_ms = None if step.fused else \
+        sum(e[0].elapsed_time(e[1]) for e in ev) / steps
     main_ev_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / steps
     p_start = torch.cuda.Event(enable_timing=True)
     p_end = torch.cuda.Event(enable_timing=True)
@@ -370,21 +407,29 @@ def measure(step, describe, steps, warmup, torch):
 
 
 def pack_roofline(nbytes, m):
-    """The activation (quantize +) pack kernel against the HBM peak, timed by
-    dispatch-stamped events; back-to-back launches and event pairs around
-    each launch beside it."""
-    gbs = nbytes / (m.pre_ms * 1e-3) / 1e9
-    return {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-            "bytes": nbytes, "kernel_ms": round(m.pre_ms, 5),
-            "timing": "dispatch-stamped events (hipExtLaunchKernel) on each "
-                      "pack launch",
-            "kernel_ms_back_to_back": round(m.pre_b2b_ms, 5),
-            "kernel_ms_events_around_launch": round(m.pre_ev_ms, 5)}
+    """The standalone activation (quantize +) pack kernel against the HBM
+    peak, timed by dispatch-stamped events (back-to-back launches when the
+    step is fused and has no pack launch of its own); the other timings
+    beside it."""
+    if m.pre_ms is not None:
+        ms, how = m.pre_ms, "dispatch-stamped events (hipExtLaunchKernel) " \
+            "on each pack launch"
+    else:
+        ms, how = m.pre_b2b_ms, "back-to-back standalone pack launches " \
+            "under one event pair (not part of the fused step)"
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    out = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+           "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+           "bytes": nbytes, "kernel_ms": round(ms, 5), "timing": how,
+           "kernel_ms_back_to_back": round(m.pre_b2b_ms, 5)}
+    if m.pre_ev_ms is not None:
+        out["kernel_ms_events_around_launch"] = round(m.pre_ev_ms, 5)
+    return out
 
 
-def case_bytes(case):
-    """Algorithmic HBM bytes of (activation pack, main kernel)."""
+def case_bytes(case, fused=False):
+    """Algorithmic HBM bytes of (activation pack, main kernel); fused: the
+    main kernel reads the unpacked activations instead of packed ones."""
     from paper_1810_11066_amd import workloads as wl
     if isinstance(case, wl.DenseCase):
         rows, k, out = case.m, case.k, case.m * case.n * 4
@@ -396,7 +441,7 @@ def case_bytes(case):
             ((case.c + 31) // 32) * 4
     packed = rows * case.abits * ((k + 31) // 32) * 4
     src = rows * k * (4 if getattr(case, "act_scale", None) else 1)
-    return src + packed, packed + wbytes + out
+    return src + packed, (src if fused else packed) + wbytes + out
 
 
 def sets_for(case, minimum: int) -> int:
@@ -418,19 +463,17 @@ def sets_for(case, minimum: int) -> int:
 ENC_NAMES = ("unipolar", "bipolar", "signed")
 
 
-def case_line(case, m, args):
-    """One JSON result object for a workload other than the headline one."""
-    from paper_1810_11066_amd import workloads as wl
-    dense = isinstance(case, wl.DenseCase)
-    ops = 2 * case.macs
+def roofline_of(case, m, ops, main_bytes):
+    """Roofline object of the step's main (conv / dense) kernel."""
     peak = popcount_roofline_tops(case.abits, case.wbits)
-    pre_bytes, main_bytes = case_bytes(case)
     t_alu = ops / (peak * 1e12)
     t_hbm = main_bytes / (HBM_PEAK_GBS * 1e9)
     bound = "alu" if t_alu >= t_hbm else "hbm"
     main_s = m.main_ms * 1e-3
     roof = {"bound": bound, "kernel": m.describe,
             "kernel_ms": round(m.main_ms, 5),
+            "timing": "dispatch-stamped events (hipExtLaunchKernel) on each "
+                      "launch",
             "kernel_ms_events_around_launch": round(m.main_ev_ms, 5)}
     if bound == "alu":
         roof.update(achieved=round(ops / main_s / 1e12, 2),
@@ -440,7 +483,28 @@ def case_line(case, m, args):
         roof.update(achieved=round(main_bytes / main_s / 1e9, 1),
                     peak=HBM_PEAK_GBS, unit="GB/s (algorithmic bytes)",
                     frac=round(t_hbm / main_s, 4))
-    return {
+    return roof
+
+
+def per_step_name(case, fused):
+    from paper_1810_11066_amd import workloads as wl
+    q = getattr(case, "act_scale", None) is not None
+    if fused:
+        return ("bs_quantize_conv2d (quantize + bit-pack of the float32 "
+                "activations inside the conv kernel)" if q else
+                "bs_conv2d_codes (bit-pack of the uint8 activation codes "
+                "inside the conv kernel)")
+    return ("bs_quantize_pack" if q else "bs_pack") + "(activations) + " + \
+        ("bs_dense" if isinstance(case, wl.DenseCase) else "bs_conv2d")
+
+
+def case_line(case, m, args, mu=None):
+    """One JSON result object for a workload other than the headline one.
+    m: the step as timed (the fused call where it covers the case); mu: the
+    unfused step (pack + conv) of the same case, when m is fused."""
+    ops = 2 * case.macs
+    pre_bytes, main_bytes = case_bytes(case, fused=mu is not None)
+    line = {
         "metric": "bitserial conv2d effective GOPS (2*MACs/s) + % of "
                   "popcount-VALU roofline",
         "value": round(ops / (m.ms_step * 1e-3) / 1e9, 1),
@@ -449,17 +513,22 @@ def case_line(case, m, args):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "u32", "data": "synthetic",
         "config": {"workload": case.name,
-                   "per_step": ("bs_quantize_pack" if getattr(
-                       case, "act_scale", None) else "bs_pack") +
-                   "(activations) + " + ("bs_dense" if dense
-                                         else "bs_conv2d"),
+                   "per_step": per_step_name(case, mu is not None),
                    "abits": case.abits, "wbits": case.wbits,
                    "encoding": ENC_NAMES[getattr(case, "wenc", 0)],
                    "act_encoding": ENC_NAMES[getattr(case, "aenc", 0)]},
-        "roofline": roof,
+        "roofline": roofline_of(case, m, ops, main_bytes),
         "pack_roofline": pack_roofline(pre_bytes, m),
         "host_enqueue_ms_per_step": round(m.host_ms, 5),
     }
+    if mu is not None:
+        _, ubytes = case_bytes(case)
+        line["unfused"] = {
+            "per_step": per_step_name(case, False),
+            "ms_per_step": round(mu.ms_step, 5),
+            "value": round(ops / (mu.ms_step * 1e-3) / 1e9, 1),
+            "roofline": roofline_of(case, mu, ops, ubytes)}
+    return line
 
 
 INT8_MFMA_PEAK_TOPS = 5000.0   # dense int8 MFMA, MI355X
@@ -625,6 +694,10 @@ def main() -> int:
                          "512 MB in all)")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="seconds of oracle time for cpu_baseline (0: skip)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="time only the two-kernel step (bs_pack or "
+                         "bs_quantize_pack, then bs_conv2d), not the fused "
+                         "call that packs inside the conv kernel")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one device copy of this size (for HBM "
                          "counter calibration under rocprofv3 --pmc)")
@@ -684,13 +757,22 @@ def main() -> int:
                      5: lambda: wl.config5(**b)}[args.config]()
         times = {}
         for case in cases:
-            sets, step, _, _, describe, _ = prepare(
-                case, sets_for(case, args.sets), bs, torch, np)
-            m = measure(step, describe, args.steps, args.warmup, torch)
-            times[(case.abits, case.wbits)] = m.main_ms
-            print(json.dumps(case_line(case, m, args)), flush=True)
-            del sets
+            n_sets = sets_for(case, args.sets)
+            sets, step, _, _, describe, _ = prepare(case, n_sets, bs, torch,
+                                                    np)
+            mu = measure(step, describe, args.steps, args.warmup, torch)
+            times[(case.abits, case.wbits)] = mu.main_ms
+            del sets, step
             torch.cuda.empty_cache()
+            fz = None if args.unfused else prepare(case, n_sets, bs, torch,
+                                                   np, fused=True)
+            if fz is not None:
+                mf = measure(fz[1], fz[4], args.steps, args.warmup, torch)
+                print(json.dumps(case_line(case, mf, args, mu)), flush=True)
+                del fz
+                torch.cuda.empty_cache()
+            else:
+                print(json.dumps(case_line(case, mu, args)), flush=True)
         if args.sweep:
             # the paper's limit study quotes W1A1 against W4A4 and W2A2
             # against W1A4 (activation width A, weight width W)
@@ -703,16 +785,19 @@ def main() -> int:
         return 0
 
     case = wl.config2(batch=args.batch or 64)
-    rows, k = case.n * case.h * case.w, case.c
     n_sets = sets_for(case, args.sets)
+    fz = None if args.unfused else prepare(case, n_sets, bs, torch, np,
+                                           fused=True)
+    mf = None
+    if fz is not None:
+        mf = measure(fz[1], fz[4], args.steps, args.warmup, torch)
     sets, step, params, w_packed, describe, _ = prepare(case, n_sets, bs,
                                                         torch, np)
-    m = measure(step, describe, args.steps, args.warmup, torch)
-    stream = torch.cuda.current_stream()
+    mu = measure(step, describe, args.steps, args.warmup, torch)
+    m = mf if mf is not None else mu
     macs = case.macs
     value_gops = 2 * macs / (m.ms_step * 1e-3) / 1e9
     peak = popcount_roofline_tops(case.abits, case.wbits)
-    achieved = 2 * macs / (m.main_ms * 1e-3) / 1e12
     pack_bytes, _ = case_bytes(case)
 
     if args.copy_calibration_mib > 0:
@@ -722,7 +807,24 @@ def main() -> int:
         dst.copy_(src)
         torch.cuda.synchronize()
 
-    workload = "a2w1_b%d_56x56x64_3x3" % case.n
+    def conv_roofline(mm, workload):
+        achieved = 2 * macs / (mm.main_ms * 1e-3) / 1e12
+        return {
+            "bound": "alu",
+            "achieved": round(achieved, 2),
+            "peak": round(peak, 1),
+            "unit": "TOPS (effective A2W1 ops, popcount VALU)",
+            "frac": round(achieved / peak, 4),
+            "traffic": committed_traffic(workload),
+            "kernel": mm.describe,
+            "kernel_ms": round(mm.main_ms, 5),
+            "timing": "dispatch-stamped events (hipExtLaunchKernel) on each "
+                      "conv launch, in a second pass over the same steps",
+            "kernel_ms_events_around_launch": round(mm.main_ev_ms, 5),
+            "kernel_trace": committed_kernel_trace(workload, 2 * macs, peak),
+        }
+
+    shape = "a2w1_b%d_56x56x64_3x3" % case.n
     result = {
         "metric": "bitserial conv2d effective GOPS (2*MACs/s) + % of "
                   "popcount-VALU roofline",
@@ -743,35 +845,35 @@ def main() -> int:
             "oc": case.oc, "kernel": case.k, "stride": case.stride,
             "pad": case.pad, "abits": case.abits, "wbits": case.wbits,
             "encoding": "unipolar", "output": "int32 NHWC",
-            "per_step": "bs_pack(activations) + bs_conv2d",
+            "per_step": per_step_name(case, mf is not None),
             "buffer_sets": n_sets,
         },
-        "roofline": {
-            "bound": "alu",
-            "achieved": round(achieved, 2),
-            "peak": round(peak, 1),
-            "unit": "TOPS (effective A2W1 ops, popcount VALU)",
-            "frac": round(achieved / peak, 4),
-            "traffic": committed_traffic(workload),
-            "kernel": m.describe,
-            "kernel_ms": round(m.main_ms, 5),
-            "timing": "dispatch-stamped events (hipExtLaunchKernel) on each "
-                      "conv launch, in a second pass over the same steps",
-            "kernel_ms_events_around_launch": round(m.main_ev_ms, 5),
-            "kernel_trace": committed_kernel_trace(workload, 2 * macs, peak),
-        },
+        "roofline": conv_roofline(
+            m, ("codes_" if mf is not None else "") + shape),
         "host_enqueue_ms_per_step": round(m.host_ms, 5),
-        "pack_roofline": pack_roofline(pack_bytes, m),
+        "pack_roofline": pack_roofline(pack_bytes, mu),
     }
+    if mf is not None:
+        result["unfused"] = {
+            "per_step": per_step_name(case, False),
+            "ms_per_step": round(mu.ms_step, 5),
+            "value": round(2 * macs / (mu.ms_step * 1e-3) / 1e9, 1),
+            "roofline": conv_roofline(mu, shape)}
 
     if args.cpu_budget > 0:
         a_host = case.activations()
         w_host = case.weights()
 
         def gpu_slice(n_img):
+            """The first images of set 0 from the unfused and (if timed) the
+            fused step, stacked; the oracle's slice must equal each."""
             step(0)
+            outs = [sets[0][2][:n_img].cpu().numpy()]
+            if fz is not None:
+                fz[1](0)
+                outs.append(fz[0][0][2][:n_img].cpu().numpy())
             torch.cuda.synchronize()
-            return sets[0][2][:n_img].cpu().numpy()
+            return outs
         cpu, ok = cpu_baseline(case, a_host, w_host, gpu_slice,
                                args.cpu_budget)
         result["cpu_baseline"] = cpu

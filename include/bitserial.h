@@ -161,6 +161,37 @@ bs_status bs_conv2d(const bs_conv2d_params *p, const uint32_t *act_packed,
                     const uint32_t *w_packed, int32_t *out,
                     bs_stream_t stream);
 
+/* Bitserial conv2d of unpacked activation codes: the activation pack of
+ * Sec. 3.1 fused into the conv.  Exactly bs_pack of act_codes followed by
+ * bs_conv2d (the paper times the activation pack with the conv; here it is
+ * part of the conv kernel): every workgroup bit-packs the input rows its
+ * outputs read into LDS and convolves from there, so the packed activations
+ * never reach HBM.
+ *   act_codes: [n][h][w][c] uint8 NHWC codes (device); bits of a code at or
+ *              above abits are ignored, as in bs_pack;
+ *   w_packed, out and the result: as bs_conv2d.
+ * p->aenc is the encoding of the codes.
+ * Errors: as bs_conv2d; BS_ERR_UNSUPPORTED when no fused kernel covers the
+ * shape (c must be a multiple of 32, oc of 4, kernels square of size 1 or 3,
+ * stride 1 or 2, activations unipolar with unipolar 1-2-bit or bipolar 1-bit
+ * filters, the whole kh x kw x abits x (c/32)-word window within 72 words,
+ * and the packed input rows that the windows of 256 consecutive output
+ * pixels span, plus 17 KB, within 64 KB of LDS -- only very narrow images
+ * miss this): pack with bs_pack and call bs_conv2d instead.
+ * Nothing is enqueued on any error. */
+bs_status bs_conv2d_codes(const bs_conv2d_params *p, const uint8_t *act_codes,
+                          const uint32_t *w_packed, int32_t *out,
+                          bs_stream_t stream);
+
+/* bs_conv2d_codes of float32 activations quantized on the fly: exactly
+ * bs_quantize_pack(x, scale, p->abits, p->aenc) followed by bs_conv2d, with
+ * quantization and packing done per workgroup into LDS.
+ *   x: [n][h][w][c] float32 NHWC (device); scale as bs_quantize.
+ * Errors: as bs_conv2d_codes, and as bs_quantize for scale and encoding. */
+bs_status bs_quantize_conv2d(const bs_conv2d_params *p, const float *x,
+                             float scale, const uint32_t *w_packed,
+                             int32_t *out, bs_stream_t stream);
+
 /* Bitserial conv2d whose result is requantized and bit-packed as the next
  * layer's activations (layer chaining, toward the end-to-end low-precision
  * inference of Sec. 7): the int32 result v of bs_conv2d for each output is

@@ -44,6 +44,7 @@ LAYOUT_BMK = 2
 EXPORTED = ("bs_packed_words", "bs_quantize", "bs_pack", "bs_pack_ex",
             "bs_quantize_pack",
             "bs_conv2d_out_shape", "bs_conv2d", "bs_conv2d_requant",
+            "bs_conv2d_codes", "bs_quantize_conv2d",
             "bs_conv2d_describe",
             "bs_dense", "bs_dense_ex", "bs_status_string",
             "bs_last_error", "bs_set_kernel_mode", "bs_set_units_per_wave",
@@ -90,6 +91,10 @@ def load_library():
                                          ctypes.POINTER(ctypes.c_int32),
                                          ctypes.POINTER(ctypes.c_int32)]),
             "bs_conv2d": (ci, [ctypes.POINTER(ConvParams), P, P, P, P]),
+            "bs_conv2d_codes": (ci, [ctypes.POINTER(ConvParams), P, P, P,
+                                     P]),
+            "bs_quantize_conv2d": (ci, [ctypes.POINTER(ConvParams), P, cf, P,
+                                        P, P]),
             "bs_conv2d_requant": (ci, [ctypes.POINTER(ConvParams), P, P, cf,
                                        ci, P, P]),
             "bs_conv2d_describe": (ci, [ctypes.POINTER(ConvParams),
@@ -227,6 +232,35 @@ def bs_conv2d(p: ConvParams, act_packed: torch.Tensor, w_packed: torch.Tensor,
              p.n * p.h * p.w * p.abits * cw),
         _dev(w_packed, "w_packed", torch.int32,
              p.oc * p.kh * p.kw * p.wbits * cw),
+        _dev(out, "out", torch.int32, p.n * oh * ow * p.oc),
+        _stream(stream)))
+
+
+def bs_conv2d_codes(p: ConvParams, act_codes: torch.Tensor,
+                    w_packed: torch.Tensor, out: torch.Tensor,
+                    stream=None) -> None:
+    """bs_pack of the uint8 NHWC codes fused into bs_conv2d."""
+    oh, ow = bs_conv2d_out_shape(p)
+    _check(load_library().bs_conv2d_codes(
+        ctypes.byref(p),
+        _dev(act_codes, "act_codes", torch.uint8, p.n * p.h * p.w * p.c),
+        _dev(w_packed, "w_packed", torch.int32,
+             p.oc * p.kh * p.kw * p.wbits * words(p.c)),
+        _dev(out, "out", torch.int32, p.n * oh * ow * p.oc),
+        _stream(stream)))
+
+
+def bs_quantize_conv2d(p: ConvParams, x: torch.Tensor, scale: float,
+                       w_packed: torch.Tensor, out: torch.Tensor,
+                       stream=None) -> None:
+    """bs_quantize_pack of the float32 NHWC activations fused into
+    bs_conv2d."""
+    oh, ow = bs_conv2d_out_shape(p)
+    _check(load_library().bs_quantize_conv2d(
+        ctypes.byref(p),
+        _dev(x, "x", torch.float32, p.n * p.h * p.w * p.c), float(scale),
+        _dev(w_packed, "w_packed", torch.int32,
+             p.oc * p.kh * p.kw * p.wbits * words(p.c)),
         _dev(out, "out", torch.int32, p.n * oh * ow * p.oc),
         _stream(stream)))
 
@@ -370,6 +404,28 @@ def conv2d(spec: Conv2dSpec, act_packed: torch.Tensor,
     out = torch.empty((spec.n, oh, ow, spec.oc), dtype=torch.int32,
                       device=act_packed.device)
     bs_conv2d(p, act_packed, w_packed, out)
+    return out
+
+
+def conv2d_codes(spec: Conv2dSpec, act_codes: torch.Tensor,
+                 w_packed: torch.Tensor) -> torch.Tensor:
+    """Conv of uint8 NHWC codes, the activation pack fused into the conv."""
+    p = spec.params()
+    oh, ow = bs_conv2d_out_shape(p)
+    out = torch.empty((spec.n, oh, ow, spec.oc), dtype=torch.int32,
+                      device=act_codes.device)
+    bs_conv2d_codes(p, act_codes, w_packed, out)
+    return out
+
+
+def quantize_conv2d(spec: Conv2dSpec, x: torch.Tensor, scale: float,
+                    w_packed: torch.Tensor) -> torch.Tensor:
+    """Conv of float32 NHWC activations, quantize + pack fused into it."""
+    p = spec.params()
+    oh, ow = bs_conv2d_out_shape(p)
+    out = torch.empty((spec.n, oh, ow, spec.oc), dtype=torch.int32,
+                      device=x.device)
+    bs_quantize_conv2d(p, x, scale, w_packed, out)
     return out
 
 

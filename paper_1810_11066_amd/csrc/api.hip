@@ -184,7 +184,7 @@ hipError_t launch_kernel(const void* fn, dim3 grid, dim3 block, void** args,
 
 extern "C" {
 
-int bs_abi_version(void) { return 105; }
+int bs_abi_version(void) { return 106; }
 
 int64_t bs_packed_words(int64_t k) { return k <= 0 ? 0 : (k + 31) / 32; }
 
@@ -335,6 +335,63 @@ bs_status bs_conv2d(const bs_conv2d_params* p, const uint32_t* act_packed,
     return from_hip(bs::launch_conv(s, act_packed, w_packed, out,
                                     g_conv_opt, (hipStream_t)stream),
                     "bs_conv2d launch");
+}
+
+// The fused pack + conv calls: validation as bs_conv2d, with the unpacked
+// activations' bytes in the overlap check.
+static bs_status conv_staged(const bs_conv2d_params* p, const void* act,
+                             uint64_t elem_bytes, const char* act_name,
+                             bool from_float, float scale,
+                             const uint32_t* w_packed, int32_t* out,
+                             bs_stream_t stream, const char* what) {
+    bs_status st;
+    if ((st = check_ptr(act, act_name)) != BS_OK) return st;
+    if ((st = check_ptr(w_packed, "w_packed")) != BS_OK) return st;
+    if ((st = check_ptr(out, "out")) != BS_OK) return st;
+    bs::ConvShape s;
+    if ((st = check_conv(p, &s)) != BS_OK) return st;
+    if (from_float &&
+        (st = check_scale_enc(scale, s.abits, (bs_encoding)s.aenc)) != BS_OK)
+        return st;
+    const uint64_t out_bytes = (uint64_t)s.n * s.oh * s.ow * (uint64_t)s.oc * 4u;
+    const uint64_t act_bytes =
+        (uint64_t)s.n * s.h * s.w * (uint64_t)s.c * elem_bytes;
+    const uint64_t w_bytes = packed_bytes((int64_t)s.oc * s.kh * s.kw,
+                                          s.wbits, s.c);
+    if ((st = check_disjoint(out, out_bytes, "out", act, act_bytes,
+                             act_name)) != BS_OK)
+        return st;
+    if ((st = check_disjoint(out, out_bytes, "out", w_packed, w_bytes,
+                             "w_packed")) != BS_OK)
+        return st;
+    const hipError_t e =
+        bs::launch_conv_staged(s, from_float, act, scale, w_packed, out,
+                               g_conv_opt, (hipStream_t)stream);
+    if (e == hipErrorNotSupported)
+        return fail(BS_ERR_UNSUPPORTED,
+                    "%s: no fused kernel covers this shape (it needs c a "
+                    "multiple of 32, oc a multiple of 4, square kernels of "
+                    "size 1 or 3, stride 1 or 2, unipolar activations with "
+                    "unipolar filters of 1-2 bits or bipolar 1-bit filters, "
+                    "the whole kh x kw x abits x c/32-word patch within "
+                    "72 words, and the input rows of one workgroup's outputs "
+                    "within its LDS); bit-pack the activations and call "
+                    "bs_conv2d", what);
+    return from_hip(e, what);
+}
+
+bs_status bs_conv2d_codes(const bs_conv2d_params* p, const uint8_t* act_codes,
+                          const uint32_t* w_packed, int32_t* out,
+                          bs_stream_t stream) {
+    return conv_staged(p, act_codes, 1, "act_codes", false, 0.0f, w_packed,
+                       out, stream, "bs_conv2d_codes");
+}
+
+bs_status bs_quantize_conv2d(const bs_conv2d_params* p, const float* x,
+                             float scale, const uint32_t* w_packed,
+                             int32_t* out, bs_stream_t stream) {
+    return conv_staged(p, x, 4, "x", true, scale, w_packed, out, stream,
+                       "bs_quantize_conv2d");
 }
 
 bs_status bs_conv2d_requant(const bs_conv2d_params* p,

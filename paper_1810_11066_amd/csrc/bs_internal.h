@@ -159,6 +159,16 @@ hipError_t launch_conv_requant(const ConvShape& s, const uint32_t* act,
                                const Requant& rq, const ConvOptions& opt,
                                hipStream_t st);
 
+// Conv of unpacked activations: uint8 codes (from_float false) or float32
+// values quantized with `scale` under s.aenc (from_float true), NHWC
+// [n][h][w][c]; the conv kernel bit-packs each block's input rows into LDS.
+// hipErrorNotSupported, with nothing enqueued, when no such kernel covers
+// the shape.
+hipError_t launch_conv_staged(const ConvShape& s, bool from_float,
+                              const void* act, float scale,
+                              const uint32_t* wts, int32_t* out,
+                              const ConvOptions& opt, hipStream_t st);
+
 // Writes the kernel and launch configuration launch_conv would use for this
 // shape and mode into buf (snprintf semantics); returns the snprintf result.
 int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,

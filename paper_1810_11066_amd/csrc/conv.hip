@@ -31,6 +31,7 @@
 // per output.
 #include <atomic>
 #include <cstdio>
+#include <cstring>
 #include <mutex>
 #include <vector>
 
@@ -233,17 +234,20 @@ int64_t pix_images_per_launch(const ConvShape& s, bool req) {
     return n;
 }
 
-// Pixels-on-lanes kernel for this shape, or nullptr.
-pix::PixKernelFn pix_kernel_for(const ConvShape& s, bool req,
+// Pixels-on-lanes kernel for this shape, or nullptr.  src: where the
+// activations come from (pix::kSrcPacked, kSrcCodes, kSrcFloat); the staged
+// forms read whole 32-code words of each pixel, so they need c % 32 == 0.
+pix::PixKernelFn pix_kernel_for(const ConvShape& s, bool req, int src,
                                 pix::PlanInfo* info) {
     const int64_t cw = (s.c + 31) / 32;
     if (s.abits > 4 || s.wbits > 4) return nullptr;
     if (s.kh != s.kw || s.sh != s.sw) return nullptr;
     // output tiles are written in 16-byte quads of channels
     if (s.oc % 4 != 0) return nullptr;
+    if (src != pix::kSrcPacked && s.c % 32 != 0) return nullptr;
     if (pix_images_per_launch(s, req) < 1) return nullptr;
     return pix::pick(s.abits, s.wbits, s.aenc, s.wenc, s.kh, s.sh, (int)cw,
-                     req, info);
+                     req, src, info);
 }
 
 // Compute units of the current device (cached per device).
@@ -288,13 +292,60 @@ int resident_blocks(pix::PixKernelFn fn, size_t lds) {
     return blocks;
 }
 
+// Largest input region, in pixels, that a block of a staged launch packs
+// into LDS (pix::block_region for every block of the plan in g; blocks are
+// only renumbered by the XCD-major order, so the set of regions is the
+// same).  Exact, by a pass over the blocks, cached per shape and run length.
+int64_t max_region_pixels(const ConvShape& s, const pix::PixArgs& g) {
+    struct Entry {
+        int32_t key[12];
+        int64_t pixels;
+    };
+    static std::mutex mu;
+    static std::vector<Entry> cache;
+    const int32_t key[12] = {s.n, s.h, s.w, s.oh, s.ow, s.ph, s.kh, s.sh,
+                             g.units, g.group_units, g.per_wave, g.npix};
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        for (const Entry& e : cache)
+            if (memcmp(e.key, key, sizeof(key)) == 0) return e.pixels;
+    }
+    const int64_t per_block = (int64_t)pix::kWavesPerBlock * g.per_wave;
+    int64_t best = 0;
+    for (int64_t ub0 = 0; ub0 < g.units; ub0 += per_block) {
+        const int64_t ub1 = ub0 + per_block < g.units ? ub0 + per_block
+                                                      : g.units;
+        const int64_t p0 = ub0 / g.group_units * 64;
+        int64_t p1 = (ub1 - 1) / g.group_units * 64 + 63;
+        if (p1 > g.npix - 1) p1 = g.npix - 1;
+        const int64_t r0 = p0 / s.ow, n0 = r0 / s.oh, y0 = r0 % s.oh;
+        const int64_t r1 = p1 / s.ow, n1 = r1 / s.oh, y1 = r1 % s.oh;
+        int64_t iy_lo = y0 * s.sh - s.ph, iy_hi = y1 * s.sh - s.ph + s.kh - 1;
+        if (iy_lo < 0) iy_lo = 0;
+        if (iy_lo > s.h) iy_lo = s.h;
+        if (iy_hi > s.h - 1) iy_hi = s.h - 1;
+        if (iy_hi < -1) iy_hi = -1;
+        const int64_t lo = (n0 * s.h + iy_lo) * s.w;
+        const int64_t hi = (n1 * s.h + iy_hi) * s.w + s.w;
+        if (hi - lo > best) best = hi - lo;
+    }
+    std::lock_guard<std::mutex> lock(mu);
+    Entry e;
+    memcpy(e.key, key, sizeof(key));
+    e.pixels = best;
+    if (cache.size() < 256) cache.push_back(e);
+    return best;
+}
+
 // Launch configuration of a pixels-on-lanes call.  The work is units of
 // (64-pixel group, 4 output channels); each wave takes a contiguous run of
 // L units.  L is the smallest run that keeps the grid resident in one round
 // (at most `resident` blocks per CU), adjusted upwards while that lowers the
 // busiest CU's load (blocks per CU x L), so that CUs end together.
-void plan_pix(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
-              const Requant* rq, pix::PixArgs* g, dim3* grid, size_t* lds) {
+// `lds` is the dynamic LDS per block the plan assumes for residency.
+void plan_pix_lds(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
+                  const Requant* rq, pix::PixArgs* g, dim3* grid,
+                  size_t lds) {
     g->h = s.h; g->w = s.w; g->oh = s.oh; g->ow = s.ow;
     g->ph = s.ph; g->pw = s.pw;
     g->c = s.c;
@@ -319,9 +370,11 @@ void plan_pix(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
     g->act_bytes = (int32_t)((int64_t)s.n * s.h * s.w * s.abits *
                              ((s.c + 31) / 32) * 4);
     g->out_bytes = rq ? 0 : (int32_t)((int64_t)g->npix * s.oc * 4);
-    *lds = (size_t)pix::kWavesPerBlock * pix::kTileWords * 4;
+    g->region_pixels = 0;
+    g->in_scale = 0.0f;
+    g->in_qmax = 0.0f;
     const int64_t cus = device_cus();
-    const int64_t slots = cus * resident_blocks(fn, *lds);   // blocks
+    const int64_t slots = cus * resident_blocks(fn, lds);   // blocks
     const int64_t wpb = pix::kWavesPerBlock;
     int64_t lmin = (units + slots * wpb - 1) / (slots * wpb);
     if (lmin < 1) lmin = 1;
@@ -348,6 +401,47 @@ void plan_pix(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
     g->per_wave = (int32_t)best;
     const int64_t waves = (units + best - 1) / best;
     *grid = dim3((uint32_t)((waves + wpb - 1) / wpb));
+}
+
+constexpr size_t kTileLds = (size_t)pix::kWavesPerBlock * pix::kTileWords * 4;
+constexpr size_t kMaxBlockLds = 64 * 1024;
+
+// Plan of a call with packed activations: the LDS holds the output tiles.
+void plan_pix(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
+              const Requant* rq, pix::PixArgs* g, dim3* grid, size_t* lds) {
+    *lds = kTileLds;
+    plan_pix_lds(s, fn, forced_run, rq, g, grid, *lds);
+}
+
+// Plan of a staged call: the LDS also holds the block's packed input region
+// plus one zero pixel, whose size depends on the run length, which depends
+// on residency, which depends on the LDS: re-plan until the residency the
+// plan assumed is the one its LDS allows.  False when the region does not
+// fit a block's LDS.
+bool plan_pix_staged(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
+                     pix::PixArgs* g, dim3* grid, size_t* lds) {
+    const size_t pwb = (size_t)s.abits * ((s.c + 31) / 32) * 4;
+    size_t assumed = kTileLds;
+    int run = forced_run;
+    for (int iter = 0; iter < 24; ++iter) {
+        plan_pix_lds(s, fn, run, nullptr, g, grid, assumed);
+        const int64_t region = max_region_pixels(s, *g);
+        const size_t need = kTileLds + (size_t)(region + 1) * pwb;
+        if (need > kMaxBlockLds) {
+            // a block's rows do not fit: shorter runs (fewer pixels per
+            // block), unless the caller fixed the run length
+            if (forced_run > 0 || g->per_wave <= 1) return false;
+            run = g->per_wave / 2;
+            continue;
+        }
+        g->region_pixels = (int32_t)region;
+        *lds = need;
+        if (need <= assumed ||
+            resident_blocks(fn, need) >= resident_blocks(fn, assumed))
+            return true;
+        assumed = need;
+    }
+    return false;
 }
 
 // Launch configuration of a channels-on-lanes call.
@@ -420,6 +514,52 @@ hipError_t launch_pix(const ConvShape& s, pix::PixKernelFn fn,
     return hipSuccess;
 }
 
+// Staged launch: activations given as uint8 codes or float32 values
+// (src = pix::kSrcCodes / kSrcFloat, NHWC [n][h][w][c]) are bit-packed into
+// each block's LDS by the conv kernel itself.  Every image chunk is planned
+// before anything is enqueued; hipErrorNotSupported (nothing enqueued) when
+// no staged kernel or no fitting plan exists.
+hipError_t launch_pix_staged(const ConvShape& s, int src, const void* act,
+                             float scale, const uint32_t* wts, int32_t* out,
+                             int forced_run, hipStream_t st) {
+    pix::PlanInfo info{};
+    const pix::PixKernelFn fn = pix_kernel_for(s, false, src, &info);
+    if (!fn) return hipErrorNotSupported;
+    const int64_t per = pix_images_per_launch(s, false);
+    const float qmax = s.aenc == kSigned ? (float)((1 << (s.abits - 1)) - 1)
+                                         : (float)((1 << s.abits) - 1);
+    struct Chunk {
+        int64_t n0;
+        pix::PixArgs g;
+        dim3 grid;
+        size_t lds;
+    };
+    std::vector<Chunk> chunks;
+    for (int64_t n0 = 0; n0 < s.n; n0 += per) {
+        ConvShape c = s;
+        c.n = (int32_t)(s.n - n0 < per ? s.n - n0 : per);
+        Chunk ch;
+        ch.n0 = n0;
+        if (!plan_pix_staged(c, fn, forced_run, &ch.g, &ch.grid, &ch.lds))
+            return hipErrorNotSupported;
+        ch.g.in_scale = scale;
+        ch.g.in_qmax = qmax;
+        chunks.push_back(ch);
+    }
+    const int64_t in_img = (int64_t)s.h * s.w * s.c *
+                           (src == pix::kSrcFloat ? 4 : 1);
+    const int64_t out_img = (int64_t)s.oh * s.ow * s.oc;
+    for (const Chunk& ch : chunks) {
+        const uint32_t* a = reinterpret_cast<const uint32_t*>(
+            static_cast<const char*>(act) + ch.n0 * in_img);
+        int32_t* o = out + ch.n0 * out_img;
+        const hipError_t e = launch(fn, ch.grid, dim3(pix::kBlock), ch.lds, st,
+                                    a, wts, o, ch.g);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 enum class Family { kPixels, kChannels, kGeneric };
 
 // The kernel family a call takes: mode 0 tries pixels-on-lanes, then
@@ -428,7 +568,8 @@ enum class Family { kPixels, kChannels, kGeneric };
 Family choose(const ConvShape& s, int mode, pix::PixKernelFn* pfn,
               pix::PlanInfo* info) {
     if (mode == 0 || mode == 3) {
-        if ((*pfn = pix_kernel_for(s, false, info)) != nullptr)
+        if ((*pfn = pix_kernel_for(s, false, pix::kSrcPacked, info)) !=
+            nullptr)
             return Family::kPixels;
     }
     if ((mode == 0 || mode == 2) && conv_has_fast_path(s))
@@ -474,7 +615,8 @@ hipError_t launch_conv_requant(const ConvShape& s, const uint32_t* act,
     // the pixels-on-lanes kernel (modes 0 and 3), else plain loops
     pix::PlanInfo info{};
     pix::PixKernelFn pfn = nullptr;
-    if (opt.mode == 0 || opt.mode == 3) pfn = pix_kernel_for(s, true, &info);
+    if (opt.mode == 0 || opt.mode == 3)
+        pfn = pix_kernel_for(s, true, pix::kSrcPacked, &info);
     if (pfn) {
         // the run-length override counts packed bytes (2 quads) here
         return launch_pix(s, pfn, act, wts, reinterpret_cast<int32_t*>(out),
@@ -499,6 +641,14 @@ hipError_t launch_conv_requant(const ConvShape& s, const uint32_t* act,
     if (blocks < 1) blocks = 1;
     return launch(conv_generic_requant_kernel, dim3((uint32_t)blocks),
                   dim3(kBlock), 0, st, g);
+}
+
+hipError_t launch_conv_staged(const ConvShape& s, bool from_float,
+                              const void* act, float scale,
+                              const uint32_t* wts, int32_t* out,
+                              const ConvOptions& opt, hipStream_t st) {
+    return launch_pix_staged(s, from_float ? pix::kSrcFloat : pix::kSrcCodes,
+                             act, scale, wts, out, opt.units_per_wave, st);
 }
 
 int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,

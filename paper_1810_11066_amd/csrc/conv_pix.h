@@ -106,7 +106,23 @@ struct PixArgs {
     int32_t c;             // input channels (+-1 activations only)
     int32_t act_bytes;     // size of the packed activations, bytes
     int32_t out_bytes;     // size of the int32 output, bytes (0: packed out)
+    // activations staged in LDS (SRC != kSrcPacked): the most input pixels
+    // any block's region holds (its LDS size), and the quantizer of float
+    // activations
+    int32_t region_pixels;
+    float in_scale, in_qmax;
 };
+
+// Where a specialisation's activations come from:
+//   kSrcPacked  bit-packed words [n][h][w][A][CW] in HBM (bs_pack output);
+//   kSrcCodes   uint8 codes [n][h][w][C], C = 32 CW: each block bit-packs the
+//               input rows its outputs read into LDS first;
+//   kSrcFloat   float32 values [n][h][w][C]: quantized (the activation
+//               encoding's quantizer) and bit-packed into LDS the same way.
+// The staged forms never write the packed activations to HBM: the separate
+// pack launch and its round trip are gone, at the price of packing each
+// block's halo rows again.
+constexpr int kSrcPacked = 0, kSrcCodes = 1, kSrcFloat = 2;
 
 __device__ __forceinline__ void bcnt_acc(uint32_t& acc, uint32_t x) {
     asm("v_bcnt_u32_b32 %0, %1, %0" : "+v"(acc) : "v"(x));
@@ -496,6 +512,162 @@ struct Window {
     int iy0, ix0;
 };
 
+// ---- staged activations ---------------------------------------------------
+
+// Bit-planes 0..A-1 of 32 codes held as bytes in d[0..7] (code 4 m + k in
+// byte k of d[m]): bit u of plane word b is bit b of code u.  Per plane and
+// dword, the plane's bits are masked (bit b of each byte) and one
+// v_dot4_u32_u8 against the byte weights 2^k (or 2^(4+k) for the second
+// dword of a pair) adds them, shifted by b, into one byte of 8 codes; four
+// such bytes make the word.
+template <int A>
+__device__ __forceinline__ void pack32_planes(const uint32_t (&d)[8],
+                                              uint32_t (&w)[A]) {
+#pragma unroll
+    for (int b = 0; b < A; ++b) {
+        const uint32_t m = 0x01010101u << b;
+        uint32_t byte[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            byte[j] = __builtin_amdgcn_udot4(d[2 * j] & m, 0x08040201u, 0u,
+                                             false);
+            byte[j] = __builtin_amdgcn_udot4(d[2 * j + 1] & m, 0x80402010u,
+                                             byte[j], false);
+        }
+        // byte[j] holds codes 8 j .. 8 j + 7 at bits b .. b + 7
+        const uint32_t lo24 = byte[0] | byte[1] << 8 | byte[2] << 16;
+        w[b] = (lo24 >> b) | (byte[3] >> b) << 24;
+    }
+}
+
+// Codes of 32 float32 activations in bytes (code 4 m + k in byte k of d[m]),
+// under the activation encoding's quantizer (bs_quantize's reading): one
+// binary32 multiply, round half to even, clamp; bipolar: x >= 0.
+template <int AE>
+__device__ __forceinline__ void quantize32(const float (&x)[32], float scale,
+                                           float qmax, uint32_t (&d)[8]) {
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+        uint32_t v = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            v |= quant_code_enc<AE>(x[4 * m + k], scale, qmax) << (8 * k);
+        d[m] = v;
+    }
+}
+
+// Input region of a block: the flat NHWC input pixels [lo, hi) that hold
+// every in-range tap of the block's output pixels, from the first tap row of
+// its first output pixel to the last tap row of its last one.
+struct Region {
+    int32_t lo, hi;
+};
+
+template <int K, int S>
+__device__ __forceinline__ Region block_region(const PixArgs& g, int p_first,
+                                               int p_last) {
+    const uint32_t r0 = g.div_ow.div((uint32_t)p_first);
+    const uint32_t n0 = g.div_oh.div(r0), y0 = r0 - n0 * (uint32_t)g.oh;
+    const uint32_t r1 = g.div_ow.div((uint32_t)p_last);
+    const uint32_t n1 = g.div_oh.div(r1), y1 = r1 - n1 * (uint32_t)g.oh;
+    // first and last input row of the block's taps, clamped to [0, h] and
+    // [-1, h - 1]: with padding above K - 1 an output row can lie wholly in
+    // the padding, and its image then contributes no row (row h of image
+    // n0 is row 0 of image n0 + 1; row -1 of image n1 ends image n1 - 1)
+    const int iy_lo = min(max((int)y0 * S - g.ph, 0), g.h);
+    const int iy_hi = max(min((int)y1 * S - g.ph + K - 1, g.h - 1), -1);
+    Region rg;
+    rg.lo = ((int)n0 * g.h + iy_lo) * g.w;
+    rg.hi = ((int)n1 * g.h + iy_hi) * g.w + g.w;
+    // an all-padding block (no in-range tap) holds nothing; the host sized
+    // the LDS for the largest region, which bounds every block's
+    rg.hi = min(max(rg.hi, rg.lo), rg.lo + g.region_pixels);
+    return rg;
+}
+
+// Fills the block's region in LDS: packed words [pixel - lo][A][CW] of the
+// input pixels [lo, hi), then one pixel of zeros (what the taps in the
+// padding read).  Each thread packs (pixel, word) items of 32 codes; the
+// loads of consecutive threads are consecutive 32-byte (codes) or 128-byte
+// (floats) pieces of the NHWC rows.
+template <int A, int AE, int CW, int SRC>
+__device__ __forceinline__ void stage_region(uint32_t* __restrict__ region,
+                                             const void* __restrict__ src,
+                                             const PixArgs& g, Region rg) {
+    constexpr int PW = A * CW;                 // words per packed pixel
+    const int items = (rg.hi - rg.lo) * CW;
+    for (int it = threadIdx.x; it < items; it += kBlock) {
+        const int pl = it / CW, t = it - pl * CW;
+        const size_t first = ((size_t)(rg.lo + pl) * CW + t) * 32;  // code
+        uint32_t d[8];
+        if constexpr (SRC == kSrcCodes) {
+            const uint4* q = reinterpret_cast<const uint4*>(
+                static_cast<const uint8_t*>(src) + first);
+            const uint4 a = q[0], b = q[1];
+            d[0] = a.x; d[1] = a.y; d[2] = a.z; d[3] = a.w;
+            d[4] = b.x; d[5] = b.y; d[6] = b.z; d[7] = b.w;
+        } else {
+            const float4* q = reinterpret_cast<const float4*>(
+                static_cast<const float*>(src) + first);
+            float x[32];
+#pragma unroll
+            for (int m = 0; m < 8; ++m) {
+                const float4 v = q[m];
+                x[4 * m] = v.x; x[4 * m + 1] = v.y;
+                x[4 * m + 2] = v.z; x[4 * m + 3] = v.w;
+            }
+            quantize32<AE>(x, g.in_scale, g.in_qmax, d);
+        }
+        uint32_t w[A];
+        pack32_planes<A>(d, w);
+#pragma unroll
+        for (int b = 0; b < A; ++b) region[pl * PW + b * CW + t] = w[b];
+    }
+    const int zero = (rg.hi - rg.lo) * PW;
+    for (int i = threadIdx.x; i < PW; i += kBlock) region[zero + i] = 0;
+}
+
+// Loads the lane's whole patch from the staged region: the same taps and
+// words as load_patch, at byte offsets relative to the region (win.base is
+// relative to its first pixel; a tap in the padding reads the zero pixel at
+// byte offset zero_off).
+template <int A, int K, int CW>
+__device__ __forceinline__ void load_patch_lds(
+    uint32_t (&patch)[K * K][A][CW], const uint32_t* __restrict__ region,
+    const PixArgs& g, const Window& win, uint32_t zero_off) {
+    constexpr uint32_t PWB = 4 * A * CW;
+    const uint32_t rowb = (uint32_t)g.w * PWB;
+    const char* base = reinterpret_cast<const char*>(region);
+#pragma unroll
+    for (int t = 0; t < K * K; ++t) {
+        const int r = t / K, s = t - r * K;
+        const bool in = (unsigned)(win.iy0 + r) < (unsigned)g.h &&
+                        (unsigned)(win.ix0 + s) < (unsigned)g.w;
+        const uint32_t off =
+            in ? win.base + (uint32_t)r * rowb + (uint32_t)s * PWB : zero_off;
+#pragma unroll
+        for (int i = 0; i < A; ++i) {
+            const char* p = base + off + 4u * (uint32_t)(i * CW);
+            if constexpr (CW % 4 == 0) {
+#pragma unroll
+                for (int k = 0; k < CW; k += 4) {
+                    const uint4 x = *reinterpret_cast<const uint4*>(p + 4 * k);
+                    patch[t][i][k] = x.x; patch[t][i][k + 1] = x.y;
+                    patch[t][i][k + 2] = x.z; patch[t][i][k + 3] = x.w;
+                }
+            } else if constexpr (CW % 2 == 0) {
+#pragma unroll
+                for (int k = 0; k < CW; k += 2) {
+                    const uint2 x = *reinterpret_cast<const uint2*>(p + 4 * k);
+                    patch[t][i][k] = x.x; patch[t][i][k + 1] = x.y;
+                }
+            } else {
+                patch[t][i][0] = *reinterpret_cast<const uint32_t*>(p);
+            }
+        }
+    }
+}
+
 // Loads the lane's input words of one reduction block: taps [t0, t0 + TB)
 // of the window and words [c0, c0 + CB) of each of the A planes (zero for
 // taps in the padding: their offset is out of the buffer's range).
@@ -694,8 +866,9 @@ constexpr int min_waves_per_simd() {
 // A, W: bit-widths; E: operand encodings (Enc); K: square kernel size;
 // S: stride; CW: words per bit-plane; REQ: requantize and bit-pack the output
 // (out then holds [npix][out_bits][out_words] uint32 words) instead of
-// storing int32.
-template <int A, int W, int E, int K, int S, int CW, bool REQ>
+// storing int32; SRC: where the activations come from (kSrcPacked, or
+// staged in LDS from kSrcCodes / kSrcFloat, whole patches only).
+template <int A, int W, int E, int K, int S, int CW, bool REQ, int SRC>
 __global__ __launch_bounds__(kBlock) __attribute__((
     amdgpu_num_sgpr(96),
     amdgpu_waves_per_eu(min_waves_per_simd<A, W, E, K, CW, REQ>())))
@@ -704,6 +877,8 @@ void conv_pix_kernel(
     int32_t* __restrict__ out, PixArgs g) {
     using Pl = Plan<A, W, K, CW>;
     constexpr int FW = Pl::FW, NB = Pl::NB;
+    static_assert(SRC == kSrcPacked || (NB == 1 && !REQ),
+                  "staged activations: whole patches, int32 output");
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(
         (int)(xcd_block() * kWavesPerBlock + (threadIdx.x >> 6)));
@@ -716,6 +891,28 @@ void conv_pix_kernel(
     gu32* gw = (gu32*)(wts);
     const Rsrc ract = make_rsrc(act, g.act_bytes);
     const Rsrc rout = make_rsrc(out, g.out_bytes);
+
+    // staged activations: the block packs its input region into LDS (after
+    // the waves' output tiles) before any wave computes; every wave of the
+    // block takes part, also one whose own run is empty
+    [[maybe_unused]] const uint32_t* region = lds + kWavesPerBlock * kTileWords;
+    [[maybe_unused]] int32_t region_lo = 0;
+    [[maybe_unused]] uint32_t zero_off = 0;
+    if constexpr (SRC != kSrcPacked) {
+        const int per_block = kWavesPerBlock * g.per_wave;
+        const int ub0 = xcd_block() * per_block;
+        if (ub0 >= g.units) return;            // the whole block is idle
+        const int ub1 = min(ub0 + per_block, g.units);
+        const int p_first = (int)g.div_units.div((uint32_t)ub0) * 64;
+        const int p_last = min(
+            (int)g.div_units.div((uint32_t)(ub1 - 1)) * 64 + 63, g.npix - 1);
+        const Region rg = block_region<K, S>(g, p_first, p_last);
+        stage_region<A, Enc<E>::AE, CW, SRC>(
+            lds + kWavesPerBlock * kTileWords, act, g, rg);
+        region_lo = rg.lo;
+        zero_off = (uint32_t)(rg.hi - rg.lo) * (uint32_t)(4 * A * CW);
+        __syncthreads();
+    }
 
     // one group visit: the run's units in the current 64-pixel group
     auto visit_at = [&](int u0) {
@@ -736,7 +933,8 @@ void conv_pix_kernel(
         v.win.iy0 = v.oy * S - g.ph;
         v.win.ix0 = v.ox * S - g.pw;
         v.win.base = ((img * (uint32_t)g.h + (uint32_t)v.win.iy0) *
-                          (uint32_t)g.w + (uint32_t)v.win.ix0) *
+                          (uint32_t)g.w + (uint32_t)v.win.ix0 -
+                      (uint32_t)region_lo) *
                      (uint32_t)(4 * A * CW);
         if constexpr (!REQ) v.fm.init(v.pix0, g.npix, g.oc);
         return v;
@@ -748,14 +946,17 @@ void conv_pix_kernel(
         // words are requested before this visit's last stores: vmcnt counts
         // loads and stores in order, so a load issued after them would wait
         // for their completion (and the HBM-bound 1x1 layers would stall).
-        constexpr bool kAhead = Pl::PB <= kAheadWords;
+        constexpr bool kAhead = Pl::PB <= kAheadWords && SRC == kSrcPacked;
         // flushes run while the patch is held: keep their registers few
         // when the patch is large (all four rounds hoisted cost 4-9 VGPRs)
         constexpr bool kSerialFlush = Pl::PB > 32;
         if (u >= u_end) return;
         Visit v = visit_at(u);
         uint32_t patch[Pl::TB][A][CW];
-        load_patch<A, K, CW, Pl::TB, CW>(patch, ract, g, v.win, 0, 0);
+        if constexpr (SRC != kSrcPacked)
+            load_patch_lds<A, K, CW>(patch, region, g, v.win, zero_off);
+        else
+            load_patch<A, K, CW, Pl::TB, CW>(patch, ract, g, v.win, 0, 0);
         if constexpr (kAhead && !REQ) {
             // an empty flush (every store out of range): the loop is then
             // entered, as it is re-entered, with the patch load followed by
@@ -853,7 +1054,12 @@ void conv_pix_kernel(
                         for (int c = 0; c < CW; ++c) patch[t][i][c] = pn[t][i][c];
             } else {
                 v = visit_at(u);
-                load_patch<A, K, CW, Pl::TB, CW>(patch, ract, g, v.win, 0, 0);
+                if constexpr (SRC != kSrcPacked)
+                    load_patch_lds<A, K, CW>(patch, region, g, v.win,
+                                             zero_off);
+                else
+                    load_patch<A, K, CW, Pl::TB, CW>(patch, ract, g, v.win, 0,
+                                                     0);
             }
         }
     } else {
@@ -957,14 +1163,18 @@ struct PlanInfo {
 //                      same width, int32 output;
 //   pick_bipolar_act   +-1 activations with 1-bit filters, int32 output.
 PixKernelFn pick(int a, int w, int ae, int we, int k, int s, int cw, bool req,
-                 PlanInfo* info);
+                 int src, PlanInfo* info);
 template <int A>
-PixKernelFn pick_a(int w, bool b, int k, int s, int cw, bool req,
+PixKernelFn pick_a(int w, bool b, int k, int s, int cw, bool req, int src,
                    PlanInfo* info);
-template <> PixKernelFn pick_a<1>(int, bool, int, int, int, bool, PlanInfo*);
-template <> PixKernelFn pick_a<2>(int, bool, int, int, int, bool, PlanInfo*);
-template <> PixKernelFn pick_a<3>(int, bool, int, int, int, bool, PlanInfo*);
-template <> PixKernelFn pick_a<4>(int, bool, int, int, int, bool, PlanInfo*);
+template <> PixKernelFn pick_a<1>(int, bool, int, int, int, bool, int,
+                                  PlanInfo*);
+template <> PixKernelFn pick_a<2>(int, bool, int, int, int, bool, int,
+                                  PlanInfo*);
+template <> PixKernelFn pick_a<3>(int, bool, int, int, int, bool, int,
+                                  PlanInfo*);
+template <> PixKernelFn pick_a<4>(int, bool, int, int, int, bool, int,
+                                  PlanInfo*);
 template <int A>
 PixKernelFn pick_signed(int w, int ae, int we, int k, int s, int cw,
                         PlanInfo* info);
@@ -975,10 +1185,14 @@ template <> PixKernelFn pick_signed<4>(int, int, int, int, int, int, PlanInfo*);
 PixKernelFn pick_bipolar_act(int we, int k, int s, int cw, PlanInfo* info);
 
 // Specialisations (included by the sources above).  Requantizing variants
-// exist for unipolar activations with unipolar or bipolar filters only.
+// exist for unipolar activations with unipolar or bipolar filters only;
+// staged activations (src != kSrcPacked) for unipolar activations with
+// unipolar filters of 1 or 2 bits or bipolar 1-bit filters, whole patches,
+// int32 output.
 template <int A, int W, int E, int K, int S, int CW>
-PixKernelFn pick_kscw(bool req, PlanInfo* info) {
+PixKernelFn pick_kscw(bool req, int src, PlanInfo* info) {
     using Pl = Plan<A, W, K, CW>;
+    constexpr int UU = 3 * kUnipolar + kUnipolar, UB = 3 * kUnipolar + kBipolar;
     if constexpr (!Pl::kFits) {
         return nullptr;
     } else {
@@ -987,32 +1201,44 @@ PixKernelFn pick_kscw(bool req, PlanInfo* info) {
         info->tb = Pl::TB;
         info->cb = Pl::CB;
         info->enc = E;
-        if constexpr (E == 3 * kUnipolar + kUnipolar ||
-                      E == 3 * kUnipolar + kBipolar)
-            return req ? conv_pix_kernel<A, W, E, K, S, CW, true>
-                       : conv_pix_kernel<A, W, E, K, S, CW, false>;
+        if (src != kSrcPacked) {
+            if constexpr (Pl::NB == 1 && (E == UU || E == UB) && W <= 2) {
+                if (req) return nullptr;
+                return src == kSrcCodes
+                           ? conv_pix_kernel<A, W, E, K, S, CW, false,
+                                             kSrcCodes>
+                           : conv_pix_kernel<A, W, E, K, S, CW, false,
+                                             kSrcFloat>;
+            } else {
+                return nullptr;
+            }
+        }
+        if constexpr (E == UU || E == UB)
+            return req ? conv_pix_kernel<A, W, E, K, S, CW, true, kSrcPacked>
+                       : conv_pix_kernel<A, W, E, K, S, CW, false, kSrcPacked>;
         else
-            return req ? nullptr : conv_pix_kernel<A, W, E, K, S, CW, false>;
+            return req ? nullptr
+                       : conv_pix_kernel<A, W, E, K, S, CW, false, kSrcPacked>;
     }
 }
 
 // Words per plane: 1..16 for 3x3 windows; 1x1 windows (and dense, a 1x1
 // conv) up to 128 words = 4096 input channels.
 template <int A, int W, int E, int K, int S>
-PixKernelFn pick_cw(int cw, bool req, PlanInfo* info) {
+PixKernelFn pick_cw(int cw, bool req, int src, PlanInfo* info) {
     switch (cw) {
-        case 1: return pick_kscw<A, W, E, K, S, 1>(req, info);
-        case 2: return pick_kscw<A, W, E, K, S, 2>(req, info);
-        case 4: return pick_kscw<A, W, E, K, S, 4>(req, info);
-        case 8: return pick_kscw<A, W, E, K, S, 8>(req, info);
-        case 16: return pick_kscw<A, W, E, K, S, 16>(req, info);
+        case 1: return pick_kscw<A, W, E, K, S, 1>(req, src, info);
+        case 2: return pick_kscw<A, W, E, K, S, 2>(req, src, info);
+        case 4: return pick_kscw<A, W, E, K, S, 4>(req, src, info);
+        case 8: return pick_kscw<A, W, E, K, S, 8>(req, src, info);
+        case 16: return pick_kscw<A, W, E, K, S, 16>(req, src, info);
         default: break;
     }
     if constexpr (K == 1) {
         switch (cw) {
-            case 32: return pick_kscw<A, W, E, K, S, 32>(req, info);
-            case 64: return pick_kscw<A, W, E, K, S, 64>(req, info);
-            case 128: return pick_kscw<A, W, E, K, S, 128>(req, info);
+            case 32: return pick_kscw<A, W, E, K, S, 32>(req, src, info);
+            case 64: return pick_kscw<A, W, E, K, S, 64>(req, src, info);
+            case 128: return pick_kscw<A, W, E, K, S, 128>(req, src, info);
             default: break;
         }
     }
@@ -1020,26 +1246,27 @@ PixKernelFn pick_cw(int cw, bool req, PlanInfo* info) {
 }
 
 template <int A, int W, int E>
-PixKernelFn pick_ks(int k, int s, int cw, bool req, PlanInfo* info) {
-    if (k == 1) return s == 1 ? pick_cw<A, W, E, 1, 1>(cw, req, info)
-                              : pick_cw<A, W, E, 1, 2>(cw, req, info);
-    if (k == 3) return s == 1 ? pick_cw<A, W, E, 3, 1>(cw, req, info)
-                              : pick_cw<A, W, E, 3, 2>(cw, req, info);
+PixKernelFn pick_ks(int k, int s, int cw, bool req, int src, PlanInfo* info) {
+    if (k == 1) return s == 1 ? pick_cw<A, W, E, 1, 1>(cw, req, src, info)
+                              : pick_cw<A, W, E, 1, 2>(cw, req, src, info);
+    if (k == 3) return s == 1 ? pick_cw<A, W, E, 3, 1>(cw, req, src, info)
+                              : pick_cw<A, W, E, 3, 2>(cw, req, src, info);
     return nullptr;
 }
 
 // Unipolar activations: every weight width 1..4 with unipolar weights;
 // bipolar weights at W = 1.
 template <int A>
-PixKernelFn pick_for_a(int w, bool b, int k, int s, int cw, bool req,
+PixKernelFn pick_for_a(int w, bool b, int k, int s, int cw, bool req, int src,
                        PlanInfo* info) {
     constexpr int UU = 3 * kUnipolar + kUnipolar, UB = 3 * kUnipolar + kBipolar;
-    if (b) return w == 1 ? pick_ks<A, 1, UB>(k, s, cw, req, info) : nullptr;
+    if (b) return w == 1 ? pick_ks<A, 1, UB>(k, s, cw, req, src, info)
+                         : nullptr;
     switch (w) {
-        case 1: return pick_ks<A, 1, UU>(k, s, cw, req, info);
-        case 2: return pick_ks<A, 2, UU>(k, s, cw, req, info);
-        case 3: return pick_ks<A, 3, UU>(k, s, cw, req, info);
-        case 4: return pick_ks<A, 4, UU>(k, s, cw, req, info);
+        case 1: return pick_ks<A, 1, UU>(k, s, cw, req, src, info);
+        case 2: return pick_ks<A, 2, UU>(k, s, cw, req, src, info);
+        case 3: return pick_ks<A, 3, UU>(k, s, cw, req, src, info);
+        case 4: return pick_ks<A, 4, UU>(k, s, cw, req, src, info);
         default: return nullptr;
     }
 }
@@ -1053,15 +1280,17 @@ PixKernelFn pick_signed_for_a(int w, int ae, int we, int k, int s, int cw,
     if (we != kSigned) return nullptr;
     if (ae == kSigned) {
         if constexpr (A >= 2)
-            return w == A ? pick_ks<A, A, SS>(k, s, cw, false, info) : nullptr;
+            return w == A ? pick_ks<A, A, SS>(k, s, cw, false, kSrcPacked,
+                                              info)
+                          : nullptr;
         else
             return nullptr;
     }
     if (ae != kUnipolar) return nullptr;
     switch (w) {
-        case 2: return pick_ks<A, 2, US>(k, s, cw, false, info);
-        case 3: return pick_ks<A, 3, US>(k, s, cw, false, info);
-        case 4: return pick_ks<A, 4, US>(k, s, cw, false, info);
+        case 2: return pick_ks<A, 2, US>(k, s, cw, false, kSrcPacked, info);
+        case 3: return pick_ks<A, 3, US>(k, s, cw, false, kSrcPacked, info);
+        case 4: return pick_ks<A, 4, US>(k, s, cw, false, kSrcPacked, info);
         default: return nullptr;
     }
 }

@@ -41,7 +41,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_words(lib):
-    assert lib.bs_abi_version() == 105
+    assert lib.bs_abi_version() == 106
     for k, w in [(0, 0), (1, 1), (31, 1), (32, 1), (33, 2), (4096, 128)]:
         assert lib.bs_packed_words(k) == w
 
@@ -154,6 +154,50 @@ def test_conv_pointer_validation(lib):
                          STREAM) == bs.BS_ERR_INVALID_ARG
     assert lib.bs_conv2d(None, FAKE, FAKE, FAKE,
                          STREAM) == bs.BS_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("bad,status", [
+    (dict(n=0), bs.BS_ERR_INVALID_ARG),
+    (dict(kh=11, pad_h=1), bs.BS_ERR_INVALID_ARG),
+    (dict(wenc=-1), bs.BS_ERR_INVALID_ARG),
+    (dict(abits=8, wbits=8, c=(1 << 31) // (255 * 255 * 9) + 1),
+     bs.BS_ERR_OVERFLOW),
+    # shapes no fused kernel covers: refused before any launch
+    (dict(c=48), bs.BS_ERR_UNSUPPORTED),            # c not a multiple of 32
+    (dict(oc=6), bs.BS_ERR_UNSUPPORTED),            # oc not a multiple of 4
+    (dict(kh=5, kw=5, pad_h=2, pad_w=2), bs.BS_ERR_UNSUPPORTED),
+    (dict(wbits=3), bs.BS_ERR_UNSUPPORTED),
+    (dict(aenc=2, wenc=2, wbits=2), bs.BS_ERR_UNSUPPORTED),  # signed
+    (dict(c=256), bs.BS_ERR_UNSUPPORTED),           # 144-word 3x3 window
+])
+def test_fused_conv_validation(lib, bad, status):
+    # disjoint fake buffers, so that the overlap check passes
+    p = params(**bad)
+    act, wts, out = at(0), at(1 << 26), at(1 << 28)
+    assert lib.bs_conv2d_codes(ctypes.byref(p), act, wts, out,
+                               STREAM) == status
+    assert lib.bs_last_error() != b""
+    assert lib.bs_quantize_conv2d(ctypes.byref(p), act, 1.0, wts, out,
+                                  STREAM) == status
+    assert lib.bs_last_error() != b""
+
+
+def test_fused_conv_pointer_and_scale_validation(lib):
+    p = params()
+    assert lib.bs_conv2d_codes(ctypes.byref(p), NULL, FAKE, FAKE,
+                               STREAM) == bs.BS_ERR_INVALID_ARG
+    assert lib.bs_conv2d_codes(ctypes.byref(p), MISALIGNED, FAKE, FAKE,
+                               STREAM) == bs.BS_ERR_INVALID_ARG
+    for scale in (0.0, -1.0, float("inf"), float("nan")):
+        assert lib.bs_quantize_conv2d(ctypes.byref(p), FAKE, scale, FAKE,
+                                      FAKE, STREAM) == bs.BS_ERR_INVALID_ARG
+    # the output may not overlap the codes (n*h*w*c bytes) or the floats
+    assert lib.bs_conv2d_codes(ctypes.byref(p), at(0), FAKE, at(4096 - 16),
+                               STREAM) == bs.BS_ERR_INVALID_ARG
+    assert b"overlaps" in lib.bs_last_error()
+    assert lib.bs_quantize_conv2d(ctypes.byref(p), at(0), 1.0, at(1 << 20),
+                                  at(16384 - 16),
+                                  STREAM) == bs.BS_ERR_INVALID_ARG
 
 
 def at(offset):
