@@ -235,15 +235,14 @@ def prepare(case, n_sets, bs, torch, np, fused=False):
     arrays (rolled along the batch axis for sets beyond the first); weights
     are packed once, outside the timed steps.
 
-    fused: the step is one call that bit-packs (and quantizes) the
-    activations inside the conv kernel (bs_conv2d_codes /
-    bs_quantize_conv2d) instead of bs_pack / bs_quantize_pack followed by
-    bs_conv2d; None is returned when the fused kernels do not cover the
-    case."""
+    fused: the step is one call that bit-packs the uint8 activation codes
+    inside the conv kernel (bs_conv2d_codes) instead of bs_pack followed by
+    bs_conv2d; None is returned when the fused kernels do not cover the case
+    (dense, float32 activations quantized per call, other shapes)."""
     from paper_1810_11066_amd import workloads as wl
     stream = torch.cuda.current_stream()
     dense = isinstance(case, wl.DenseCase)
-    if dense and fused:
+    if fused and (dense or case.act_scale is not None):
         return None
     if dense:
         rows, k, abits = case.m, case.k, case.abits
@@ -289,9 +288,6 @@ def prepare(case, n_sets, bs, torch, np, fused=False):
         if dense:
             bs.bs_dense(case.m, case.n, case.k, case.abits, case.wbits,
                         bs.UNIPOLAR, packed, w_packed, out, stream)
-        elif fused and quantized:
-            bs.bs_quantize_conv2d(params, x, case.act_scale, w_packed, out,
-                                  stream)
         elif fused:
             bs.bs_conv2d_codes(params, x, w_packed, out, stream)
         else:
@@ -337,8 +333,7 @@ def prepare(case, n_sets, bs, torch, np, fused=False):
     else:
         describe = bs.bs_conv2d_describe(params)
     if fused:
-        describe = ("staged activations (%s into LDS): " % (
-            "quantize + bit-pack" if quantized else "bit-pack") + describe)
+        describe = "activation codes bit-packed into LDS: " + describe
     # initialisation: one step per set writes every packed and output buffer
     # once, so that no buffer is first written inside a timed region
     for i in range(n_sets):
@@ -490,9 +485,7 @@ def per_step_name(case, fused):
     from paper_1810_11066_amd import workloads as wl
     q = getattr(case, "act_scale", None) is not None
     if fused:
-        return ("bs_quantize_conv2d (quantize + bit-pack of the float32 "
-                "activations inside the conv kernel)" if q else
-                "bs_conv2d_codes (bit-pack of the uint8 activation codes "
+        return ("bs_conv2d_codes (bit-pack of the uint8 activation codes "
                 "inside the conv kernel)")
     return ("bs_quantize_pack" if q else "bs_pack") + "(activations) + " + \
         ("bs_dense" if isinstance(case, wl.DenseCase) else "bs_conv2d")
@@ -503,7 +496,8 @@ def case_line(case, m, args, mu=None):
     m: the step as timed (the fused call where it covers the case); mu: the
     unfused step (pack + conv) of the same case, when m is fused."""
     ops = 2 * case.macs
-    pre_bytes, main_bytes = case_bytes(case, fused=mu is not None)
+    fused = m.describe.startswith("activation codes")
+    pre_bytes, main_bytes = case_bytes(case, fused=fused)
     line = {
         "metric": "bitserial conv2d effective GOPS (2*MACs/s) + % of "
                   "popcount-VALU roofline",
@@ -513,7 +507,7 @@ def case_line(case, m, args, mu=None):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "u32", "data": "synthetic",
         "config": {"workload": case.name,
-                   "per_step": per_step_name(case, mu is not None),
+                   "per_step": per_step_name(case, fused),
                    "abits": case.abits, "wbits": case.wbits,
                    "encoding": ENC_NAMES[getattr(case, "wenc", 0)],
                    "act_encoding": ENC_NAMES[getattr(case, "aenc", 0)]},
@@ -521,7 +515,7 @@ def case_line(case, m, args, mu=None):
         "pack_roofline": pack_roofline(pre_bytes, m),
         "host_enqueue_ms_per_step": round(m.host_ms, 5),
     }
-    if mu is not None:
+    if mu is not None and mu is not m:
         _, ubytes = case_bytes(case)
         line["unfused"] = {
             "per_step": per_step_name(case, False),
@@ -529,6 +523,99 @@ def case_line(case, m, args, mu=None):
             "value": round(ops / (mu.ms_step * 1e-3) / 1e9, 1),
             "roofline": roofline_of(case, mu, ops, ubytes)}
     return line
+
+
+def pairs_lines(args, bs, torch, np, wl) -> int:
+    """ResNet-18's downsampling pairs (Table 1 layers 4/5, 7/8, 10/11) at
+    batch 128, A2W1: one step quantizes and packs the float32 input, then
+    runs the 3x3 stride-2 conv and its 1x1 stride-2 shortcut -- as one paired
+    launch (bs_conv2d_pair) and, for comparison, as two bs_conv2d launches.
+    One line per pair, with the step and kernel times of both."""
+    layers = {c.name: c for c in wl.config4(batch=args.batch or 128)}
+    stream = torch.cuda.current_stream()
+    for main, short in ((4, 5), (7, 8), (10, 11)):
+        c3 = layers["resnet18_L%d_b%d" % (main, args.batch or 128)]
+        c1 = layers["resnet18_L%d_b%d" % (short, args.batch or 128)]
+        rows = c3.n * c3.h * c3.w
+        spec3 = bs.Conv2dSpec(c3.n, c3.h, c3.w, c3.c, c3.oc, 3, 3, c3.stride,
+                              1, c3.abits, c3.wbits).params()
+        spec1 = bs.Conv2dSpec(c1.n, c1.h, c1.w, c1.c, c1.oc, 1, 1, c1.stride,
+                              0, c1.abits, c1.wbits).params()
+        oh, ow = bs.bs_conv2d_out_shape(spec3)
+        w3 = bs.pack(torch.from_numpy(c3.weights()).cuda(), c3.wbits)
+        w1 = bs.pack(torch.from_numpy(c1.weights()).cuda(), c1.wbits)
+        x_host = c3.activations()
+        per_set = x_host.nbytes + 2 * c3.n * oh * ow * c3.oc * 4
+        n_sets = max(args.sets, min(64, -(-512 * 10**6 // per_set)))
+        sets = []
+        for i in range(n_sets):
+            xi = x_host if i == 0 else np.roll(x_host, i, axis=0)
+            sets.append((torch.from_numpy(np.ascontiguousarray(xi)).cuda(),
+                         torch.empty((rows, c3.abits, bs.words(c3.c)),
+                                     dtype=torch.int32, device="cuda"),
+                         torch.empty((c3.n, oh, ow, c3.oc), dtype=torch.int32,
+                                     device="cuda"),
+                         torch.empty((c3.n, oh, ow, c3.oc), dtype=torch.int32,
+                                     device="cuda")))
+
+        def mk_step(paired):
+            def step(i, ev=None, pack_only=False, dispatch_ev=None):
+                x, packed, o3, o1 = sets[i % n_sets]
+                if not pack_only and dispatch_ev is not None:
+                    bs.bs_set_timing_events(*dispatch_ev[0])
+                bs.bs_quantize_pack(x, packed, rows, c3.c, c3.act_scale,
+                                    c3.abits, bs.UNIPOLAR, stream)
+                if pack_only:
+                    return
+                if ev is not None:
+                    ev[0].record(stream)
+                    ev[1].record(stream)
+                if dispatch_ev is not None:
+                    bs.bs_set_timing_events(*dispatch_ev[1])
+                if paired:
+                    bs.bs_conv2d_pair(spec3, packed, w3, w1, o3, o1, stream)
+                else:
+                    # one pair of dispatch events over both launches: start
+                    # stamped by the first, stop by the last
+                    bs.bs_conv2d(spec3, packed, w3, o3, stream)
+                    bs.bs_conv2d(spec1, packed, w1, o1, stream)
+                if dispatch_ev is not None:
+                    bs.bs_set_timing_events(None, None)
+                if ev is not None:
+                    ev[2].record(stream)
+            step.fused = False
+            return step
+
+        res = {}
+        for paired in (True, False):
+            step = mk_step(paired)
+            for i in range(n_sets):
+                step(i)
+            torch.cuda.synchronize()
+            res[paired] = measure(step, "", args.steps, args.warmup, torch)
+        macs = c3.macs + c1.macs
+        mp, ms = res[True], res[False]
+        print(json.dumps({
+            "pairs": "resnet18 L%d (3x3 s2) + L%d (1x1 s2 shortcut), batch "
+                     "%d, A2W1, float32 input quantized + packed per step"
+                     % (main, short, c3.n),
+            "paired_kernel": bs.bs_conv2d_describe(spec3).split(" patch=")[0]
+                             + " with the centre-tap 1x1 conv (bs_conv2d_pair;"
+                             " runs of 4 units where oc % 16 == 0; 8 words "
+                             "per plane run as two launches)",
+            "paired_ms_per_step": round(mp.ms_step, 5),
+            "separate_ms_per_step": round(ms.ms_step, 5),
+            "paired_conv_ms": round(mp.main_ms, 5),
+            "separate_convs_ms": round(ms.main_ms, 5),
+            "quantize_pack_ms": round(mp.pre_ms, 5),
+            "paired_step_effective_tops": round(
+                2 * macs / (mp.ms_step * 1e-3) / 1e12, 1),
+            "separate_step_effective_tops": round(
+                2 * macs / (ms.ms_step * 1e-3) / 1e12, 1),
+        }), flush=True)
+        del sets
+        torch.cuda.empty_cache()
+    return 0
 
 
 INT8_MFMA_PEAK_TOPS = 5000.0   # dense int8 MFMA, MI355X
@@ -694,10 +781,14 @@ def main() -> int:
                          "512 MB in all)")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="seconds of oracle time for cpu_baseline (0: skip)")
-    ap.add_argument("--unfused", action="store_true",
-                    help="time only the two-kernel step (bs_pack or "
-                         "bs_quantize_pack, then bs_conv2d), not the fused "
-                         "call that packs inside the conv kernel")
+    ap.add_argument("--path", choices=["both", "fused", "unfused"],
+                    default="both",
+                    help="which steps to time: the fused call that bit-packs "
+                         "the activation codes inside the conv kernel "
+                         "(bs_conv2d_codes, where it covers the workload), "
+                         "the two-kernel step (bs_pack or bs_quantize_pack, "
+                         "then bs_conv2d), or both (default; the line's "
+                         "value is the fused step where there is one)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one device copy of this size (for HBM "
                          "counter calibration under rocprofv3 --pmc)")
@@ -714,6 +805,11 @@ def main() -> int:
                          "chained with bs_conv2d_requant: quantize+pack of "
                          "the float input, 15 requantizing convs, one int32 "
                          "conv; one line with the total and per-layer times")
+    ap.add_argument("--pairs", action="store_true",
+                    help="ResNet-18's downsampling pairs (layers 4/5, 7/8, "
+                         "10/11, batch 128): the 3x3 stride-2 conv and its "
+                         "1x1 shortcut as one paired launch against two "
+                         "launches; one line per pair")
     ap.add_argument("--encodings", action="store_true",
                     help="config 5's shapes with +-1 activations and weights "
                          "(XNOR), signed A3W3, and unipolar A2 x signed W2: "
@@ -744,6 +840,8 @@ def main() -> int:
         return int8_baseline_lines(args, bs, torch, np, wl)
     if args.chain:
         return chain_line(args, bs, torch, np, wl)
+    if args.pairs:
+        return pairs_lines(args, bs, torch, np, wl)
 
     if args.sweep or args.encodings or args.config != 2:
         b = {} if args.batch is None else {"batch": args.batch}
@@ -758,22 +856,25 @@ def main() -> int:
         times = {}
         for case in cases:
             n_sets = sets_for(case, args.sets)
-            sets, step, _, _, describe, _ = prepare(case, n_sets, bs, torch,
-                                                    np)
-            mu = measure(step, describe, args.steps, args.warmup, torch)
-            times[(case.abits, case.wbits)] = mu.main_ms
-            del sets, step
-            torch.cuda.empty_cache()
-            fz = None if args.unfused else prepare(case, n_sets, bs, torch,
-                                                   np, fused=True)
+            mu = mf = None
+            if args.path != "fused":
+                sets, step, _, _, describe, _ = prepare(case, n_sets, bs,
+                                                        torch, np)
+                mu = measure(step, describe, args.steps, args.warmup, torch)
+                times[(case.abits, case.wbits)] = mu.main_ms
+                del sets, step
+                torch.cuda.empty_cache()
+            fz = None if args.path == "unfused" else prepare(
+                case, n_sets, bs, torch, np, fused=True)
             if fz is not None:
                 mf = measure(fz[1], fz[4], args.steps, args.warmup, torch)
-                print(json.dumps(case_line(case, mf, args, mu)), flush=True)
                 del fz
                 torch.cuda.empty_cache()
-            else:
+            if mf is not None:
+                print(json.dumps(case_line(case, mf, args, mu)), flush=True)
+            elif mu is not None:
                 print(json.dumps(case_line(case, mu, args)), flush=True)
-        if args.sweep:
+        if args.sweep and len(times) == 16:
             # the paper's limit study quotes W1A1 against W4A4 and W2A2
             # against W1A4 (activation width A, weight width W)
             print(json.dumps({
@@ -786,14 +887,16 @@ def main() -> int:
 
     case = wl.config2(batch=args.batch or 64)
     n_sets = sets_for(case, args.sets)
-    fz = None if args.unfused else prepare(case, n_sets, bs, torch, np,
-                                           fused=True)
-    mf = None
+    fz = None if args.path == "unfused" else prepare(case, n_sets, bs, torch,
+                                                     np, fused=True)
+    mf = mu = None
     if fz is not None:
         mf = measure(fz[1], fz[4], args.steps, args.warmup, torch)
-    sets, step, params, w_packed, describe, _ = prepare(case, n_sets, bs,
-                                                        torch, np)
-    mu = measure(step, describe, args.steps, args.warmup, torch)
+    sets = step = None
+    if args.path != "fused" or fz is None:
+        sets, step, params, w_packed, describe, _ = prepare(case, n_sets, bs,
+                                                            torch, np)
+        mu = measure(step, describe, args.steps, args.warmup, torch)
     m = mf if mf is not None else mu
     macs = case.macs
     value_gops = 2 * macs / (m.ms_step * 1e-3) / 1e9
@@ -851,9 +954,10 @@ def main() -> int:
         "roofline": conv_roofline(
             m, ("codes_" if mf is not None else "") + shape),
         "host_enqueue_ms_per_step": round(m.host_ms, 5),
-        "pack_roofline": pack_roofline(pack_bytes, mu),
+        "pack_roofline": pack_roofline(pack_bytes, mu if mu is not None
+                                       else m),
     }
-    if mf is not None:
+    if mf is not None and mu is not None:
         result["unfused"] = {
             "per_step": per_step_name(case, False),
             "ms_per_step": round(mu.ms_step, 5),
@@ -867,8 +971,10 @@ def main() -> int:
         def gpu_slice(n_img):
             """The first images of set 0 from the unfused and (if timed) the
             fused step, stacked; the oracle's slice must equal each."""
-            step(0)
-            outs = [sets[0][2][:n_img].cpu().numpy()]
+            outs = []
+            if step is not None:
+                step(0)
+                outs.append(sets[0][2][:n_img].cpu().numpy())
             if fz is not None:
                 fz[1](0)
                 outs.append(fz[0][0][2][:n_img].cpu().numpy())

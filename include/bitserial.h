@@ -183,15 +183,6 @@ bs_status bs_conv2d_codes(const bs_conv2d_params *p, const uint8_t *act_codes,
                           const uint32_t *w_packed, int32_t *out,
                           bs_stream_t stream);
 
-/* bs_conv2d_codes of float32 activations quantized on the fly: exactly
- * bs_quantize_pack(x, scale, p->abits, p->aenc) followed by bs_conv2d, with
- * quantization and packing done per workgroup into LDS.
- *   x: [n][h][w][c] float32 NHWC (device); scale as bs_quantize.
- * Errors: as bs_conv2d_codes, and as bs_quantize for scale and encoding. */
-bs_status bs_quantize_conv2d(const bs_conv2d_params *p, const float *x,
-                             float scale, const uint32_t *w_packed,
-                             int32_t *out, bs_stream_t stream);
-
 /* Bitserial conv2d whose result is requantized and bit-packed as the next
  * layer's activations (layer chaining, toward the end-to-end low-precision
  * inference of Sec. 7): the int32 result v of bs_conv2d for each output is
@@ -210,6 +201,40 @@ bs_status bs_conv2d_requant(const bs_conv2d_params *p,
                             const uint32_t *w_packed, float out_scale,
                             int out_bits, uint32_t *out_packed,
                             bs_stream_t stream);
+
+/* A ResNet downsampling block's two convolutions of one input in one pass
+ * (Table 1 layers 4 and 5, 7 and 8, 10 and 11): the KxK conv p, and the 1x1
+ * conv with the same stride, no padding and oc filters w1_packed, whose
+ * input pixel for every output position is the centre tap of the KxK
+ * window; p must have kh == kw odd, pad (kh - 1) / 2 on both axes and equal
+ * strides, so that both convolutions have the same output grid.  Exactly
+ * bs_conv2d(p, act_packed, w_packed, out) and bs_conv2d of the 1x1 conv
+ * (w1_packed, out1), with the packed activations read once and the 1x1
+ * conv's products taken from the KxK window's centre-tap words already in
+ * registers: its added work is 1/(kh kw) of the KxK conv's.
+ *   w1_packed: [oc][1][1][wbits][ceil(c/32)] uint32 (bs_pack of [oc][c]);
+ *   out, out1: [n][oh][ow][oc] int32 each; every element is written.
+ * Shapes no paired kernel covers run as the two convolutions one after the
+ * other, with the same results.
+ * Errors: as bs_conv2d; BS_ERR_INVALID_ARG for a window that is not square
+ * and odd, other padding, unequal strides, or outputs that overlap each
+ * other or an input. */
+bs_status bs_conv2d_pair(const bs_conv2d_params *p, const uint32_t *act_packed,
+                         const uint32_t *w_packed, const uint32_t *w1_packed,
+                         int32_t *out, int32_t *out1, bs_stream_t stream);
+
+/* bs_conv2d_pair with both outputs requantized and bit-packed as
+ * bs_conv2d_requant does (out_bits-bit unipolar codes; out_scale for the
+ * KxK conv, out1_scale for the 1x1 conv):
+ *   out_packed, out1_packed: [n][oh][ow][out_bits][ceil(oc/32)] uint32.
+ * Errors: as bs_conv2d_pair and bs_conv2d_requant. */
+bs_status bs_conv2d_pair_requant(const bs_conv2d_params *p,
+                                 const uint32_t *act_packed,
+                                 const uint32_t *w_packed,
+                                 const uint32_t *w1_packed, float out_scale,
+                                 float out1_scale, int out_bits,
+                                 uint32_t *out_packed, uint32_t *out1_packed,
+                                 bs_stream_t stream);
 
 /* Describes, as text, the kernel and launch configuration that bs_conv2d
  * would use for p under the calling thread's kernel mode (template
@@ -266,17 +291,18 @@ bs_status bs_set_kernel_mode(int mode);
  * for tuning.  Errors: BS_ERR_INVALID_ARG for units < 0. */
 bs_status bs_set_units_per_wave(int units);
 
-/* Timing of the library's own kernels, for benchmarks.  Until cleared, every
- * kernel the library launches for calls made on the calling host thread is
- * launched with `start` and `stop` (hipEvent_t handles the caller created,
- * e.g. with hipEventCreate) as the dispatch's start and stop events
- * (hipExtLaunchKernel): the runtime stamps them with the dispatch's own
- * start and end on the GPU, so hipEventElapsedTime(start, stop) after a call
- * is its kernel's execution time -- the duration a kernel trace reports --
- * without the gaps that events recorded between launches add.  A call that
- * launches several kernels (a batch split into several launches) leaves the
- * pair on its last kernel.  Either handle may be NULL; NULL, NULL clears.
- * The library neither creates nor destroys the events.  Returns BS_OK. */
+/* Timing of the library's own kernels, for benchmarks.  The next kernel the
+ * library launches for a call made on the calling host thread is launched
+ * with `start` as its dispatch's start event, and every kernel until the
+ * events are cleared with `stop` as its stop event (hipExtLaunchKernel; the
+ * handles are hipEvent_t the caller created, e.g. with hipEventCreate).  The
+ * runtime stamps them with the dispatches' own start and end on the GPU, so
+ * after one call hipEventElapsedTime(start, stop) is the time from its first
+ * kernel's start to its last kernel's end -- for a one-kernel call, the
+ * duration a kernel trace reports -- without the gaps that events recorded
+ * between launches add.  Set the pair again before each call to be timed.
+ * Either handle may be NULL; NULL, NULL clears.  The library neither creates
+ * nor destroys the events.  Returns BS_OK. */
 bs_status bs_set_timing_events(void *start, void *stop);
 
 /* ABI version of this header (major * 100 + minor). */

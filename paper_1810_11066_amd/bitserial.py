@@ -44,7 +44,7 @@ LAYOUT_BMK = 2
 EXPORTED = ("bs_packed_words", "bs_quantize", "bs_pack", "bs_pack_ex",
             "bs_quantize_pack",
             "bs_conv2d_out_shape", "bs_conv2d", "bs_conv2d_requant",
-            "bs_conv2d_codes", "bs_quantize_conv2d",
+            "bs_conv2d_codes", "bs_conv2d_pair", "bs_conv2d_pair_requant",
             "bs_conv2d_describe",
             "bs_dense", "bs_dense_ex", "bs_status_string",
             "bs_last_error", "bs_set_kernel_mode", "bs_set_units_per_wave",
@@ -93,8 +93,10 @@ def load_library():
             "bs_conv2d": (ci, [ctypes.POINTER(ConvParams), P, P, P, P]),
             "bs_conv2d_codes": (ci, [ctypes.POINTER(ConvParams), P, P, P,
                                      P]),
-            "bs_quantize_conv2d": (ci, [ctypes.POINTER(ConvParams), P, cf, P,
-                                        P, P]),
+            "bs_conv2d_pair": (ci, [ctypes.POINTER(ConvParams), P, P, P, P, P,
+                                    P]),
+            "bs_conv2d_pair_requant": (ci, [ctypes.POINTER(ConvParams), P, P,
+                                            P, cf, cf, ci, P, P, P]),
             "bs_conv2d_requant": (ci, [ctypes.POINTER(ConvParams), P, P, cf,
                                        ci, P, P]),
             "bs_conv2d_describe": (ci, [ctypes.POINTER(ConvParams),
@@ -250,18 +252,43 @@ def bs_conv2d_codes(p: ConvParams, act_codes: torch.Tensor,
         _stream(stream)))
 
 
-def bs_quantize_conv2d(p: ConvParams, x: torch.Tensor, scale: float,
-                       w_packed: torch.Tensor, out: torch.Tensor,
-                       stream=None) -> None:
-    """bs_quantize_pack of the float32 NHWC activations fused into
-    bs_conv2d."""
+def bs_conv2d_pair(p: ConvParams, act_packed: torch.Tensor,
+                   w_packed: torch.Tensor, w1_packed: torch.Tensor,
+                   out: torch.Tensor, out1: torch.Tensor,
+                   stream=None) -> None:
+    """The KxK conv p and its centre-tap 1x1 conv in one pass."""
     oh, ow = bs_conv2d_out_shape(p)
-    _check(load_library().bs_quantize_conv2d(
+    cw = words(p.c)
+    _check(load_library().bs_conv2d_pair(
         ctypes.byref(p),
-        _dev(x, "x", torch.float32, p.n * p.h * p.w * p.c), float(scale),
+        _dev(act_packed, "act_packed", torch.int32,
+             p.n * p.h * p.w * p.abits * cw),
         _dev(w_packed, "w_packed", torch.int32,
-             p.oc * p.kh * p.kw * p.wbits * words(p.c)),
+             p.oc * p.kh * p.kw * p.wbits * cw),
+        _dev(w1_packed, "w1_packed", torch.int32, p.oc * p.wbits * cw),
         _dev(out, "out", torch.int32, p.n * oh * ow * p.oc),
+        _dev(out1, "out1", torch.int32, p.n * oh * ow * p.oc),
+        _stream(stream)))
+
+
+def bs_conv2d_pair_requant(p: ConvParams, act_packed: torch.Tensor,
+                           w_packed: torch.Tensor, w1_packed: torch.Tensor,
+                           out_scale: float, out1_scale: float,
+                           out_bits: int, out_packed: torch.Tensor,
+                           out1_packed: torch.Tensor, stream=None) -> None:
+    oh, ow = bs_conv2d_out_shape(p)
+    cw = words(p.c)
+    n_out = p.n * oh * ow * out_bits * words(p.oc)
+    _check(load_library().bs_conv2d_pair_requant(
+        ctypes.byref(p),
+        _dev(act_packed, "act_packed", torch.int32,
+             p.n * p.h * p.w * p.abits * cw),
+        _dev(w_packed, "w_packed", torch.int32,
+             p.oc * p.kh * p.kw * p.wbits * cw),
+        _dev(w1_packed, "w1_packed", torch.int32, p.oc * p.wbits * cw),
+        float(out_scale), float(out1_scale), int(out_bits),
+        _dev(out_packed, "out_packed", torch.int32, n_out),
+        _dev(out1_packed, "out1_packed", torch.int32, n_out),
         _stream(stream)))
 
 
@@ -418,15 +445,29 @@ def conv2d_codes(spec: Conv2dSpec, act_codes: torch.Tensor,
     return out
 
 
-def quantize_conv2d(spec: Conv2dSpec, x: torch.Tensor, scale: float,
-                    w_packed: torch.Tensor) -> torch.Tensor:
-    """Conv of float32 NHWC activations, quantize + pack fused into it."""
+def conv2d_pair(spec: Conv2dSpec, act_packed: torch.Tensor,
+                w_packed: torch.Tensor, w1_packed: torch.Tensor):
+    """(out, out1): the KxK conv and its centre-tap 1x1 conv."""
     p = spec.params()
     oh, ow = bs_conv2d_out_shape(p)
     out = torch.empty((spec.n, oh, ow, spec.oc), dtype=torch.int32,
-                      device=x.device)
-    bs_quantize_conv2d(p, x, scale, w_packed, out)
-    return out
+                      device=act_packed.device)
+    out1 = torch.empty_like(out)
+    bs_conv2d_pair(p, act_packed, w_packed, w1_packed, out, out1)
+    return out, out1
+
+
+def conv2d_pair_requant(spec: Conv2dSpec, act_packed: torch.Tensor,
+                        w_packed: torch.Tensor, w1_packed: torch.Tensor,
+                        out_scale: float, out1_scale: float, out_bits: int):
+    p = spec.params()
+    oh, ow = bs_conv2d_out_shape(p)
+    shape = (p.n, oh, ow, out_bits, words(p.oc))
+    out = torch.empty(shape, dtype=torch.int32, device=act_packed.device)
+    out1 = torch.empty(shape, dtype=torch.int32, device=act_packed.device)
+    bs_conv2d_pair_requant(p, act_packed, w_packed, w1_packed, out_scale,
+                           out1_scale, out_bits, out, out1)
+    return out, out1
 
 
 def dense(a_packed: torch.Tensor, w_packed: torch.Tensor, m: int, n: int,

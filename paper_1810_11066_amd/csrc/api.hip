@@ -173,10 +173,15 @@ TimingEvents& timing_events() { return g_timing; }
 
 hipError_t launch_kernel(const void* fn, dim3 grid, dim3 block, void** args,
                          size_t lds, hipStream_t st) {
-    const TimingEvents& t = g_timing;
-    if (t.start || t.stop)
-        return hipExtLaunchKernel(fn, grid, block, args, lds, st, t.start,
-                                  t.stop, 0);
+    TimingEvents& t = g_timing;
+    if (t.start || t.stop) {
+        const hipError_t e = hipExtLaunchKernel(fn, grid, block, args, lds, st,
+                                                t.start, t.stop, 0);
+        // the start event belongs to the first dispatch only; the stop
+        // event to every one, so the last stamps it
+        t.start = nullptr;
+        return e;
+    }
     return hipLaunchKernel(fn, grid, block, args, lds, st);
 }
 
@@ -184,7 +189,7 @@ hipError_t launch_kernel(const void* fn, dim3 grid, dim3 block, void** args,
 
 extern "C" {
 
-int bs_abi_version(void) { return 106; }
+int bs_abi_version(void) { return 107; }
 
 int64_t bs_packed_words(int64_t k) { return k <= 0 ? 0 : (k + 31) / 32; }
 
@@ -337,61 +342,128 @@ bs_status bs_conv2d(const bs_conv2d_params* p, const uint32_t* act_packed,
                     "bs_conv2d launch");
 }
 
-// The fused pack + conv calls: validation as bs_conv2d, with the unpacked
-// activations' bytes in the overlap check.
-static bs_status conv_staged(const bs_conv2d_params* p, const void* act,
-                             uint64_t elem_bytes, const char* act_name,
-                             bool from_float, float scale,
-                             const uint32_t* w_packed, int32_t* out,
-                             bs_stream_t stream, const char* what) {
+// The checks of a paired call beyond bs_conv2d's: the 1x1 conv's input pixel
+// must be the window's centre tap (square odd window, pad (K-1)/2, equal
+// strides), and no output may overlap an input or the other output.
+static bs_status check_pair(const bs_conv2d_params* p,
+                            const bs::ConvShape& s, const void* act,
+                            const void* wts, const void* wts1,
+                            const void* out, const void* out1,
+                            uint64_t out_bytes) {
+    if (p->kh != p->kw || p->kh % 2 == 0 || p->pad_h != (p->kh - 1) / 2 ||
+        p->pad_w != (p->kw - 1) / 2 || p->stride_h != p->stride_w)
+        return fail(BS_ERR_INVALID_ARG,
+                    "the paired 1x1 conv reads the window's centre tap: it "
+                    "needs kh == kw odd, pad (kh - 1) / 2 on both axes and "
+                    "equal strides");
     bs_status st;
-    if ((st = check_ptr(act, act_name)) != BS_OK) return st;
+    if ((st = check_conv_buffers(s, act, wts, out, out_bytes)) != BS_OK)
+        return st;
+    if ((st = check_conv_buffers(s, act, wts, out1, out_bytes)) != BS_OK)
+        return st;
+    const uint64_t w1_bytes = packed_bytes(s.oc, s.wbits, s.c);
+    if ((st = check_disjoint(out, out_bytes, "out", wts1, w1_bytes,
+                             "w1_packed")) != BS_OK)
+        return st;
+    if ((st = check_disjoint(out1, out_bytes, "out1", wts1, w1_bytes,
+                             "w1_packed")) != BS_OK)
+        return st;
+    return check_disjoint(out1, out_bytes, "out1", out, out_bytes, "out");
+}
+
+bs_status bs_conv2d_pair(const bs_conv2d_params* p, const uint32_t* act_packed,
+                         const uint32_t* w_packed, const uint32_t* w1_packed,
+                         int32_t* out, int32_t* out1, bs_stream_t stream) {
+    bs_status st;
+    if ((st = check_ptr(act_packed, "act_packed")) != BS_OK) return st;
+    if ((st = check_ptr(w_packed, "w_packed")) != BS_OK) return st;
+    if ((st = check_ptr(w1_packed, "w1_packed")) != BS_OK) return st;
+    if ((st = check_ptr(out, "out")) != BS_OK) return st;
+    if ((st = check_ptr(out1, "out1")) != BS_OK) return st;
+    bs::ConvShape s;
+    if ((st = check_conv(p, &s)) != BS_OK) return st;
+    if ((st = check_pair(p, s, act_packed, w_packed, w1_packed, out, out1,
+                         (uint64_t)s.n * s.oh * s.ow * (uint64_t)s.oc * 4u)) !=
+        BS_OK)
+        return st;
+    return from_hip(bs::launch_conv_pair(s, act_packed, w_packed, w1_packed,
+                                         out, out1, nullptr, 0.0f, g_conv_opt,
+                                         (hipStream_t)stream),
+                    "bs_conv2d_pair launch");
+}
+
+bs_status bs_conv2d_pair_requant(const bs_conv2d_params* p,
+                                 const uint32_t* act_packed,
+                                 const uint32_t* w_packed,
+                                 const uint32_t* w1_packed, float out_scale,
+                                 float out1_scale, int out_bits,
+                                 uint32_t* out_packed, uint32_t* out1_packed,
+                                 bs_stream_t stream) {
+    bs_status st;
+    if ((st = check_ptr(act_packed, "act_packed")) != BS_OK) return st;
+    if ((st = check_ptr(w_packed, "w_packed")) != BS_OK) return st;
+    if ((st = check_ptr(w1_packed, "w1_packed")) != BS_OK) return st;
+    if ((st = check_ptr(out_packed, "out_packed")) != BS_OK) return st;
+    if ((st = check_ptr(out1_packed, "out1_packed")) != BS_OK) return st;
+    if ((st = check_bits(out_bits, "out_bits")) != BS_OK) return st;
+    if ((st = check_scale_enc(out_scale, out_bits, BS_UNIPOLAR)) != BS_OK)
+        return st;
+    if ((st = check_scale_enc(out1_scale, out_bits, BS_UNIPOLAR)) != BS_OK)
+        return st;
+    bs::ConvShape s;
+    if ((st = check_conv(p, &s)) != BS_OK) return st;
+    if ((int64_t)s.n * s.oh * s.ow * ((s.oc + 31) / 32) >= INT32_MAX)
+        return fail(BS_ERR_UNSUPPORTED, "output too large");
+    if ((st = check_pair(p, s, act_packed, w_packed, w1_packed, out_packed,
+                         out1_packed,
+                         packed_bytes((int64_t)s.n * s.oh * s.ow, out_bits,
+                                      s.oc))) != BS_OK)
+        return st;
+    bs::Requant rq;
+    rq.scale = out_scale;
+    rq.bits = out_bits;
+    return from_hip(bs::launch_conv_pair(
+                        s, act_packed, w_packed, w1_packed,
+                        reinterpret_cast<int32_t*>(out_packed),
+                        reinterpret_cast<int32_t*>(out1_packed), &rq,
+                        out1_scale, g_conv_opt, (hipStream_t)stream),
+                    "bs_conv2d_pair_requant launch");
+}
+
+// bs_pack of the codes fused into bs_conv2d: validation as bs_conv2d, with
+// the codes' bytes in the overlap check.
+bs_status bs_conv2d_codes(const bs_conv2d_params* p, const uint8_t* act_codes,
+                          const uint32_t* w_packed, int32_t* out,
+                          bs_stream_t stream) {
+    bs_status st;
+    if ((st = check_ptr(act_codes, "act_codes")) != BS_OK) return st;
     if ((st = check_ptr(w_packed, "w_packed")) != BS_OK) return st;
     if ((st = check_ptr(out, "out")) != BS_OK) return st;
     bs::ConvShape s;
     if ((st = check_conv(p, &s)) != BS_OK) return st;
-    if (from_float &&
-        (st = check_scale_enc(scale, s.abits, (bs_encoding)s.aenc)) != BS_OK)
-        return st;
     const uint64_t out_bytes = (uint64_t)s.n * s.oh * s.ow * (uint64_t)s.oc * 4u;
-    const uint64_t act_bytes =
-        (uint64_t)s.n * s.h * s.w * (uint64_t)s.c * elem_bytes;
+    const uint64_t act_bytes = (uint64_t)s.n * s.h * s.w * (uint64_t)s.c;
     const uint64_t w_bytes = packed_bytes((int64_t)s.oc * s.kh * s.kw,
                                           s.wbits, s.c);
-    if ((st = check_disjoint(out, out_bytes, "out", act, act_bytes,
-                             act_name)) != BS_OK)
+    if ((st = check_disjoint(out, out_bytes, "out", act_codes, act_bytes,
+                             "act_codes")) != BS_OK)
         return st;
     if ((st = check_disjoint(out, out_bytes, "out", w_packed, w_bytes,
                              "w_packed")) != BS_OK)
         return st;
-    const hipError_t e =
-        bs::launch_conv_staged(s, from_float, act, scale, w_packed, out,
-                               g_conv_opt, (hipStream_t)stream);
+    const hipError_t e = bs::launch_conv_codes(s, act_codes, w_packed, out,
+                                               g_conv_opt, (hipStream_t)stream);
     if (e == hipErrorNotSupported)
         return fail(BS_ERR_UNSUPPORTED,
-                    "%s: no fused kernel covers this shape (it needs c a "
-                    "multiple of 32, oc a multiple of 4, square kernels of "
-                    "size 1 or 3, stride 1 or 2, unipolar activations with "
-                    "unipolar filters of 1-2 bits or bipolar 1-bit filters, "
-                    "the whole kh x kw x abits x c/32-word patch within "
-                    "72 words, and the input rows of one workgroup's outputs "
-                    "within its LDS); bit-pack the activations and call "
-                    "bs_conv2d", what);
-    return from_hip(e, what);
-}
-
-bs_status bs_conv2d_codes(const bs_conv2d_params* p, const uint8_t* act_codes,
-                          const uint32_t* w_packed, int32_t* out,
-                          bs_stream_t stream) {
-    return conv_staged(p, act_codes, 1, "act_codes", false, 0.0f, w_packed,
-                       out, stream, "bs_conv2d_codes");
-}
-
-bs_status bs_quantize_conv2d(const bs_conv2d_params* p, const float* x,
-                             float scale, const uint32_t* w_packed,
-                             int32_t* out, bs_stream_t stream) {
-    return conv_staged(p, x, 4, "x", true, scale, w_packed, out, stream,
-                       "bs_quantize_conv2d");
+                    "bs_conv2d_codes: no fused kernel covers this shape (it "
+                    "needs c a multiple of 32, oc a multiple of 4, square "
+                    "kernels of size 1 or 3, stride 1 or 2, unipolar "
+                    "activations with unipolar filters of 1-2 bits or "
+                    "bipolar 1-bit filters, the whole kh x kw x abits x "
+                    "c/32-word patch within 72 words, and the input rows of "
+                    "one workgroup's outputs within its LDS); bit-pack the "
+                    "activations and call bs_conv2d");
+    return from_hip(e, "bs_conv2d_codes launch");
 }
 
 bs_status bs_conv2d_requant(const bs_conv2d_params* p,

@@ -159,15 +159,24 @@ hipError_t launch_conv_requant(const ConvShape& s, const uint32_t* act,
                                const Requant& rq, const ConvOptions& opt,
                                hipStream_t st);
 
-// Conv of unpacked activations: uint8 codes (from_float false) or float32
-// values quantized with `scale` under s.aenc (from_float true), NHWC
-// [n][h][w][c]; the conv kernel bit-packs each block's input rows into LDS.
-// hipErrorNotSupported, with nothing enqueued, when no such kernel covers
-// the shape.
-hipError_t launch_conv_staged(const ConvShape& s, bool from_float,
-                              const void* act, float scale,
-                              const uint32_t* wts, int32_t* out,
-                              const ConvOptions& opt, hipStream_t st);
+// A KxK conv s (odd K, pad (K-1)/2) and the 1x1 conv of the same stride
+// over the same input, whose input pixel is the window's centre tap, so that
+// both share the output grid: wts1 [oc][1][1][wbits][cw] filters, out1
+// shaped like out.  rq: both outputs requantized and packed (scale1 for
+// out1) instead of int32.  One paired launch where a kernel covers the
+// shape, otherwise the two convolutions one after the other.
+hipError_t launch_conv_pair(const ConvShape& s, const uint32_t* act,
+                            const uint32_t* wts, const uint32_t* wts1,
+                            int32_t* out, int32_t* out1, const Requant* rq,
+                            float scale1, const ConvOptions& opt,
+                            hipStream_t st);
+
+// Conv of unpacked uint8 activation codes, NHWC [n][h][w][c]: the conv
+// kernel bit-packs each block's input rows into LDS.  hipErrorNotSupported,
+// with nothing enqueued, when no such kernel covers the shape.
+hipError_t launch_conv_codes(const ConvShape& s, const uint8_t* act,
+                             const uint32_t* wts, int32_t* out,
+                             const ConvOptions& opt, hipStream_t st);
 
 // Writes the kernel and launch configuration launch_conv would use for this
 // shape and mode into buf (snprintf semantics); returns the snprintf result.

@@ -107,22 +107,25 @@ struct PixArgs {
     int32_t act_bytes;     // size of the packed activations, bytes
     int32_t out_bytes;     // size of the int32 output, bytes (0: packed out)
     // activations staged in LDS (SRC != kSrcPacked): the most input pixels
-    // any block's region holds (its LDS size), and the quantizer of float
-    // activations
+    // any block's region holds (its LDS size)
     int32_t region_pixels;
-    float in_scale, in_qmax;
+    // paired 1x1 conv (DUAL kernels; its packed filters [oc][W][CW] are the
+    // kernel's wts1 argument): its output (int32 [npix][oc], or packed codes
+    // with out1_scale), and the int32 output's size in bytes (0 for packed
+    // output)
+    int32_t* out1;
+    float out1_scale;
+    int32_t out1_bytes;
 };
 
 // Where a specialisation's activations come from:
 //   kSrcPacked  bit-packed words [n][h][w][A][CW] in HBM (bs_pack output);
 //   kSrcCodes   uint8 codes [n][h][w][C], C = 32 CW: each block bit-packs the
-//               input rows its outputs read into LDS first;
-//   kSrcFloat   float32 values [n][h][w][C]: quantized (the activation
-//               encoding's quantizer) and bit-packed into LDS the same way.
-// The staged forms never write the packed activations to HBM: the separate
-// pack launch and its round trip are gone, at the price of packing each
-// block's halo rows again.
-constexpr int kSrcPacked = 0, kSrcCodes = 1, kSrcFloat = 2;
+//               input rows its outputs read into LDS first.  The packed
+//               activations never reach HBM: the separate pack launch and
+//               its round trip are gone, at the price of packing each
+//               block's halo rows again.
+constexpr int kSrcPacked = 0, kSrcCodes = 1;
 
 __device__ __forceinline__ void bcnt_acc(uint32_t& acc, uint32_t x) {
     asm("v_bcnt_u32_b32 %0, %1, %0" : "+v"(acc) : "v"(x));
@@ -268,11 +271,16 @@ struct PackedOut {
     // clamp of the quantizer is one v_med3
     __device__ __forceinline__ void add4(const uint32_t (&val)[4],
                                          const PixArgs& g, int half) {
+        add4(val, g.out_scale, g, half);
+    }
+    __device__ __forceinline__ void add4(const uint32_t (&val)[4],
+                                         float scale, const PixArgs& g,
+                                         int half) {
         uint32_t bytes = 0;
 #pragma unroll
         for (int o = 0; o < 4; ++o) {
             const float r =
-                __builtin_rintf((float)(int32_t)val[o] * g.out_scale);
+                __builtin_rintf((float)(int32_t)val[o] * scale);
             bytes |= (uint32_t)__builtin_amdgcn_fmed3f(r, 0.0f, g.out_qmax)
                      << (8 * o);
         }
@@ -379,6 +387,40 @@ __device__ __forceinline__ void flush_tile(const uint32_t* __restrict__ tile,
             v, out, in ? o0 + (uint32_t)r * rstep : kOutOfRange, 0, 0);
         if constexpr (SERIAL) __builtin_amdgcn_sched_barrier(0);
     }
+}
+
+// One output channel of the paired 1x1 conv: Eq. 2 over the centre tap's
+// words pc (A planes x CW words) and the channel's filter words f (W planes
+// x CW words, uniform), plus the bipolar-filter correction with lc1, the
+// plane-weighted popcount of pc.
+template <int A, int W, int E, int CW>
+__device__ __forceinline__ uint32_t centre_1x1(const uint32_t (&pc)[A][CW],
+                                               const uint32_t* f,
+                                               uint32_t lc1) {
+    constexpr int NS = A + W - 1;
+    uint32_t acc[NS];
+    bool fresh[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) fresh[s] = true;
+#pragma unroll
+    for (int c = 0; c < CW; ++c)
+#pragma unroll
+        for (int j = 0; j < W; ++j)
+#pragma unroll
+            for (int i = 0; i < A; ++i) {
+                const uint32_t x = pc[i][c] & f[j * CW + c];
+                if (fresh[i + j]) {
+                    bcnt_first(acc[i + j], x);
+                    fresh[i + j] = false;
+                } else {
+                    bcnt_acc(acc[i + j], x);
+                }
+            }
+    uint32_t v = 0;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) v += (fresh[s] ? 0u : acc[s]) << s;
+    if constexpr (E % 3 == kBipolar) v = 2u * v - (uint32_t)((1 << W) - 1) * lc1;
+    return v;
 }
 
 // One quad of output channels over one reduction block: 4 / OCB batches of
@@ -540,22 +582,6 @@ __device__ __forceinline__ void pack32_planes(const uint32_t (&d)[8],
     }
 }
 
-// Codes of 32 float32 activations in bytes (code 4 m + k in byte k of d[m]),
-// under the activation encoding's quantizer (bs_quantize's reading): one
-// binary32 multiply, round half to even, clamp; bipolar: x >= 0.
-template <int AE>
-__device__ __forceinline__ void quantize32(const float (&x)[32], float scale,
-                                           float qmax, uint32_t (&d)[8]) {
-#pragma unroll
-    for (int m = 0; m < 8; ++m) {
-        uint32_t v = 0;
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-            v |= quant_code_enc<AE>(x[4 * m + k], scale, qmax) << (8 * k);
-        d[m] = v;
-    }
-}
-
 // Input region of a block: the flat NHWC input pixels [lo, hi) that hold
 // every in-range tap of the block's output pixels, from the first tap row of
 // its first output pixel to the last tap row of its last one.
@@ -588,40 +614,44 @@ __device__ __forceinline__ Region block_region(const PixArgs& g, int p_first,
 // Fills the block's region in LDS: packed words [pixel - lo][A][CW] of the
 // input pixels [lo, hi), then one pixel of zeros (what the taps in the
 // padding read).  Each thread packs (pixel, word) items of 32 codes; the
-// loads of consecutive threads are consecutive 32-byte (codes) or 128-byte
-// (floats) pieces of the NHWC rows.
-template <int A, int AE, int CW, int SRC>
+// loads of consecutive threads are consecutive 32-byte pieces of the NHWC
+// rows.  A thread issues the loads of U items before it packs any of them,
+// so that the fill waits for memory about once rather than once per item.
+template <int A, int CW>
 __device__ __forceinline__ void stage_region(uint32_t* __restrict__ region,
-                                             const void* __restrict__ src,
-                                             const PixArgs& g, Region rg) {
+                                             const uint8_t* __restrict__ src,
+                                             Region rg) {
     constexpr int PW = A * CW;                 // words per packed pixel
+    constexpr int U = 4;
     const int items = (rg.hi - rg.lo) * CW;
-    for (int it = threadIdx.x; it < items; it += kBlock) {
-        const int pl = it / CW, t = it - pl * CW;
-        const size_t first = ((size_t)(rg.lo + pl) * CW + t) * 32;  // code
-        uint32_t d[8];
-        if constexpr (SRC == kSrcCodes) {
-            const uint4* q = reinterpret_cast<const uint4*>(
-                static_cast<const uint8_t*>(src) + first);
-            const uint4 a = q[0], b = q[1];
-            d[0] = a.x; d[1] = a.y; d[2] = a.z; d[3] = a.w;
-            d[4] = b.x; d[5] = b.y; d[6] = b.z; d[7] = b.w;
-        } else {
-            const float4* q = reinterpret_cast<const float4*>(
-                static_cast<const float*>(src) + first);
-            float x[32];
+    for (int it0 = threadIdx.x; it0 < items; it0 += U * kBlock) {
+        uint32_t d[U][8];
 #pragma unroll
-            for (int m = 0; m < 8; ++m) {
-                const float4 v = q[m];
-                x[4 * m] = v.x; x[4 * m + 1] = v.y;
-                x[4 * m + 2] = v.z; x[4 * m + 3] = v.w;
+        for (int u = 0; u < U; ++u) {
+            const int it = it0 + u * kBlock;
+            uint4 a = make_uint4(0, 0, 0, 0), b = a;
+            if (it < items) {
+                const int pl = it / CW, t = it - pl * CW;
+                const uint4* q = reinterpret_cast<const uint4*>(
+                    src + ((size_t)(rg.lo + pl) * CW + t) * 32);
+                a = q[0];
+                b = q[1];
             }
-            quantize32<AE>(x, g.in_scale, g.in_qmax, d);
+            d[u][0] = a.x; d[u][1] = a.y; d[u][2] = a.z; d[u][3] = a.w;
+            d[u][4] = b.x; d[u][5] = b.y; d[u][6] = b.z; d[u][7] = b.w;
         }
-        uint32_t w[A];
-        pack32_planes<A>(d, w);
 #pragma unroll
-        for (int b = 0; b < A; ++b) region[pl * PW + b * CW + t] = w[b];
+        for (int u = 0; u < U; ++u) {
+            const int it = it0 + u * kBlock;
+            if (it < items) {
+                const int pl = it / CW, t = it - pl * CW;
+                uint32_t w[A];
+                pack32_planes<A>(d[u], w);
+#pragma unroll
+                for (int b = 0; b < A; ++b)
+                    region[pl * PW + b * CW + t] = w[b];
+            }
+        }
     }
     const int zero = (rg.hi - rg.lo) * PW;
     for (int i = threadIdx.x; i < PW; i += kBlock) region[zero + i] = 0;
@@ -854,7 +884,9 @@ constexpr int kAheadWords = 16;
 // or two over 72 would cost a wave and change the launch plan (ResNet-18
 // layer 10: 73 VGPRs, 6 waves, 40.1 us; 72 VGPRs, 7 waves, 38.2 us); for the
 // others whatever their patch needs.
-template <int A, int W, int E, int K, int CW, bool REQ>
+// Paired kernels (DUAL) follow the same rule (at 96 VGPRs the 72-word-patch
+// ones would spill to scratch; they take 4 waves).
+template <int A, int W, int E, int K, int CW, bool REQ, bool DUAL>
 constexpr int min_waves_per_simd() {
     using Pl = Plan<A, W, K, CW>;
     return !REQ && A * W <= 2 && E / 3 == kUnipolar && E % 3 != kSigned &&
@@ -867,18 +899,28 @@ constexpr int min_waves_per_simd() {
 // S: stride; CW: words per bit-plane; REQ: requantize and bit-pack the output
 // (out then holds [npix][out_bits][out_words] uint32 words) instead of
 // storing int32; SRC: where the activations come from (kSrcPacked, or
-// staged in LDS from kSrcCodes / kSrcFloat, whole patches only).
-template <int A, int W, int E, int K, int S, int CW, bool REQ, int SRC>
+// kSrcCodes staged in LDS, whole patches only); DUAL: also the 1x1 conv of
+// the same stride whose input pixel is the window's centre tap (pad
+// (K-1)/2), over the same output grid and channels, with filters wts1 and
+// output g.out1 (whole patches only).  wts1 is a kernel argument, read-only
+// and unaliased like wts, so that its uniform loads may be scalar loads.
+template <int A, int W, int E, int K, int S, int CW, bool REQ, int SRC,
+          bool DUAL>
 __global__ __launch_bounds__(kBlock) __attribute__((
     amdgpu_num_sgpr(96),
-    amdgpu_waves_per_eu(min_waves_per_simd<A, W, E, K, CW, REQ>())))
+    amdgpu_waves_per_eu(min_waves_per_simd<A, W, E, K, CW, REQ, DUAL>())))
 void conv_pix_kernel(
     const uint32_t* __restrict__ act, const uint32_t* __restrict__ wts,
-    int32_t* __restrict__ out, PixArgs g) {
+    const uint32_t* __restrict__ wts1, int32_t* __restrict__ out,
+    PixArgs g) {
     using Pl = Plan<A, W, K, CW>;
     constexpr int FW = Pl::FW, NB = Pl::NB;
     static_assert(SRC == kSrcPacked || (NB == 1 && !REQ),
                   "staged activations: whole patches, int32 output");
+    static_assert(!DUAL || (NB == 1 && K % 2 == 1 && SRC == kSrcPacked &&
+                            (E == 3 * kUnipolar + kUnipolar ||
+                             E == 3 * kUnipolar + kBipolar)),
+                  "paired 1x1 conv: whole patches, unipolar activations");
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(
         (int)(xcd_block() * kWavesPerBlock + (threadIdx.x >> 6)));
@@ -891,6 +933,7 @@ void conv_pix_kernel(
     gu32* gw = (gu32*)(wts);
     const Rsrc ract = make_rsrc(act, g.act_bytes);
     const Rsrc rout = make_rsrc(out, g.out_bytes);
+    [[maybe_unused]] const Rsrc rout1 = make_rsrc(g.out1, g.out1_bytes);
 
     // staged activations: the block packs its input region into LDS (after
     // the waves' output tiles) before any wave computes; every wave of the
@@ -907,8 +950,8 @@ void conv_pix_kernel(
         const int p_last = min(
             (int)g.div_units.div((uint32_t)(ub1 - 1)) * 64 + 63, g.npix - 1);
         const Region rg = block_region<K, S>(g, p_first, p_last);
-        stage_region<A, Enc<E>::AE, CW, SRC>(
-            lds + kWavesPerBlock * kTileWords, act, g, rg);
+        stage_region<A, CW>(lds + kWavesPerBlock * kTileWords,
+                            reinterpret_cast<const uint8_t*>(act), rg);
         region_lo = rg.lo;
         zero_off = (uint32_t)(rg.hi - rg.lo) * (uint32_t)(4 * A * CW);
         __syncthreads();
@@ -947,6 +990,10 @@ void conv_pix_kernel(
         // loads and stores in order, so a load issued after them would wait
         // for their completion (and the HBM-bound 1x1 layers would stall).
         constexpr bool kAhead = Pl::PB <= kAheadWords && SRC == kSrcPacked;
+        // the paired 1x1 conv's filter words of one quad, and the centre tap
+        [[maybe_unused]] constexpr int F1 = 4 * W * CW;
+        [[maybe_unused]] constexpr int kCentre = K * K / 2;
+        [[maybe_unused]] gu32* gw1 = (gu32*)(wts1);
         // flushes run while the patch is held: keep their registers few
         // when the patch is large (all four rounds hoisted cost 4-9 VGPRs)
         constexpr bool kSerialFlush = Pl::PB > 32;
@@ -963,6 +1010,8 @@ void conv_pix_kernel(
             // one flush's stores, so the wait for the patch can leave those
             // in flight
             flush_tile<kSerialFlush>(tile, rout, v.fm, 0, 0, lane);
+            if constexpr (DUAL)
+                flush_tile<kSerialFlush>(tile, rout1, v.fm, 0, 0, lane);
         }
         while (true) {
             if constexpr (kAhead) {
@@ -981,14 +1030,75 @@ void conv_pix_kernel(
             TapInfo<A, W, K, CW> tv;
             const uint32_t lc =
                 block_consts<A, W, E, K, S, CW>(patch, tv, g, v.oy, v.ox, 0);
+            // bipolar filters of the paired 1x1 conv: SA of the centre tap
+            [[maybe_unused]] uint32_t lc1 = 0;
+            if constexpr (DUAL && E % 3 == kBipolar) {
+#pragma unroll
+                for (int i = 0; i < A; ++i)
+#pragma unroll
+                    for (int c = 0; c < CW; ++c)
+                        lc1 += (uint32_t)__builtin_popcount(
+                                   patch[kCentre][i][c]) << i;
+            }
             gu32* src = gw + (size_t)(4 * v.q0) * FW;
             Slice<Pl::SW> f[2];
             load_slice<A, W, K, CW>(f[0], src);
             const int nq = v.q1 - v.q0;
             int chunk_base = 4 * v.q0;   // first channel held in the tile
             int held = 0;                // quads held in the tile
-            PackedOut po;
+            PackedOut po, po1;
             po.clear();
+            po1.clear();
+            // the paired 1x1 conv's 4 channels of quad qg (its filters by one
+            // scalar load), computed after the main conv's results of the
+            // tile chunk have been flushed, so only the centre tap and one
+            // accumulator set are live
+            // channel by channel, each result handed to `put` before the
+            // next channel starts (a scheduling barrier keeps the compiler
+            // from interleaving the channels' accumulators)
+            [[maybe_unused]] auto quad1 = [&](int qg, auto&& put)
+                __attribute__((always_inline)) {
+                uint32_t f1[F1];
+                // scalar loads (uniform index, read-only unaliased filters):
+                // a vector load here would wait, through vmcnt, for the tile
+                // stores issued just before
+                gu32* q1 =
+                    gw1 + (size_t)__builtin_amdgcn_readfirstlane(qg) * F1;
+#pragma unroll
+                for (int k = 0; k < F1; ++k) f1[k] = q1[k];
+#pragma unroll
+                for (int o = 0; o < 4; ++o) {
+                    put(o, centre_1x1<A, W, E, CW>(patch[kCentre],
+                                                   f1 + o * W * CW, lc1));
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            };
+            // the tile chunk's stores: the main conv's channels
+            // [chunk_base, chunk_base + 4 held), then, for paired kernels,
+            // the same channels of the 1x1 conv through the same tile (every
+            // flush writes 64-byte pieces of the pixel rows)
+            auto flush_chunk = [&]() __attribute__((always_inline)) {
+                wave_lds_sync();
+                flush_tile<kSerialFlush>(tile, rout, v.fm, chunk_base,
+                                         held * 4, lane);
+                if constexpr (DUAL) {
+                    wave_lds_sync();
+                    uint32_t* row = tile + lane * kTileStride;
+#pragma unroll 1
+                    for (int h = 0; h < held; ++h)
+                        quad1(chunk_base / 4 + h,
+                              [&](int o, uint32_t x)
+                                  __attribute__((always_inline)) {
+                                      row[h * 4 + o] = x;
+                                  });
+                    wave_lds_sync();
+                    flush_tile<kSerialFlush>(tile, rout1, v.fm, chunk_base,
+                                             held * 4, lane);
+                }
+                wave_lds_sync();
+                chunk_base += held * 4;
+                held = 0;
+            };
             auto quad = [&](int qi) __attribute__((always_inline)) {
                 uint32_t val[4];
                 gu32* q = src + (size_t)qi * 4 * FW;
@@ -998,23 +1108,29 @@ void conv_pix_kernel(
                     // a packed byte holds 2 quads; runs start on a byte
                     const int qg = v.q0 + qi;
                     po.add4(val, g, qg & 1);
+                    if constexpr (DUAL) {
+                        uint32_t val1[4];
+                        quad1(qg, [&](int o, uint32_t x)
+                                      __attribute__((always_inline)) {
+                                          val1[o] = x;
+                                      });
+                        po1.add4(val1, g.out1_scale, g, qg & 1);
+                    }
                     if ((qg & 1) == 1 && qi + 1 < nq) {
-                        if (v.p < g.npix) po.store(out, g, v.p, qg >> 1);
+                        if (v.p < g.npix) {
+                            po.store(out, g, v.p, qg >> 1);
+                            if constexpr (DUAL)
+                                po1.store(g.out1, g, v.p, qg >> 1);
+                        }
                         po.clear();
+                        po1.clear();
                     }
                 } else {
 #pragma unroll
                     for (int o = 0; o < 4; ++o)
                         tile[lane * kTileStride + held * 4 + o] = val[o];
                     ++held;
-                    if (held == kChunk / 4 && qi + 1 < nq) {
-                        wave_lds_sync();
-                        flush_tile<kSerialFlush>(tile, rout, v.fm,
-                                                 chunk_base, held * 4, lane);
-                        wave_lds_sync();
-                        chunk_base += held * 4;
-                        held = 0;
-                    }
+                    if (held == kChunk / 4 && qi + 1 < nq) flush_chunk();
                 }
             };
             // the visit's first quad outside the loop: its taps are used in
@@ -1036,12 +1152,13 @@ void conv_pix_kernel(
             }
             // the visit's last byte or tile chunk
             if constexpr (REQ) {
-                if (v.p < g.npix) po.store(out, g, v.p, (v.q1 - 1) >> 1);
+                if (v.p < g.npix) {
+                    po.store(out, g, v.p, (v.q1 - 1) >> 1);
+                    if constexpr (DUAL)
+                        po1.store(g.out1, g, v.p, (v.q1 - 1) >> 1);
+                }
             } else {
-                wave_lds_sync();
-                flush_tile<kSerialFlush>(tile, rout, v.fm, chunk_base,
-                                         held * 4, lane);
-                wave_lds_sync();
+                flush_chunk();
             }
             if (!more) break;
             if constexpr (kAhead) {
@@ -1141,8 +1258,8 @@ void conv_pix_kernel(
     }
 }
 
-using PixKernelFn = void (*)(const uint32_t*, const uint32_t*, int32_t*,
-                             PixArgs);
+using PixKernelFn = void (*)(const uint32_t*, const uint32_t*,
+                             const uint32_t*, int32_t*, PixArgs);
 
 // Plan of a kernel as the host reports it.
 struct PlanInfo {
@@ -1162,18 +1279,19 @@ struct PlanInfo {
 //                      and signed activations with signed filters of the
 //                      same width, int32 output;
 //   pick_bipolar_act   +-1 activations with 1-bit filters, int32 output.
+// dual: the paired kernel that also computes the centre-tap 1x1 conv.
 PixKernelFn pick(int a, int w, int ae, int we, int k, int s, int cw, bool req,
-                 int src, PlanInfo* info);
+                 int src, bool dual, PlanInfo* info);
 template <int A>
 PixKernelFn pick_a(int w, bool b, int k, int s, int cw, bool req, int src,
-                   PlanInfo* info);
-template <> PixKernelFn pick_a<1>(int, bool, int, int, int, bool, int,
+                   bool dual, PlanInfo* info);
+template <> PixKernelFn pick_a<1>(int, bool, int, int, int, bool, int, bool,
                                   PlanInfo*);
-template <> PixKernelFn pick_a<2>(int, bool, int, int, int, bool, int,
+template <> PixKernelFn pick_a<2>(int, bool, int, int, int, bool, int, bool,
                                   PlanInfo*);
-template <> PixKernelFn pick_a<3>(int, bool, int, int, int, bool, int,
+template <> PixKernelFn pick_a<3>(int, bool, int, int, int, bool, int, bool,
                                   PlanInfo*);
-template <> PixKernelFn pick_a<4>(int, bool, int, int, int, bool, int,
+template <> PixKernelFn pick_a<4>(int, bool, int, int, int, bool, int, bool,
                                   PlanInfo*);
 template <int A>
 PixKernelFn pick_signed(int w, int ae, int we, int k, int s, int cw,
@@ -1188,9 +1306,12 @@ PixKernelFn pick_bipolar_act(int we, int k, int s, int cw, PlanInfo* info);
 // exist for unipolar activations with unipolar or bipolar filters only;
 // staged activations (src != kSrcPacked) for unipolar activations with
 // unipolar filters of 1 or 2 bits or bipolar 1-bit filters, whole patches,
-// int32 output.
+// int32 output; paired kernels (dual) for unipolar activations with
+// unipolar or bipolar filters, 3x3 windows, whole patches, and at most 16
+// filter words per quad of the 1x1 conv (W CW <= 4), int32 or requantized
+// output.
 template <int A, int W, int E, int K, int S, int CW>
-PixKernelFn pick_kscw(bool req, int src, PlanInfo* info) {
+PixKernelFn pick_kscw(bool req, int src, bool dual, PlanInfo* info) {
     using Pl = Plan<A, W, K, CW>;
     constexpr int UU = 3 * kUnipolar + kUnipolar, UB = 3 * kUnipolar + kBipolar;
     if constexpr (!Pl::kFits) {
@@ -1201,44 +1322,57 @@ PixKernelFn pick_kscw(bool req, int src, PlanInfo* info) {
         info->tb = Pl::TB;
         info->cb = Pl::CB;
         info->enc = E;
+        if (dual) {
+            if constexpr (Pl::NB == 1 && K == 3 && W * CW <= 4 &&
+                          (E == UU || E == UB)) {
+                if (src != kSrcPacked) return nullptr;
+                return req ? conv_pix_kernel<A, W, E, K, S, CW, true,
+                                             kSrcPacked, true>
+                           : conv_pix_kernel<A, W, E, K, S, CW, false,
+                                             kSrcPacked, true>;
+            } else {
+                return nullptr;
+            }
+        }
         if (src != kSrcPacked) {
             if constexpr (Pl::NB == 1 && (E == UU || E == UB) && W <= 2) {
-                if (req) return nullptr;
-                return src == kSrcCodes
-                           ? conv_pix_kernel<A, W, E, K, S, CW, false,
-                                             kSrcCodes>
-                           : conv_pix_kernel<A, W, E, K, S, CW, false,
-                                             kSrcFloat>;
+                if (req || src != kSrcCodes) return nullptr;
+                return conv_pix_kernel<A, W, E, K, S, CW, false, kSrcCodes,
+                                       false>;
             } else {
                 return nullptr;
             }
         }
         if constexpr (E == UU || E == UB)
-            return req ? conv_pix_kernel<A, W, E, K, S, CW, true, kSrcPacked>
-                       : conv_pix_kernel<A, W, E, K, S, CW, false, kSrcPacked>;
+            return req ? conv_pix_kernel<A, W, E, K, S, CW, true, kSrcPacked,
+                                         false>
+                       : conv_pix_kernel<A, W, E, K, S, CW, false, kSrcPacked,
+                                         false>;
         else
             return req ? nullptr
-                       : conv_pix_kernel<A, W, E, K, S, CW, false, kSrcPacked>;
+                       : conv_pix_kernel<A, W, E, K, S, CW, false, kSrcPacked,
+                                         false>;
     }
 }
 
 // Words per plane: 1..16 for 3x3 windows; 1x1 windows (and dense, a 1x1
 // conv) up to 128 words = 4096 input channels.
 template <int A, int W, int E, int K, int S>
-PixKernelFn pick_cw(int cw, bool req, int src, PlanInfo* info) {
+PixKernelFn pick_cw(int cw, bool req, int src, bool dual, PlanInfo* info) {
     switch (cw) {
-        case 1: return pick_kscw<A, W, E, K, S, 1>(req, src, info);
-        case 2: return pick_kscw<A, W, E, K, S, 2>(req, src, info);
-        case 4: return pick_kscw<A, W, E, K, S, 4>(req, src, info);
-        case 8: return pick_kscw<A, W, E, K, S, 8>(req, src, info);
-        case 16: return pick_kscw<A, W, E, K, S, 16>(req, src, info);
+        case 1: return pick_kscw<A, W, E, K, S, 1>(req, src, dual, info);
+        case 2: return pick_kscw<A, W, E, K, S, 2>(req, src, dual, info);
+        case 4: return pick_kscw<A, W, E, K, S, 4>(req, src, dual, info);
+        case 8: return pick_kscw<A, W, E, K, S, 8>(req, src, dual, info);
+        case 16: return pick_kscw<A, W, E, K, S, 16>(req, src, dual, info);
         default: break;
     }
     if constexpr (K == 1) {
         switch (cw) {
-            case 32: return pick_kscw<A, W, E, K, S, 32>(req, src, info);
-            case 64: return pick_kscw<A, W, E, K, S, 64>(req, src, info);
-            case 128: return pick_kscw<A, W, E, K, S, 128>(req, src, info);
+            case 32: return pick_kscw<A, W, E, K, S, 32>(req, src, dual, info);
+            case 64: return pick_kscw<A, W, E, K, S, 64>(req, src, dual, info);
+            case 128:
+                return pick_kscw<A, W, E, K, S, 128>(req, src, dual, info);
             default: break;
         }
     }
@@ -1246,11 +1380,14 @@ PixKernelFn pick_cw(int cw, bool req, int src, PlanInfo* info) {
 }
 
 template <int A, int W, int E>
-PixKernelFn pick_ks(int k, int s, int cw, bool req, int src, PlanInfo* info) {
-    if (k == 1) return s == 1 ? pick_cw<A, W, E, 1, 1>(cw, req, src, info)
-                              : pick_cw<A, W, E, 1, 2>(cw, req, src, info);
-    if (k == 3) return s == 1 ? pick_cw<A, W, E, 3, 1>(cw, req, src, info)
-                              : pick_cw<A, W, E, 3, 2>(cw, req, src, info);
+PixKernelFn pick_ks(int k, int s, int cw, bool req, int src, bool dual,
+                    PlanInfo* info) {
+    if (k == 1)
+        return s == 1 ? pick_cw<A, W, E, 1, 1>(cw, req, src, dual, info)
+                      : pick_cw<A, W, E, 1, 2>(cw, req, src, dual, info);
+    if (k == 3)
+        return s == 1 ? pick_cw<A, W, E, 3, 1>(cw, req, src, dual, info)
+                      : pick_cw<A, W, E, 3, 2>(cw, req, src, dual, info);
     return nullptr;
 }
 
@@ -1258,15 +1395,15 @@ PixKernelFn pick_ks(int k, int s, int cw, bool req, int src, PlanInfo* info) {
 // bipolar weights at W = 1.
 template <int A>
 PixKernelFn pick_for_a(int w, bool b, int k, int s, int cw, bool req, int src,
-                       PlanInfo* info) {
+                       bool dual, PlanInfo* info) {
     constexpr int UU = 3 * kUnipolar + kUnipolar, UB = 3 * kUnipolar + kBipolar;
-    if (b) return w == 1 ? pick_ks<A, 1, UB>(k, s, cw, req, src, info)
+    if (b) return w == 1 ? pick_ks<A, 1, UB>(k, s, cw, req, src, dual, info)
                          : nullptr;
     switch (w) {
-        case 1: return pick_ks<A, 1, UU>(k, s, cw, req, src, info);
-        case 2: return pick_ks<A, 2, UU>(k, s, cw, req, src, info);
-        case 3: return pick_ks<A, 3, UU>(k, s, cw, req, src, info);
-        case 4: return pick_ks<A, 4, UU>(k, s, cw, req, src, info);
+        case 1: return pick_ks<A, 1, UU>(k, s, cw, req, src, dual, info);
+        case 2: return pick_ks<A, 2, UU>(k, s, cw, req, src, dual, info);
+        case 3: return pick_ks<A, 3, UU>(k, s, cw, req, src, dual, info);
+        case 4: return pick_ks<A, 4, UU>(k, s, cw, req, src, dual, info);
         default: return nullptr;
     }
 }
@@ -1281,16 +1418,22 @@ PixKernelFn pick_signed_for_a(int w, int ae, int we, int k, int s, int cw,
     if (ae == kSigned) {
         if constexpr (A >= 2)
             return w == A ? pick_ks<A, A, SS>(k, s, cw, false, kSrcPacked,
-                                              info)
+                                              false, info)
                           : nullptr;
         else
             return nullptr;
     }
     if (ae != kUnipolar) return nullptr;
     switch (w) {
-        case 2: return pick_ks<A, 2, US>(k, s, cw, false, kSrcPacked, info);
-        case 3: return pick_ks<A, 3, US>(k, s, cw, false, kSrcPacked, info);
-        case 4: return pick_ks<A, 4, US>(k, s, cw, false, kSrcPacked, info);
+        case 2:
+            return pick_ks<A, 2, US>(k, s, cw, false, kSrcPacked, false,
+                                      info);
+        case 3:
+            return pick_ks<A, 3, US>(k, s, cw, false, kSrcPacked, false,
+                                      info);
+        case 4:
+            return pick_ks<A, 4, US>(k, s, cw, false, kSrcPacked, false,
+                                      info);
         default: return nullptr;
     }
 }

@@ -22,8 +22,8 @@ namespace pix {
 #if BS_PIX_FAMILY == 0
 template <>
 PixKernelFn pick_a<BS_A>(int w, bool b, int k, int s, int cw, bool req,
-                         int src, PlanInfo* info) {
-    return pick_for_a<BS_A>(w, b, k, s, cw, req, src, info);
+                         int src, bool dual, PlanInfo* info) {
+    return pick_for_a<BS_A>(w, b, k, s, cw, req, src, dual, info);
 }
 #elif BS_PIX_FAMILY == 1
 template <>
@@ -35,9 +35,9 @@ PixKernelFn pick_signed<BS_A>(int w, int ae, int we, int k, int s, int cw,
 PixKernelFn pick_bipolar_act(int we, int k, int s, int cw, PlanInfo* info) {
     constexpr int BB = 3 * kBipolar + kBipolar, BU = 3 * kBipolar + kUnipolar;
     if (we == kBipolar)
-        return pick_ks<1, 1, BB>(k, s, cw, false, kSrcPacked, info);
+        return pick_ks<1, 1, BB>(k, s, cw, false, kSrcPacked, false, info);
     if (we == kUnipolar)
-        return pick_ks<1, 1, BU>(k, s, cw, false, kSrcPacked, info);
+        return pick_ks<1, 1, BU>(k, s, cw, false, kSrcPacked, false, info);
     return nullptr;
 }
 #endif

@@ -41,7 +41,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_words(lib):
-    assert lib.bs_abi_version() == 106
+    assert lib.bs_abi_version() == 107
     for k, w in [(0, 0), (1, 1), (31, 1), (32, 1), (33, 2), (4096, 128)]:
         assert lib.bs_packed_words(k) == w
 
@@ -177,27 +177,23 @@ def test_fused_conv_validation(lib, bad, status):
     assert lib.bs_conv2d_codes(ctypes.byref(p), act, wts, out,
                                STREAM) == status
     assert lib.bs_last_error() != b""
-    assert lib.bs_quantize_conv2d(ctypes.byref(p), act, 1.0, wts, out,
-                                  STREAM) == status
-    assert lib.bs_last_error() != b""
 
 
-def test_fused_conv_pointer_and_scale_validation(lib):
+def test_fused_conv_pointer_validation(lib):
     p = params()
     assert lib.bs_conv2d_codes(ctypes.byref(p), NULL, FAKE, FAKE,
                                STREAM) == bs.BS_ERR_INVALID_ARG
     assert lib.bs_conv2d_codes(ctypes.byref(p), MISALIGNED, FAKE, FAKE,
                                STREAM) == bs.BS_ERR_INVALID_ARG
-    for scale in (0.0, -1.0, float("inf"), float("nan")):
-        assert lib.bs_quantize_conv2d(ctypes.byref(p), FAKE, scale, FAKE,
-                                      FAKE, STREAM) == bs.BS_ERR_INVALID_ARG
-    # the output may not overlap the codes (n*h*w*c bytes) or the floats
-    assert lib.bs_conv2d_codes(ctypes.byref(p), at(0), FAKE, at(4096 - 16),
+    # the output may not overlap the codes (n*h*w*c = 4096 bytes) ...
+    assert lib.bs_conv2d_codes(ctypes.byref(p), at(0), at(1 << 20),
+                               at(4096 - 16), STREAM) == bs.BS_ERR_INVALID_ARG
+    assert b"overlaps act_codes" in lib.bs_last_error()
+    # ... nor the packed filters (64 x 9 x 1 plane x 2 words x 4 B)
+    assert lib.bs_conv2d_codes(ctypes.byref(p), at(0), at(1 << 20),
+                               at((1 << 20) + 4608 - 16),
                                STREAM) == bs.BS_ERR_INVALID_ARG
-    assert b"overlaps" in lib.bs_last_error()
-    assert lib.bs_quantize_conv2d(ctypes.byref(p), at(0), 1.0, at(1 << 20),
-                                  at(16384 - 16),
-                                  STREAM) == bs.BS_ERR_INVALID_ARG
+    assert b"overlaps w_packed" in lib.bs_last_error()
 
 
 def at(offset):

@@ -1,7 +1,6 @@
-"""GPU parity of the fused calls: bs_conv2d_codes (bit-pack of uint8 codes
-inside the conv kernel) and bs_quantize_conv2d (quantize + bit-pack of float32
-activations inside it), each against the oracle's quantize -> pack -> conv2d
-on the same seeded inputs.
+"""GPU parity of the fused call bs_conv2d_codes (bit-pack of uint8 codes
+inside the conv kernel) against the oracle's pack -> conv2d on the same
+seeded inputs.
 
 Each workgroup of these kernels packs the input rows its outputs read into
 LDS, so the tests vary what decides those regions: image sizes, strides,
@@ -197,50 +196,6 @@ def test_conv2d_codes_shapes(oracle, shape, run):
     run_codes(oracle, shape, seed=run + 17 * shape[4], run=run)
 
 
-def special_floats(rng, shape):
-    x = rng.standard_normal(size=shape).astype(np.float32) * 2
-    flat = x.reshape(-1)
-    idx = rng.integers(0, flat.size, size=max(1, flat.size // 8))
-    pool = np.array([np.nan, np.inf, -np.inf, -0.0, 0.0, 0.5, 1.5, 2.5, 3.5,
-                     -0.5, 1e-40, 1e30, 0.49999997], np.float32)
-    flat[idx] = pool[rng.integers(0, pool.size, size=idx.size)]
-    return x
-
-
-def run_float(oracle, args, seed, scale, run=0):
-    n, h, w, c, oc, k, s, pad, abits, wbits, bip = args
-    rng = np.random.default_rng(seed)
-    x = special_floats(rng, (n, h, w, c))
-    wq = rng.integers(0, 1 << wbits, size=(oc, k, k, c), dtype=np.uint8)
-    codes = oracle.quantize(x, scale, abits)
-    want = expect(oracle, codes, wq, *args)
-    spec = bs.Conv2dSpec(n, h, w, c, oc, k, k, s, pad, abits, wbits,
-                         int(bip))
-    p = spec.params()
-    oh, ow = bs.bs_conv2d_out_shape(p)
-    g = Guarded(n * oh * ow * oc)
-    w_dev = bs.pack(dev(wq), wbits)
-    x_dev = dev(x)
-    if not call_fused(
-            lambda: bs.bs_quantize_conv2d(p, x_dev, scale, w_dev, g.t), p,
-            run, (n, h, w, c, oc, k, s, pad, abits)):
-        return
-    torch.cuda.synchronize()
-    got = g.t.cpu().numpy().reshape(n, oh, ow, oc)
-    g.check_guards()
-    assert np.array_equal(got, want)
-
-
-@pytest.mark.parametrize("seed", range(40))
-def test_quantize_conv2d_random(oracle, seed):
-    rng = np.random.default_rng(7300 + seed)
-    args = random_staged(rng)
-    run = int(rng.choice([0, 0, 1, 2, 5, 13]))
-    scale = float(rng.choice([1.0, 1.5, 0.7, 3.0, 1.0 / 3.0]))
-    say("quantize_conv2d", args, "scale", scale, "run", run)
-    run_float(oracle, args, seed=seed, scale=scale, run=run)
-
-
 def test_conv2d_codes_unsupported_writes_nothing(oracle):
     # c not a multiple of 32: the fused kernels do not cover it
     n, h, w, c, oc = 1, 6, 6, 48, 8
@@ -270,27 +225,4 @@ def test_config2_conv2d_codes_full(oracle):
                          case.k, case.stride, case.pad, case.abits,
                          case.wbits)
     got = bs.conv2d_codes(spec, dev(codes), bs.pack(dev(wq), case.wbits))
-    assert np.array_equal(got.cpu().numpy(), want)
-
-
-STAGED_LAYERS = [c for c in wl.config4()
-                 if c.k * c.k * c.abits * (c.c // 32) <= 72]
-
-
-@pytest.mark.parametrize("case", STAGED_LAYERS, ids=lambda c: c.name)
-def test_config4_quantize_conv2d_full(oracle, case):
-    """Config 4's layers that the fused quantize + pack + conv covers, at
-    batch 128, every output element against the oracle."""
-    say(case.name)
-    x = case.activations()
-    wq = case.weights()
-    codes = oracle.quantize(x, case.act_scale, case.abits)
-    want = expect(oracle, codes, wq, case.n, case.h, case.w, case.c, case.oc,
-                  case.k, case.stride, case.pad, case.abits, case.wbits,
-                  False)
-    spec = bs.Conv2dSpec(case.n, case.h, case.w, case.c, case.oc, case.k,
-                         case.k, case.stride, case.pad, case.abits,
-                         case.wbits)
-    got = bs.quantize_conv2d(spec, dev(x), case.act_scale,
-                             bs.pack(dev(wq), case.wbits))
     assert np.array_equal(got.cpu().numpy(), want)
