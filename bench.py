@@ -622,16 +622,19 @@ INT8_MFMA_PEAK_TOPS = 5000.0   # dense int8 MFMA, MI355X
 
 
 def chain_line(args, bs, torch, np, wl, batch=128, abits=2, wbits=1) -> int:
-    """ResNet-18's 3x3 conv path chained on the GPU: the float32 input is
-    quantized and packed once, every conv but the last writes the next
-    layer's packed codes (bs_conv2d_requant), the last writes int32."""
+    """ResNet-18's conv path chained on the GPU: the float32 input is
+    quantized and packed once, every 3x3 conv but the last writes the next
+    layer's packed codes (bs_conv2d_requant), the three downsampling layers
+    with their 1x1 shortcuts in one paired launch (bs_conv2d_pair_requant,
+    the shortcut's packed codes for the residual branch), the last writes
+    int32."""
     layers = wl.resnet18_chain(abits, wbits)
     stream = torch.cuda.current_stream()
     x = torch.from_numpy(wl.normal_floats((batch, 56, 56, 64),
                                           wl.seed_for(7))).cuda()
     packed_in = torch.empty((batch * 56 * 56, abits, bs.words(64)),
                             dtype=torch.int32, device="cuda")
-    specs, wts, outs = [], [], []
+    specs, wts, outs, wts1, outs1 = [], [], [], [], []
     for L in layers:
         spec = bs.Conv2dSpec(batch, L.h, L.w, L.c, L.oc, L.k, L.k, L.stride,
                              L.pad, abits, wbits)
@@ -644,9 +647,17 @@ def chain_line(args, bs, torch, np, wl, batch=128, abits=2, wbits=1) -> int:
         else:
             outs.append(torch.empty((batch, oh, ow, abits, bs.words(L.oc)),
                                     dtype=torch.int32, device="cuda"))
+        if L.shortcut_scale is not None:
+            wts1.append(bs.pack(torch.from_numpy(
+                L.shortcut_weights(wbits)).cuda(), wbits))
+            outs1.append(torch.empty_like(outs[-1]))
+        else:
+            wts1.append(None)
+            outs1.append(None)
         specs.append(p)
     macs = sum(batch * ((L.h + 2 * L.pad - L.k) // L.stride + 1) ** 2 *
-               L.oc * L.k * L.k * L.c for L in layers)
+               L.oc * (L.k * L.k + (1 if L.shortcut_scale else 0)) * L.c
+               for L in layers)
 
     def run(ev=None):
         bs.bs_quantize_pack(x, packed_in, batch * 56 * 56, 64, 1.0, abits,
@@ -657,6 +668,10 @@ def chain_line(args, bs, torch, np, wl, batch=128, abits=2, wbits=1) -> int:
                 ev[i][0].record(stream)
             if L.out_scale is None:
                 bs.bs_conv2d(specs[i], src, wts[i], outs[i], stream)
+            elif L.shortcut_scale is not None:
+                bs.bs_conv2d_pair_requant(specs[i], src, wts[i], wts1[i],
+                                          L.out_scale, L.shortcut_scale,
+                                          abits, outs[i], outs1[i], stream)
             else:
                 bs.bs_conv2d_requant(specs[i], src, wts[i], L.out_scale,
                                      abits, outs[i], stream)
@@ -685,9 +700,12 @@ def chain_line(args, bs, torch, np, wl, batch=128, abits=2, wbits=1) -> int:
                for r in range(args.steps)) / args.steps
            for i in range(len(layers))]
     print(json.dumps({
-        "chain": "resnet18 3x3 conv path, batch %d, A%dW%d, layers chained "
-                 "by bs_conv2d_requant" % (batch, abits, wbits),
+        "chain": "resnet18 convs after conv1 (16 3x3 chained by "
+                 "bs_conv2d_requant, the 3 downsampling ones paired with "
+                 "their 1x1 shortcuts by bs_conv2d_pair_requant), batch %d, "
+                 "A%dW%d, no residual adds" % (batch, abits, wbits),
         "layers": len(layers),
+        "shortcuts": sum(1 for L in layers if L.shortcut_scale is not None),
         "ms_per_pass": round(ms, 4),
         "effective_tops": round(2 * macs / (ms * 1e-3) / 1e12, 1),
         "frac_of_roofline": round(2 * macs / (ms * 1e-3) / 1e12 /
@@ -698,69 +716,97 @@ def chain_line(args, bs, torch, np, wl, batch=128, abits=2, wbits=1) -> int:
 
 
 def int8_baseline_lines(args, bs, torch, np, wl) -> int:
-    """The int8 matrix-core comparison (a baseline, not the bitserial path):
-    config 2 as im2col + int8 GEMM, config 3 as one int8 GEMM, each timed
-    with per-launch events and checked equal to the bitserial result."""
+    """The int8 matrix-core comparison (baselines, not the bitserial path):
+    config 2 through the hand-written implicit-GEMM MFMA conv and through
+    im2col + the library int8 GEMM, config 3 through one library GEMM, each
+    next to the bitserial step and checked equal to the bitserial result
+    (both are checked against the oracle by the GPU tests)."""
     from paper_1810_11066_amd import int8_baseline as ib
 
-    def timed(fn, steps):
-        for _ in range(args.warmup):
-            fn()
+    def per_launch(fn, n_sets):
+        """ms per launch: back-to-back launches under one event pair, over
+        n_sets rotated buffer sets, after warmup."""
+        for i in range(max(args.warmup, n_sets)):
+            fn(i)
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for i in range(args.steps):
+            fn(i)
+        t1.record()
         torch.cuda.synchronize()
-        ev = [(torch.cuda.Event(enable_timing=True),
-               torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-        for e in ev:
-            e[0].record()
-            fn()
-            e[1].record()
-        torch.cuda.synchronize()
-        return sum(a.elapsed_time(b) for a, b in ev) / steps
+        return t0.elapsed_time(t1) / args.steps
 
     ok_all = True
     for case in (wl.config2(), wl.config3()):
         dense = isinstance(case, wl.DenseCase)
-        sets, step, params, w_packed, describe, _ = prepare(case, 1, bs,
+        n_sets = sets_for(case, args.sets)
+        fz = prepare(case, n_sets, bs, torch, np, fused=True)
+        sets, step, params, w_packed, describe, _ = prepare(case, n_sets, bs,
                                                             torch, np)
         m = measure(step, describe, args.steps, args.warmup, torch)
-        x = torch.from_numpy(case.activations()).cuda()
-        wq = torch.from_numpy(case.weights()).cuda()
-        x8, w8 = x.to(torch.int8), wq.to(torch.int8)
+        mf = (measure(fz[1], fz[4], args.steps, args.warmup, torch)
+              if fz is not None else None)
+        ops = 2 * case.macs
+        line = {"baseline": ib.LABEL, "workload": case.name,
+                "bitserial_kernel_ms": round(m.main_ms, 5),
+                "bitserial_step_ms": round(m.ms_step, 5),
+                "bitserial_fused_step_ms": round(mf.ms_step, 5)
+                if mf is not None else None}
         if dense:
-            wt = w8.t().contiguous()
-            gemm_ms = timed(lambda: torch._int_mm(x8, wt), args.steps)
-            im2col_ms = 0.0
-            ref = ib.dense_int8(x, wq)
+            a8 = torch.from_numpy(case.activations()).cuda()
+            w8 = torch.from_numpy(case.weights()).cuda()
+            wt = w8.to(torch.int8).t().contiguous()
+            a8 = a8.to(torch.int8)
+            gemm_ms = per_launch(lambda i: torch._int_mm(a8, wt), 1)
+            ref = torch._int_mm(a8, wt)
+            line.update(int8_gemm=ib.LABEL_GEMM,
+                        int8_gemm_ms=round(gemm_ms, 5),
+                        int8_gemm_tops=round(ops / (gemm_ms * 1e-3) / 1e12, 1),
+                        int8_gemm_frac_of_mfma_peak=round(
+                            ops / (gemm_ms * 1e-3) / 1e12 /
+                            INT8_MFMA_PEAK_TOPS, 4))
         else:
-            k = case.k
-            cols = ib.im2col_nhwc(x8, k, case.stride, case.pad).contiguous()
+            x8s = [s_[0].to(torch.int8) for s_ in sets]
+            w8 = torch.from_numpy(case.weights()).cuda().to(torch.int8)
+            outs = [torch.empty_like(s_[2]) for s_ in sets]
+            mfma_ms = per_launch(lambda i: ib.conv2d_mfma(
+                x8s[i % n_sets], w8, case.stride, case.pad,
+                out=outs[i % n_sets]), n_sets)
+            ref = ib.conv2d_mfma(x8s[0], w8, case.stride, case.pad)
+            in_b = case.n * case.h * case.w * case.c
+            out_b = case.n * case.oh * case.ow * case.oc * 4
+            w_b = case.oc * case.k * case.k * case.c
+            hbm = (in_b + out_b + w_b) / (mfma_ms * 1e-3) / 1e9
+            cols = ib.im2col_nhwc(x8s[0], case.k, case.stride,
+                                  case.pad).contiguous()
             wt = w8.reshape(case.oc, -1).t().contiguous()
-            im2col_ms = timed(lambda: ib.im2col_nhwc(
-                x8, k, case.stride, case.pad).contiguous(), args.steps)
-            gemm_ms = timed(lambda: torch._int_mm(cols, wt), args.steps)
-            ref = ib.conv2d_int8(x, wq, case.stride, case.pad)
+            gemm_ms = per_launch(lambda i: torch._int_mm(cols, wt), 1)
+            im2col_ms = per_launch(lambda i: ib.im2col_nhwc(
+                x8s[i % n_sets], case.k, case.stride, case.pad).contiguous(),
+                n_sets)
+            line.update(
+                int8_conv=ib.LABEL_CONV,
+                int8_conv_ms=round(mfma_ms, 5),
+                int8_conv_tops=round(ops / (mfma_ms * 1e-3) / 1e12, 1),
+                int8_conv_frac_of_mfma_peak=round(
+                    ops / (mfma_ms * 1e-3) / 1e12 / INT8_MFMA_PEAK_TOPS, 4),
+                int8_conv_hbm_gbs=round(hbm, 1),
+                int8_conv_frac_of_hbm=round(hbm / HBM_PEAK_GBS, 4),
+                int8_conv_over_bitserial_step=round(
+                    mfma_ms / (mf.ms_step if mf is not None else m.ms_step),
+                    3),
+                int8_gemm=ib.LABEL_GEMM,
+                int8_gemm_ms=round(gemm_ms, 5),
+                int8_im2col_ms=round(im2col_ms, 5),
+                int8_gemm_tops=round(ops / (gemm_ms * 1e-3) / 1e12, 1))
         step(0)
         torch.cuda.synchronize()
         same = bool(torch.equal(ref.reshape(-1), sets[0][2].reshape(-1)))
         ok_all &= same
-        ops = 2 * case.macs
-        print(json.dumps({
-            "baseline": ib.LABEL,
-            "workload": case.name,
-            "int8_gemm_ms": round(gemm_ms, 5),
-            "int8_im2col_ms": round(im2col_ms, 5),
-            "int8_total_ms": round(gemm_ms + im2col_ms, 5),
-            "int8_gemm_tops": round(ops / (gemm_ms * 1e-3) / 1e12, 1),
-            "int8_gemm_frac_of_mfma_peak": round(
-                ops / (gemm_ms * 1e-3) / 1e12 / INT8_MFMA_PEAK_TOPS, 4),
-            "bitserial_kernel_ms": round(m.main_ms, 5),
-            "bitserial_step_ms": round(m.ms_step, 5),
-            "bitserial_kernel_tops": round(ops / (m.main_ms * 1e-3) / 1e12,
-                                           1),
-            "int8_gemm_over_bitserial_kernel_time": round(
-                gemm_ms / m.main_ms, 3),
-            "outputs_equal": same,
-        }), flush=True)
-        del sets
+        line["outputs_equal_bitserial"] = same
+        print(json.dumps(line), flush=True)
+        del sets, fz
         torch.cuda.empty_cache()
     return 0 if ok_all else 1
 
@@ -797,9 +843,11 @@ def main() -> int:
                          "layer-2 A2W1 line; 1, 3, 4, 5 print one line per "
                          "case of that workload")
     ap.add_argument("--int8-baseline", action="store_true",
-                    help="time the labelled int8 matrix-core baseline "
-                         "(im2col + int8 GEMM) on configs 2 and 3 next to "
-                         "the bitserial kernels, checking equal outputs")
+                    help="time the labelled int8 matrix-core baselines "
+                         "(hand-written implicit-GEMM MFMA conv; im2col + "
+                         "library int8 GEMM; library GEMM for dense) on "
+                         "configs 2 and 3 next to the bitserial steps, "
+                         "checking equal outputs")
     ap.add_argument("--chain", action="store_true",
                     help="the 16 3x3 convs of ResNet-18 (batch 128, A2W1) "
                          "chained with bs_conv2d_requant: quantize+pack of "

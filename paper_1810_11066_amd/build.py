@@ -27,6 +27,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libbitserial.so")
+# the int8 matrix-core comparison baseline: a library of its own
+INT8_LIB = os.path.join(HERE, "libint8mfma.so")
+INT8_SOURCE = "int8_mfma.hip"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # (source, object name, defines)
@@ -60,6 +63,27 @@ def _compile(src: str, obj: str, extra=()) -> None:
                                                           r.stderr))
 
 
+def _link(objs, out):
+    out_tmp = out + ".tmp%d" % os.getpid()
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC"] + objs + \
+          ["-o", out_tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("link failed:\n%s%s" % (r.stdout, r.stderr))
+    os.replace(out_tmp, out)
+
+
+def build_int8(verbose: bool = False, out: str = INT8_LIB) -> str:
+    """Compile and link the int8 MFMA baseline library; returns its path."""
+    with tempfile.TemporaryDirectory(prefix="i8_build_") as tmp:
+        obj = os.path.join(tmp, "int8_mfma.o")
+        _compile(INT8_SOURCE, obj)
+        _link([obj], out)
+    if verbose:
+        print("built", out)
+    return out
+
+
 def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
     """Compile and link the library (to `out`, with extra -D `defines`);
     returns its path."""
@@ -70,13 +94,7 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
             list(ex.map(lambda a: _compile(
                 a[0][0], a[1], extra + ["-D" + d for d in a[0][2]]),
                 zip(UNITS, objs)))
-        out_tmp = out + ".tmp%d" % os.getpid()
-        cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC"] + objs + \
-              ["-o", out_tmp]
-        r = subprocess.run(cmd, capture_output=True, text=True)
-        if r.returncode != 0:
-            raise RuntimeError("link failed:\n%s%s" % (r.stdout, r.stderr))
-        os.replace(out_tmp, out)
+        _link(objs, out)
     if verbose:
         print("built", out)
     return out
@@ -84,4 +102,5 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
 
 if __name__ == "__main__":
     build(verbose=True)
+    build_int8(verbose=True)
     sys.exit(0)

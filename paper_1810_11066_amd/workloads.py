@@ -231,7 +231,10 @@ def bitwidth_sweep(batch: int = 128) -> List[ConvCase]:
 @dataclass
 class ChainLayer:
     """One conv of a chained network: input shape, filters, next-layer
-    requantization scale (None for the last layer, which keeps int32)."""
+    requantization scale (None for the last layer, which keeps int32).
+    A downsampling layer also has its 1x1 projection shortcut (same input,
+    stride and output grid), whose requantized output the residual branch
+    would take."""
     name: str
     h: int
     w: int
@@ -242,29 +245,37 @@ class ChainLayer:
     pad: int
     seed: int
     out_scale: Optional[float] = None
+    shortcut_scale: Optional[float] = None   # set: the layer has a shortcut
 
     def weights(self, wbits: int) -> np.ndarray:
         return uniform_codes((self.oc, self.k, self.k, self.c), wbits,
                              self.seed + 1)
 
+    def shortcut_weights(self, wbits: int) -> np.ndarray:
+        return uniform_codes((self.oc, 1, 1, self.c), wbits, self.seed + 2)
+
 
 def resnet18_chain(abits: int = 2, wbits: int = 1) -> List[ChainLayer]:
-    """The 16 3x3 convs of ResNet-18 after conv1 (Table 1 layers 2, 4, 6, 7,
-    9, 10, 12 with their multiplicities 4, 1, 3, 1, 3, 1, 3), chained without
-    the residual adds and the 1x1 shortcut convs.  Each layer's output is
+    """The 19 convs of ResNet-18 after conv1: the 16 3x3 convs (Table 1
+    layers 2, 4, 6, 7, 9, 10, 12 with their multiplicities 4, 1, 3, 1, 3, 1,
+    3), chained, and the 1x1 stride-2 shortcuts (layers 5, 8, 11) on the
+    inputs of layers 4, 7 and 10, without the residual adds.  Each output is
     requantized to abits-bit codes with a scale that maps twice the mean
-    result of uniform codes, (2^A - 1)/2 * (2^W - 1)/2 * 9 C, to the top
+    result of uniform codes, (2^A - 1)/2 * (2^W - 1)/2 * K*K*C, to the top
     code; the last layer keeps its int32 output."""
     stages = [(2, 56, 64, 64, 1, 4), (4, 56, 64, 128, 2, 1),
               (6, 28, 128, 128, 1, 3), (7, 28, 128, 256, 2, 1),
               (9, 14, 256, 256, 1, 3), (10, 14, 256, 512, 2, 1),
               (12, 7, 512, 512, 1, 3)]
+    qa, qw = (1 << abits) - 1, (1 << wbits) - 1
     out = []
     for (layer, hw, c, oc, s, reps) in stages:
         for r in range(reps):
-            mean = ((1 << abits) - 1) / 2 * ((1 << wbits) - 1) / 2 * 9 * c
+            mean = qa / 2 * qw / 2 * 9 * c
+            mean1 = qa / 2 * qw / 2 * c
             out.append(ChainLayer("L%d.%d" % (layer, r), hw, hw, c, oc, 3, s,
                                   1, seed_for(7, 10 * len(out)),
-                                  ((1 << abits) - 1) / (2 * mean)))
+                                  qa / (2 * mean),
+                                  qa / (2 * mean1) if s == 2 else None))
     out[-1].out_scale = None
     return out

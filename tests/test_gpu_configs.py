@@ -194,8 +194,9 @@ def test_bitwidth_sweep_layer9(oracle, case):
 
 
 def test_resnet18_chain_batch2(oracle):
-    # the 16 chained 3x3 convs (bs_conv2d_requant between layers) on two
-    # images, against the oracle's conv -> quantize(float32) -> pack per layer
+    # the 16 chained 3x3 convs (bs_conv2d_requant between layers, the three
+    # downsampling ones paired with their 1x1 shortcuts) on two images,
+    # against the oracle's conv -> quantize(float32) -> pack per layer
     batch, abits, wbits = 2, 2, 1
     layers = wl.resnet18_chain(abits, wbits)
     x = wl.normal_floats((batch, 56, 56, 64), wl.seed_for(7))
@@ -216,6 +217,25 @@ def test_resnet18_chain_batch2(oracle):
         if L.out_scale is None:
             got = bs.conv2d(spec, cur_dev, w_dev).cpu().numpy()
             assert np.array_equal(got, conv)
+        elif L.shortcut_scale is not None:
+            # the downsampling layer and its 1x1 shortcut in one pass
+            w1 = L.shortcut_weights(wbits)
+            short = oracle.conv2d(
+                oracle.conv_params(batch, L.h, L.w, L.c, L.oc, 1, 1,
+                                   L.stride, 0, abits, wbits),
+                cur, oracle.pack(w1, wbits))
+            want1 = oracle.pack(oracle.quantize(short.astype(np.float32),
+                                                L.shortcut_scale, abits),
+                                abits)
+            cur = oracle.pack(oracle.quantize(conv.astype(np.float32),
+                                              L.out_scale, abits), abits)
+            cur_dev, sc_dev = bs.conv2d_pair_requant(
+                spec, cur_dev, w_dev, bs.pack(dev(w1), wbits), L.out_scale,
+                L.shortcut_scale, abits)
+            torch.cuda.synchronize()
+            assert np.array_equal(words_np(cur_dev).reshape(cur.shape), cur)
+            assert np.array_equal(words_np(sc_dev).reshape(want1.shape),
+                                  want1)
         else:
             cur = oracle.pack(oracle.quantize(conv.astype(np.float32),
                                               L.out_scale, abits), abits)

@@ -668,28 +668,6 @@ def test_conv_requant_special_scales(oracle):
 
 # ------------------------------------------------- int8 comparison baseline --
 
-def test_int8_baseline_equals_bitserial(oracle):
-    # the labelled int8 matrix-core baseline and the bitserial kernels give
-    # the same integers (the baseline is timed next to them in bench.py)
-    from paper_1810_11066_amd import int8_baseline as ib
-    rng = np.random.default_rng(5)
-    n, h, w, c, oc = 4, 14, 14, 64, 64
-    a = rng.integers(0, 4, size=(n, h, w, c), dtype=np.uint8)
-    wq = rng.integers(0, 2, size=(oc, 3, 3, c), dtype=np.uint8)
-    base = ib.conv2d_int8(dev(a), dev(wq), 1, 1)
-    spec = bs.Conv2dSpec(n, h, w, c, oc, 3, 3, 1, 1, 2, 1)
-    got = bs.conv2d(spec, bs.pack(dev(a), 2), bs.pack(dev(wq), 1))
-    torch.cuda.synchronize()
-    assert torch.equal(base, got)
-    m, nn, k = 64, 128, 4096
-    a = rng.integers(0, 4, size=(m, k), dtype=np.uint8)
-    wd = rng.integers(0, 4, size=(nn, k), dtype=np.uint8)
-    base = ib.dense_int8(dev(a), dev(wd))
-    got = bs.dense(bs.pack(dev(a), 2), bs.pack(dev(wd), 2), m, nn, k, 2, 2)
-    torch.cuda.synchronize()
-    assert torch.equal(base, got)
-
-
 # ------------------------------------------------ batch split past 2 GB --
 
 def test_conv_batch_split_over_2gb(oracle):
