@@ -158,10 +158,15 @@ __global__ __launch_bounds__(kBlock) void conv_generic_requant_kernel(
                                               ox, 32 * w + c);
             const uint32_t code =
                 quant_code<false>((float)(int32_t)v, g.scale, g.qmax);
-            for (int b = 0; b < g.bits; ++b) word[b] |= ((code >> b) & 1u) << c;
+            // constant indices keep word[] in registers
+#pragma unroll
+            for (int b = 0; b < 8; ++b)
+                if (b < g.bits) word[b] |= ((code >> b) & 1u) << c;
         }
         uint32_t* dst = g.out + (size_t)pix * (uint32_t)(g.bits * g.words) + w;
-        for (int b = 0; b < g.bits; ++b) dst[(size_t)b * g.words] = word[b];
+#pragma unroll
+        for (int b = 0; b < 8; ++b)
+            if (b < g.bits) dst[(size_t)b * g.words] = word[b];
     }
 }
 
