@@ -75,6 +75,25 @@ def test_mfma_conv_random(oracle, seed):
     assert np.array_equal(got, oracle_conv(oracle, x, wq, s, pad, 7, 8, 2))
 
 
+@pytest.mark.parametrize("shape", [
+    # (n, h, w, c, oc, k, stride, pad)
+    (1, 6, 300, 64, 64, 3, 1, 1),    # input rows too wide for LDS: direct
+    (2, 5, 260, 64, 128, 1, 2, 0),   # direct 1x1
+    (3, 23, 29, 64, 64, 3, 2, 1),    # staged, tiles across images
+    (2, 17, 19, 128, 128, 1, 1, 0),  # staged 1x1, two slices, two blocks
+    (1, 1, 1, 64, 64, 3, 1, 1),      # one pixel, eight padded taps
+    (5, 7, 9, 64, 64, 3, 1, 2),      # pad wider than the window reach
+])
+def test_mfma_conv_kernel_paths(oracle, shape):
+    n, h, w, c, oc, k, s, pad = shape
+    rng = np.random.default_rng(hash(shape) & 0xFFFF)
+    say("int8 mfma conv", shape)
+    x = rng.integers(0, 128, size=(n, h, w, c), dtype=np.int8)
+    wq = rng.integers(-128, 128, size=(oc, k, k, c), dtype=np.int8)
+    got = run_mfma(x, wq, s, pad)
+    assert np.array_equal(got, oracle_conv(oracle, x, wq, s, pad, 7, 8, 2))
+
+
 def test_mfma_conv_config2_full(oracle):
     """Config 2 (A2W1 ResNet-18 layer 2 at batch 64): the codes as int8
     through the matrix cores, every output against the oracle."""
