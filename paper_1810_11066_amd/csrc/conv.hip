@@ -222,9 +222,12 @@ namespace {
 // as keep the packed activations and the int32 output (not the packed
 // output of a requantizing call) within the kernel's 32-bit buffer offsets
 // and its unit counts within int32; 0 when one image is already too large.
-int64_t pix_images_per_launch(const ConvShape& s, bool req) {
+int64_t pix_images_per_launch(const ConvShape& s, bool req,
+                              bool codes = false) {
     const int64_t cw = (s.c + 31) / 32;
-    const int64_t act_img = (int64_t)s.h * s.w * s.abits * cw * 4;
+    // activations: bit-packed words, or (codes) the uint8 codes
+    const int64_t act_img = codes ? (int64_t)s.h * s.w * s.c
+                                  : (int64_t)s.h * s.w * s.abits * cw * 4;
     const int64_t pix_img = (int64_t)s.oh * s.ow;
     const int64_t out_img = req ? 0 : pix_img * s.oc * 4;
     const int64_t lim = pix::kMaxBufferBytes;
@@ -250,7 +253,8 @@ pix::PixKernelFn pix_kernel_for(const ConvShape& s, bool req, int src,
     // output tiles are written in 16-byte quads of channels
     if (s.oc % 4 != 0) return nullptr;
     if (src != pix::kSrcPacked && s.c % 32 != 0) return nullptr;
-    if (pix_images_per_launch(s, req) < 1) return nullptr;
+    if (pix_images_per_launch(s, req, src == pix::kSrcCodes) < 1)
+        return nullptr;
     return pix::pick(s.abits, s.wbits, s.aenc, s.wenc, s.kh, s.sh, (int)cw,
                      req, src, dual, info);
 }
@@ -441,6 +445,9 @@ bool plan_pix_staged(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
             continue;
         }
         g->region_pixels = (int32_t)region;
+        // the kernel reads the uint8 codes (within kMaxBufferBytes:
+        // pix_images_per_launch with codes)
+        g->act_bytes = (int32_t)((int64_t)s.n * s.h * s.w * s.c);
         *lds = need;
         if (need <= assumed ||
             resident_blocks(fn, need) >= resident_blocks(fn, assumed))
@@ -557,7 +564,7 @@ hipError_t launch_pix_staged(const ConvShape& s, const uint8_t* act,
     const pix::PixKernelFn fn =
         pix_kernel_for(s, false, pix::kSrcCodes, &info);
     if (!fn) return hipErrorNotSupported;
-    const int64_t per = pix_images_per_launch(s, false);
+    const int64_t per = pix_images_per_launch(s, false, true);
     struct Chunk {
         int64_t n0;
         pix::PixArgs g;

@@ -104,7 +104,8 @@ struct PixArgs {
     int32_t out_words;     // ceil(oc / 32): words per plane of a pixel
     FastDiv div_ow, div_oh, div_units;
     int32_t c;             // input channels (+-1 activations only)
-    int32_t act_bytes;     // size of the packed activations, bytes
+    int32_t act_bytes;     // size of the activations, bytes: the packed
+                           // words, or the uint8 codes (kSrcCodes)
     int32_t out_bytes;     // size of the int32 output, bytes (0: packed out)
     // activations staged in LDS (SRC != kSrcPacked): the most input pixels
     // any block's region holds (its LDS size)
@@ -619,26 +620,28 @@ __device__ __forceinline__ Region block_region(const PixArgs& g, int p_first,
 // so that the fill waits for memory about once rather than once per item.
 template <int A, int CW>
 __device__ __forceinline__ void stage_region(uint32_t* __restrict__ region,
-                                             const uint8_t* __restrict__ src,
-                                             Region rg) {
+                                             Rsrc src, Region rg) {
     constexpr int PW = A * CW;                 // words per packed pixel
     constexpr int U = 4;
+    // item = 32 codes (one word of every plane of one pixel); items are
+    // numbered in memory order, so item i starts at byte 32 i of the region
     const int items = (rg.hi - rg.lo) * CW;
+    const uint32_t base = (uint32_t)rg.lo * (uint32_t)(32 * CW);
     for (int it0 = threadIdx.x; it0 < items; it0 += U * kBlock) {
         uint32_t d[U][8];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int it = it0 + u * kBlock;
-            uint4 a = make_uint4(0, 0, 0, 0), b = a;
             if (it < items) {
-                const int pl = it / CW, t = it - pl * CW;
-                const uint4* q = reinterpret_cast<const uint4*>(
-                    src + ((size_t)(rg.lo + pl) * CW + t) * 32);
-                a = q[0];
-                b = q[1];
+                const uint32_t off = base + 32u * (uint32_t)it;
+                const uint4 a = __builtin_bit_cast(
+                    uint4, __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0));
+                const uint4 b = __builtin_bit_cast(
+                    uint4,
+                    __builtin_amdgcn_raw_buffer_load_b128(src, off + 16u, 0, 0));
+                d[u][0] = a.x; d[u][1] = a.y; d[u][2] = a.z; d[u][3] = a.w;
+                d[u][4] = b.x; d[u][5] = b.y; d[u][6] = b.z; d[u][7] = b.w;
             }
-            d[u][0] = a.x; d[u][1] = a.y; d[u][2] = a.z; d[u][3] = a.w;
-            d[u][4] = b.x; d[u][5] = b.y; d[u][6] = b.z; d[u][7] = b.w;
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -950,8 +953,7 @@ void conv_pix_kernel(
         const int p_last = min(
             (int)g.div_units.div((uint32_t)(ub1 - 1)) * 64 + 63, g.npix - 1);
         const Region rg = block_region<K, S>(g, p_first, p_last);
-        stage_region<A, CW>(lds + kWavesPerBlock * kTileWords,
-                            reinterpret_cast<const uint8_t*>(act), rg);
+        stage_region<A, CW>(lds + kWavesPerBlock * kTileWords, ract, rg);
         region_lo = rg.lo;
         zero_off = (uint32_t)(rg.hi - rg.lo) * (uint32_t)(4 * A * CW);
         __syncthreads();

@@ -50,6 +50,30 @@ int fail(int st, const char* fmt, ...) {
     return st;
 }
 
+// Division by a fixed divisor d >= 1 for dividends below 2^31, by one
+// multiply-high, an add and a shift (the round-up method of Granlund and
+// Montgomery, "Division by invariant integers using multiplication", 1994):
+// l = ceil(log2 d), m = floor(2^32 (2^l - d) / d) + 1,
+// n / d = (mulhi(n, m) + n) >> l.
+struct Div {
+    uint32_t m;
+    int32_t l;
+};
+
+Div make_div(int32_t d) {
+    int l = 0;
+    while ((1ll << l) < d) ++l;
+    const uint64_t m =
+        ((uint64_t)1 << 32) * (((uint64_t)1 << l) - (uint64_t)d) / (uint64_t)d + 1;
+    return Div{(uint32_t)m, l};
+}
+
+__host__ __device__ inline int32_t div(int32_t n, Div d) {
+    const uint32_t t =
+        (uint32_t)(((uint64_t)(uint32_t)n * (uint64_t)d.m) >> 32);
+    return (int32_t)((t + (uint32_t)n) >> d.l);
+}
+
 struct Args {
     int32_t h, w, c, oc, stride, pad, oh, ow;
     int32_t npix;     // n * oh * ow
@@ -58,6 +82,7 @@ struct Args {
     int32_t act_bytes, out_bytes;
     int32_t tiles;    // staged kernel: ceil(npix / kTilePx)
     int32_t fbytes;   // filter bytes (oc * kh * kw * c)
+    Div by_ow, by_oh;
 };
 
 // Staged kernel: a workgroup takes tiles of kTilePx consecutive output
@@ -75,8 +100,8 @@ __host__ __device__ inline void tile_rows(const Args& g, int k, int tile,
                                           int32_t* lo, int32_t* hi) {
     const int p0 = tile * kTilePx;
     const int p1 = (p0 + kTilePx < g.npix ? p0 + kTilePx : g.npix) - 1;
-    const int r0 = p0 / g.ow, r1 = p1 / g.ow;
-    const int img0 = r0 / g.oh, img1 = r1 / g.oh;
+    const int r0 = div(p0, g.by_ow), r1 = div(p1, g.by_ow);
+    const int img0 = div(r0, g.by_oh), img1 = div(r1, g.by_oh);
     int ylo = (r0 - img0 * g.oh) * g.stride - g.pad;
     int yhi = (r1 - img1 * g.oh) * g.stride - g.pad + k - 1;
     ylo = ylo < 0 ? 0 : (ylo > g.h - 1 ? g.h - 1 : ylo);
@@ -124,8 +149,8 @@ __device__ __forceinline__ Pix pixel_geometry(const Args& g, int tile,
     for (int m = 0; m < 2; ++m) {
         int p = tile * 32 + 16 * m + (lane & 15);
         p = p < g.npix ? p : g.npix - 1;
-        const int row = p / g.ow, ox = p - row * g.ow;
-        const int img = row / g.oh, oy = row - img * g.oh;
+        const int row = div(p, g.by_ow), ox = p - row * g.ow;
+        const int img = div(row, g.by_oh), oy = row - img * g.oh;
         q.iy0[m] = oy * g.stride - g.pad;
         q.ix0[m] = ox * g.stride - g.pad;
         q.base[m] = ((uint32_t)(img * g.h + q.iy0[m]) * (uint32_t)g.w +
@@ -294,7 +319,7 @@ __global__ __launch_bounds__(kBlock) void conv_i8_mfma_3x3_kernel(
 // ds_read_b128 from the rows (or from a 64-byte zero block for a tap in the
 // padding).  A wave computes its 32 pixels against every 64-channel filter
 // block in turn.
-template <int K, int kPieces>
+template <int K, int kPieces, int KC>
 __global__ __launch_bounds__(kBlock) void conv_i8_staged_kernel(
     const int8_t* __restrict__ act, const int8_t* __restrict__ wts,
     int32_t* __restrict__ out, Args g) {
@@ -349,34 +374,68 @@ __global__ __launch_bounds__(kBlock) void conv_i8_staged_kernel(
             // a pixel past the end reads the last pixel's window; its
             // results are not stored
             const int p = pix[m] < g.npix ? pix[m] : g.npix - 1;
-            const int row = p / g.ow, ox = p - row * g.ow;
-            const int img = row / g.oh, oy = row - img * g.oh;
+            const int row = div(p, g.by_ow), ox = p - row * g.ow;
+            const int img = div(row, g.by_oh), oy = row - img * g.oh;
             iy0[m] = oy * g.stride - g.pad;
             ix0[m] = ox * g.stride - g.pad;
             q0[m] = (img * g.h + iy0[m]) * g.w + ix0[m] - lo;
         }
+        // the pixel fragments (A) and filter fragments (B) of one step
+        auto fragments = [&](int tap, int sl, int cb, v4i (&a)[2],
+                             v4i (&b)[4]) {
+            const int r = tap / K, s = tap - r * K;
+#pragma unroll
+            for (int m = 0; m < 2; ++m) {
+                const bool in = (unsigned)(iy0[m] + r) < (unsigned)g.h &&
+                                (unsigned)(ix0[m] + s) < (unsigned)g.w;
+                const uint4* src = in ? rows + (q0[m] + r * g.w + s) * cw +
+                                            sl * 4 + (lane >> 4)
+                                      : zero + (lane >> 4);
+                a[m] = __builtin_bit_cast(v4i, *src);
+            }
+            const uint4* fb =
+                frag + ((size_t)((tap * g.kc + sl) * (g.oc / 16) + cb * 4)) *
+                           64 + lane;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) b[t] = __builtin_bit_cast(v4i, fb[t * 64]);
+        };
+        auto products = [&](const v4i (&a)[2], const v4i (&b)[4],
+                            v4i (&acc)[2][4]) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+                for (int m = 0; m < 2; ++m)
+                    acc[m][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
+                        b[t], a[m], acc[m][t], 0, 0, 0);
+        };
         auto compute = [&](int cb, v4i (&acc)[2][4]) {
 #pragma unroll
             for (int m = 0; m < 2; ++m)
 #pragma unroll
                 for (int t = 0; t < 4; ++t) acc[m][t] = v4i{0, 0, 0, 0};
-            for (int sl = 0; sl < g.kc; ++sl) {
+            if constexpr (KC > 0) {
+                // every step unrolled, the next step's fragments read from
+                // LDS while this step's products run
+                constexpr int kSteps = KC * KK;
+                v4i a[2][2], b[2][4];
+                fragments(0, 0, cb, a[0], b[0]);
 #pragma unroll
-                for (int tap = 0; tap < KK; ++tap) {
-                    const int r = tap / K, s = tap - r * K;
-                    v4i a[2];
+                for (int j = 0; j < kSteps; ++j) {
+                    if (j + 1 < kSteps)
+                        fragments((j + 1) % KK, (j + 1) / KK, cb,
+                                  a[(j + 1) & 1], b[(j + 1) & 1]);
+                    products(a[j & 1], b[j & 1], acc);
+                    // keep the reads a step ahead of their products
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            } else {
+                for (int sl = 0; sl < g.kc; ++sl) {
 #pragma unroll
-                    for (int m = 0; m < 2; ++m) {
-                        const bool in =
-                            (unsigned)(iy0[m] + r) < (unsigned)g.h &&
-                            (unsigned)(ix0[m] + s) < (unsigned)g.w;
-                        const uint4* src =
-                            in ? rows + (q0[m] + r * g.w + s) * cw + sl * 4 +
-                                     (lane >> 4)
-                               : zero + (lane >> 4);
-                        a[m] = __builtin_bit_cast(v4i, *src);
+                    for (int tap = 0; tap < KK; ++tap) {
+                        v4i a[2], b[4];
+                        fragments(tap, sl, cb, a, b);
+                        products(a, b, acc);
                     }
-                    mfma_tap<KK>(frag, g, tap, sl, cb, lane, a, acc);
                 }
             }
         };
@@ -421,18 +480,24 @@ __global__ __launch_bounds__(kBlock) void conv_i8_staged_kernel(
     }
 }
 
-template <int K>
-const void* staged_for(int pieces) {
-    switch (pieces) {
-        case 1: return (const void*)conv_i8_staged_kernel<K, 1>;
-        case 2: return (const void*)conv_i8_staged_kernel<K, 2>;
-        case 3: return (const void*)conv_i8_staged_kernel<K, 3>;
-        case 4: return (const void*)conv_i8_staged_kernel<K, 4>;
-        case 5: return (const void*)conv_i8_staged_kernel<K, 5>;
-        case 6: return (const void*)conv_i8_staged_kernel<K, 6>;
-        case 7: return (const void*)conv_i8_staged_kernel<K, 7>;
-        default: return (const void*)conv_i8_staged_kernel<K, 8>;
+// pieces rounded up to an even count; KC slices unrolled (0: a loop)
+template <int K, int KC>
+const void* staged_for_kc(int pieces) {
+    switch ((pieces + 1) / 2) {
+        case 1: return (const void*)conv_i8_staged_kernel<K, 2, KC>;
+        case 2: return (const void*)conv_i8_staged_kernel<K, 4, KC>;
+        case 3: return (const void*)conv_i8_staged_kernel<K, 6, KC>;
+        default: return (const void*)conv_i8_staged_kernel<K, 8, KC>;
     }
+}
+
+// (3x3 filters within 64 KiB have c = oc = 64: one slice)
+const void* staged_for(int k, int pieces, int kc) {
+    if (k == 3) return kc == 1 ? staged_for_kc<3, 1>(pieces)
+                               : staged_for_kc<3, 0>(pieces);
+    return kc == 1 ? staged_for_kc<1, 1>(pieces)
+         : kc == 2 ? staged_for_kc<1, 2>(pieces)
+                   : staged_for_kc<1, 0>(pieces);
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
@@ -479,6 +544,8 @@ int i8mfma_conv2d(const i8mfma_conv_params* p, const int8_t* act,
     g.act_bytes = (int32_t)act_bytes;
     g.out_bytes = (int32_t)out_bytes;
     g.tiles = (int32_t)((npix + kTilePx - 1) / kTilePx);
+    g.by_ow = make_div(g.ow);
+    g.by_oh = make_div(g.oh);
     g.fbytes = (int32_t)wbytes;
     int dev = 0, cus = 256, max_lds = 160 * 1024;
     if (hipGetDevice(&dev) == hipSuccess) {
@@ -503,7 +570,7 @@ int i8mfma_conv2d(const i8mfma_conv_params* p, const int8_t* act,
     size_t lds;
     int64_t need;
     if (staged) {
-        fn = p->kh == 3 ? staged_for<3>(pieces) : staged_for<1>(pieces);
+        fn = staged_for(p->kh, pieces, g.kc);
         lds = (size_t)staged_lds;
         need = g.tiles;
     } else {

@@ -226,3 +226,26 @@ def test_config2_conv2d_codes_full(oracle):
                          case.wbits)
     got = bs.conv2d_codes(spec, dev(codes), bs.pack(dev(wq), case.wbits))
     assert np.array_equal(got.cpu().numpy(), want)
+
+
+def test_conv2d_codes_split_by_codes_size(oracle):
+    """Codes of more than 2 GiB: the call splits the batch into launches
+    whose uint8 codes stay within one buffer (the packed words, a quarter
+    of the size, would fit one launch).  Every output against the oracle."""
+    n, h, w, c, oc = 1025, 64, 64, 512, 4
+    args = (n, h, w, c, oc, 1, 1, 0, 2, 1, False)
+    say("conv2d_codes split", args)
+    assert n * h * w * c > 2 ** 31
+    rng = np.random.default_rng(424242)
+    codes = rng.integers(0, 256, size=(n, h, w, c), dtype=np.uint8)
+    wq = rng.integers(0, 2, size=(oc, 1, 1, c), dtype=np.uint8)
+    want = expect(oracle, codes, wq, *args)
+    spec = bs.Conv2dSpec(n, h, w, c, oc, 1, 1, 1, 0, 2, 1)
+    g = Guarded(n * h * w * oc)
+    c_dev = dev(codes)
+    del codes
+    bs.bs_conv2d_codes(spec.params(), c_dev, bs.pack(dev(wq), 1), g.t)
+    torch.cuda.synchronize()
+    got = g.t.cpu().numpy().reshape(n, h, w, oc)
+    g.check_guards()
+    assert np.array_equal(got, want)
