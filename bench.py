@@ -350,16 +350,16 @@ def measure(step, describe, steps, warmup, torch):
     and once more with event pairs around each launch, then the activation
     pack launches alone, back to back under one event pair.
 
-    The start event is recorded behind the warmup steps while they are still
-    queued, with no synchronisation in between: the GPU goes from the last
-    warmup step straight into the first timed one, and the timed region
-    never waits for the host to enqueue its first launch."""
+    The timed region is bracketed by device synchronisations: it starts on
+    an idle GPU after the warmup steps have finished, so it includes the
+    host's enqueue of its first launch."""
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     for i in range(warmup):
         step(i)
+    torch.cuda.synchronize()
     h0 = time.perf_counter()
     t_start.record(stream)
     for i in range(steps):
@@ -491,10 +491,11 @@ def per_step_name(case, fused):
         ("bs_dense" if isinstance(case, wl.DenseCase) else "bs_conv2d")
 
 
-def case_line(case, m, args, mu=None):
+def case_line(case, m, args, other=None):
     """One JSON result object for a workload other than the headline one.
-    m: the step as timed (the fused call where it covers the case); mu: the
-    unfused step (pack + conv) of the same case, when m is fused."""
+    m: the step reported (the faster of the fused call and pack + conv
+    where both cover the case); other: the other path's step, reported
+    beside it under "fused" or "unfused"."""
     ops = 2 * case.macs
     fused = m.describe.startswith("activation codes")
     pre_bytes, main_bytes = case_bytes(case, fused=fused)
@@ -515,13 +516,14 @@ def case_line(case, m, args, mu=None):
         "pack_roofline": pack_roofline(pre_bytes, m),
         "host_enqueue_ms_per_step": round(m.host_ms, 5),
     }
-    if mu is not None and mu is not m:
-        _, ubytes = case_bytes(case)
-        line["unfused"] = {
-            "per_step": per_step_name(case, False),
-            "ms_per_step": round(mu.ms_step, 5),
-            "value": round(ops / (mu.ms_step * 1e-3) / 1e9, 1),
-            "roofline": roofline_of(case, mu, ops, ubytes)}
+    if other is not None and other is not m:
+        ofused = other.describe.startswith("activation codes")
+        _, obytes = case_bytes(case, fused=ofused)
+        line["fused" if ofused else "unfused"] = {
+            "per_step": per_step_name(case, ofused),
+            "ms_per_step": round(other.ms_step, 5),
+            "value": round(ops / (other.ms_step * 1e-3) / 1e9, 1),
+            "roofline": roofline_of(case, other, ops, obytes)}
     return line
 
 
@@ -728,6 +730,7 @@ def int8_baseline_lines(args, bs, torch, np, wl) -> int:
         n_sets rotated buffer sets, after warmup."""
         for i in range(max(args.warmup, n_sets)):
             fn(i)
+        torch.cuda.synchronize()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
         t0.record()
@@ -928,10 +931,15 @@ def main() -> int:
                 mf = measure(fz[1], fz[4], args.steps, args.warmup, torch)
                 del fz
                 torch.cuda.empty_cache()
-            if mf is not None:
-                print(json.dumps(case_line(case, mf, args, mu)), flush=True)
-            elif mu is not None:
-                print(json.dumps(case_line(case, mu, args)), flush=True)
+            if mf is not None and mu is not None:
+                # the faster path first, the other beside it
+                first, second = (mf, mu) if mf.ms_step <= mu.ms_step \
+                    else (mu, mf)
+                print(json.dumps(case_line(case, first, args, second)),
+                      flush=True)
+            elif mf is not None or mu is not None:
+                print(json.dumps(case_line(case, mf or mu, args)),
+                      flush=True)
         if args.sweep and len(times) == 16:
             # the paper's limit study quotes W1A1 against W4A4 and W2A2
             # against W1A4 (activation width A, weight width W)
@@ -955,7 +963,13 @@ def main() -> int:
         sets, step, params, w_packed, describe, _ = prepare(case, n_sets, bs,
                                                             torch, np)
         mu = measure(step, describe, args.steps, args.warmup, torch)
-    m = mf if mf is not None else mu
+    # the faster of the fused call and pack + conv (the fused call where
+    # only it ran); the other is reported beside it
+    m = mf if mf is not None and (mu is None or mf.ms_step <= mu.ms_step) \
+        else mu
+    other = (mu if m is mf else mf) if mf is not None and mu is not None \
+        else None
+    m_fused = m is mf
     macs = case.macs
     value_gops = 2 * macs / (m.ms_step * 1e-3) / 1e9
     peak = popcount_roofline_tops(case.abits, case.wbits)
@@ -999,21 +1013,22 @@ def main() -> int:
             "oc": case.oc, "kernel": case.k, "stride": case.stride,
             "pad": case.pad, "abits": case.abits, "wbits": case.wbits,
             "encoding": "unipolar", "output": "int32 NHWC",
-            "per_step": per_step_name(case, mf is not None),
+            "per_step": per_step_name(case, m_fused),
             "buffer_sets": n_sets,
         },
         "roofline": conv_roofline(
-            m, ("codes_" if mf is not None else "") + shape),
+            m, ("codes_" if m_fused else "") + shape),
         "host_enqueue_ms_per_step": round(m.host_ms, 5),
         "pack_roofline": pack_roofline(pack_bytes, mu if mu is not None
                                        else m),
     }
-    if mf is not None and mu is not None:
-        result["unfused"] = {
-            "per_step": per_step_name(case, False),
-            "ms_per_step": round(mu.ms_step, 5),
-            "value": round(2 * macs / (mu.ms_step * 1e-3) / 1e9, 1),
-            "roofline": conv_roofline(mu, shape)}
+    if other is not None:
+        result["unfused" if m_fused else "fused"] = {
+            "per_step": per_step_name(case, not m_fused),
+            "ms_per_step": round(other.ms_step, 5),
+            "value": round(2 * macs / (other.ms_step * 1e-3) / 1e9, 1),
+            "roofline": conv_roofline(
+                other, ("" if m_fused else "codes_") + shape)}
 
     if args.cpu_budget > 0:
         a_host = case.activations()
