@@ -1,6 +1,6 @@
 """Host-side logic of bench.py (no GPU): the roofline peaks, the rotated
-buffer sets, the committed-traffic lookup and its source hash, and the
-one-GPU guard."""
+buffer sets and their assignment to streams, the committed-traffic lookup
+and its source hash, and the one-GPU guard."""
 import os
 import subprocess
 import sys
@@ -63,6 +63,30 @@ def test_rotated_sets_pass_twice_the_infinity_cache():
         if n < 256:
             assert n * (pre + out) >= 512 * 10**6, case.name
     assert bench.sets_for(wl.config2(), 6) == 8
+    for case in cases:
+        assert bench.sets_for(case, 5) % bench.N_STREAMS == 0, case.name
+
+
+@pytest.mark.parametrize("n_sets,n_streams", [(8, 2), (6, 2), (6, 3),
+                                              (12, 4), (7, 1)])
+@pytest.mark.parametrize("first,steps", [(0, 20), (5, 20), (3, 7), (20, 1)])
+def test_steps_that_share_buffers_share_a_stream(n_sets, n_streams, first,
+                                                 steps):
+    bench.check_sets_streams(n_sets, n_streams)
+    streams = [bench.stream_of(j, steps, n_streams) for j in range(steps)]
+    assert streams[-1] == 0                       # stop event's stream
+    for j in range(steps):
+        for k in range(j + 1, steps):
+            if (first + j) % n_sets == (first + k) % n_sets:
+                assert streams[j] == streams[k]
+            if k == j + 1 and n_streams > 1:
+                assert streams[j] != streams[k]   # neighbours alternate
+
+
+def test_sets_not_a_multiple_of_the_streams_are_refused():
+    with pytest.raises(ValueError):
+        bench.check_sets_streams(7, 2)
+    bench.check_sets_streams(0, 2)                # fresh outputs only
 
 
 def test_more_than_one_gpu_is_refused():
