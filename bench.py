@@ -12,8 +12,10 @@ Effective ops = 2 * MACs, MACs = n*oh*ow*oc*kh*kw*c (padded taps counted).
 Inputs are resident in HBM before timing starts; several input/output sets
 are rotated so the working set exceeds the 256 MB Infinity Cache.
 
-Steps are independent batches, each with its own buffer set.  The timed
-region runs them alternately on two HIP streams, so that one batch's conv
+Steps are independent batches, each with its own buffer set.  The warmup
+is --warmup steps and at least 0.2 s of them (the GPU's clocks settle only
+after tens of ms of load); the timed region runs the steps alternately on
+two HIP streams, so that one batch's conv
 starts while the previous one drains (a serving loop with two batches in
 flight), and then once more on one stream; a line reports the faster of the
 two with both beside it.  Kernel durations come from separate passes on one
@@ -406,6 +408,27 @@ def timed_steps(step, first, steps, torch, streams):
 
 
 N_STREAMS = 2
+# the GPU's clocks settle only after tens of ms of sustained load: a config-2
+# step timed right after an idle period runs up to 20 % slower than one timed
+# after 30 ms of work, so the warmup runs at least this long
+WARMUP_MIN_S = 0.2
+
+
+def warm_up(step, warmup, torch, streams, chunk=32):
+    """At least `warmup` steps, and more until the GPU has been busy for
+    WARMUP_MIN_S of wall time, spread over the streams as timed steps are
+    (step i on streams[i % len]); ends with a device synchronisation.
+    Returns the number of steps issued (the next step index)."""
+    ns = len(streams)
+    check_sets_streams(getattr(step, "n_sets", 0), ns)
+    t0 = time.perf_counter()
+    i = 0
+    while i < warmup or time.perf_counter() - t0 < WARMUP_MIN_S:
+        for _ in range(chunk):
+            step(i, stream=streams[i % ns])
+            i += 1
+        torch.cuda.synchronize()
+    return i
 
 
 def make_streams(torch, n):
@@ -427,10 +450,9 @@ def measure(step, describe, steps, warmup, torch):
     host's enqueue of its first launch."""
     streams = make_streams(torch, N_STREAMS)
     stream = streams[0]
-    for i in range(warmup):
-        step(i, stream=streams[i % N_STREAMS])
-    ms_multi, host_ms = timed_steps(step, warmup, steps, torch, streams)
-    ms_one, _ = timed_steps(step, warmup, steps, torch, streams[:1])
+    first = warm_up(step, warmup, torch, streams)
+    ms_multi, host_ms = timed_steps(step, first, steps, torch, streams)
+    ms_one, _ = timed_steps(step, first, steps, torch, streams[:1])
     # kernel durations: events the runtime stamps with each dispatch's own
     # start and end (the library launches through hipExtLaunchKernel while
     # they are set), the figure a kernel trace reports
@@ -771,11 +793,10 @@ def chain_line(args, bs, torch, np, wl, batch=128, abits=2, wbits=1) -> int:
     run.n_sets = len(sets)
 
     streams = make_streams(torch, N_STREAMS)
-    for i in range(args.warmup):
-        run(i, stream=streams[i % len(streams)])
-    by = {len(streams): timed_steps(run, args.warmup, args.steps, torch,
+    first = warm_up(run, args.warmup, torch, streams, chunk=4)
+    by = {len(streams): timed_steps(run, first, args.steps, torch,
                                     streams)[0],
-          1: timed_steps(run, args.warmup, args.steps, torch, streams[:1])[0]}
+          1: timed_steps(run, first, args.steps, torch, streams[:1])[0]}
     n_best = min(by, key=by.get)
     ms = by[n_best]
     ev = [[(torch.cuda.Event(enable_timing=True),
@@ -824,9 +845,8 @@ def int8_baseline_lines(args, bs, torch, np, wl) -> int:
             with torch.cuda.stream(stream or streams[0]):
                 fn(i)
         step.n_sets = n_sets
-        for i in range(max(args.warmup, n_sets)):
-            step(i, streams[i % len(streams)])
-        return timed_steps(step, 0, args.steps, torch, streams)[0]
+        first = warm_up(step, max(args.warmup, n_sets), torch, streams)
+        return timed_steps(step, first, args.steps, torch, streams)[0]
 
     ok_all = True
     for case in (wl.config2(), wl.config3()):
