@@ -71,6 +71,8 @@ _lib = None
 def load_library():
     """Load libbitserial.so (built in-tree by paper_1810_11066_amd.build)."""
     global _lib
+    if _lib is not None:
+        return _lib
     with _lock:
         if _lib is not None:
             return _lib
@@ -131,6 +133,11 @@ def _stream(stream=None):
 
 
 def _dev(t: torch.Tensor, name: str, dtype: torch.dtype, numel: int):
+    """Device address of a contiguous GPU tensor of the given dtype and
+    element count; raises with the reason otherwise."""
+    if (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == dtype
+            and t.numel() == numel and t.is_contiguous()):
+        return t.data_ptr()
     if not isinstance(t, torch.Tensor):
         raise TypeError("%s must be a torch.Tensor" % name)
     if t.device.type != "cuda":
@@ -176,6 +183,17 @@ def bs_quantize_pack(x: torch.Tensor, packed: torch.Tensor, rows: int, k: int,
         rows, k, float(scale), int(bits), int(enc), _stream(stream)))
 
 
+def _out_hw(p: ConvParams):
+    """(oh, ow) of the conv p as bs_conv2d_out_shape computes it, without a
+    library call; for parameters it would reject, the library's error."""
+    if p.stride_h >= 1 and p.stride_w >= 1:
+        eh = p.h + 2 * p.pad_h - p.kh
+        ew = p.w + 2 * p.pad_w - p.kw
+        if eh >= 0 and ew >= 0:
+            return eh // p.stride_h + 1, ew // p.stride_w + 1
+    return bs_conv2d_out_shape(p)
+
+
 def bs_conv2d_out_shape(p: ConvParams):
     oh, ow = ctypes.c_int32(), ctypes.c_int32()
     _check(load_library().bs_conv2d_out_shape(ctypes.byref(p),
@@ -190,7 +208,7 @@ def bs_conv2d_requant(p: ConvParams, act_packed: torch.Tensor,
     """bs_conv2d with its result requantized to out_bits and bit-packed as
     [n][oh][ow][out_bits][ceil(oc/32)] words (the next layer's input)."""
     lib = load_library()
-    oh, ow = bs_conv2d_out_shape(p)
+    oh, ow = _out_hw(p)
     cw = words(p.c)
     _check(lib.bs_conv2d_requant(
         ctypes.byref(p),
@@ -208,7 +226,7 @@ def conv2d_requant(spec: "Conv2dSpec", act_packed: torch.Tensor,
                    w_packed: torch.Tensor, out_scale: float,
                    out_bits: int) -> torch.Tensor:
     p = spec.params()
-    oh, ow = bs_conv2d_out_shape(p)
+    oh, ow = _out_hw(p)
     out = torch.empty((p.n, oh, ow, out_bits, words(p.oc)), dtype=torch.int32,
                       device=act_packed.device)
     bs_conv2d_requant(p, act_packed, w_packed, out_scale, out_bits, out)
@@ -226,7 +244,7 @@ def bs_conv2d_describe(p: ConvParams) -> str:
 def bs_conv2d(p: ConvParams, act_packed: torch.Tensor, w_packed: torch.Tensor,
               out: torch.Tensor, stream=None) -> None:
     lib = load_library()
-    oh, ow = bs_conv2d_out_shape(p)
+    oh, ow = _out_hw(p)
     cw = words(p.c)
     _check(lib.bs_conv2d(
         ctypes.byref(p),
@@ -242,7 +260,7 @@ def bs_conv2d_codes(p: ConvParams, act_codes: torch.Tensor,
                     w_packed: torch.Tensor, out: torch.Tensor,
                     stream=None) -> None:
     """bs_pack of the uint8 NHWC codes fused into bs_conv2d."""
-    oh, ow = bs_conv2d_out_shape(p)
+    oh, ow = _out_hw(p)
     _check(load_library().bs_conv2d_codes(
         ctypes.byref(p),
         _dev(act_codes, "act_codes", torch.uint8, p.n * p.h * p.w * p.c),
@@ -257,7 +275,7 @@ def bs_conv2d_pair(p: ConvParams, act_packed: torch.Tensor,
                    out: torch.Tensor, out1: torch.Tensor,
                    stream=None) -> None:
     """The KxK conv p and its centre-tap 1x1 conv in one pass."""
-    oh, ow = bs_conv2d_out_shape(p)
+    oh, ow = _out_hw(p)
     cw = words(p.c)
     _check(load_library().bs_conv2d_pair(
         ctypes.byref(p),
@@ -276,7 +294,7 @@ def bs_conv2d_pair_requant(p: ConvParams, act_packed: torch.Tensor,
                            out_scale: float, out1_scale: float,
                            out_bits: int, out_packed: torch.Tensor,
                            out1_packed: torch.Tensor, stream=None) -> None:
-    oh, ow = bs_conv2d_out_shape(p)
+    oh, ow = _out_hw(p)
     cw = words(p.c)
     n_out = p.n * oh * ow * out_bits * words(p.oc)
     _check(load_library().bs_conv2d_pair_requant(
@@ -427,7 +445,7 @@ def quantize_pack(x: torch.Tensor, scale: float, bits: int,
 def conv2d(spec: Conv2dSpec, act_packed: torch.Tensor,
            w_packed: torch.Tensor) -> torch.Tensor:
     p = spec.params()
-    oh, ow = bs_conv2d_out_shape(p)
+    oh, ow = _out_hw(p)
     out = torch.empty((spec.n, oh, ow, spec.oc), dtype=torch.int32,
                       device=act_packed.device)
     bs_conv2d(p, act_packed, w_packed, out)
@@ -438,7 +456,7 @@ def conv2d_codes(spec: Conv2dSpec, act_codes: torch.Tensor,
                  w_packed: torch.Tensor) -> torch.Tensor:
     """Conv of uint8 NHWC codes, the activation pack fused into the conv."""
     p = spec.params()
-    oh, ow = bs_conv2d_out_shape(p)
+    oh, ow = _out_hw(p)
     out = torch.empty((spec.n, oh, ow, spec.oc), dtype=torch.int32,
                       device=act_codes.device)
     bs_conv2d_codes(p, act_codes, w_packed, out)
@@ -449,7 +467,7 @@ def conv2d_pair(spec: Conv2dSpec, act_packed: torch.Tensor,
                 w_packed: torch.Tensor, w1_packed: torch.Tensor):
     """(out, out1): the KxK conv and its centre-tap 1x1 conv."""
     p = spec.params()
-    oh, ow = bs_conv2d_out_shape(p)
+    oh, ow = _out_hw(p)
     out = torch.empty((spec.n, oh, ow, spec.oc), dtype=torch.int32,
                       device=act_packed.device)
     out1 = torch.empty_like(out)
@@ -461,7 +479,7 @@ def conv2d_pair_requant(spec: Conv2dSpec, act_packed: torch.Tensor,
                         w_packed: torch.Tensor, w1_packed: torch.Tensor,
                         out_scale: float, out1_scale: float, out_bits: int):
     p = spec.params()
-    oh, ow = bs_conv2d_out_shape(p)
+    oh, ow = _out_hw(p)
     shape = (p.n, oh, ow, out_bits, words(p.oc))
     out = torch.empty(shape, dtype=torch.int32, device=act_packed.device)
     out1 = torch.empty(shape, dtype=torch.int32, device=act_packed.device)

@@ -293,6 +293,27 @@ def test_out_shape(lib):
         assert ow.value == (h + 1 + 2 * pd - k) // s + 1
 
 
+def test_binding_out_shape_matches_the_library(lib):
+    # the binding computes (oh, ow) itself to size its tensor checks; it must
+    # agree with bs_conv2d_out_shape wherever that accepts the parameters,
+    # and report the library's error wherever it does not
+    import itertools
+    oh, ow = ctypes.c_int32(), ctypes.c_int32()
+    for h, w, k, s, pd in itertools.product((1, 2, 7, 14, 57), (1, 3, 56),
+                                            (1, 2, 3, 5), (0, 1, 2, 3),
+                                            (0, 1, 2)):
+        p = params(h=h, w=w, kh=k, kw=k, stride_h=s, stride_w=s, pad_h=pd,
+                   pad_w=pd)
+        st = lib.bs_conv2d_out_shape(ctypes.byref(p), ctypes.byref(oh),
+                                     ctypes.byref(ow))
+        if st == bs.BS_OK:
+            assert bs._out_hw(p) == (oh.value, ow.value)
+        else:
+            with pytest.raises(bs.BitserialError) as e:
+                bs._out_hw(p)
+            assert e.value.status == st
+
+
 def test_kernel_mode(lib):
     assert lib.bs_set_kernel_mode(4) == bs.BS_ERR_INVALID_ARG
     assert lib.bs_set_kernel_mode(-1) == bs.BS_ERR_INVALID_ARG
