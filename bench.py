@@ -227,6 +227,8 @@ class Measured:
     """Times of one workload: the clean step (steps spread over the bench's
     streams, and on one stream), and per-launch kernel times."""
 
+    main_tput_ms = None   # main kernel alone, launches spread over streams
+
     def __init__(self, ms_by_streams, host_ms, pre_ms, main_ms, describe,
                  pre_b2b_ms, pre_ev_ms, main_ev_ms):
         # the step as timed with each stream count; the faster one counts
@@ -306,16 +308,22 @@ def prepare(case, n_sets, bs, torch, np, fused=False):
         else:
             bs.bs_conv2d(params, packed, w_packed, out, stream)
 
-    def step(i, ev=None, pack_only=False, dispatch_ev=None, stream=None):
+    def step(i, ev=None, pack_only=False, dispatch_ev=None, stream=None,
+             main_only=False):
         """One step on set i, on `stream` (default: the current stream at
         preparation).  ev: three events recorded around the launches;
         dispatch_ev: two (start, stop) pairs the library attaches to the pack
         and the conv dispatch themselves.  pack_only: the standalone
-        activation pack alone (also for a fused step, as a reference)."""
+        activation pack alone (also for a fused step, as a reference);
+        main_only: the conv (or dense) launch alone, on the set's packed
+        activations of an earlier step."""
         stream = main_stream if stream is None else stream
         x, packed, out = sets[i % len(sets)]
         if pack_only:
             pack_launch(x, packed, stream)
+            return
+        if main_only:
+            main_launch(x, packed, out, stream)
             return
         if ev is not None:
             ev[0].record(stream)
@@ -487,8 +495,26 @@ def measure(step, describe, steps, warmup, torch):
     p_end.record(stream)
     torch.cuda.synchronize()
     pre_b2b_ms = p_start.elapsed_time(p_end) / steps
-    return Measured(by, host_ms, pre_ms, main_ms, describe, pre_b2b_ms,
-                    pre_ev_ms, main_ev_ms)
+    m = Measured(by, host_ms, pre_ms, main_ms, describe, pre_b2b_ms,
+                 pre_ev_ms, main_ev_ms)
+    if N_STREAMS > 1:
+        # the main kernel alone with its launches spread over the streams:
+        # its throughput once the launches' fixed costs overlap (the
+        # activation pack of a fused step is inside this kernel)
+        def main_only(i, stream=None):
+            step(i, stream=stream, main_only=True)
+        main_only.n_sets = getattr(step, "n_sets", 0)
+        m.main_tput_ms = timed_steps(main_only, 0, steps, torch, streams)[0]
+    return m
+
+
+def throughput_of(m, t_roof_s):
+    """The main kernel alone, launches spread over the streams: ms per
+    launch and its fraction of the roofline (None on one stream)."""
+    if m.main_tput_ms is None:
+        return None
+    return {"streams": N_STREAMS, "ms_per_launch": round(m.main_tput_ms, 5),
+            "frac": round(t_roof_s / (m.main_tput_ms * 1e-3), 4)}
 
 
 def by_streams(m):
@@ -574,6 +600,8 @@ def roofline_of(case, m, ops, main_bytes):
         roof.update(achieved=round(main_bytes / main_s / 1e9, 1),
                     peak=HBM_PEAK_GBS, unit="GB/s (algorithmic bytes)",
                     frac=round(t_hbm / main_s, 4))
+    roof["throughput_streams"] = throughput_of(m, t_alu if bound == "alu"
+                                               else t_hbm)
     return roof
 
 
@@ -662,13 +690,14 @@ def pairs_lines(args, bs, torch, np, wl) -> int:
 
         def mk_step(paired):
             def step(i, ev=None, pack_only=False, dispatch_ev=None,
-                     stream=None):
+                     stream=None, main_only=False):
                 stream = main_stream if stream is None else stream
                 x, packed, o3, o1 = sets[i % n_sets]
                 if not pack_only and dispatch_ev is not None:
                     bs.bs_set_timing_events(*dispatch_ev[0])
-                bs.bs_quantize_pack(x, packed, rows, c3.c, c3.act_scale,
-                                    c3.abits, bs.UNIPOLAR, stream)
+                if not main_only:
+                    bs.bs_quantize_pack(x, packed, rows, c3.c, c3.act_scale,
+                                        c3.abits, bs.UNIPOLAR, stream)
                 if pack_only:
                     return
                 if ev is not None:
@@ -714,6 +743,10 @@ def pairs_lines(args, bs, torch, np, wl) -> int:
             "separate_ms_per_step_by_streams": by_streams(ms),
             "paired_conv_ms": round(mp.main_ms, 5),
             "separate_convs_ms": round(ms.main_ms, 5),
+            "paired_conv_ms_streams": round(mp.main_tput_ms, 5)
+            if mp.main_tput_ms is not None else None,
+            "separate_convs_ms_streams": round(ms.main_tput_ms, 5)
+            if ms.main_tput_ms is not None else None,
             "quantize_pack_ms": round(mp.pre_ms, 5),
             "paired_step_effective_tops": round(
                 2 * macs / (mp.ms_step * 1e-3) / 1e12, 1),
@@ -1112,6 +1145,7 @@ def main() -> int:
                       "conv launch, in a second pass over the same steps",
             "kernel_ms_events_around_launch": round(mm.main_ev_ms, 5),
             "kernel_trace": committed_kernel_trace(workload, 2 * macs, peak),
+            "throughput_streams": throughput_of(mm, 2 * macs / (peak * 1e12)),
         }
 
     shape = "a2w1_b%d_56x56x64_3x3" % case.n
