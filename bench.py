@@ -628,7 +628,8 @@ def case_line(case, m, args, other=None):
                   "popcount-VALU roofline",
         "value": round(ops / (m.ms_step * 1e-3) / 1e9, 1),
         "unit": "GOPS", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(m.ms_step, 5),
+        "warmup": args.warmup, "warmup_min_s": WARMUP_MIN_S,
+        "ms_per_step": round(m.ms_step, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "u32", "data": "synthetic",
         "config": {"workload": case.name,
@@ -1157,6 +1158,7 @@ def main() -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_min_s": WARMUP_MIN_S,
         "ms_per_step": round(m.ms_step, 5),
         "higher_is_better": True,
         "scaling": "weak",
