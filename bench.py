@@ -387,13 +387,13 @@ def check_sets_streams(n_sets, n_streams):
 
 def timed_steps(step, first, steps, torch, streams):
     """Wall time per step of `steps` steps from index `first`, bracketed by
-    device synchronisations and one event pair on the current stream.  Step
-    j runs on streams[(steps - 1 - j) % len(streams)], so consecutive steps
+    device synchronisations and one event pair on streams[0].  Step j runs
+    on streams[(steps - 1 - j) % len(streams)], so consecutive steps
     (independent batches with buffers of their own) alternate streams and
-    the last one runs on the current stream; the other streams wait for the
-    start event, and the current stream for their last step before the stop
-    event.  Returns (ms per step, host enqueue ms per step)."""
-    main = torch.cuda.current_stream()
+    the last one runs on streams[0]; the other streams wait for the start
+    event, and streams[0] for their last step before the stop event.
+    Returns (ms per step, host enqueue ms per step)."""
+    main = streams[0]
     ns = len(streams)
     check_sets_streams(getattr(step, "n_sets", 0), ns)
     torch.cuda.synchronize()
@@ -439,10 +439,20 @@ def warm_up(step, warmup, torch, streams, chunk=32):
     return i
 
 
+_STREAMS = []
+
+
 def make_streams(torch, n):
-    """The current stream and n - 1 more, all at the default priority."""
-    return [torch.cuda.current_stream()] + \
-        [torch.cuda.Stream() for _ in range(n - 1)]
+    """Streams for timed steps: the current stream when n is 1, else n
+    streams of the default priority created once per process and reused.
+    The runtime spreads streams over a few hardware queues (4 by default)
+    as they are created, so streams made afresh for every measurement would
+    sooner or later share one queue and run one after the other."""
+    if n == 1:
+        return [torch.cuda.current_stream()]
+    while len(_STREAMS) < n:
+        _STREAMS.append(torch.cuda.Stream())
+    return _STREAMS[:n]
 
 
 def measure(step, describe, steps, warmup, torch):
@@ -457,13 +467,14 @@ def measure(step, describe, steps, warmup, torch):
     an idle GPU after the warmup steps have finished, so it includes the
     host's enqueue of its first launch."""
     streams = make_streams(torch, N_STREAMS)
-    stream = streams[0]
+    stream = torch.cuda.current_stream()     # the single-stream passes
     first = warm_up(step, warmup, torch, streams)
     by = {}
     if N_STREAMS > 1:
         by[N_STREAMS], host_ms = timed_steps(step, first, steps, torch,
                                              streams)
-    by[1], host_one = timed_steps(step, first, steps, torch, streams[:1])
+    by[1], host_one = timed_steps(step, first, steps, torch,
+                                  make_streams(torch, 1))
     if N_STREAMS == 1:
         host_ms = host_one
     # kernel durations: events the runtime stamps with each dispatch's own
@@ -833,7 +844,8 @@ def chain_line(args, bs, torch, np, wl, batch=128, abits=2, wbits=1) -> int:
 
     streams = make_streams(torch, N_STREAMS)
     first = warm_up(run, args.warmup, torch, streams, chunk=4)
-    by = {1: timed_steps(run, first, args.steps, torch, streams[:1])[0]}
+    by = {1: timed_steps(run, first, args.steps, torch,
+                         make_streams(torch, 1))[0]}
     if len(streams) > 1:
         by[len(streams)] = timed_steps(run, first, args.steps, torch,
                                        streams)[0]
