@@ -458,10 +458,11 @@ def make_streams(torch, n):
 def measure(step, describe, steps, warmup, torch):
     """Clean timed regions: the steps spread over N_STREAMS streams, then
     the same steps on one stream (the step counts at the faster of the two;
-    both are reported).  Then the same steps again with dispatch-stamped
-    events on each launch for kernel times and once more with event pairs
-    around each launch, then the activation pack launches alone, back to
-    back under one event pair.  The kernel-time passes run on one stream.
+    both are reported), then the main kernel alone spread over the streams.
+    Then the same steps again with dispatch-stamped events on each launch
+    for kernel times and once more with event pairs around each launch,
+    then the activation pack launches alone, back to back under one event
+    pair.  The kernel-time passes run on one stream.
 
     Each timed region is bracketed by device synchronisations: it starts on
     an idle GPU after the warmup steps have finished, so it includes the
@@ -477,6 +478,18 @@ def measure(step, describe, steps, warmup, torch):
                                   make_streams(torch, 1))
     if N_STREAMS == 1:
         host_ms = host_one
+    main_tput_ms = None
+    if N_STREAMS > 1:
+        # the main kernel alone with its launches spread over the streams:
+        # its throughput once the launches' fixed costs overlap (the
+        # activation pack of a fused step is inside this kernel).  Timed
+        # before the passes below: the memory-bound pack launches leave
+        # the GPU at clocks that slow the next compute-bound pass.
+        def main_only(i, stream=None):
+            step(i, stream=stream, main_only=True)
+        main_only.n_sets = getattr(step, "n_sets", 0)
+        main_tput_ms = timed_steps(main_only, first, steps, torch,
+                                   streams)[0]
     # kernel durations: events the runtime stamps with each dispatch's own
     # start and end (the library launches through hipExtLaunchKernel while
     # they are set), the figure a kernel trace reports
@@ -508,14 +521,7 @@ def measure(step, describe, steps, warmup, torch):
     pre_b2b_ms = p_start.elapsed_time(p_end) / steps
     m = Measured(by, host_ms, pre_ms, main_ms, describe, pre_b2b_ms,
                  pre_ev_ms, main_ev_ms)
-    if N_STREAMS > 1:
-        # the main kernel alone with its launches spread over the streams:
-        # its throughput once the launches' fixed costs overlap (the
-        # activation pack of a fused step is inside this kernel)
-        def main_only(i, stream=None):
-            step(i, stream=stream, main_only=True)
-        main_only.n_sets = getattr(step, "n_sets", 0)
-        m.main_tput_ms = timed_steps(main_only, 0, steps, torch, streams)[0]
+    m.main_tput_ms = main_tput_ms
     return m
 
 
