@@ -30,6 +30,12 @@
  *  - Thread safety: calls from several host threads are safe; the only
  *    library state is per thread (the error string, the kernel mode, the
  *    run-length override and the timing events).
+ *  - Concurrency: calls on different streams may run on the GPU at the same
+ *    time.  A call touches device memory only through its own inputs and
+ *    outputs, so concurrent calls are independent unless one writes what
+ *    another reads or writes; order those on one stream or with events.
+ *    Independent batches spread over two streams let one call's kernel fill
+ *    the GPU while the previous one drains.
  */
 #ifndef BITSERIAL_H
 #define BITSERIAL_H
