@@ -178,12 +178,13 @@ bs_status bs_conv2d(const bs_conv2d_params *p, const uint32_t *act_packed,
  *   w_packed, out and the result: as bs_conv2d.
  * p->aenc is the encoding of the codes.
  * Errors: as bs_conv2d; BS_ERR_UNSUPPORTED when no fused kernel covers the
- * shape (c must be a multiple of 32, oc of 4, kernels square of size 1 or 3,
- * stride 1 or 2, activations unipolar with unipolar 1-2-bit or bipolar 1-bit
- * filters, the whole kh x kw x abits x (c/32)-word window within 72 words,
- * and the packed input rows that the windows of 256 consecutive output
- * pixels span, plus 17 KB, within 64 KB of LDS -- only very narrow images
- * miss this): pack with bs_pack and call bs_conv2d instead.
+ * shape (c must be 32 times a power of two, at most 512 for 3x3 windows
+ * and 4096 for 1x1 ones, oc a multiple of 4, kernels square of size 1 or 3,
+ * stride 1 or 2, unipolar activations of 1-4 bits with unipolar filters of
+ * 1-4 bits or bipolar 1-bit filters, and the packed input rows that the
+ * windows of 256 consecutive output pixels span, plus 17 KB, within 64 KB
+ * of LDS -- only very wide rows or very many channels miss this): pack
+ * with bs_pack and call bs_conv2d instead.
  * Nothing is enqueued on any error. */
 bs_status bs_conv2d_codes(const bs_conv2d_params *p, const uint8_t *act_codes,
                           const uint32_t *w_packed, int32_t *out,

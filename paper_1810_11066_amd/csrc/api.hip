@@ -456,11 +456,11 @@ bs_status bs_conv2d_codes(const bs_conv2d_params* p, const uint8_t* act_codes,
     if (e == hipErrorNotSupported)
         return fail(BS_ERR_UNSUPPORTED,
                     "bs_conv2d_codes: no fused kernel covers this shape (it "
-                    "needs c a multiple of 32, oc a multiple of 4, square "
+                    "needs c = 32 times a power of two (at most 512 for 3x3 "
+                    "windows, 4096 for 1x1 ones), oc a multiple of 4, square "
                     "kernels of size 1 or 3, stride 1 or 2, unipolar "
-                    "activations with unipolar filters of 1-2 bits or "
-                    "bipolar 1-bit filters, the whole kh x kw x abits x "
-                    "c/32-word patch within 72 words, and the input rows of "
+                    "activations of 1-4 bits with unipolar filters of 1-4 "
+                    "bits or bipolar 1-bit filters, and the input rows of "
                     "one workgroup's outputs within its LDS); bit-pack the "
                     "activations and call bs_conv2d");
     return from_hip(e, "bs_conv2d_codes launch");

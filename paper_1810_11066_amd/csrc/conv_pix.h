@@ -660,42 +660,48 @@ __device__ __forceinline__ void stage_region(uint32_t* __restrict__ region,
     for (int i = threadIdx.x; i < PW; i += kBlock) region[zero + i] = 0;
 }
 
-// Loads the lane's whole patch from the staged region: the same taps and
-// words as load_patch, at byte offsets relative to the region (win.base is
-// relative to its first pixel; a tap in the padding reads the zero pixel at
-// byte offset zero_off).
-template <int A, int K, int CW>
+// Loads the lane's words of one reduction block from the staged region: the
+// same taps [t0, t0 + TB) and words [c0, c0 + CB) of each plane as
+// load_patch, at byte offsets relative to the region (win.base is relative
+// to its first pixel; a tap in the padding reads the zero pixel at byte
+// offset zero_off).  With TB = K*K and CB = CW: the whole patch.
+template <int A, int K, int CW, int TB, int CB>
 __device__ __forceinline__ void load_patch_lds(
-    uint32_t (&patch)[K * K][A][CW], const uint32_t* __restrict__ region,
-    const PixArgs& g, const Window& win, uint32_t zero_off) {
+    uint32_t (&patch)[TB][A][CB], const uint32_t* __restrict__ region,
+    const PixArgs& g, const Window& win, uint32_t zero_off, int t0, int c0) {
     constexpr uint32_t PWB = 4 * A * CW;
     const uint32_t rowb = (uint32_t)g.w * PWB;
     const char* base = reinterpret_cast<const char*>(region);
 #pragma unroll
-    for (int t = 0; t < K * K; ++t) {
+    for (int tt = 0; tt < TB; ++tt) {
+        const int t = t0 + tt;
         const int r = t / K, s = t - r * K;
         const bool in = (unsigned)(win.iy0 + r) < (unsigned)g.h &&
                         (unsigned)(win.ix0 + s) < (unsigned)g.w;
         const uint32_t off =
-            in ? win.base + (uint32_t)r * rowb + (uint32_t)s * PWB : zero_off;
+            (in ? win.base + (uint32_t)r * rowb + (uint32_t)s * PWB
+                : zero_off) + 4u * (uint32_t)c0;
 #pragma unroll
         for (int i = 0; i < A; ++i) {
             const char* p = base + off + 4u * (uint32_t)(i * CW);
-            if constexpr (CW % 4 == 0) {
+            if constexpr (CB % 4 == 0) {
 #pragma unroll
-                for (int k = 0; k < CW; k += 4) {
+                for (int k = 0; k < CB; k += 4) {
                     const uint4 x = *reinterpret_cast<const uint4*>(p + 4 * k);
-                    patch[t][i][k] = x.x; patch[t][i][k + 1] = x.y;
-                    patch[t][i][k + 2] = x.z; patch[t][i][k + 3] = x.w;
+                    patch[tt][i][k] = x.x; patch[tt][i][k + 1] = x.y;
+                    patch[tt][i][k + 2] = x.z; patch[tt][i][k + 3] = x.w;
                 }
-            } else if constexpr (CW % 2 == 0) {
+            } else if constexpr (CB % 2 == 0) {
 #pragma unroll
-                for (int k = 0; k < CW; k += 2) {
+                for (int k = 0; k < CB; k += 2) {
                     const uint2 x = *reinterpret_cast<const uint2*>(p + 4 * k);
-                    patch[t][i][k] = x.x; patch[t][i][k + 1] = x.y;
+                    patch[tt][i][k] = x.x; patch[tt][i][k + 1] = x.y;
                 }
             } else {
-                patch[t][i][0] = *reinterpret_cast<const uint32_t*>(p);
+#pragma unroll
+                for (int k = 0; k < CB; ++k)
+                    patch[tt][i][k] =
+                        *reinterpret_cast<const uint32_t*>(p + 4 * k);
             }
         }
     }
@@ -902,7 +908,7 @@ constexpr int min_waves_per_simd() {
 // S: stride; CW: words per bit-plane; REQ: requantize and bit-pack the output
 // (out then holds [npix][out_bits][out_words] uint32 words) instead of
 // storing int32; SRC: where the activations come from (kSrcPacked, or
-// kSrcCodes staged in LDS, whole patches only); DUAL: also the 1x1 conv of
+// kSrcCodes staged in LDS); DUAL: also the 1x1 conv of
 // the same stride whose input pixel is the window's centre tap (pad
 // (K-1)/2), over the same output grid and channels, with filters wts1 and
 // output g.out1 (whole patches only).  wts1 is a kernel argument, read-only
@@ -918,8 +924,8 @@ void conv_pix_kernel(
     PixArgs g) {
     using Pl = Plan<A, W, K, CW>;
     constexpr int FW = Pl::FW, NB = Pl::NB;
-    static_assert(SRC == kSrcPacked || (NB == 1 && !REQ),
-                  "staged activations: whole patches, int32 output");
+    static_assert(SRC == kSrcPacked || !REQ,
+                  "staged activations: int32 output");
     static_assert(!DUAL || (NB == 1 && K % 2 == 1 && SRC == kSrcPacked &&
                             (E == 3 * kUnipolar + kUnipolar ||
                              E == 3 * kUnipolar + kBipolar)),
@@ -1003,7 +1009,8 @@ void conv_pix_kernel(
         Visit v = visit_at(u);
         uint32_t patch[Pl::TB][A][CW];
         if constexpr (SRC != kSrcPacked)
-            load_patch_lds<A, K, CW>(patch, region, g, v.win, zero_off);
+            load_patch_lds<A, K, CW, K * K, CW>(patch, region, g, v.win,
+                                                zero_off, 0, 0);
         else
             load_patch<A, K, CW, Pl::TB, CW>(patch, ract, g, v.win, 0, 0);
         if constexpr (kAhead && !REQ) {
@@ -1174,8 +1181,8 @@ void conv_pix_kernel(
             } else {
                 v = visit_at(u);
                 if constexpr (SRC != kSrcPacked)
-                    load_patch_lds<A, K, CW>(patch, region, g, v.win,
-                                             zero_off);
+                    load_patch_lds<A, K, CW, K * K, CW>(patch, region, g,
+                                                        v.win, zero_off, 0, 0);
                 else
                     load_patch<A, K, CW, Pl::TB, CW>(patch, ract, g, v.win, 0,
                                                      0);
@@ -1201,9 +1208,14 @@ void conv_pix_kernel(
                 };
                 auto load_block = [&](Patch& pt, int nb) {
                     const int tb = nb / Pl::NCB;
-                    load_patch<A, K, CW, Pl::TB, Pl::CB>(
-                        pt, ract, g, v.win, tb * Pl::TB,
-                        (nb - tb * Pl::NCB) * Pl::CB);
+                    if constexpr (SRC != kSrcPacked)
+                        load_patch_lds<A, K, CW, Pl::TB, Pl::CB>(
+                            pt, region, g, v.win, zero_off, tb * Pl::TB,
+                            (nb - tb * Pl::NCB) * Pl::CB);
+                    else
+                        load_patch<A, K, CW, Pl::TB, Pl::CB>(
+                            pt, ract, g, v.win, tb * Pl::TB,
+                            (nb - tb * Pl::NCB) * Pl::CB);
                 };
                 if constexpr (Pl::DBUF) {
                     // block nb + 1 loads while block nb computes
@@ -1307,8 +1319,7 @@ PixKernelFn pick_bipolar_act(int we, int k, int s, int cw, PlanInfo* info);
 // Specialisations (included by the sources above).  Requantizing variants
 // exist for unipolar activations with unipolar or bipolar filters only;
 // staged activations (src != kSrcPacked) for unipolar activations with
-// unipolar filters of 1 or 2 bits or bipolar 1-bit filters, whole patches,
-// int32 output; paired kernels (dual) for unipolar activations with
+// unipolar or bipolar filters, int32 output; paired kernels (dual) for unipolar activations with
 // unipolar or bipolar filters, 3x3 windows, whole patches, and at most 16
 // filter words per quad of the 1x1 conv (W CW <= 4), int32 or requantized
 // output.
@@ -1337,7 +1348,7 @@ PixKernelFn pick_kscw(bool req, int src, bool dual, PlanInfo* info) {
             }
         }
         if (src != kSrcPacked) {
-            if constexpr (Pl::NB == 1 && (E == UU || E == UB) && W <= 2) {
+            if constexpr (E == UU || E == UB) {
                 if (req || src != kSrcCodes) return nullptr;
                 return conv_pix_kernel<A, W, E, K, S, CW, false, kSrcCodes,
                                        false>;

@@ -166,9 +166,12 @@ def test_conv_pointer_validation(lib):
     (dict(c=48), bs.BS_ERR_UNSUPPORTED),            # c not a multiple of 32
     (dict(oc=6), bs.BS_ERR_UNSUPPORTED),            # oc not a multiple of 4
     (dict(kh=5, kw=5, pad_h=2, pad_w=2), bs.BS_ERR_UNSUPPORTED),
-    (dict(wbits=3), bs.BS_ERR_UNSUPPORTED),
+    (dict(wbits=5), bs.BS_ERR_UNSUPPORTED),         # filters above 4 bits
+    (dict(abits=5), bs.BS_ERR_UNSUPPORTED),         # codes above 4 bits
     (dict(aenc=2, wenc=2, wbits=2), bs.BS_ERR_UNSUPPORTED),  # signed
-    (dict(c=256), bs.BS_ERR_UNSUPPORTED),           # 144-word 3x3 window
+    (dict(aenc=1, abits=1), bs.BS_ERR_UNSUPPORTED),  # +-1 activations
+    (dict(c=96), bs.BS_ERR_UNSUPPORTED),            # 3 words per plane
+    (dict(c=1024), bs.BS_ERR_UNSUPPORTED),          # 32 words, 3x3 window
 ])
 def test_fused_conv_validation(lib, bad, status):
     # disjoint fake buffers, so that the overlap check passes

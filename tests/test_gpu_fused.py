@@ -1,6 +1,7 @@
 """GPU parity of the fused call bs_conv2d_codes (bit-pack of uint8 codes
 inside the conv kernel) against the oracle's pack -> conv2d on the same
-seeded inputs.
+seeded inputs, for whole-window kernels and for kernels that split the
+reduction into blocks read from the staged region.
 
 Each workgroup of these kernels packs the input rows its outputs read into
 LDS, so the tests vary what decides those regions: image sizes, strides,
@@ -170,6 +171,37 @@ def test_conv2d_codes_random(oracle, seed):
     run_codes(oracle, args, seed=seed, run=run)
 
 
+def random_staged_blocks(rng):
+    """A shape whose fused kernel splits the reduction into blocks (the
+    kh x kw x abits x c/32-word window above 72 words: one filter row, one
+    tap, or one tap and part of each plane per block), or whose filters
+    have 3 or 4 bits."""
+    while True:
+        k = int(rng.choice([1, 3]))
+        s = int(rng.choice([1, 2]))
+        pad = int(rng.integers(0, 2)) if k == 3 else 0
+        abits = int(rng.integers(1, 5))
+        bipolar = bool(rng.integers(0, 3) == 0)
+        wbits = 1 if bipolar else int(rng.integers(1, 5))
+        cw = int(rng.choice([4, 8, 16] if k == 3 else [16, 32, 64, 128]))
+        if window_words(k, abits, cw) > 72 or wbits >= 3:
+            break
+    n = int(rng.integers(1, 3))
+    h, w = int(rng.integers(1, 13)), int(rng.integers(1, 13))
+    h, w = max(h, k - 2 * pad), max(w, k - 2 * pad)
+    oc = 4 * int(rng.integers(1, 13))
+    return n, h, w, 32 * cw, oc, k, s, pad, abits, wbits, bipolar
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_conv2d_codes_blocks_random(oracle, seed):
+    rng = np.random.default_rng(7300 + seed)
+    args = random_staged_blocks(rng)
+    run = int(rng.choice([0, 0, 1, 2, 3, 5, 7, 13]))
+    say("conv2d_codes blocks", args, "run", run)
+    run_codes(oracle, args, seed=seed, run=run)
+
+
 # fixed shapes: ResNet-style layers at small batch, blocks spanning images
 CODES_SHAPES = [
     # n, h, w, c, oc, k, s, pad, abits, wbits, bipolar
@@ -185,6 +217,15 @@ CODES_SHAPES = [
     (2, 24, 22, 64, 68, 1, 1, 2, 4, 1, False),
     (3, 5, 6, 64, 8, 1, 2, 2, 2, 1, False),
     (2, 4, 4, 32, 8, 3, 1, 3, 2, 1, False),
+    # reduction blocks: filter rows, taps, taps x part of each plane
+    (2, 14, 14, 256, 64, 3, 1, 1, 2, 1, False),
+    (2, 14, 14, 256, 32, 3, 1, 1, 4, 4, False),
+    (2, 14, 14, 256, 64, 3, 2, 1, 3, 3, False),
+    (3, 7, 7, 512, 16, 3, 1, 1, 2, 1, False),
+    (2, 9, 9, 512, 8, 3, 1, 1, 1, 1, True),
+    (2, 10, 9, 128, 36, 3, 2, 1, 3, 3, False),
+    (1, 5, 7, 4096, 16, 1, 1, 0, 2, 2, False),
+    (2, 6, 6, 1024, 8, 1, 2, 0, 4, 3, False),
 ]
 
 
