@@ -342,6 +342,21 @@ __device__ __forceinline__ Rsrc make_rsrc(const void* p, int32_t bytes) {
                                              bytes, kRsrcWord3);
 }
 
+// Cache policy of the int32 result stores (the buffer instruction's aux
+// bits): 0, the default write-back through the XCD's L2, or kStoreAgent
+// (sc1), agent scope, which writes through that L2.  Measured per launch on
+// ResNet-18 layers 6-12 and the 128- and 256-channel layers of the encodings
+// workloads (at least 4 words per plane, A >= 2), agent-scope stores are
+// 1-2.7 us shorter: less is left dirty for the write-back that ends each
+// launch.  For the 64-channel layers (2 words per plane) and the one-bit
+// activation kernels they are neutral or up to 4.7 us longer, and there the
+// default stays.
+constexpr int kStoreAgent = 16;
+template <int A, int CW>
+constexpr int out_store_policy() {
+    return CW >= 4 && A >= 2 ? kStoreAgent : 0;
+}
+
 // Where a lane's 16-byte pieces of a tile flush go.  A flush moves the
 // tile's 64 pixels x kChunk channels in kFlushRounds rounds: in round r lane
 // l stores quad l % kFlushRounds of pixel r * 64 / kFlushRounds +
@@ -367,8 +382,8 @@ struct FlushMap {
 // wave's tile (nch a multiple of 4 up to kChunk: the lanes of quads below
 // nch / 4 take part, the others store out of range).  SERIAL: one round's
 // data in registers at a time, for flushes that run while a large input
-// patch is held.
-template <bool SERIAL>
+// patch is held.  CPOL: the stores' cache policy (out_store_policy).
+template <bool SERIAL, int CPOL>
 __device__ __forceinline__ void flush_tile(const uint32_t* __restrict__ tile,
                                            Rsrc out, const FlushMap& fm,
                                            int oc_base, int nch, int lane) {
@@ -385,7 +400,7 @@ __device__ __forceinline__ void flush_tile(const uint32_t* __restrict__ tile,
         const u32x4 v = {e[0], e[1], e[2], e[3]};
         const bool in = qin && fm.pix0 + kFlushPixels * r + pr < fm.npix;
         __builtin_amdgcn_raw_buffer_store_b128(
-            v, out, in ? o0 + (uint32_t)r * rstep : kOutOfRange, 0, 0);
+            v, out, in ? o0 + (uint32_t)r * rstep : kOutOfRange, 0, CPOL);
         if constexpr (SERIAL) __builtin_amdgcn_sched_barrier(0);
     }
 }
@@ -924,6 +939,7 @@ void conv_pix_kernel(
     PixArgs g) {
     using Pl = Plan<A, W, K, CW>;
     constexpr int FW = Pl::FW, NB = Pl::NB;
+    constexpr int kCpol = out_store_policy<A, CW>();
     static_assert(SRC == kSrcPacked || !REQ,
                   "staged activations: int32 output");
     static_assert(!DUAL || (NB == 1 && K % 2 == 1 && SRC == kSrcPacked &&
@@ -1018,9 +1034,10 @@ void conv_pix_kernel(
             // entered, as it is re-entered, with the patch load followed by
             // one flush's stores, so the wait for the patch can leave those
             // in flight
-            flush_tile<kSerialFlush>(tile, rout, v.fm, 0, 0, lane);
+            flush_tile<kSerialFlush, kCpol>(tile, rout, v.fm, 0, 0, lane);
             if constexpr (DUAL)
-                flush_tile<kSerialFlush>(tile, rout1, v.fm, 0, 0, lane);
+                flush_tile<kSerialFlush, kCpol>(tile, rout1, v.fm, 0, 0,
+                                                lane);
         }
         while (true) {
             if constexpr (kAhead) {
@@ -1088,8 +1105,8 @@ void conv_pix_kernel(
             // flush writes 64-byte pieces of the pixel rows)
             auto flush_chunk = [&]() __attribute__((always_inline)) {
                 wave_lds_sync();
-                flush_tile<kSerialFlush>(tile, rout, v.fm, chunk_base,
-                                         held * 4, lane);
+                flush_tile<kSerialFlush, kCpol>(tile, rout, v.fm,
+                                                chunk_base, held * 4, lane);
                 if constexpr (DUAL) {
                     wave_lds_sync();
                     uint32_t* row = tile + lane * kTileStride;
@@ -1101,8 +1118,9 @@ void conv_pix_kernel(
                                       row[h * 4 + o] = x;
                                   });
                     wave_lds_sync();
-                    flush_tile<kSerialFlush>(tile, rout1, v.fm, chunk_base,
-                                             held * 4, lane);
+                    flush_tile<kSerialFlush, kCpol>(tile, rout1, v.fm,
+                                                    chunk_base, held * 4,
+                                                    lane);
                 }
                 wave_lds_sync();
                 chunk_base += held * 4;
@@ -1262,8 +1280,8 @@ void conv_pix_kernel(
                     }
                 } else {
                     wave_lds_sync();
-                    flush_tile<false>(tile, rout, v.fm, 4 * sub, nq * 4,
-                                      lane);
+                    flush_tile<false, kCpol>(tile, rout, v.fm, 4 * sub,
+                                             nq * 4, lane);
                     wave_lds_sync();
                 }
             }
