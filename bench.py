@@ -370,9 +370,10 @@ def prepare(case, n_sets, bs, torch, np, fused=False):
 
 def stream_of(j, steps, n_streams):
     """Stream index of step j of `steps` timed steps: consecutive steps
-    alternate, and the last one runs on stream 0 (the one that records the
-    stop event)."""
-    return (steps - 1 - j) % n_streams
+    alternate, and the first one runs on stream 0, right behind the start
+    event (a first launch on another stream sits behind a wait for that
+    event and starts several us later)."""
+    return j % n_streams
 
 
 def check_sets_streams(n_sets, n_streams):
@@ -388,10 +389,11 @@ def check_sets_streams(n_sets, n_streams):
 def timed_steps(step, first, steps, torch, streams):
     """Wall time per step of `steps` steps from index `first`, bracketed by
     device synchronisations and one event pair on streams[0].  Step j runs
-    on streams[(steps - 1 - j) % len(streams)], so consecutive steps
-    (independent batches with buffers of their own) alternate streams and
-    the last one runs on streams[0]; the other streams wait for the start
-    event, and streams[0] for their last step before the stop event.
+    on streams[stream_of(j, ...)], so consecutive steps (independent
+    batches with buffers of their own) alternate streams and the first one
+    follows the start event on streams[0]; each other stream waits for the
+    start event just before its first step, and streams[0] waits for the
+    other streams' last steps before the stop event.
     Returns (ms per step, host enqueue ms per step)."""
     main = streams[0]
     ns = len(streams)
@@ -401,11 +403,12 @@ def timed_steps(step, first, steps, torch, streams):
     t_end = torch.cuda.Event(enable_timing=True)
     h0 = time.perf_counter()
     t_start.record(main)
-    for s in streams[1:]:
-        s.wait_event(t_start)
     for j in range(steps):
-        step(first + j, stream=streams[stream_of(j, steps, ns)])
-    for s in streams[1:]:
+        k = stream_of(j, steps, ns)
+        if j == k and k > 0:
+            streams[k].wait_event(t_start)
+        step(first + j, stream=streams[k])
+    for s in streams[1:min(ns, steps)]:
         done = torch.cuda.Event()
         done.record(s)
         main.wait_event(done)

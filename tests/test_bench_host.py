@@ -74,7 +74,7 @@ def test_steps_that_share_buffers_share_a_stream(n_sets, n_streams, first,
                                                  steps):
     bench.check_sets_streams(n_sets, n_streams)
     streams = [bench.stream_of(j, steps, n_streams) for j in range(steps)]
-    assert streams[-1] == 0                       # stop event's stream
+    assert streams[0] == 0                        # start event's stream
     for j in range(steps):
         for k in range(j + 1, steps):
             if (first + j) % n_sets == (first + k) % n_sets:
