@@ -354,10 +354,11 @@ def prepare(case, n_sets, bs, torch, np, fused=False):
         describe = bs.bs_conv2d_describe(bs.Conv2dSpec(
             1, 1, case.m, case.k, case.n, 1, 1, 1, 0, case.abits,
             case.wbits).params())
+    elif fused:
+        describe = "activation codes bit-packed into LDS: " + \
+            bs.bs_conv2d_codes_describe(params)
     else:
         describe = bs.bs_conv2d_describe(params)
-    if fused:
-        describe = "activation codes bit-packed into LDS: " + describe
     # initialisation: one step per set writes every packed and output buffer
     # once, so that no buffer is first written inside a timed region
     for i in range(n_sets):

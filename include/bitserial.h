@@ -254,6 +254,16 @@ bs_status bs_conv2d_pair_requant(const bs_conv2d_params *p,
 bs_status bs_conv2d_describe(const bs_conv2d_params *p, char *buf,
                              int32_t len);
 
+/* As bs_conv2d_describe, for bs_conv2d_codes (the activation pack fused
+ * into the conv, Sec. 3.1 bitpack with Eq. 2): the staged kernel and its
+ * launch plan -- grid, block, LDS bytes (output tiles plus the largest
+ * input region a workgroup packs), that region in pixels, run length.
+ * Host only, nothing is enqueued.
+ * Errors: as bs_conv2d_describe; BS_ERR_UNSUPPORTED (buf empty) where
+ * bs_conv2d_codes would return it. */
+bs_status bs_conv2d_codes_describe(const bs_conv2d_params *p, char *buf,
+                                   int32_t len);
+
 /* Bitserial dense / matrix multiply (Sec. 3.2; evaluated in Sec. 6.2.1):
  *   a_packed: [m][abits][ceil(k/32)], w_packed: [n][wbits][ceil(k/32)] uint32
  *   (each output neuron's weights contiguous along the reduction axis),

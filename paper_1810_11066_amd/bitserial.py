@@ -45,7 +45,7 @@ EXPORTED = ("bs_packed_words", "bs_quantize", "bs_pack", "bs_pack_ex",
             "bs_quantize_pack",
             "bs_conv2d_out_shape", "bs_conv2d", "bs_conv2d_requant",
             "bs_conv2d_codes", "bs_conv2d_pair", "bs_conv2d_pair_requant",
-            "bs_conv2d_describe",
+            "bs_conv2d_describe", "bs_conv2d_codes_describe",
             "bs_dense", "bs_dense_ex", "bs_status_string",
             "bs_last_error", "bs_set_kernel_mode", "bs_set_units_per_wave",
             "bs_set_timing_events", "bs_abi_version")
@@ -103,6 +103,9 @@ def load_library():
                                        ci, P, P]),
             "bs_conv2d_describe": (ci, [ctypes.POINTER(ConvParams),
                                         ctypes.c_char_p, ctypes.c_int32]),
+            "bs_conv2d_codes_describe": (ci, [ctypes.POINTER(ConvParams),
+                                              ctypes.c_char_p,
+                                              ctypes.c_int32]),
             "bs_dense": (ci, [i64, i64, i64, ci, ci, ci, P, P, P, P]),
             "bs_dense_ex": (ci, [i64, i64, i64, ci, ci, ci, ci, P, P, P, P]),
             "bs_status_string": (ctypes.c_char_p, [ci]),
@@ -238,6 +241,14 @@ def bs_conv2d_describe(p: ConvParams) -> str:
     this thread's kernel mode (host only)."""
     buf = ctypes.create_string_buffer(256)
     _check(load_library().bs_conv2d_describe(ctypes.byref(p), buf, 256))
+    return buf.value.decode()
+
+
+def bs_conv2d_codes_describe(p: ConvParams) -> str:
+    """Kernel and launch plan bs_conv2d_codes would use for ``p`` (the
+    staged plan, with its LDS region; host only)."""
+    buf = ctypes.create_string_buffer(320)
+    _check(load_library().bs_conv2d_codes_describe(ctypes.byref(p), buf, 320))
     return buf.value.decode()
 
 

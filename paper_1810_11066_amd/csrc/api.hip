@@ -189,7 +189,7 @@ hipError_t launch_kernel(const void* fn, dim3 grid, dim3 block, void** args,
 
 extern "C" {
 
-int bs_abi_version(void) { return 107; }
+int bs_abi_version(void) { return 108; }
 
 int64_t bs_packed_words(int64_t k) { return k <= 0 ? 0 : (k + 31) / 32; }
 
@@ -430,6 +430,15 @@ bs_status bs_conv2d_pair_requant(const bs_conv2d_params* p,
                     "bs_conv2d_pair_requant launch");
 }
 
+// Why bs_conv2d_codes refuses a shape.
+const char* const kNoFusedKernel =
+    "no fused kernel covers this shape (it needs c = 32 times a power of "
+    "two (at most 512 for 3x3 windows, 4096 for 1x1 ones), oc a multiple of "
+    "4, square kernels of size 1 or 3, stride 1 or 2, unipolar activations "
+    "of 1-4 bits with unipolar filters of 1-4 bits or bipolar 1-bit "
+    "filters, and the input rows of one workgroup's outputs within its "
+    "LDS); bit-pack the activations and call bs_conv2d";
+
 // bs_pack of the codes fused into bs_conv2d: validation as bs_conv2d, with
 // the codes' bytes in the overlap check.
 bs_status bs_conv2d_codes(const bs_conv2d_params* p, const uint8_t* act_codes,
@@ -454,15 +463,7 @@ bs_status bs_conv2d_codes(const bs_conv2d_params* p, const uint8_t* act_codes,
     const hipError_t e = bs::launch_conv_codes(s, act_codes, w_packed, out,
                                                g_conv_opt, (hipStream_t)stream);
     if (e == hipErrorNotSupported)
-        return fail(BS_ERR_UNSUPPORTED,
-                    "bs_conv2d_codes: no fused kernel covers this shape (it "
-                    "needs c = 32 times a power of two (at most 512 for 3x3 "
-                    "windows, 4096 for 1x1 ones), oc a multiple of 4, square "
-                    "kernels of size 1 or 3, stride 1 or 2, unipolar "
-                    "activations of 1-4 bits with unipolar filters of 1-4 "
-                    "bits or bipolar 1-bit filters, and the input rows of "
-                    "one workgroup's outputs within its LDS); bit-pack the "
-                    "activations and call bs_conv2d");
+        return fail(BS_ERR_UNSUPPORTED, "bs_conv2d_codes: %s", kNoFusedKernel);
     return from_hip(e, "bs_conv2d_codes launch");
 }
 
@@ -504,6 +505,21 @@ bs_status bs_conv2d_describe(const bs_conv2d_params* p, char* buf,
     bs::ConvShape s;
     if ((st = check_conv(p, &s)) != BS_OK) return st;
     bs::describe_conv(s, g_conv_opt, buf, (size_t)len);
+    return ok();
+}
+
+bs_status bs_conv2d_codes_describe(const bs_conv2d_params* p, char* buf,
+                                   int32_t len) {
+    if (!buf || len < 1) return fail(BS_ERR_INVALID_ARG, "buf/len");
+    buf[0] = '\0';
+    bs_status st;
+    bs::ConvShape s;
+    if ((st = check_conv(p, &s)) != BS_OK) return st;
+    if (bs::describe_conv_codes(s, g_conv_opt, buf, (size_t)len) < 0) {
+        buf[0] = '\0';
+        return fail(BS_ERR_UNSUPPORTED, "bs_conv2d_codes: %s",
+                    kNoFusedKernel);
+    }
     return ok();
 }
 

@@ -183,6 +183,11 @@ hipError_t launch_conv_codes(const ConvShape& s, const uint8_t* act,
 int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
                   size_t len);
 
+// The same for launch_conv_codes (the staged plan); -1, with buf untouched,
+// where launch_conv_codes would return hipErrorNotSupported.
+int describe_conv_codes(const ConvShape& s, const ConvOptions& opt, char* buf,
+                        size_t len);
+
 // True when launch_conv with mode 0 would use a specialised kernel.
 bool conv_has_fast_path(const ConvShape& s);
 

@@ -29,6 +29,7 @@
 // accumulating v_bcnt_u32_b32 per word pair, into A+W-1 per-shift
 // accumulators per output; the shift-add (and bipolar correction) runs once
 // per output.
+#include <algorithm>
 #include <atomic>
 #include <cstdio>
 #include <cstring>
@@ -329,13 +330,24 @@ int64_t max_region_pixels(const ConvShape& s, const pix::PixArgs& g) {
         if (p1 > g.npix - 1) p1 = g.npix - 1;
         const int64_t r0 = p0 / s.ow, n0 = r0 / s.oh, y0 = r0 % s.oh;
         const int64_t r1 = p1 / s.ow, n1 = r1 / s.oh, y1 = r1 % s.oh;
-        int64_t iy_lo = y0 * s.sh - s.ph, iy_hi = y1 * s.sh - s.ph + s.kh - 1;
-        if (iy_lo < 0) iy_lo = 0;
-        if (iy_lo > s.h) iy_lo = s.h;
-        if (iy_hi > s.h - 1) iy_hi = s.h - 1;
-        if (iy_hi < -1) iy_hi = -1;
-        const int64_t lo = (n0 * s.h + iy_lo) * s.w;
-        const int64_t hi = (n1 * s.h + iy_hi) * s.w + s.w;
+        const int64_t x0 = p0 - r0 * s.ow, x1 = p1 - r1 * s.ow;
+        const int64_t a = y0 * s.sh - s.ph, b = y1 * s.sh - s.ph + s.kh - 1;
+        const int64_t iy_lo = std::min<int64_t>(std::max<int64_t>(a, 0), s.h);
+        const int64_t iy_hi =
+            std::max<int64_t>(std::min<int64_t>(b, s.h - 1), -1);
+        int64_t lo = (n0 * s.h + iy_lo) * s.w;
+        int64_t hi = (n1 * s.h + iy_hi) * s.w + s.w;
+        // the columns of the first and last tap rows that no tap reads
+        // (pix::block_region)
+        if (a >= 0 && a < s.h)
+            lo += std::min<int64_t>(std::max<int64_t>(x0 * s.sw - s.pw, 0),
+                                    s.w - 1);
+        if (b >= 0 && b < s.h)
+            hi -= s.w - 1 - std::max<int64_t>(
+                                std::min<int64_t>(x1 * s.sw - s.pw + s.kw - 1,
+                                                  s.w - 1),
+                                0);
+        if (hi < lo) hi = lo;
         if (hi - lo > best) best = hi - lo;
     }
     std::lock_guard<std::mutex> lock(mu);
@@ -724,6 +736,49 @@ hipError_t launch_conv_codes(const ConvShape& s, const uint8_t* act,
     return launch_pix_staged(s, act, wts, out, opt.units_per_wave, st);
 }
 
+namespace {
+
+// The encodings a pixel-kernel specialisation was compiled for, as text.
+void kernel_encodings(const pix::PlanInfo& info, char* out, size_t len) {
+    static const char* const names[3] = {"unipolar", "bipolar", "signed"};
+    if (info.enc / 3 == kUnipolar)
+        snprintf(out, len, "%s", names[info.enc % 3]);
+    else
+        snprintf(out, len, "%s x %s", names[info.enc / 3],
+                 names[info.enc % 3]);
+}
+
+}  // namespace
+
+int describe_conv_codes(const ConvShape& s, const ConvOptions& opt, char* buf,
+                        size_t len) {
+    pix::PlanInfo info{};
+    const pix::PixKernelFn fn =
+        pix_kernel_for(s, false, pix::kSrcCodes, &info);
+    if (!fn) return -1;
+    // the plan of the first launch (of `launches` image chunks)
+    const int64_t per = pix_images_per_launch(s, false, true);
+    ConvShape c = s;
+    c.n = (int32_t)(s.n < per ? s.n : per);
+    pix::PixArgs g;
+    dim3 grid;
+    size_t lds = 0;
+    if (!plan_pix_staged(c, fn, opt.units_per_wave, &g, &grid, &lds))
+        return -1;
+    const int64_t launches = (s.n + per - 1) / per;
+    char kenc[48];
+    kernel_encodings(info, kenc, sizeof(kenc));
+    return snprintf(buf, len,
+                    "conv_pix_kernel<A=%d,W=%d,%s,K=%d,S=%d,CW=%d> "
+                    "staged codes: patch=%dtaps x %dwords slice=%dch x "
+                    "%dtaps grid=%u block=%d lds=%zu region=%dpx units=%d "
+                    "units_per_wave=%d%s",
+                    s.abits, s.wbits, kenc, s.kh, s.sh, (s.c + 31) / 32,
+                    info.tb, info.cb, info.ocb, info.ts, grid.x, pix::kBlock,
+                    lds, g.region_pixels, g.units, g.per_wave,
+                    launches > 1 ? " (per launch; batch split)" : "");
+}
+
 int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
                   size_t len) {
     const int mode = opt.mode;
@@ -747,13 +802,8 @@ int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
             pix::PixArgs g;
             plan_pix(c, pfn, opt.units_per_wave, nullptr, &g, &grid, &lds);
             const int64_t launches = (s.n + per - 1) / per;
-            // the encodings the specialisation was compiled for
             char kenc[48];
-            if (info.enc / 3 == kUnipolar)
-                snprintf(kenc, sizeof(kenc), "%s", names[info.enc % 3]);
-            else
-                snprintf(kenc, sizeof(kenc), "%s x %s", names[info.enc / 3],
-                         names[info.enc % 3]);
+            kernel_encodings(info, kenc, sizeof(kenc));
             return snprintf(buf, len,
                             "conv_pix_kernel<A=%d,W=%d,%s,K=%d,S=%d,CW=%d> "
                             "patch=%dtaps x %dwords slice=%dch x %dtaps "

@@ -599,8 +599,13 @@ __device__ __forceinline__ void pack32_planes(const uint32_t (&d)[8],
 }
 
 // Input region of a block: the flat NHWC input pixels [lo, hi) that hold
-// every in-range tap of the block's output pixels, from the first tap row of
-// its first output pixel to the last tap row of its last one.
+// every in-range tap of the block's output pixels, from the first tap of
+// its first output pixel to the last tap of its last one.  The first tap row
+// a of the first output row y0 is read by no other output row (the next
+// one's taps start S rows lower), and only by the block's pixels at x >= x0,
+// so its columns left of x0 S - pw stay out; likewise the last tap row of the
+// last output row right of x1 S - pw + K - 1.  The host sizes the LDS with
+// the same rule.
 struct Region {
     int32_t lo, hi;
 };
@@ -610,17 +615,23 @@ __device__ __forceinline__ Region block_region(const PixArgs& g, int p_first,
                                                int p_last) {
     const uint32_t r0 = g.div_ow.div((uint32_t)p_first);
     const uint32_t n0 = g.div_oh.div(r0), y0 = r0 - n0 * (uint32_t)g.oh;
+    const int x0 = p_first - (int)(r0 * (uint32_t)g.ow);
     const uint32_t r1 = g.div_ow.div((uint32_t)p_last);
     const uint32_t n1 = g.div_oh.div(r1), y1 = r1 - n1 * (uint32_t)g.oh;
+    const int x1 = p_last - (int)(r1 * (uint32_t)g.ow);
     // first and last input row of the block's taps, clamped to [0, h] and
     // [-1, h - 1]: with padding above K - 1 an output row can lie wholly in
     // the padding, and its image then contributes no row (row h of image
     // n0 is row 0 of image n0 + 1; row -1 of image n1 ends image n1 - 1)
-    const int iy_lo = min(max((int)y0 * S - g.ph, 0), g.h);
-    const int iy_hi = max(min((int)y1 * S - g.ph + K - 1, g.h - 1), -1);
+    const int a = (int)y0 * S - g.ph, b = (int)y1 * S - g.ph + K - 1;
+    const int iy_lo = min(max(a, 0), g.h);
+    const int iy_hi = max(min(b, g.h - 1), -1);
     Region rg;
     rg.lo = ((int)n0 * g.h + iy_lo) * g.w;
     rg.hi = ((int)n1 * g.h + iy_hi) * g.w + g.w;
+    if (a >= 0 && a < g.h) rg.lo += min(max(x0 * S - g.pw, 0), g.w - 1);
+    if (b >= 0 && b < g.h)
+        rg.hi -= g.w - 1 - max(min(x1 * S - g.pw + K - 1, g.w - 1), 0);
     // an all-padding block (no in-range tap) holds nothing; the host sized
     // the LDS for the largest region, which bounds every block's
     rg.hi = min(max(rg.hi, rg.lo), rg.lo + g.region_pixels);

@@ -41,7 +41,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_words(lib):
-    assert lib.bs_abi_version() == 107
+    assert lib.bs_abi_version() == 108
     for k, w in [(0, 0), (1, 1), (31, 1), (32, 1), (33, 2), (4096, 128)]:
         assert lib.bs_packed_words(k) == w
 
@@ -502,3 +502,74 @@ def test_requant_validation(lib):
              STREAM) == bs.BS_ERR_INVALID_ARG
     assert r(ctypes.byref(params(abits=8, wbits=8, c=4000)), FAKE, FAKE, 0.5,
              2, FAKE, STREAM) == bs.BS_ERR_OVERFLOW
+
+
+def _staged_region(n, h, w, k, s, pad, oc, run):
+    """Largest input region (pixels) a 4-wave block of `run` units per wave
+    packs for a fused conv: the flat NHWC input rows from the first tap row
+    of the block's first output pixel to the last tap row of its last one,
+    without the columns of those two rows (when they are inside the image)
+    that only pixels outside the block read.  Checked here to hold every
+    in-range tap of every output pixel of the block."""
+    oh = (h + 2 * pad - k) // s + 1
+    ow = (w + 2 * pad - k) // s + 1
+    npix = n * oh * ow
+    gu = oc // 4
+    units = -(-npix // 64) * gu
+    best = 0
+    for ub0 in range(0, units, 4 * run):
+        ub1 = min(ub0 + 4 * run, units)
+        p0, p1 = ub0 // gu * 64, min((ub1 - 1) // gu * 64 + 63, npix - 1)
+        (n0, y0, x0), (n1, y1, x1) = [
+            ((p // ow) // oh, (p // ow) % oh, p % ow) for p in (p0, p1)]
+        a, b = y0 * s - pad, y1 * s - pad + k - 1
+        lo = (n0 * h + min(max(a, 0), h)) * w
+        hi = (n1 * h + max(min(b, h - 1), -1)) * w + w
+        if 0 <= a < h:
+            lo += min(max(x0 * s - pad, 0), w - 1)
+        if 0 <= b < h:
+            hi -= w - 1 - max(min(x1 * s - pad + k - 1, w - 1), 0)
+        hi = max(hi, lo)
+        for p in range(p0, p1 + 1):
+            img, y, x = (p // ow) // oh, (p // ow) % oh, p % ow
+            for dy in range(k):
+                for dx in range(k):
+                    iy, ix = y * s - pad + dy, x * s - pad + dx
+                    if 0 <= iy < h and 0 <= ix < w:
+                        assert lo <= (img * h + iy) * w + ix < hi
+        best = max(best, hi - lo)
+    return best
+
+
+@pytest.mark.parametrize("shape", [
+    dict(n=2, h=9, w=10, k=3, s=1, pad=1, oc=16, run=3),
+    dict(n=3, h=7, w=13, k=3, s=2, pad=1, oc=64, run=5),
+    dict(n=2, h=12, w=12, k=1, s=2, pad=0, oc=128, run=2)])
+def test_codes_describe_reports_the_staged_plan(lib, shape):
+    # the fused call's plan: its own kernel (staged codes), run length and
+    # the input region of its largest block
+    sh = dict(shape)
+    run = sh.pop("run")
+    p = params(n=sh["n"], h=sh["h"], w=sh["w"], c=64, oc=sh["oc"],
+               kh=sh["k"], kw=sh["k"], stride_h=sh["s"], stride_w=sh["s"],
+               pad_h=sh["pad"], pad_w=sh["pad"], abits=2, wbits=1)
+    try:
+        assert lib.bs_set_units_per_wave(run) == bs.BS_OK
+        d = bs.bs_conv2d_codes_describe(p)
+    finally:
+        assert lib.bs_set_units_per_wave(0) == bs.BS_OK
+    assert d.startswith("conv_pix_kernel<A=2,W=1,unipolar,K=%d,S=%d,CW=2> "
+                        "staged codes:" % (sh["k"], sh["s"]))
+    assert "units_per_wave=%d" % run in d
+    assert " region=%dpx " % _staged_region(run=run, **sh) in d
+
+
+def test_codes_describe_refusals(lib):
+    buf = ctypes.create_string_buffer(64)
+    d = lib.bs_conv2d_codes_describe
+    assert d(ctypes.byref(params()), None, 64) == bs.BS_ERR_INVALID_ARG
+    assert d(ctypes.byref(params()), buf, 0) == bs.BS_ERR_INVALID_ARG
+    # c = 96 has no fused kernel: refused as bs_conv2d_codes refuses it
+    assert d(ctypes.byref(params(c=96)), buf, 64) == bs.BS_ERR_UNSUPPORTED
+    assert buf.value == b""
+    assert b"no fused kernel" in lib.bs_last_error()
