@@ -303,9 +303,10 @@ int resident_blocks(pix::PixKernelFn fn, size_t lds) {
 }
 
 // Largest input region, in pixels, that a block of a staged launch packs
-// into LDS (pix::block_region for every block of the plan in g; blocks are
-// only renumbered by the XCD-major order, so the set of regions is the
-// same).  Exact, by a pass over the blocks, cached per shape and run length.
+// into LDS (pix::block_region, or for strided 1x1 windows the block's output
+// pixel count, for every block of the plan in g; blocks are only renumbered
+// by the XCD-major order, so the set of regions is the same).  Exact, by a
+// pass over the blocks, cached per shape and run length.
 int64_t max_region_pixels(const ConvShape& s, const pix::PixArgs& g) {
     struct Entry {
         int32_t key[12];
@@ -328,6 +329,12 @@ int64_t max_region_pixels(const ConvShape& s, const pix::PixArgs& g) {
         const int64_t p0 = ub0 / g.group_units * 64;
         int64_t p1 = (ub1 - 1) / g.group_units * 64 + 63;
         if (p1 > g.npix - 1) p1 = g.npix - 1;
+        if (s.kh == 1 && s.sh > 1) {
+            // strided 1x1 windows gather one input pixel per output pixel
+            // (pix::stage_gather)
+            if (p1 + 1 - p0 > best) best = p1 + 1 - p0;
+            continue;
+        }
         const int64_t r0 = p0 / s.ow, n0 = r0 / s.oh, y0 = r0 % s.oh;
         const int64_t r1 = p1 / s.ow, n1 = r1 / s.oh, y1 = r1 % s.oh;
         const int64_t x0 = p0 - r0 * s.ow, x1 = p1 - r1 * s.ow;

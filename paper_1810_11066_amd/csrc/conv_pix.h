@@ -686,6 +686,65 @@ __device__ __forceinline__ void stage_region(uint32_t* __restrict__ region,
     for (int i = threadIdx.x; i < PW; i += kBlock) region[zero + i] = 0;
 }
 
+// Strided 1x1 windows read one input pixel per output pixel, S rows and S
+// columns apart.  Their region is gathered instead: the input pixels of the
+// block's output pixels [q_lo, q_hi), in output order ([q - q_lo][A][CW]
+// words), so that the rows and columns no tap reads are neither loaded nor
+// packed; an output pixel whose input pixel lies in the padding gets zeros
+// (its loads fall past the buffer).  Then the zero pixel, as stage_region.
+template <int A, int CW, int S>
+__device__ __forceinline__ void stage_gather(uint32_t* __restrict__ region,
+                                             Rsrc src, const PixArgs& g,
+                                             int q_lo, int q_hi) {
+    constexpr int PW = A * CW;
+    constexpr int U = 4;
+    const int items = (q_hi - q_lo) * CW;
+    for (int it0 = threadIdx.x; it0 < items; it0 += U * kBlock) {
+        uint32_t d[U][8];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int it = it0 + u * kBlock;
+            if (it < items) {
+                const int q = q_lo + it / CW, t = it % CW;
+                const uint32_t row = g.div_ow.div((uint32_t)q);
+                const int x = q - (int)(row * (uint32_t)g.ow);
+                const uint32_t img = g.div_oh.div(row);
+                const int y = (int)(row - img * (uint32_t)g.oh);
+                const int iy = y * S - g.ph, ix = x * S - g.pw;
+                const bool in = (unsigned)iy < (unsigned)g.h &&
+                                (unsigned)ix < (unsigned)g.w;
+                const uint32_t off =
+                    in ? ((img * (uint32_t)g.h + (uint32_t)iy) *
+                              (uint32_t)g.w + (uint32_t)ix) *
+                                 (uint32_t)(32 * CW) +
+                             32u * (uint32_t)t
+                       : kOutOfRange;
+                const uint4 a = __builtin_bit_cast(
+                    uint4, __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0));
+                const uint4 b = __builtin_bit_cast(
+                    uint4,
+                    __builtin_amdgcn_raw_buffer_load_b128(src, off + 16u, 0, 0));
+                d[u][0] = a.x; d[u][1] = a.y; d[u][2] = a.z; d[u][3] = a.w;
+                d[u][4] = b.x; d[u][5] = b.y; d[u][6] = b.z; d[u][7] = b.w;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int it = it0 + u * kBlock;
+            if (it < items) {
+                const int pl = it / CW, t = it % CW;
+                uint32_t w[A];
+                pack32_planes<A>(d[u], w);
+#pragma unroll
+                for (int b = 0; b < A; ++b)
+                    region[pl * PW + b * CW + t] = w[b];
+            }
+        }
+    }
+    const int zero = (q_hi - q_lo) * PW;
+    for (int i = threadIdx.x; i < PW; i += kBlock) region[zero + i] = 0;
+}
+
 // Loads the lane's words of one reduction block from the staged region: the
 // same taps [t0, t0 + TB) and words [c0, c0 + CB) of each plane as
 // load_patch, at byte offsets relative to the region (win.base is relative
@@ -973,7 +1032,9 @@ void conv_pix_kernel(
 
     // staged activations: the block packs its input region into LDS (after
     // the waves' output tiles) before any wave computes; every wave of the
-    // block takes part, also one whose own run is empty
+    // block takes part, also one whose own run is empty.  Strided 1x1
+    // windows gather one input pixel per output pixel (stage_gather).
+    constexpr bool kGather = SRC != kSrcPacked && K == 1 && S > 1;
     [[maybe_unused]] const uint32_t* region = lds + kWavesPerBlock * kTileWords;
     [[maybe_unused]] int32_t region_lo = 0;
     [[maybe_unused]] uint32_t zero_off = 0;
@@ -985,10 +1046,19 @@ void conv_pix_kernel(
         const int p_first = (int)g.div_units.div((uint32_t)ub0) * 64;
         const int p_last = min(
             (int)g.div_units.div((uint32_t)(ub1 - 1)) * 64 + 63, g.npix - 1);
-        const Region rg = block_region<K, S>(g, p_first, p_last);
-        stage_region<A, CW>(lds + kWavesPerBlock * kTileWords, ract, rg);
-        region_lo = rg.lo;
-        zero_off = (uint32_t)(rg.hi - rg.lo) * (uint32_t)(4 * A * CW);
+        if constexpr (kGather) {
+            // the host sized the LDS for the largest block's pixel count
+            const int q_hi = min(p_last + 1, p_first + g.region_pixels);
+            stage_gather<A, CW, S>(lds + kWavesPerBlock * kTileWords, ract,
+                                   g, p_first, q_hi);
+            region_lo = p_first;
+            zero_off = (uint32_t)(q_hi - p_first) * (uint32_t)(4 * A * CW);
+        } else {
+            const Region rg = block_region<K, S>(g, p_first, p_last);
+            stage_region<A, CW>(lds + kWavesPerBlock * kTileWords, ract, rg);
+            region_lo = rg.lo;
+            zero_off = (uint32_t)(rg.hi - rg.lo) * (uint32_t)(4 * A * CW);
+        }
         __syncthreads();
     }
 
@@ -1010,10 +1080,13 @@ void conv_pix_kernel(
         v.oy = (int)(rowi - img * (uint32_t)g.oh);
         v.win.iy0 = v.oy * S - g.ph;
         v.win.ix0 = v.ox * S - g.pw;
-        v.win.base = ((img * (uint32_t)g.h + (uint32_t)v.win.iy0) *
-                          (uint32_t)g.w + (uint32_t)v.win.ix0 -
-                      (uint32_t)region_lo) *
-                     (uint32_t)(4 * A * CW);
+        if constexpr (kGather)
+            v.win.base = (pc - (uint32_t)region_lo) * (uint32_t)(4 * A * CW);
+        else
+            v.win.base = ((img * (uint32_t)g.h + (uint32_t)v.win.iy0) *
+                              (uint32_t)g.w + (uint32_t)v.win.ix0 -
+                          (uint32_t)region_lo) *
+                         (uint32_t)(4 * A * CW);
         if constexpr (!REQ) v.fm.init(v.pix0, g.npix, g.oc);
         return v;
     };

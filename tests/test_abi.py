@@ -509,8 +509,9 @@ def _staged_region(n, h, w, k, s, pad, oc, run):
     packs for a fused conv: the flat NHWC input rows from the first tap row
     of the block's first output pixel to the last tap row of its last one,
     without the columns of those two rows (when they are inside the image)
-    that only pixels outside the block read.  Checked here to hold every
-    in-range tap of every output pixel of the block."""
+    that only pixels outside the block read, checked here to hold every
+    in-range tap of every output pixel of the block; for strided 1x1
+    windows, one gathered input pixel per output pixel of the block."""
     oh = (h + 2 * pad - k) // s + 1
     ow = (w + 2 * pad - k) // s + 1
     npix = n * oh * ow
@@ -520,6 +521,10 @@ def _staged_region(n, h, w, k, s, pad, oc, run):
     for ub0 in range(0, units, 4 * run):
         ub1 = min(ub0 + 4 * run, units)
         p0, p1 = ub0 // gu * 64, min((ub1 - 1) // gu * 64 + 63, npix - 1)
+        if k == 1 and s > 1:
+            # strided 1x1 windows: one gathered input pixel per output pixel
+            best = max(best, p1 + 1 - p0)
+            continue
         (n0, y0, x0), (n1, y1, x1) = [
             ((p // ow) // oh, (p // ow) % oh, p % ow) for p in (p0, p1)]
         a, b = y0 * s - pad, y1 * s - pad + k - 1
