@@ -244,20 +244,31 @@ class Measured:
         self.describe = describe
 
 
+# how the description of a fused step's kernel starts
+FUSED_CODES = "activation codes bit-packed into LDS: "
+FUSED_FLOAT = "float32 activations quantized and bit-packed into LDS: "
+
+
+def is_fused(describe: str) -> bool:
+    return describe.startswith((FUSED_CODES, FUSED_FLOAT))
+
+
 def prepare(case, n_sets, bs, torch, np, fused=False):
     """Device buffers for `n_sets` rotated steps of a conv or dense case, and
     the per-step launch function.  Inputs are the workload's seeded host
     arrays (rolled along the batch axis for sets beyond the first); weights
     are packed once, outside the timed steps.
 
-    fused: the step is one call that bit-packs the uint8 activation codes
-    inside the conv kernel (bs_conv2d_codes) instead of bs_pack followed by
-    bs_conv2d; None is returned when the fused kernels do not cover the case
-    (dense, float32 activations quantized per call, other shapes)."""
+    fused: the step is one call that bit-packs the activations inside the
+    conv kernel -- uint8 codes (bs_conv2d_codes) instead of bs_pack followed
+    by bs_conv2d, or float32 values quantized per call (bs_conv2d_quantized,
+    1x1 windows) instead of bs_quantize_pack followed by bs_conv2d; None is
+    returned when the fused kernels do not cover the case (dense, other
+    shapes)."""
     from paper_1810_11066_amd import workloads as wl
     main_stream = torch.cuda.current_stream()
     dense = isinstance(case, wl.DenseCase)
-    if fused and (dense or case.act_scale is not None):
+    if fused and dense:
         return None
     if dense:
         rows, k, abits = case.m, case.k, case.abits
@@ -303,6 +314,9 @@ def prepare(case, n_sets, bs, torch, np, fused=False):
         if dense:
             bs.bs_dense(case.m, case.n, case.k, case.abits, case.wbits,
                         bs.UNIPOLAR, packed, w_packed, out, stream)
+        elif fused and quantized:
+            bs.bs_conv2d_quantized(params, x, case.act_scale, w_packed, out,
+                                   stream)
         elif fused:
             bs.bs_conv2d_codes(params, x, w_packed, out, stream)
         else:
@@ -354,9 +368,10 @@ def prepare(case, n_sets, bs, torch, np, fused=False):
         describe = bs.bs_conv2d_describe(bs.Conv2dSpec(
             1, 1, case.m, case.k, case.n, 1, 1, 1, 0, case.abits,
             case.wbits).params())
+    elif fused and quantized:
+        describe = FUSED_FLOAT + bs.bs_conv2d_quantized_describe(params)
     elif fused:
-        describe = "activation codes bit-packed into LDS: " + \
-            bs.bs_conv2d_codes_describe(params)
+        describe = FUSED_CODES + bs.bs_conv2d_codes_describe(params)
     else:
         describe = bs.bs_conv2d_describe(params)
     # initialisation: one step per set writes every packed and output buffer
@@ -566,19 +581,26 @@ def pack_roofline(nbytes, m):
 
 def case_bytes(case, fused=False):
     """Algorithmic HBM bytes of (activation pack, main kernel); fused: the
-    main kernel reads the unpacked activations instead of packed ones."""
+    main kernel reads the unpacked activations instead of packed ones.  The
+    pack handles every input pixel; the main kernel reads the pixels its
+    windows touch: all of them, except for 1x1 windows at stride 2 (one per
+    output pixel)."""
     from paper_1810_11066_amd import workloads as wl
     if isinstance(case, wl.DenseCase):
         rows, k, out = case.m, case.k, case.m * case.n * 4
+        read = rows
         wbytes = case.n * case.wbits * ((case.k + 31) // 32) * 4
     else:
         rows, k = case.n * case.h * case.w, case.c
         out = case.n * case.oh * case.ow * case.oc * 4
+        read = case.n * case.oh * case.ow if case.k == 1 and \
+            case.stride > 1 else rows
         wbytes = case.oc * case.k * case.k * case.wbits * \
             ((case.c + 31) // 32) * 4
-    packed = rows * case.abits * ((k + 31) // 32) * 4
-    src = rows * k * (4 if getattr(case, "act_scale", None) else 1)
-    return src + packed, (src if fused else packed) + wbytes + out
+    per_packed = case.abits * ((k + 31) // 32) * 4
+    per_src = k * (4 if getattr(case, "act_scale", None) else 1)
+    return (rows * (per_src + per_packed),
+            read * (per_src if fused else per_packed) + wbytes + out)
 
 
 def sets_for(case, minimum: int) -> int:
@@ -629,6 +651,9 @@ def roofline_of(case, m, ops, main_bytes):
 def per_step_name(case, fused):
     from paper_1810_11066_amd import workloads as wl
     q = getattr(case, "act_scale", None) is not None
+    if fused and q:
+        return ("bs_conv2d_quantized (quantize and bit-pack of the float32 "
+                "activations inside the conv kernel)")
     if fused:
         return ("bs_conv2d_codes (bit-pack of the uint8 activation codes "
                 "inside the conv kernel)")
@@ -642,7 +667,7 @@ def case_line(case, m, args, other=None):
     where both cover the case); other: the other path's step, reported
     beside it under "fused" or "unfused"."""
     ops = 2 * case.macs
-    fused = m.describe.startswith("activation codes")
+    fused = is_fused(m.describe)
     pre_bytes, main_bytes = case_bytes(case, fused=fused)
     line = {
         "metric": "bitserial conv2d effective GOPS (2*MACs/s) + % of "
@@ -665,7 +690,7 @@ def case_line(case, m, args, other=None):
         "ms_per_step_by_streams": by_streams(m),
     }
     if other is not None and other is not m:
-        ofused = other.describe.startswith("activation codes")
+        ofused = is_fused(other.describe)
         _, obytes = case_bytes(case, fused=ofused)
         line["fused" if ofused else "unfused"] = {
             "per_step": per_step_name(case, ofused),

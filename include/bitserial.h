@@ -190,6 +190,29 @@ bs_status bs_conv2d_codes(const bs_conv2d_params *p, const uint8_t *act_codes,
                           const uint32_t *w_packed, int32_t *out,
                           bs_stream_t stream);
 
+/* Bitserial conv2d of float32 activations: the quantization and bit-pack
+ * of Sec. 3.1 fused into the conv, for 1x1 windows.  Exactly
+ * bs_quantize_pack of act (unipolar, act_scale, p->abits bits) followed by
+ * bs_conv2d: every workgroup quantizes and bit-packs, into LDS, the input
+ * pixels its outputs read -- at stride 2 only those, a quarter of the
+ * input -- and convolves from there; neither codes nor packed words reach
+ * HBM.
+ *   act: [n][h][w][c] float32 NHWC (device), quantized as bs_quantize
+ *        does (round half to even of act * act_scale, clamped to
+ *        [0, 2^abits - 1], NaN to 0);
+ *   w_packed, out and the result: as bs_conv2d.
+ * Errors: as bs_conv2d; BS_ERR_INVALID_ARG for a scale bs_quantize
+ * refuses; BS_ERR_UNSUPPORTED for activations that are not unipolar and
+ * when no fused kernel covers the shape (a 1x1 window at stride 1 or 2,
+ * c 32 times a power of two up to 4096, oc a multiple of 4, activations
+ * of 1-4 bits with unipolar filters of 1-4 bits or bipolar 1-bit filters,
+ * and the packed input pixels of 256 consecutive output pixels, plus
+ * 17 KB, within 64 KB of LDS): quantize and pack with bs_quantize_pack
+ * and call bs_conv2d instead.  Nothing is enqueued on any error. */
+bs_status bs_conv2d_quantized(const bs_conv2d_params *p, const float *act,
+                              float act_scale, const uint32_t *w_packed,
+                              int32_t *out, bs_stream_t stream);
+
 /* Bitserial conv2d whose result is requantized and bit-packed as the next
  * layer's activations (layer chaining, toward the end-to-end low-precision
  * inference of Sec. 7): the int32 result v of bs_conv2d for each output is
@@ -263,6 +286,12 @@ bs_status bs_conv2d_describe(const bs_conv2d_params *p, char *buf,
  * bs_conv2d_codes would return it. */
 bs_status bs_conv2d_codes_describe(const bs_conv2d_params *p, char *buf,
                                    int32_t len);
+
+/* As bs_conv2d_codes_describe, for bs_conv2d_quantized.
+ * Errors: as bs_conv2d_describe; BS_ERR_UNSUPPORTED (buf empty) where
+ * bs_conv2d_quantized would return it. */
+bs_status bs_conv2d_quantized_describe(const bs_conv2d_params *p, char *buf,
+                                       int32_t len);
 
 /* Bitserial dense / matrix multiply (Sec. 3.2; evaluated in Sec. 6.2.1):
  *   a_packed: [m][abits][ceil(k/32)], w_packed: [n][wbits][ceil(k/32)] uint32

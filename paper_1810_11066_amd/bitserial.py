@@ -46,6 +46,7 @@ EXPORTED = ("bs_packed_words", "bs_quantize", "bs_pack", "bs_pack_ex",
             "bs_conv2d_out_shape", "bs_conv2d", "bs_conv2d_requant",
             "bs_conv2d_codes", "bs_conv2d_pair", "bs_conv2d_pair_requant",
             "bs_conv2d_describe", "bs_conv2d_codes_describe",
+            "bs_conv2d_quantized", "bs_conv2d_quantized_describe",
             "bs_dense", "bs_dense_ex", "bs_status_string",
             "bs_last_error", "bs_set_kernel_mode", "bs_set_units_per_wave",
             "bs_set_timing_events", "bs_abi_version")
@@ -106,6 +107,11 @@ def load_library():
             "bs_conv2d_codes_describe": (ci, [ctypes.POINTER(ConvParams),
                                               ctypes.c_char_p,
                                               ctypes.c_int32]),
+            "bs_conv2d_quantized": (ci, [ctypes.POINTER(ConvParams), P, cf,
+                                         P, P, P]),
+            "bs_conv2d_quantized_describe": (ci, [ctypes.POINTER(ConvParams),
+                                                  ctypes.c_char_p,
+                                                  ctypes.c_int32]),
             "bs_dense": (ci, [i64, i64, i64, ci, ci, ci, P, P, P, P]),
             "bs_dense_ex": (ci, [i64, i64, i64, ci, ci, ci, ci, P, P, P, P]),
             "bs_status_string": (ctypes.c_char_p, [ci]),
@@ -252,6 +258,15 @@ def bs_conv2d_codes_describe(p: ConvParams) -> str:
     return buf.value.decode()
 
 
+def bs_conv2d_quantized_describe(p: ConvParams) -> str:
+    """Kernel and launch plan bs_conv2d_quantized would use for ``p`` (host
+    only)."""
+    buf = ctypes.create_string_buffer(320)
+    _check(load_library().bs_conv2d_quantized_describe(ctypes.byref(p), buf,
+                                                        320))
+    return buf.value.decode()
+
+
 def bs_conv2d(p: ConvParams, act_packed: torch.Tensor, w_packed: torch.Tensor,
               out: torch.Tensor, stream=None) -> None:
     lib = load_library()
@@ -275,6 +290,22 @@ def bs_conv2d_codes(p: ConvParams, act_codes: torch.Tensor,
     _check(load_library().bs_conv2d_codes(
         ctypes.byref(p),
         _dev(act_codes, "act_codes", torch.uint8, p.n * p.h * p.w * p.c),
+        _dev(w_packed, "w_packed", torch.int32,
+             p.oc * p.kh * p.kw * p.wbits * words(p.c)),
+        _dev(out, "out", torch.int32, p.n * oh * ow * p.oc),
+        _stream(stream)))
+
+
+def bs_conv2d_quantized(p: ConvParams, act: torch.Tensor, act_scale: float,
+                        w_packed: torch.Tensor, out: torch.Tensor,
+                        stream=None) -> None:
+    """bs_quantize_pack of the float32 NHWC activations (unipolar,
+    act_scale, p.abits bits) fused into bs_conv2d (1x1 windows)."""
+    oh, ow = _out_hw(p)
+    _check(load_library().bs_conv2d_quantized(
+        ctypes.byref(p),
+        _dev(act, "act", torch.float32, p.n * p.h * p.w * p.c),
+        float(act_scale),
         _dev(w_packed, "w_packed", torch.int32,
              p.oc * p.kh * p.kw * p.wbits * words(p.c)),
         _dev(out, "out", torch.int32, p.n * oh * ow * p.oc),

@@ -189,7 +189,7 @@ hipError_t launch_kernel(const void* fn, dim3 grid, dim3 block, void** args,
 
 extern "C" {
 
-int bs_abi_version(void) { return 108; }
+int bs_abi_version(void) { return 109; }
 
 int64_t bs_packed_words(int64_t k) { return k <= 0 ? 0 : (k + 31) / 32; }
 
@@ -467,6 +467,51 @@ bs_status bs_conv2d_codes(const bs_conv2d_params* p, const uint8_t* act_codes,
     return from_hip(e, "bs_conv2d_codes launch");
 }
 
+// Why bs_conv2d_quantized refuses a shape.
+const char* const kNoQuantizedKernel =
+    "no fused kernel covers this shape (it needs a 1x1 window, stride 1 or "
+    "2, c = 32 times a power of two up to 4096, oc a multiple of 4, "
+    "unipolar activations of 1-4 bits with unipolar filters of 1-4 bits or "
+    "bipolar 1-bit filters, and one workgroup's input pixels within its "
+    "LDS); quantize and bit-pack the activations (bs_quantize_pack) and call "
+    "bs_conv2d";
+
+// bs_quantize_pack of float32 activations fused into bs_conv2d: validation
+// as bs_conv2d and bs_quantize_pack (unipolar), with the float32 bytes in
+// the overlap check.
+bs_status bs_conv2d_quantized(const bs_conv2d_params* p, const float* act,
+                              float act_scale, const uint32_t* w_packed,
+                              int32_t* out, bs_stream_t stream) {
+    bs_status st;
+    if ((st = check_ptr(act, "act")) != BS_OK) return st;
+    if ((st = check_ptr(w_packed, "w_packed")) != BS_OK) return st;
+    if ((st = check_ptr(out, "out")) != BS_OK) return st;
+    bs::ConvShape s;
+    if ((st = check_conv(p, &s)) != BS_OK) return st;
+    if (p->aenc != BS_UNIPOLAR)
+        return fail(BS_ERR_UNSUPPORTED,
+                    "bs_conv2d_quantized: unipolar activations only");
+    if ((st = check_scale_enc(act_scale, p->abits, BS_UNIPOLAR)) != BS_OK)
+        return st;
+    const uint64_t out_bytes = (uint64_t)s.n * s.oh * s.ow * (uint64_t)s.oc * 4u;
+    const uint64_t act_bytes =
+        (uint64_t)s.n * s.h * s.w * (uint64_t)s.c * 4u;
+    const uint64_t w_bytes = packed_bytes((int64_t)s.oc * s.kh * s.kw,
+                                          s.wbits, s.c);
+    if ((st = check_disjoint(out, out_bytes, "out", act, act_bytes, "act")) !=
+        BS_OK)
+        return st;
+    if ((st = check_disjoint(out, out_bytes, "out", w_packed, w_bytes,
+                             "w_packed")) != BS_OK)
+        return st;
+    const hipError_t e = bs::launch_conv_quantized(
+        s, act, act_scale, w_packed, out, g_conv_opt, (hipStream_t)stream);
+    if (e == hipErrorNotSupported)
+        return fail(BS_ERR_UNSUPPORTED, "bs_conv2d_quantized: %s",
+                    kNoQuantizedKernel);
+    return from_hip(e, "bs_conv2d_quantized launch");
+}
+
 bs_status bs_conv2d_requant(const bs_conv2d_params* p,
                             const uint32_t* act_packed,
                             const uint32_t* w_packed, float out_scale,
@@ -515,10 +560,29 @@ bs_status bs_conv2d_codes_describe(const bs_conv2d_params* p, char* buf,
     bs_status st;
     bs::ConvShape s;
     if ((st = check_conv(p, &s)) != BS_OK) return st;
-    if (bs::describe_conv_codes(s, g_conv_opt, buf, (size_t)len) < 0) {
+    if (bs::describe_conv_staged(s, false, g_conv_opt, buf, (size_t)len) <
+        0) {
         buf[0] = '\0';
         return fail(BS_ERR_UNSUPPORTED, "bs_conv2d_codes: %s",
                     kNoFusedKernel);
+    }
+    return ok();
+}
+
+bs_status bs_conv2d_quantized_describe(const bs_conv2d_params* p, char* buf,
+                                       int32_t len) {
+    if (!buf || len < 1) return fail(BS_ERR_INVALID_ARG, "buf/len");
+    buf[0] = '\0';
+    bs_status st;
+    bs::ConvShape s;
+    if ((st = check_conv(p, &s)) != BS_OK) return st;
+    if (p->aenc != BS_UNIPOLAR)
+        return fail(BS_ERR_UNSUPPORTED,
+                    "bs_conv2d_quantized: unipolar activations only");
+    if (bs::describe_conv_staged(s, true, g_conv_opt, buf, (size_t)len) < 0) {
+        buf[0] = '\0';
+        return fail(BS_ERR_UNSUPPORTED, "bs_conv2d_quantized: %s",
+                    kNoQuantizedKernel);
     }
     return ok();
 }

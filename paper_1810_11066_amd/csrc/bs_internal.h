@@ -178,15 +178,25 @@ hipError_t launch_conv_codes(const ConvShape& s, const uint8_t* act,
                              const uint32_t* wts, int32_t* out,
                              const ConvOptions& opt, hipStream_t st);
 
+// Conv of float32 activations, NHWC [n][h][w][c], quantized (unipolar,
+// scale) and bit-packed into each block's LDS by the conv kernel (1x1
+// windows).  hipErrorNotSupported, with nothing enqueued, when no such
+// kernel covers the shape.
+hipError_t launch_conv_quantized(const ConvShape& s, const float* act,
+                                 float scale, const uint32_t* wts,
+                                 int32_t* out, const ConvOptions& opt,
+                                 hipStream_t st);
+
 // Writes the kernel and launch configuration launch_conv would use for this
 // shape and mode into buf (snprintf semantics); returns the snprintf result.
 int describe_conv(const ConvShape& s, const ConvOptions& opt, char* buf,
                   size_t len);
 
-// The same for launch_conv_codes (the staged plan); -1, with buf untouched,
-// where launch_conv_codes would return hipErrorNotSupported.
-int describe_conv_codes(const ConvShape& s, const ConvOptions& opt, char* buf,
-                        size_t len);
+// The same for launch_conv_codes (from_float false) or
+// launch_conv_quantized (true): the staged plan; -1, with buf untouched,
+// where the launch would return hipErrorNotSupported.
+int describe_conv_staged(const ConvShape& s, bool from_float,
+                         const ConvOptions& opt, char* buf, size_t len);
 
 // True when launch_conv with mode 0 would use a specialised kernel.
 bool conv_has_fast_path(const ConvShape& s);

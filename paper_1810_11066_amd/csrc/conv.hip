@@ -223,12 +223,19 @@ namespace {
 // as keep the packed activations and the int32 output (not the packed
 // output of a requantizing call) within the kernel's 32-bit buffer offsets
 // and its unit counts within int32; 0 when one image is already too large.
+// Bytes of one image's activations as a pixels-on-lanes kernel with
+// activation source src reads them: bit-packed words, uint8 codes or
+// float32 values.
+int64_t pix_act_image_bytes(const ConvShape& s, int src) {
+    const int64_t hw = (int64_t)s.h * s.w;
+    if (src == pix::kSrcCodes) return hw * s.c;
+    if (src == pix::kSrcFloat) return hw * s.c * 4;
+    return hw * s.abits * ((s.c + 31) / 32) * 4;
+}
+
 int64_t pix_images_per_launch(const ConvShape& s, bool req,
-                              bool codes = false) {
-    const int64_t cw = (s.c + 31) / 32;
-    // activations: bit-packed words, or (codes) the uint8 codes
-    const int64_t act_img = codes ? (int64_t)s.h * s.w * s.c
-                                  : (int64_t)s.h * s.w * s.abits * cw * 4;
+                              int src = pix::kSrcPacked) {
+    const int64_t act_img = pix_act_image_bytes(s, src);
     const int64_t pix_img = (int64_t)s.oh * s.ow;
     const int64_t out_img = req ? 0 : pix_img * s.oc * 4;
     const int64_t lim = pix::kMaxBufferBytes;
@@ -244,8 +251,8 @@ int64_t pix_images_per_launch(const ConvShape& s, bool req,
 }
 
 // Pixels-on-lanes kernel for this shape, or nullptr.  src: where the
-// activations come from (pix::kSrcPacked, kSrcCodes); the staged form reads
-// whole 32-code words of each pixel, so it needs c % 32 == 0.
+// activations come from (pix::kSrcPacked, kSrcCodes, kSrcFloat); the staged
+// forms read whole 32-code words of each pixel, so they need c % 32 == 0.
 pix::PixKernelFn pix_kernel_for(const ConvShape& s, bool req, int src,
                                 pix::PlanInfo* info, bool dual = false) {
     const int64_t cw = (s.c + 31) / 32;
@@ -254,8 +261,7 @@ pix::PixKernelFn pix_kernel_for(const ConvShape& s, bool req, int src,
     // output tiles are written in 16-byte quads of channels
     if (s.oc % 4 != 0) return nullptr;
     if (src != pix::kSrcPacked && s.c % 32 != 0) return nullptr;
-    if (pix_images_per_launch(s, req, src == pix::kSrcCodes) < 1)
-        return nullptr;
+    if (pix_images_per_launch(s, req, src) < 1) return nullptr;
     return pix::pick(s.abits, s.wbits, s.aenc, s.wenc, s.kh, s.sh, (int)cw,
                      req, src, dual, info);
 }
@@ -399,6 +405,8 @@ void plan_pix_lds(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
                              ((s.c + 31) / 32) * 4);
     g->out_bytes = rq ? 0 : (int32_t)((int64_t)g->npix * s.oc * 4);
     g->region_pixels = 0;
+    g->in_scale = 0.0f;
+    g->in_qmax = 0.0f;
     g->out1 = nullptr;
     g->out1_scale = 0.0f;
     g->out1_bytes = 0;
@@ -446,9 +454,11 @@ void plan_pix(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
 // plus one zero pixel, whose size depends on the run length, which depends
 // on residency, which depends on the LDS: re-plan until the residency the
 // plan assumed is the one its LDS allows.  False when the region does not
-// fit a block's LDS.
+// fit a block's LDS.  src: kSrcCodes, or kSrcFloat with the quantizer's
+// scale in_scale.
 bool plan_pix_staged(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
-                     pix::PixArgs* g, dim3* grid, size_t* lds) {
+                     int src, float in_scale, pix::PixArgs* g, dim3* grid,
+                     size_t* lds) {
     const size_t pwb = (size_t)s.abits * ((s.c + 31) / 32) * 4;
     size_t assumed = kTileLds;
     int run = forced_run;
@@ -464,9 +474,11 @@ bool plan_pix_staged(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
             continue;
         }
         g->region_pixels = (int32_t)region;
-        // the kernel reads the uint8 codes (within kMaxBufferBytes:
-        // pix_images_per_launch with codes)
-        g->act_bytes = (int32_t)((int64_t)s.n * s.h * s.w * s.c);
+        // the kernel reads the uint8 codes or float32 values (within
+        // kMaxBufferBytes: pix_images_per_launch with src)
+        g->act_bytes = (int32_t)(s.n * pix_act_image_bytes(s, src));
+        g->in_scale = in_scale;
+        g->in_qmax = (float)((1 << s.abits) - 1);
         *lds = need;
         if (need <= assumed ||
             resident_blocks(fn, need) >= resident_blocks(fn, assumed))
@@ -572,18 +584,18 @@ hipError_t launch_pix(const ConvShape& s, pix::PixKernelFn fn,
     return hipSuccess;
 }
 
-// Staged launch: uint8 activation codes (NHWC [n][h][w][c]) are bit-packed
+// Staged launch: uint8 activation codes (src kSrcCodes) or float32 values
+// quantized with in_scale (kSrcFloat), NHWC [n][h][w][c], are bit-packed
 // into each block's LDS by the conv kernel itself.  Every image chunk is
 // planned before anything is enqueued; hipErrorNotSupported (nothing
 // enqueued) when no staged kernel or no fitting plan exists.
-hipError_t launch_pix_staged(const ConvShape& s, const uint8_t* act,
-                             const uint32_t* wts, int32_t* out,
-                             int forced_run, hipStream_t st) {
+hipError_t launch_pix_staged(const ConvShape& s, const void* act, int src,
+                             float in_scale, const uint32_t* wts,
+                             int32_t* out, int forced_run, hipStream_t st) {
     pix::PlanInfo info{};
-    const pix::PixKernelFn fn =
-        pix_kernel_for(s, false, pix::kSrcCodes, &info);
+    const pix::PixKernelFn fn = pix_kernel_for(s, false, src, &info);
     if (!fn) return hipErrorNotSupported;
-    const int64_t per = pix_images_per_launch(s, false, true);
+    const int64_t per = pix_images_per_launch(s, false, src);
     struct Chunk {
         int64_t n0;
         pix::PixArgs g;
@@ -596,15 +608,16 @@ hipError_t launch_pix_staged(const ConvShape& s, const uint8_t* act,
         c.n = (int32_t)(s.n - n0 < per ? s.n - n0 : per);
         Chunk ch;
         ch.n0 = n0;
-        if (!plan_pix_staged(c, fn, forced_run, &ch.g, &ch.grid, &ch.lds))
+        if (!plan_pix_staged(c, fn, forced_run, src, in_scale, &ch.g,
+                             &ch.grid, &ch.lds))
             return hipErrorNotSupported;
         chunks.push_back(ch);
     }
-    const int64_t in_img = (int64_t)s.h * s.w * s.c;
+    const int64_t in_img = pix_act_image_bytes(s, src);
     const int64_t out_img = (int64_t)s.oh * s.ow * s.oc;
     for (const Chunk& ch : chunks) {
-        const uint32_t* a =
-            reinterpret_cast<const uint32_t*>(act + ch.n0 * in_img);
+        const uint32_t* a = reinterpret_cast<const uint32_t*>(
+            static_cast<const uint8_t*>(act) + ch.n0 * in_img);
         int32_t* o = out + ch.n0 * out_img;
         const hipError_t e = launch(fn, ch.grid, dim3(pix::kBlock), ch.lds, st,
                                     a, wts, wts, o, ch.g);
@@ -740,7 +753,16 @@ hipError_t launch_conv_pair(const ConvShape& s, const uint32_t* act,
 hipError_t launch_conv_codes(const ConvShape& s, const uint8_t* act,
                              const uint32_t* wts, int32_t* out,
                              const ConvOptions& opt, hipStream_t st) {
-    return launch_pix_staged(s, act, wts, out, opt.units_per_wave, st);
+    return launch_pix_staged(s, act, pix::kSrcCodes, 0.0f, wts, out,
+                             opt.units_per_wave, st);
+}
+
+hipError_t launch_conv_quantized(const ConvShape& s, const float* act,
+                                 float scale, const uint32_t* wts,
+                                 int32_t* out, const ConvOptions& opt,
+                                 hipStream_t st) {
+    return launch_pix_staged(s, act, pix::kSrcFloat, scale, wts, out,
+                             opt.units_per_wave, st);
 }
 
 namespace {
@@ -757,30 +779,32 @@ void kernel_encodings(const pix::PlanInfo& info, char* out, size_t len) {
 
 }  // namespace
 
-int describe_conv_codes(const ConvShape& s, const ConvOptions& opt, char* buf,
-                        size_t len) {
+int describe_conv_staged(const ConvShape& s, bool from_float,
+                         const ConvOptions& opt, char* buf, size_t len) {
+    const int src = from_float ? pix::kSrcFloat : pix::kSrcCodes;
     pix::PlanInfo info{};
-    const pix::PixKernelFn fn =
-        pix_kernel_for(s, false, pix::kSrcCodes, &info);
+    const pix::PixKernelFn fn = pix_kernel_for(s, false, src, &info);
     if (!fn) return -1;
     // the plan of the first launch (of `launches` image chunks)
-    const int64_t per = pix_images_per_launch(s, false, true);
+    const int64_t per = pix_images_per_launch(s, false, src);
     ConvShape c = s;
     c.n = (int32_t)(s.n < per ? s.n : per);
     pix::PixArgs g;
     dim3 grid;
     size_t lds = 0;
-    if (!plan_pix_staged(c, fn, opt.units_per_wave, &g, &grid, &lds))
+    if (!plan_pix_staged(c, fn, opt.units_per_wave, src, 1.0f, &g, &grid,
+                         &lds))
         return -1;
     const int64_t launches = (s.n + per - 1) / per;
     char kenc[48];
     kernel_encodings(info, kenc, sizeof(kenc));
     return snprintf(buf, len,
                     "conv_pix_kernel<A=%d,W=%d,%s,K=%d,S=%d,CW=%d> "
-                    "staged codes: patch=%dtaps x %dwords slice=%dch x "
+                    "staged %s: patch=%dtaps x %dwords slice=%dch x "
                     "%dtaps grid=%u block=%d lds=%zu region=%dpx units=%d "
                     "units_per_wave=%d%s",
                     s.abits, s.wbits, kenc, s.kh, s.sh, (s.c + 31) / 32,
+                    from_float ? "float32" : "codes",
                     info.tb, info.cb, info.ocb, info.ts, grid.x, pix::kBlock,
                     lds, g.region_pixels, g.units, g.per_wave,
                     launches > 1 ? " (per launch; batch split)" : "");

@@ -105,11 +105,14 @@ struct PixArgs {
     FastDiv div_ow, div_oh, div_units;
     int32_t c;             // input channels (+-1 activations only)
     int32_t act_bytes;     // size of the activations, bytes: the packed
-                           // words, or the uint8 codes (kSrcCodes)
+                           // words, the uint8 codes (kSrcCodes) or the
+                           // float32 values (kSrcFloat)
     int32_t out_bytes;     // size of the int32 output, bytes (0: packed out)
     // activations staged in LDS (SRC != kSrcPacked): the most input pixels
     // any block's region holds (its LDS size)
     int32_t region_pixels;
+    // float32 activations (kSrcFloat): the quantizer's scale and top code
+    float in_scale, in_qmax;
     // paired 1x1 conv (DUAL kernels; its packed filters [oc][W][CW] are the
     // kernel's wts1 argument): its output (int32 [npix][oc], or packed codes
     // with out1_scale), and the int32 output's size in bytes (0 for packed
@@ -126,7 +129,10 @@ struct PixArgs {
 //               activations never reach HBM: the separate pack launch and
 //               its round trip are gone, at the price of packing each
 //               block's halo rows again.
-constexpr int kSrcPacked = 0, kSrcCodes = 1;
+//   kSrcFloat   float32 activations [n][h][w][C] (1x1 windows): as
+//               kSrcCodes, each value quantized on the way (unipolar, scale
+//               and qmax in PixArgs) before it is packed.
+constexpr int kSrcPacked = 0, kSrcCodes = 1, kSrcFloat = 2;
 
 __device__ __forceinline__ void bcnt_acc(uint32_t& acc, uint32_t x) {
     asm("v_bcnt_u32_b32 %0, %1, %0" : "+v"(acc) : "v"(x));
@@ -598,6 +604,47 @@ __device__ __forceinline__ void pack32_planes(const uint32_t (&d)[8],
     }
 }
 
+// The 32 codes of one staged item (channels 32 t .. 32 t + 31 of one input
+// pixel, starting at element e of the NHWC activations) as bytes in d[0..7]
+// (code 4 m + k in byte k of d[m]).  Codes: two 16-byte loads.  Float32:
+// eight, each value quantized as bs_quantize does (quant_code).  in false
+// (a pixel in the padding): the loads fall past the buffer and read zeros,
+// which are code 0 either way.
+template <int SRC>
+__device__ __forceinline__ void load_item(uint32_t (&d)[8], Rsrc src,
+                                          uint32_t e, bool in,
+                                          const PixArgs& g) {
+    if constexpr (SRC == kSrcFloat) {
+        const uint32_t off = in ? 4u * e : kOutOfRange;
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            const float4 f = __builtin_bit_cast(
+                float4, __builtin_amdgcn_raw_buffer_load_b128(
+                            src, off + 16u * (uint32_t)m, 0, 0));
+            d[m] = quant_code<false>(f.x, g.in_scale, g.in_qmax) |
+                   quant_code<false>(f.y, g.in_scale, g.in_qmax) << 8 |
+                   quant_code<false>(f.z, g.in_scale, g.in_qmax) << 16 |
+                   quant_code<false>(f.w, g.in_scale, g.in_qmax) << 24;
+        }
+    } else {
+        const uint32_t off = in ? e : kOutOfRange;
+        const uint4 a = __builtin_bit_cast(
+            uint4, __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0));
+        const uint4 b = __builtin_bit_cast(
+            uint4, __builtin_amdgcn_raw_buffer_load_b128(src, off + 16u, 0, 0));
+        d[0] = a.x; d[1] = a.y; d[2] = a.z; d[3] = a.w;
+        d[4] = b.x; d[5] = b.y; d[6] = b.z; d[7] = b.w;
+    }
+}
+
+// Items of one staging pass a thread has in flight before it packs any:
+// four 32-byte code loads, or one item's eight float32 loads (32 values, as
+// many registers as the four code items).
+template <int SRC>
+constexpr int stage_items_in_flight() {
+    return SRC == kSrcFloat ? 1 : 4;
+}
+
 // Input region of a block: the flat NHWC input pixels [lo, hi) that hold
 // every in-range tap of the block's output pixels, from the first tap of
 // its first output pixel to the last tap of its last one.  The first tap row
@@ -644,13 +691,15 @@ __device__ __forceinline__ Region block_region(const PixArgs& g, int p_first,
 // loads of consecutive threads are consecutive 32-byte pieces of the NHWC
 // rows.  A thread issues the loads of U items before it packs any of them,
 // so that the fill waits for memory about once rather than once per item.
-template <int A, int CW>
+template <int A, int CW, int SRC>
 __device__ __forceinline__ void stage_region(uint32_t* __restrict__ region,
-                                             Rsrc src, Region rg) {
+                                             Rsrc src, Region rg,
+                                             const PixArgs& g) {
     constexpr int PW = A * CW;                 // words per packed pixel
-    constexpr int U = 4;
+    constexpr int U = stage_items_in_flight<SRC>();
     // item = 32 codes (one word of every plane of one pixel); items are
-    // numbered in memory order, so item i starts at byte 32 i of the region
+    // numbered in memory order, so item i starts at element 32 i of the
+    // region
     const int items = (rg.hi - rg.lo) * CW;
     const uint32_t base = (uint32_t)rg.lo * (uint32_t)(32 * CW);
     for (int it0 = threadIdx.x; it0 < items; it0 += U * kBlock) {
@@ -658,16 +707,8 @@ __device__ __forceinline__ void stage_region(uint32_t* __restrict__ region,
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int it = it0 + u * kBlock;
-            if (it < items) {
-                const uint32_t off = base + 32u * (uint32_t)it;
-                const uint4 a = __builtin_bit_cast(
-                    uint4, __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0));
-                const uint4 b = __builtin_bit_cast(
-                    uint4,
-                    __builtin_amdgcn_raw_buffer_load_b128(src, off + 16u, 0, 0));
-                d[u][0] = a.x; d[u][1] = a.y; d[u][2] = a.z; d[u][3] = a.w;
-                d[u][4] = b.x; d[u][5] = b.y; d[u][6] = b.z; d[u][7] = b.w;
-            }
+            if (it < items)
+                load_item<SRC>(d[u], src, base + 32u * (uint32_t)it, true, g);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -692,12 +733,12 @@ __device__ __forceinline__ void stage_region(uint32_t* __restrict__ region,
 // words), so that the rows and columns no tap reads are neither loaded nor
 // packed; an output pixel whose input pixel lies in the padding gets zeros
 // (its loads fall past the buffer).  Then the zero pixel, as stage_region.
-template <int A, int CW, int S>
+template <int A, int CW, int S, int SRC>
 __device__ __forceinline__ void stage_gather(uint32_t* __restrict__ region,
                                              Rsrc src, const PixArgs& g,
                                              int q_lo, int q_hi) {
     constexpr int PW = A * CW;
-    constexpr int U = 4;
+    constexpr int U = stage_items_in_flight<SRC>();
     const int items = (q_hi - q_lo) * CW;
     for (int it0 = threadIdx.x; it0 < items; it0 += U * kBlock) {
         uint32_t d[U][8];
@@ -713,19 +754,10 @@ __device__ __forceinline__ void stage_gather(uint32_t* __restrict__ region,
                 const int iy = y * S - g.ph, ix = x * S - g.pw;
                 const bool in = (unsigned)iy < (unsigned)g.h &&
                                 (unsigned)ix < (unsigned)g.w;
-                const uint32_t off =
-                    in ? ((img * (uint32_t)g.h + (uint32_t)iy) *
-                              (uint32_t)g.w + (uint32_t)ix) *
-                                 (uint32_t)(32 * CW) +
-                             32u * (uint32_t)t
-                       : kOutOfRange;
-                const uint4 a = __builtin_bit_cast(
-                    uint4, __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0));
-                const uint4 b = __builtin_bit_cast(
-                    uint4,
-                    __builtin_amdgcn_raw_buffer_load_b128(src, off + 16u, 0, 0));
-                d[u][0] = a.x; d[u][1] = a.y; d[u][2] = a.z; d[u][3] = a.w;
-                d[u][4] = b.x; d[u][5] = b.y; d[u][6] = b.z; d[u][7] = b.w;
+                const uint32_t e =
+                    ((img * (uint32_t)g.h + (uint32_t)iy) * (uint32_t)g.w +
+                     (uint32_t)ix) * (uint32_t)(32 * CW) + 32u * (uint32_t)t;
+                load_item<SRC>(d[u], src, e, in, g);
             }
         }
 #pragma unroll
@@ -993,7 +1025,7 @@ constexpr int min_waves_per_simd() {
 // S: stride; CW: words per bit-plane; REQ: requantize and bit-pack the output
 // (out then holds [npix][out_bits][out_words] uint32 words) instead of
 // storing int32; SRC: where the activations come from (kSrcPacked, or
-// kSrcCodes staged in LDS); DUAL: also the 1x1 conv of
+// kSrcCodes / kSrcFloat staged in LDS); DUAL: also the 1x1 conv of
 // the same stride whose input pixel is the window's centre tap (pad
 // (K-1)/2), over the same output grid and channels, with filters wts1 and
 // output g.out1 (whole patches only).  wts1 is a kernel argument, read-only
@@ -1012,6 +1044,8 @@ void conv_pix_kernel(
     constexpr int kCpol = out_store_policy<A, CW>();
     static_assert(SRC == kSrcPacked || !REQ,
                   "staged activations: int32 output");
+    static_assert(SRC != kSrcFloat || K == 1,
+                  "float32 activations: 1x1 windows");
     static_assert(!DUAL || (NB == 1 && K % 2 == 1 && SRC == kSrcPacked &&
                             (E == 3 * kUnipolar + kUnipolar ||
                              E == 3 * kUnipolar + kBipolar)),
@@ -1049,13 +1083,14 @@ void conv_pix_kernel(
         if constexpr (kGather) {
             // the host sized the LDS for the largest block's pixel count
             const int q_hi = min(p_last + 1, p_first + g.region_pixels);
-            stage_gather<A, CW, S>(lds + kWavesPerBlock * kTileWords, ract,
-                                   g, p_first, q_hi);
+            stage_gather<A, CW, S, SRC>(lds + kWavesPerBlock * kTileWords,
+                                        ract, g, p_first, q_hi);
             region_lo = p_first;
             zero_off = (uint32_t)(q_hi - p_first) * (uint32_t)(4 * A * CW);
         } else {
             const Region rg = block_region<K, S>(g, p_first, p_last);
-            stage_region<A, CW>(lds + kWavesPerBlock * kTileWords, ract, rg);
+            stage_region<A, CW, SRC>(lds + kWavesPerBlock * kTileWords, ract,
+                                     rg, g);
             region_lo = rg.lo;
             zero_off = (uint32_t)(rg.hi - rg.lo) * (uint32_t)(4 * A * CW);
         }
@@ -1451,9 +1486,19 @@ PixKernelFn pick_kscw(bool req, int src, bool dual, PlanInfo* info) {
         }
         if (src != kSrcPacked) {
             if constexpr (E == UU || E == UB) {
-                if (req || src != kSrcCodes) return nullptr;
-                return conv_pix_kernel<A, W, E, K, S, CW, false, kSrcCodes,
-                                       false>;
+                if (req) return nullptr;
+                if (src == kSrcCodes)
+                    return conv_pix_kernel<A, W, E, K, S, CW, false,
+                                           kSrcCodes, false>;
+                // float32 activations: 1x1 windows only (a 3x3 window's
+                // staging would read its float rows in one burst before
+                // any arithmetic, as long as a separate quantize + pack)
+                if constexpr (K == 1) {
+                    if (src == kSrcFloat)
+                        return conv_pix_kernel<A, W, E, K, S, CW, false,
+                                               kSrcFloat, false>;
+                }
+                return nullptr;
             } else {
                 return nullptr;
             }

@@ -41,7 +41,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_words(lib):
-    assert lib.bs_abi_version() == 108
+    assert lib.bs_abi_version() == 109
     for k, w in [(0, 0), (1, 1), (31, 1), (32, 1), (33, 2), (4096, 128)]:
         assert lib.bs_packed_words(k) == w
 
@@ -578,3 +578,46 @@ def test_codes_describe_refusals(lib):
     assert d(ctypes.byref(params(c=96)), buf, 64) == bs.BS_ERR_UNSUPPORTED
     assert buf.value == b""
     assert b"no fused kernel" in lib.bs_last_error()
+
+
+def test_quantized_refusals(lib):
+    buf = ctypes.create_string_buffer(64)
+    q = lib.bs_conv2d_quantized
+    one = params(kh=1, kw=1, pad_h=0, pad_w=0)
+    assert q(ctypes.byref(one), None, ctypes.c_float(1.0), FAKE, FAKE,
+             STREAM) == bs.BS_ERR_INVALID_ARG
+    for bad_scale in (0.0, -1.0, float("inf"), float("nan")):
+        assert q(ctypes.byref(one), FAKE, ctypes.c_float(bad_scale), FAKE,
+                 FAKE, STREAM) == bs.BS_ERR_INVALID_ARG
+    # the quantizer is unipolar; signed or +-1 activations are refused
+    for aenc in (1, 2):
+        assert q(ctypes.byref(params(kh=1, kw=1, pad_h=0, pad_w=0,
+                                     abits=2 if aenc == 2 else 1,
+                                     aenc=aenc)),
+                 FAKE, ctypes.c_float(1.0), FAKE, FAKE,
+                 STREAM) == bs.BS_ERR_UNSUPPORTED
+    # 3x3 windows have no fused float32 kernel (refused before any launch,
+    # as the describe call shows without a GPU)
+    d = lib.bs_conv2d_quantized_describe
+    assert d(ctypes.byref(params()), buf, 64) == bs.BS_ERR_UNSUPPORTED
+    assert buf.value == b""
+    assert b"no fused kernel" in lib.bs_last_error()
+    assert d(ctypes.byref(one), None, 64) == bs.BS_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("s,run", [(1, 4), (2, 3)])
+def test_quantized_describe_reports_the_staged_plan(lib, s, run):
+    sh = dict(n=2, h=13, w=11, k=1, s=s, pad=0, oc=64)
+    p = params(n=2, h=13, w=11, c=128, oc=64, kh=1, kw=1, stride_h=s,
+               stride_w=s, pad_h=0, pad_w=0, abits=3, wbits=2)
+    try:
+        assert lib.bs_set_units_per_wave(run) == bs.BS_OK
+        d = bs.bs_conv2d_quantized_describe(p)
+        codes = bs.bs_conv2d_codes_describe(p)
+    finally:
+        assert lib.bs_set_units_per_wave(0) == bs.BS_OK
+    assert d.startswith("conv_pix_kernel<A=3,W=2,unipolar,K=1,S=%d,CW=4> "
+                        "staged float32:" % s)
+    assert " region=%dpx " % _staged_region(run=run, **sh) in d
+    # the same plan as the fused call on codes
+    assert d.split(": ", 1)[1] == codes.split(": ", 1)[1]
