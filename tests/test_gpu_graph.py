@@ -7,7 +7,8 @@ exactly those kernels.  The captured graph -- quantize + pack of float32
 activations, the conv, the requantizing conv and the next layer's conv on
 its packed output, and the fused conv of uint8 codes -- is replayed several
 times with new inputs copied into the captured buffers and eager calls of
-the same entry points in between, and every replay is checked against the
+the same entry points in between (and, quantized inside the kernel, a 1x1
+stride-2 conv of the float32 input), and every replay is checked against the
 oracle, element by element."""
 import numpy as np
 import pytest
@@ -18,6 +19,8 @@ from paper_1810_11066_amd import bitserial as bs
 pytestmark = pytest.mark.gpu
 
 N, H, W, C, OC, OC2, K = 2, 9, 10, 64, 68, 32, 3
+OC3 = 36   # the 1x1 stride-2 conv of the float32 input
+OH3, OW3 = (H - 1) // 2 + 1, (W - 1) // 2 + 1
 ABITS, WBITS, OBITS = 2, 1, 2
 SCALE = 1.3
 # spreads the first conv's results over the 2-bit output codes
@@ -44,8 +47,9 @@ def inputs(replay):
     return x, codes
 
 
-def expected(oracle, x, codes, w1, w2):
+def expected(oracle, x, codes, w1, w2, w3):
     p1 = oracle.conv_params(N, H, W, C, OC, K, K, 1, 1, ABITS, WBITS)
+    p3 = oracle.conv_params(N, H, W, C, OC3, 1, 1, 2, 0, ABITS, WBITS)
     p2 = oracle.conv_params(N, H, W, OC, OC2, K, K, 1, 1, OBITS, WBITS)
     wp1, wp2 = oracle.pack(w1, WBITS), oracle.pack(w2, WBITS)
     ap = oracle.pack(oracle.quantize(x, SCALE, ABITS), ABITS)
@@ -54,19 +58,23 @@ def expected(oracle, x, codes, w1, w2):
                                       OBITS), OBITS)
     conv2 = oracle.conv2d(p2, req, wp2)
     convc = oracle.conv2d(p1, oracle.pack(codes, ABITS), wp1)
-    return ap, conv1, req, conv2, convc
+    conv3 = oracle.conv2d(p3, ap, oracle.pack(w3, WBITS))
+    return ap, conv1, req, conv2, convc, conv3
 
 
 def test_hot_path_in_a_graph(oracle):
     rng = np.random.default_rng(4399)
     w1 = rng.integers(0, 2, size=(OC, K, K, C), dtype=np.uint8)
     w2 = rng.integers(0, 2, size=(OC2, K, K, OC), dtype=np.uint8)
+    w3 = rng.integers(0, 2, size=(OC3, 1, 1, C), dtype=np.uint8)
     dev = torch.device("cuda")
     w1_dev = bs.pack(torch.from_numpy(w1).to(dev), WBITS)
     w2_dev = bs.pack(torch.from_numpy(w2).to(dev), WBITS)
+    w3_dev = bs.pack(torch.from_numpy(w3).to(dev), WBITS)
     p1 = bs.ConvParams(N, H, W, C, OC, K, K, 1, 1, 1, 1, ABITS, WBITS, 0, 0)
     p2 = bs.ConvParams(N, H, W, OC, OC2, K, K, 1, 1, 1, 1, OBITS, WBITS, 0,
                        0)
+    p3 = bs.ConvParams(N, H, W, C, OC3, 1, 1, 2, 2, 0, 0, ABITS, WBITS, 0, 0)
     # every buffer the graph touches exists before the capture
     x_dev = torch.empty((N, H, W, C), dtype=torch.float32, device=dev)
     codes_dev = torch.empty((N, H, W, C), dtype=torch.uint8, device=dev)
@@ -77,6 +85,7 @@ def test_hot_path_in_a_graph(oracle):
                       device=dev)
     out2 = torch.empty((N, H, W, OC2), dtype=torch.int32, device=dev)
     outc = torch.empty((N, H, W, OC), dtype=torch.int32, device=dev)
+    out3 = torch.empty((N, OH3, OW3, OC3), dtype=torch.int32, device=dev)
 
     def path():
         bs.bs_quantize_pack(x_dev, a_dev, N * H * W, C, SCALE, ABITS)
@@ -84,6 +93,7 @@ def test_hot_path_in_a_graph(oracle):
         bs.bs_conv2d_requant(p1, a_dev, w1_dev, SCALE2, OBITS, req)
         bs.bs_conv2d(p2, req, w2_dev, out2)
         bs.bs_conv2d_codes(p1, codes_dev, w1_dev, outc)
+        bs.bs_conv2d_quantized(p3, x_dev, SCALE, w3_dev, out3)
 
     x, codes = inputs(0)
     x_dev.copy_(torch.from_numpy(x))
@@ -113,7 +123,8 @@ def test_hot_path_in_a_graph(oracle):
         torch.cuda.synchronize()
         graph.replay()
         torch.cuda.synchronize()
-        ap, conv1, rq, conv2, convc = expected(oracle, x, codes, w1, w2)
+        ap, conv1, rq, conv2, convc, conv3 = expected(oracle, x, codes, w1,
+                                                      w2, w3)
         say("replay", replay)
         assert np.array_equal(a_dev.cpu().numpy().view(np.uint32)
                               .reshape(ap.shape), ap)
@@ -122,3 +133,4 @@ def test_hot_path_in_a_graph(oracle):
                               .reshape(rq.shape), rq)
         assert np.array_equal(out2.cpu().numpy(), conv2)
         assert np.array_equal(outc.cpu().numpy(), convc)
+        assert np.array_equal(out3.cpu().numpy(), conv3)
