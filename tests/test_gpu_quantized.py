@@ -187,3 +187,37 @@ def test_config4_1x1_layers_quantized(oracle, case):
     bad = np.flatnonzero(got.ravel() != want.ravel())
     assert bad.size == 0, "%d outputs differ from the oracle, first at %d" % (
         bad.size, bad[0])
+
+
+@pytest.mark.parametrize("stride", [1, 2])
+def test_conv2d_quantized_split_by_input_size(oracle, stride):
+    """Float32 activations of more than 2 GiB: the call splits the batch
+    into launches whose float32 input stays within one buffer (32-bit
+    offsets); at stride 2 each launch gathers its pixels.  Every output
+    against the oracle."""
+    n, h, w, c, oc, abits, scale = 257, 64, 64, 512, 4, 2, 1.3
+    say("conv2d_quantized split", (n, h, w, c, oc, stride))
+    assert n * h * w * c * 4 > 2 ** 31
+    rng = np.random.default_rng(515151 + stride)
+    x = rng.standard_normal((n, h, w, c), dtype=np.float32)
+    wq = rng.integers(0, 2, size=(oc, 1, 1, c), dtype=np.uint8)
+    op = oracle.conv_params(n, h, w, c, oc, 1, 1, stride, 0, abits, 1)
+    want = oracle.conv2d(op, oracle.pack(oracle.quantize(x, scale, abits),
+                                         abits), oracle.pack(wq, 1))
+    p = bs.ConvParams(n, h, w, c, oc, 1, 1, stride, stride, 0, 0, abits, 1,
+                      0, 0)
+    oh, ow = bs.bs_conv2d_out_shape(p)
+    numel = n * oh * ow * oc
+    buf = torch.full((numel + 2 * GUARD,), SENT32, dtype=torch.int32,
+                     device="cuda")
+    x_dev = dev(x)
+    del x
+    bs.bs_conv2d_quantized(p, x_dev, scale, bs.pack(dev(wq), 1),
+                           buf[GUARD:GUARD + numel])
+    torch.cuda.synchronize()
+    del x_dev
+    b = buf.cpu()
+    assert bool((b[:GUARD] == SENT32).all()), "write before output"
+    assert bool((b[GUARD + numel:] == SENT32).all()), "write past output"
+    got = b[GUARD:GUARD + numel].numpy().reshape(want.shape)
+    assert np.array_equal(got, want)
