@@ -221,3 +221,26 @@ def test_conv2d_quantized_split_by_input_size(oracle, stride):
     assert bool((b[GUARD + numel:] == SENT32).all()), "write past output"
     got = b[GUARD:GUARD + numel].numpy().reshape(want.shape)
     assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("stride", [1, 2])
+def test_conv2d_quantized_subnormals(oracle, stride):
+    """Subnormal activations times a scale of 2e38 land on codes 0-2 (the
+    quantizer keeps subnormals; flushed to zero they would all give 0)."""
+    n, h, w, c, oc, abits, scale = 2, 11, 13, 128, 20, 2, 2e38
+    say("conv2d_quantized subnormals", (n, h, w, c, oc, stride))
+    rng = np.random.default_rng(616 + stride)
+    x = rng.uniform(-1.2e-38, 1.2e-38, size=(n, h, w, c)).astype(np.float32)
+    assert (np.abs(x) < np.finfo(np.float32).tiny).mean() > 0.9
+    wq = rng.integers(0, 2, size=(oc, 1, 1, c), dtype=np.uint8)
+    codes = oracle.quantize(x, scale, abits)
+    assert codes.max() == 2 and (codes > 0).mean() > 0.3
+    op = oracle.conv_params(n, h, w, c, oc, 1, 1, stride, 0, abits, 1)
+    want = oracle.conv2d(op, oracle.pack(codes, abits), oracle.pack(wq, 1))
+    p = bs.ConvParams(n, h, w, c, oc, 1, 1, stride, stride, 0, 0, abits, 1,
+                      0, 0)
+    oh, ow = bs.bs_conv2d_out_shape(p)
+    out = torch.empty((n, oh, ow, oc), dtype=torch.int32, device="cuda")
+    bs.bs_conv2d_quantized(p, dev(x), scale, bs.pack(dev(wq), 1), out)
+    torch.cuda.synchronize()
+    assert np.array_equal(out.cpu().numpy(), want)
