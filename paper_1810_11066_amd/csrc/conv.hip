@@ -462,6 +462,23 @@ bool plan_pix_staged(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
     const size_t pwb = (size_t)s.abits * ((s.c + 31) / 32) * 4;
     size_t assumed = kTileLds;
     int run = forced_run;
+    if (run == 0 && src == pix::kSrcFloat && s.kh == 1 && s.sh > 1) {
+        // float32 pixels gathered for strided 1x1 windows: each workgroup
+        // that takes part of a 64-pixel group loads and quantizes all of
+        // the group's pixels, so runs are lengthened until at most two
+        // workgroups share a group, as long as the grid keeps a workgroup
+        // for at least every other CU (ResNet-18 layers 8 and 11 at batch
+        // 128: 18.3 -> 15.5 and 13.7 -> 11.3 us per launch; layer 5
+        // already had two; at batch 16 layer 11's grid would fall to 26
+        // workgroups and its launch took 10.8 instead of 7.5 us)
+        plan_pix_lds(s, fn, 0, nullptr, g, grid, assumed);
+        const int two = 2 * pix::kWavesPerBlock;
+        const int min_run = (g->group_units + two - 1) / two;
+        const int64_t per_block = (int64_t)pix::kWavesPerBlock * min_run;
+        const int64_t blocks = ((int64_t)g->units + per_block - 1) / per_block;
+        if (g->per_wave < min_run && 2 * blocks >= device_cus())
+            run = min_run;
+    }
     for (int iter = 0; iter < 24; ++iter) {
         plan_pix_lds(s, fn, run, nullptr, g, grid, assumed);
         const int64_t region = max_region_pixels(s, *g);
