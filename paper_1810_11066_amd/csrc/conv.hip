@@ -468,9 +468,9 @@ bool plan_pix_staged(const ConvShape& s, pix::PixKernelFn fn, int forced_run,
         // the group's pixels, so runs are lengthened until at most two
         // workgroups share a group, as long as the grid keeps a workgroup
         // for at least every other CU (ResNet-18 layers 8 and 11 at batch
-        // 128: 18.3 -> 15.5 and 13.7 -> 11.3 us per launch; layer 5
-        // already had two; at batch 16 layer 11's grid would fall to 26
-        // workgroups and its launch took 10.8 instead of 7.5 us)
+        // 128: 18.3 -> 15.5-16.8 and 13.7 -> 11.3-12.1 us per launch;
+        // layer 5 already had two; at batch 16 layer 11's grid would fall
+        // to 26 workgroups and its launch took 10.8 instead of 7.5 us)
         plan_pix_lds(s, fn, 0, nullptr, g, grid, assumed);
         const int two = 2 * pix::kWavesPerBlock;
         const int min_run = (g->group_units + two - 1) / two;
