@@ -332,7 +332,10 @@ bs_status bs_set_kernel_mode(int mode);
 /* Overrides, for later conv/dense calls on the calling host thread, how much
  * work each wave of the pixels-on-lanes kernel takes: a contiguous run of
  * `units` units of (64 output pixels x 4 output channels).  0 (the default)
- * lets the library choose the run that fills the GPU in one balanced round.
+ * lets the library choose the run that fills the GPU in one balanced round
+ * (for bs_conv2d_quantized with strided 1x1 windows, lengthened until at
+ * most two workgroups share a group of 64 output pixels, while the grid
+ * keeps a workgroup for at least every other compute unit).
  * Results do not depend on it; it exists for tests of the run boundaries and
  * for tuning.  Errors: BS_ERR_INVALID_ARG for units < 0. */
 bs_status bs_set_units_per_wave(int units);
